@@ -1,0 +1,253 @@
+"""Python face of the CPU oracle (oracle.c).
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, by ``__graft_entry__.smoke()``
+and by the CPU-baseline leg of ``bench.py``; the product package never imports
+it.  It shares no code with the GPU path: the C file is compiled here with gcc
+and driven through ctypes, and this module only marshals numpy arrays.
+
+Every routine follows a passage of the paper (D^2MoE, arXiv 2504.15299):
+  * ``mwq_quantize``   -- Sec. 3.3.1, Eq. 2-5, Algorithm 1 read with X = I;
+  * ``mwq_dequant``    -- the nested dequantized weight defined under Eq. 5;
+  * ``mwq_pack``       -- the canonical bit-plane layout (planes 0..b-1 are a
+                          b-bit read; Sec. 3.4 nested reuse of low bit-widths);
+  * ``gate_logits`` / ``route_from_logits`` -- dual routing (Fig. 1): top-k
+                          expert IDs plus a bit-width per activated expert, and
+                          the selection counts B_{j,k} of Sec. 3.4.3;
+  * ``expert_ffn`` / ``combine`` / ``moe_layer`` -- a SwiGLU expert FFN at the
+                          selected bit-width and the weighted combine.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile oracle.c with gcc (no FMA contraction, no fast math)."""
+    stale = (not os.path.exists(_LIB_PATH)) or (
+        os.path.getmtime(_LIB_PATH) < max(os.path.getmtime(_SRC),
+                                          os.path.getmtime(os.path.join(_HERE, "oracle.h"))))
+    if force or stale:
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+                               "-shared", "-fPIC", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _L():
+    global _lib
+    if _lib is None:
+        build()
+        lib = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        I = ctypes.c_int
+        lib.oracle_f32_to_f16.argtypes = [ctypes.c_float]
+        lib.oracle_f32_to_f16.restype = ctypes.c_uint16
+        lib.oracle_f16_to_f32.argtypes = [ctypes.c_uint16]
+        lib.oracle_f16_to_f32.restype = ctypes.c_float
+        lib.oracle_round_bf16.argtypes = [ctypes.c_float]
+        lib.oracle_round_bf16.restype = ctypes.c_float
+        lib.oracle_mwq_quantize.argtypes = [P, I, I, I, I, I, P, P, P, P, P]
+        lib.oracle_mwq_dequant.argtypes = [I, I, I, I, I, I, P, P, P, P, P]
+        lib.oracle_mwq_pack.argtypes = [I, I, I, I, I, P, P, P, P, P, P, P]
+        lib.oracle_gate_logits.argtypes = [P, I, I, P, P, I, P]
+        lib.oracle_route_from_logits.argtypes = [P, I, I, I, P, P, I, I, I, P, P, P, P, P, P, P, P]
+        lib.oracle_expert_ffn.argtypes = [I, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P, I, P]
+        lib.oracle_combine.argtypes = [I, I, I, P, P, P]
+        for name in ("oracle_mwq_quantize", "oracle_mwq_dequant", "oracle_mwq_pack",
+                     "oracle_gate_logits", "oracle_route_from_logits", "oracle_expert_ffn",
+                     "oracle_combine"):
+            getattr(lib, name).restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _p(a: np.ndarray | None):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _ok(rc: int, what: str):
+    if rc != 0:
+        raise ValueError(f"oracle {what} failed with code {rc}")
+
+
+# ---- number formats --------------------------------------------------------
+
+def f32_to_f16_bits(values) -> np.ndarray:
+    L = _L()
+    v = np.asarray(values, dtype=np.float32).ravel()
+    return np.array([L.oracle_f32_to_f16(float(x)) for x in v], dtype=np.uint16)
+
+
+def f16_bits_to_f32(bits) -> np.ndarray:
+    L = _L()
+    v = np.asarray(bits, dtype=np.uint16).ravel()
+    return np.array([L.oracle_f16_to_f32(int(x)) for x in v], dtype=np.float32)
+
+
+def round_bf16(values) -> np.ndarray:
+    L = _L()
+    v = np.asarray(values, dtype=np.float32).ravel()
+    return np.array([L.oracle_round_bf16(float(x)) for x in v], dtype=np.float32)
+
+
+# ---- MWQ -------------------------------------------------------------------
+
+class MWQCodes:
+    """Logical MWQ codes of one [rows][cols] matrix."""
+
+    def __init__(self, rows, cols, group, b_min, b_max, q1, zeros, scales, signs, resid_sq):
+        self.rows, self.cols, self.group = rows, cols, group
+        self.b_min, self.b_max = b_min, b_max
+        self.q1, self.zeros, self.scales, self.signs = q1, zeros, scales, signs
+        self.resid_sq = resid_sq
+
+    @property
+    def levels(self):
+        return self.b_max - self.b_min + 1
+
+
+def mwq_quantize(W: np.ndarray, group: int, b_min: int = 2, b_max: int = 8) -> MWQCodes:
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    rows, cols = W.shape
+    ng = cols // group
+    L = b_max - b_min + 1
+    q1 = np.zeros((rows, cols), np.uint8)
+    zeros = np.zeros((rows, ng), np.uint8)
+    scales = np.zeros((L, rows, ng), np.uint16)
+    signs = np.zeros((max(b_max - b_min, 1), rows, cols), np.uint8)
+    resid = np.zeros((L, rows, ng), np.float64)
+    _ok(_L().oracle_mwq_quantize(_p(W), rows, cols, group, b_min, b_max, _p(q1), _p(zeros),
+                                 _p(scales), _p(signs), _p(resid)), "mwq_quantize")
+    return MWQCodes(rows, cols, group, b_min, b_max, q1, zeros, scales,
+                    signs[: b_max - b_min], resid)
+
+
+def mwq_dequant(c: MWQCodes, b: int) -> np.ndarray:
+    out = np.zeros((c.rows, c.cols), np.float64)
+    signs = c.signs if c.signs.size else np.zeros((1, c.rows, c.cols), np.uint8)
+    _ok(_L().oracle_mwq_dequant(c.rows, c.cols, c.group, c.b_min, c.b_max, b, _p(c.q1),
+                                _p(c.zeros), _p(c.scales), _p(np.ascontiguousarray(signs)),
+                                _p(out)), "mwq_dequant")
+    return out
+
+
+def mwq_sizes(rows: int, cols: int, group: int, b_min: int, b_max: int):
+    """(plane words, scale entries, zero entries) of one packed matrix."""
+    return rows * cols // 32 * b_max, rows * (cols // group) * (b_max - b_min + 1), \
+        rows * (cols // group)
+
+
+def mwq_pack(c: MWQCodes):
+    nw, ns, nz = mwq_sizes(c.rows, c.cols, c.group, c.b_min, c.b_max)
+    planes = np.zeros(nw, np.uint32)
+    scales = np.zeros(ns, np.uint16)
+    zeros = np.zeros(nz, np.uint8)
+    signs = c.signs if c.signs.size else np.zeros((1, c.rows, c.cols), np.uint8)
+    _ok(_L().oracle_mwq_pack(c.rows, c.cols, c.group, c.b_min, c.b_max, _p(c.q1), _p(c.zeros),
+                             _p(c.scales), _p(np.ascontiguousarray(signs)), _p(planes),
+                             _p(scales), _p(zeros)), "mwq_pack")
+    return planes, scales, zeros
+
+
+# ---- routing ---------------------------------------------------------------
+
+def gate_logits(x: np.ndarray, Wg: np.ndarray, bias: np.ndarray | None = None) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    Wg = np.ascontiguousarray(Wg, dtype=np.float32)
+    T, d = x.shape
+    E = Wg.shape[0]
+    out = np.zeros((T, E), np.float64)
+    b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+    _ok(_L().oracle_gate_logits(_p(x), T, d, _p(Wg), _p(b), E, _p(out)), "gate_logits")
+    return out
+
+
+def route_from_logits(logits: np.ndarray, k: int, token_req: np.ndarray | None,
+                      bit_table: np.ndarray, b_min: int = 2, b_max: int = 8) -> dict:
+    logits = np.ascontiguousarray(logits, dtype=np.float64)
+    T, E = logits.shape
+    bit_table = np.ascontiguousarray(bit_table, dtype=np.uint8)
+    R = bit_table.shape[0]
+    req = None if token_req is None else np.ascontiguousarray(token_req, dtype=np.int32)
+    L = b_max - b_min + 1
+    o = dict(topk_idx=np.zeros((T, k), np.int32), topk_w=np.zeros((T, k), np.float64),
+             topk_bits=np.zeros((T, k), np.uint8), hist=np.zeros((E, L), np.int32),
+             offsets=np.zeros(E * L + 1, np.int32), perm=np.zeros(T * k, np.int32),
+             slot_of=np.zeros(T * k, np.int32), maxbit=np.zeros(E, np.uint8))
+    rc = _L().oracle_route_from_logits(
+        _p(logits), T, E, k, _p(req), _p(bit_table), R, b_min, b_max, _p(o["topk_idx"]),
+        _p(o["topk_w"]), _p(o["topk_bits"]), _p(o["hist"]), _p(o["offsets"]), _p(o["perm"]),
+        _p(o["slot_of"]), _p(o["maxbit"]))
+    _ok(rc, "route_from_logits")
+    return o
+
+
+# ---- expert FFN, combine, whole layer --------------------------------------
+
+def expert_ffn(c13: MWQCodes, c2: MWQCodes, b: int, x: np.ndarray) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    n, d = x.shape
+    f = c2.cols
+    assert c13.rows == 2 * f and c13.cols == d and c2.rows == d
+    y = np.zeros((n, d), np.float64)
+    s13 = c13.signs if c13.signs.size else np.zeros((1, c13.rows, c13.cols), np.uint8)
+    s2 = c2.signs if c2.signs.size else np.zeros((1, c2.rows, c2.cols), np.uint8)
+    _ok(_L().oracle_expert_ffn(d, f, c13.group, c2.group, c13.b_min, c13.b_max, b, _p(c13.q1),
+                               _p(c13.zeros), _p(c13.scales), _p(np.ascontiguousarray(s13)),
+                               _p(c2.q1), _p(c2.zeros), _p(c2.scales),
+                               _p(np.ascontiguousarray(s2)), _p(x), n, _p(y)), "expert_ffn")
+    return y
+
+
+def combine(topk_w: np.ndarray, y_slot: np.ndarray) -> np.ndarray:
+    topk_w = np.ascontiguousarray(topk_w, dtype=np.float64)
+    T, k = topk_w.shape
+    d = y_slot.shape[-1]
+    y_slot = np.ascontiguousarray(y_slot.reshape(T * k, d), dtype=np.float64)
+    out = np.zeros((T, d), np.float64)
+    _ok(_L().oracle_combine(T, k, d, _p(topk_w), _p(y_slot), _p(out)), "combine")
+    return out
+
+
+def moe_layer(x: np.ndarray, route: dict, codes13: list, codes2: list, tokens=None,
+              shared=None) -> np.ndarray:
+    """MoE layer output for the listed tokens (all if None), binary64.
+
+    ``route`` is the output of ``route_from_logits``; ``codes13[e]`` and
+    ``codes2[e]`` are the logical codes of expert e; ``shared`` is None or
+    (codes13, codes2, bits) of an always-on expert added with weight 1.
+    Expert outputs are computed per (expert, bit-width) group of slots."""
+    x = np.asarray(x, dtype=np.float32)
+    T, d = x.shape
+    idx, bits, w = route["topk_idx"], route["topk_bits"], route["topk_w"]
+    k = idx.shape[1]
+    toks = np.arange(T) if tokens is None else np.asarray(tokens)
+    y_slot = np.zeros((len(toks), k, d), np.float64)
+    for e in range(len(codes13)):
+        for b in sorted(set(int(v) for v in bits[toks][idx[toks] == e])):
+            sel = [(j, i) for j, t in enumerate(toks) for i in range(k)
+                   if idx[t, i] == e and bits[t, i] == b]
+            if not sel:
+                continue
+            xs = np.stack([x[toks[j]] for j, _ in sel]).astype(np.float64)
+            ys = expert_ffn(codes13[e], codes2[e], b, xs)
+            for (j, i), yv in zip(sel, ys):
+                y_slot[j, i] = yv
+    out = combine(w[toks], y_slot)
+    if shared is not None:
+        s13, s2, sb = shared
+        out = out + expert_ffn(s13, s2, sb, x[toks].astype(np.float64))
+    return out
