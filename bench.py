@@ -1,0 +1,223 @@
+"""Benchmark of the D^2MoE MoE-layer hot path on one MI355X.
+
+Workload: a Mixtral-8x7B-shaped MoE layer in decode (d_model 4096, d_ff 14336,
+8 SwiGLU experts, top-2), a batch of 16 tokens, one request per token, each
+(request, expert) bit-width drawn from {2,3,4,8} with probabilities
+{.2,.3,.3,.2}; weights N(0, 0.02) MWQ-packed with group 128 and an 8-bit nest;
+bf16 activations N(0,1).  Eight independently drawn layers rotate from step to
+step so that the weight reads miss the 256 MB last-level cache.  A step is one
+layer call: route (gate, top-k, bit lookup, histogram/permutation) plus the
+expert forward (W1/W3 + SwiGLU, W2, combine).
+
+Prints one JSON line.  `value` = tokens per second of the whole step with
+inputs resident in HBM; `roofline` = algorithmic bytes of the dominant kernel
+(W1/W3 expert kernel: packed planes, scales and zeros of every active expert
+up to its largest requested bit-width) per launch over its average duration,
+timed with HIP events on the stream it runs on; `cpu_baseline` = the CPU
+oracle on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("MoE-layer tokens/s + achieved HBM GB/s (fraction of peak) at mixed 2/3/4/8-bit "
+          "experts")
+HBM_PEAK_GBPS = 8000.0
+
+
+def mwq_bytes(rows, cols, group, b_min, bits):
+    """Packed bytes of a b-bit read of one [rows][cols] matrix: b planes,
+    the scales of levels <= b and the zeros."""
+    if bits <= 0:
+        return 0
+    ng = cols // group
+    return rows * cols * bits // 8 + rows * ng * 2 * (bits - b_min + 1) + rows * ng
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=60)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--batch", type=int, default=16)
+    ap.add_argument("--layers", type=int, default=8)
+    ap.add_argument("--sweep", default="1,4", help="extra batch sizes reported alongside")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build runs the MoE layer on a single "
+              "MI355X and has no multi-GPU path; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2504_15299_amd import api
+
+    dev = torch.device("cuda:0")
+    d, f, E, k, g, b_min, b_max = 4096, 14336, 8, 2, 128, 2, 8
+    NL = args.layers
+
+    # ---- resident packed weights, one set per rotating layer ----
+    t0 = time.time()
+    gen = torch.Generator(device=dev)
+    layers = []
+    for l in range(NL):
+        w13 = api.MWQ.empty(E, 2 * f, d, g, b_min, b_max, device=dev)
+        w2 = api.MWQ.empty(E, d, f, g, b_min, b_max, device=dev)
+        for e in range(E):
+            gen.manual_seed(1_000_003 * l + 2 * e)
+            W = torch.randn((1, 2 * f, d), generator=gen, device=dev) * 0.02
+            api.pack_mwq(W, w13.expert(e))
+            gen.manual_seed(1_000_003 * l + 2 * e + 1)
+            W = torch.randn((1, d, f), generator=gen, device=dev) * 0.02
+            api.pack_mwq(W, w2.expert(e))
+            del W
+        gen.manual_seed(7_000_000 + l)
+        Wg = torch.randn((E, d), generator=gen, device=dev) * 0.02
+        layers.append((w13, w2, Wg))
+    torch.cuda.synchronize()
+    pack_s = time.time() - t0
+
+    def run_batch(T, steps, warmup, profile):
+        rng = np.random.default_rng(2 + T)
+        x = torch.from_numpy(rng.standard_normal((T, d), dtype=np.float32)).to(dev).to(torch.bfloat16)
+        req = torch.arange(T, dtype=torch.int32, device=dev)
+        tables = [torch.from_numpy(rng.choice(np.array([2, 3, 4, 8], np.uint8), size=(T, E),
+                                              p=[0.2, 0.3, 0.3, 0.2])).to(dev)
+                  for _ in range(NL)]
+        routs = [api.Routing.empty(T, E, k, b_min, b_max, device=dev) for _ in range(NL)]
+        out = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+        ws = torch.empty(api.moe_forward_workspace(T, d, f, E, k), dtype=torch.uint8, device=dev)
+
+        def step(i, events=None):
+            l = i % NL
+            w13, w2, Wg = layers[l]
+            api.route(x, Wg, None, k, req, tables[l], b_min, b_max, out=routs[l])
+            api.moe_forward(x, w13, w2, routs[l], k, out=out, workspace=ws, events=events)
+
+        for i in range(warmup):
+            step(i)
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+        for row in evs:            # torch creates the HIP event at its first record
+            for ev in row:
+                ev.record()
+        torch.cuda.synchronize()
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_stop = torch.cuda.Event(enable_timing=True)
+        t_start.record()
+        for i in range(steps):
+            step(warmup + i, evs[i] if profile else None)
+        t_stop.record()
+        torch.cuda.synchronize()
+        ms = t_start.elapsed_time(t_stop) / steps
+        # algorithmic bytes per layer call from each layer's routing
+        alg13, alg2 = [], []
+        for l in range(NL):
+            mb = routs[l].expert_maxbit.cpu().numpy()
+            alg13.append(sum(mwq_bytes(2 * f, d, g, b_min, int(b)) for b in mb))
+            alg2.append(sum(mwq_bytes(d, f, g, b_min, int(b)) for b in mb))
+        per_step13 = [alg13[(warmup + i) % NL] for i in range(steps)]
+        per_step2 = [alg2[(warmup + i) % NL] for i in range(steps)]
+        res = dict(T=T, ms_per_step=ms, tokens_per_s=T / (ms * 1e-3),
+                   layer_bytes=float(np.mean([a + b for a, b in zip(per_step13, per_step2)])))
+        res["layer_GBps"] = res["layer_bytes"] / (ms * 1e-3) / 1e9
+        if profile:
+            d13 = np.array([e[0].elapsed_time(e[1]) for e in evs])
+            d2 = np.array([e[2].elapsed_time(e[3]) for e in evs])
+            res["w13_ms"] = float(d13.mean())
+            res["w2_ms"] = float(d2.mean())
+            res["w13_GBps"] = float(np.mean(per_step13) / (d13.mean() * 1e-3) / 1e9)
+            res["w2_GBps"] = float(np.mean(per_step2) / (d2.mean() * 1e-3) / 1e9)
+            res["w13_bytes"] = float(np.mean(per_step13))
+        return res
+
+    main_res = run_batch(args.batch, args.steps, args.warmup, profile=True)
+    sweep = []
+    for T in [int(v) for v in args.sweep.split(",") if v.strip()]:
+        r = run_batch(T, max(args.steps // 2, 5), args.warmup, profile=True)
+        sweep.append({kk: (round(v, 4) if isinstance(v, float) else v) for kk, v in r.items()})
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(d, f, E, k, g)
+
+    line = {
+        "metric": METRIC,
+        "value": round(main_res["tokens_per_s"], 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(main_res["ms_per_step"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"Mixtral-8x7B-shaped MoE layer decode (d_model 4096, d_ff 14336, "
+                               f"8 SwiGLU experts, top-2), batch {args.batch}, MWQ group 128 nested "
+                               f"to 8 bits, per-(request,expert) bits from {{2,3,4,8}} p "
+                               f"{{.2,.3,.3,.2}}, {NL} rotating layers",
+                   "batch": args.batch, "d_model": d, "d_ff": f, "experts": E, "top_k": k,
+                   "group": g},
+        "hbm_GBps": round(main_res["layer_GBps"], 1),
+        "hbm_frac": round(main_res["layer_GBps"] / HBM_PEAK_GBPS, 4),
+        "roofline": {"bound": "hbm", "kernel": "W1/W3 expert kernel",
+                     "achieved": round(main_res["w13_GBps"], 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(main_res["w13_GBps"] / HBM_PEAK_GBPS, 4),
+                     "traffic": None,
+                     "alg_bytes_per_launch": main_res["w13_bytes"],
+                     "avg_ms": round(main_res["w13_ms"], 5)},
+        "w2_kernel": {"achieved": round(main_res["w2_GBps"], 1), "avg_ms": round(main_res["w2_ms"], 5)},
+        "sweep": sweep,
+        "cpu_baseline": cpu,
+        "pack_seconds": round(pack_s, 2),
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(d, f, E, k, g):
+    """The CPU oracle (single thread, as it stands) on one decode token of the
+    same layer shape: gate logits, dual routing, the two selected experts'
+    SwiGLU FFNs from their MWQ codes, combine.  Quantizing the two experts is
+    setup and is not timed."""
+    import numpy as np
+
+    from oracle import oracle as O
+
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((1, d), dtype=np.float32)
+    Wg = (rng.standard_normal((E, d), dtype=np.float32) * 0.02)
+    table = np.array([[2, 3, 4, 8, 2, 3, 4, 8]], np.uint8)
+    logits = O.gate_logits(x, Wg)
+    route = O.route_from_logits(logits, k, None, table)
+    codes13, codes2 = {}, {}
+    for e in route["topk_idx"][0]:
+        e = int(e)
+        codes13[e] = O.mwq_quantize((rng.standard_normal((2 * f, d), dtype=np.float32) * 0.02), g)
+        codes2[e] = O.mwq_quantize((rng.standard_normal((d, f), dtype=np.float32) * 0.02), g)
+    t0 = time.perf_counter()
+    logits = O.gate_logits(x, Wg)
+    route = O.route_from_logits(logits, k, None, table)
+    ys = []
+    for i in range(k):
+        e = int(route["topk_idx"][0, i])
+        ys.append(O.expert_ffn(codes13[e], codes2[e], int(route["topk_bits"][0, i]),
+                               x.astype(np.float64))[0])
+    O.combine(route["topk_w"], np.stack(ys)[None])
+    secs = time.perf_counter() - t0
+    return {"value": round(1.0 / secs, 5), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "seconds": round(secs, 3),
+            "sample": "1 decode token of the same layer shape (gate, routing, its 2 experts' "
+                      "SwiGLU FFNs from MWQ codes at bits from {2,3,4,8}, combine); expert "
+                      "quantization untimed"}
+
+
+if __name__ == "__main__":
+    main()

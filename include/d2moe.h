@@ -1,0 +1,202 @@
+/*
+ * d2moe.h -- C ABI of the MI355X (gfx950) MoE-layer hot path of D^2MoE
+ * (dual routing + matryoshka weight quantization, arXiv 2504.15299).
+ *
+ * One MoE layer forward under dual routing: every token gets its top-k expert
+ * IDs, every activated expert gets a bit-width from a per-(request, expert)
+ * table (Fig. 1: expert ID *and* bit-width), and each expert's SwiGLU FFN
+ * reads its nested MWQ weights (Sec. 3.3) only up to that bit-width.
+ *
+ * Conventions for every entry point
+ *  - Pointers named as device buffers are caller-owned device memory (HIP);
+ *    the library never allocates, frees or keeps them, and keeps no global
+ *    state, so calls on different streams are independent.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    All argument checks run on the host before any launch; on failure a
+ *    negative status is returned and nothing is launched.  Work after a
+ *    successful return is asynchronous on `stream`; a launch failure is
+ *    reported as D2MOE_EHIP.  Nothing here synchronizes with the host.
+ *  - Shapes: a weight matrix is [rows][cols] with groups of `group`
+ *    consecutive columns (the reduction dimension); group is 64 or 128,
+ *    cols % group == 0 and rows % (2048/group) == 0.  Bit-width ladder
+ *    1 <= b_min <= b_max <= 8, one bit per step (Sec. 3.3.1).
+ */
+#ifndef D2MOE_H
+#define D2MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t d2moe_status;
+enum {
+  D2MOE_OK = 0,
+  D2MOE_EINVAL = -1,        /* bad argument (shape, null pointer, range) */
+  D2MOE_EUNSUPPORTED = -2,  /* valid but not implemented (e.g. dtype) */
+  D2MOE_EHIP = -3,          /* a HIP launch or runtime call failed */
+  D2MOE_EWORKSPACE = -4     /* workspace missing or smaller than required */
+};
+
+typedef enum { D2MOE_F32 = 0, D2MOE_BF16 = 1 } d2moe_dtype;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* d2moe_status_string(d2moe_status s);
+
+/*
+ * Packed MWQ weights of n_experts matrices of [rows][cols] (Sec. 3.3.1,
+ * DS: nested codes Q_b1, residual sign planes, per-group scales and zeros).
+ * Canonical tiled bit-plane layout, experts outermost, BR = 2048/group rows
+ * per block, KB = cols/group blocks per block-row, levels = b_max-b_min+1:
+ *   planes [E][rows/BR][KB][b_max][64] uint32: plane p < b_min holds bit p of
+ *          the base code, plane p >= b_min holds the residual sign of
+ *          bit-width p+1 (1 = +1); word w of a (block, plane) covers row
+ *          w % BR of the block and columns 32*(w/BR) .. +31 of the group,
+ *          bit j <-> column 32*(w/BR)+j.  A b-bit read touches planes 0..b-1
+ *          only, so lower bit-widths are prefixes of higher ones.
+ *   scales [E][rows/BR][KB][levels][BR] binary16: level 0 = base scale s_b1,
+ *          level l = residual scale of bit-width b_min+l;
+ *   zeros  [E][rows/BR][KB][BR] uint8: integer zero point of the base code.
+ * All three are device buffers of the sizes reported by d2moe_mwq_size.
+ */
+typedef struct {
+  int32_t n_experts, rows, cols, group, b_min, b_max;
+  uint32_t* planes;
+  uint16_t* scales;
+  uint8_t* zeros;
+} d2moe_mwq;
+
+/* Byte sizes of the three packed buffers.  Pure host function. */
+d2moe_status d2moe_mwq_size(int32_t n_experts, int32_t rows, int32_t cols,
+                            int32_t group, int32_t b_min, int32_t b_max,
+                            size_t* planes_bytes, size_t* scales_bytes,
+                            size_t* zeros_bytes);
+
+/*
+ * MWQ quantize + pack (Sec. 3.3.1: Eq. 2 asymmetric base level, Eq. 4-5
+ * binary residual levels, Algorithm 1 with X = I, i.e. no calibration
+ * activations).  W: device [n_experts][rows][cols] binary32 (w_dtype must be
+ * D2MOE_F32).  Per (row, group): base scale = binary16 of
+ * (max(0,max W) - min(0,min W)) / (2^b_min - 1), zero = rint(-min/scale)
+ * clamped, codes = clamp(rint(W/scale + zero)); for every further bit:
+ * scale = binary16 of mean |residual|, sign plane = [residual >= 0], residual
+ * -= scale * sign.  Binary32 arithmetic without contraction, identical to the
+ * CPU reference bit for bit.  `out` describes caller-allocated buffers.
+ */
+d2moe_status d2moe_pack_mwq(const void* W, d2moe_dtype w_dtype,
+                            const d2moe_mwq* out, void* stream);
+
+/*
+ * Test hook: unpack expert `expert` of `w` at bit-width `bits` with the
+ * device decoding routine the forward kernels use.
+ *   q1    device [rows][cols] uint8, base codes;
+ *   signs device [bits-b_min][rows][cols] int8 (+1/-1), may be NULL when
+ *         bits == b_min.
+ */
+d2moe_status d2moe_debug_unpack(const d2moe_mwq* w, int32_t expert,
+                                int32_t bits, uint8_t* q1, int8_t* signs,
+                                void* stream);
+
+/*
+ * Outputs of the dual router (Fig. 1), all caller-owned device buffers:
+ *   logits        [T][E] float   gate logits (x W_g^T + bias, fp32 accumulate)
+ *   topk_idx      [T][k] int32   experts, largest logit first, ties to the
+ *                                lower index
+ *   topk_w        [T][k] float   softmax over the k selected logits
+ *   topk_bits     [T][k] uint8   bit_table[token_req[t]][topk_idx[t][i]]
+ *   hist          [E][L] int32   selection counts B_{j,k} (Sec. 3.4.3),
+ *                                L = b_max-b_min+1, column = bit - b_min
+ *   offsets       [E*L+1] int32  exclusive scan of hist (expert major)
+ *   perm          [T*k] int32    slot ids t*k+i sorted stably by
+ *                                (expert, bit): perm[position] = slot
+ *   slot_of       [T*k] int32    inverse of perm: slot -> position
+ *   expert_maxbit [E] uint8      largest requested bit-width, 0 if unused
+ *   flags         [1] int32      bit 0: a table entry outside [b_min,b_max]
+ *                                (clamped), bit 1: a token_req outside
+ *                                [0,R) (clamped); 0 when all inputs valid
+ */
+typedef struct {
+  float* logits;
+  int32_t* topk_idx;
+  float* topk_w;
+  uint8_t* topk_bits;
+  int32_t* hist;
+  int32_t* offsets;
+  int32_t* perm;
+  int32_t* slot_of;
+  uint8_t* expert_maxbit;
+  int32_t* flags;
+} d2moe_routing;
+
+/*
+ * Dual routing (Fig. 1, Sec. 3.2 bit-width per activated expert, Sec. 3.4
+ * selection counts).  x: device [T][d] (x_dtype), Wg: device [E][d] float,
+ * bias: device [E] float or NULL, token_req: device [T] int32 request id of
+ * each token or NULL (all request 0), bit_table: device [R][E] uint8.
+ * 1 <= k <= E <= 64, d >= 1, T >= 0.  The bit-width table stands in for the
+ * paper's learned bit-width router, whose trained weights are not available.
+ */
+d2moe_status d2moe_route(const void* x, d2moe_dtype x_dtype, int32_t T,
+                         int32_t d, const float* Wg, const float* bias,
+                         int32_t E, int32_t k, const int32_t* token_req,
+                         const uint8_t* bit_table, int32_t R, int32_t b_min,
+                         int32_t b_max, const d2moe_routing* out,
+                         void* stream);
+
+/* Workspace bytes needed by d2moe_moe_forward for these sizes (host). */
+d2moe_status d2moe_moe_forward_workspace(int32_t T, int32_t d, int32_t d_ff,
+                                         int32_t E, int32_t k,
+                                         int32_t shared_d_ff, size_t* bytes);
+
+/*
+ * MoE layer forward (Sec. 3.3.2 dequantization fused into the expert GEMMs):
+ * for every routed (token, expert) pair at bit-width b,
+ *     y = W2_b (silu(W1_b x) * (W3_b x)),
+ *     out[t] = sum_i topk_w[t][i] * y(t, i)  [+ shared expert at shared_bits]
+ * Each expert reads its planes only up to the bit-widths requested of it.
+ *   x:    device [T][d] (x_dtype); out: device [T][d] (x_dtype)
+ *   w13:  E experts of [2*d_ff][d] (W1 rows, then W3 rows)
+ *   w2:   E experts of [d][d_ff]
+ *   r:    routing produced by d2moe_route for the same T, E, k, ladder
+ *         (uses topk_w, topk_bits, hist, offsets, perm, slot_of,
+ *         expert_maxbit)
+ *   shared_w13 / shared_w2: NULL, or 1 expert of [2*shared_d_ff][d] and
+ *         [d][shared_d_ff], applied to every token with weight 1 at
+ *         shared_bits (an always-on expert of fine-grained MoE layers)
+ *   workspace: device buffer of at least d2moe_moe_forward_workspace bytes,
+ *         256-byte aligned; contents need no initialisation.
+ * Accumulation is fp32; bf16 outputs are rounded to nearest even.
+ */
+d2moe_status d2moe_moe_forward(const void* x, d2moe_dtype x_dtype, int32_t T,
+                               int32_t d, int32_t d_ff, int32_t E, int32_t k,
+                               const d2moe_mwq* w13, const d2moe_mwq* w2,
+                               const d2moe_routing* r,
+                               const d2moe_mwq* shared_w13,
+                               const d2moe_mwq* shared_w2,
+                               int32_t shared_bits, int32_t shared_d_ff,
+                               void* out, void* workspace, size_t ws_bytes,
+                               void* stream);
+
+/*
+ * Same as d2moe_moe_forward, and additionally records events[0] / events[1]
+ * (hipEvent_t) on `stream` immediately before / after the W1-W3 expert
+ * kernel and events[2] / events[3] around the W2 expert kernel, so a caller
+ * can time the expert kernels on the stream they run on.  events must hold
+ * four created events.  Nothing is recorded when T == 0.
+ */
+d2moe_status d2moe_moe_forward_profiled(const void* x, d2moe_dtype x_dtype, int32_t T,
+                                        int32_t d, int32_t d_ff, int32_t E, int32_t k,
+                                        const d2moe_mwq* w13, const d2moe_mwq* w2,
+                                        const d2moe_routing* r,
+                                        const d2moe_mwq* shared_w13,
+                                        const d2moe_mwq* shared_w2, int32_t shared_bits,
+                                        int32_t shared_d_ff, void* out, void* workspace,
+                                        size_t ws_bytes, void* stream,
+                                        void* const* events);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* D2MOE_H */

@@ -1,0 +1,257 @@
+"""Python binding of libd2moe (ctypes).  Argument marshalling only: every step
+of the MoE layer runs in the HIP library; torch provides device memory and the
+current stream.  The names mirror the C ABI in include/d2moe.h.
+
+The library is loaded from this package directory; if it is missing the call
+fails loudly (run ``paper_2504_15299_amd.build.build()`` first).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libd2moe.so")
+
+D2MOE_F32, D2MOE_BF16 = 0, 1
+OK, EINVAL, EUNSUPPORTED, EHIP, EWORKSPACE = 0, -1, -2, -3, -4
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int32
+
+
+class _Mwq(ctypes.Structure):
+    _fields_ = [("n_experts", _I), ("rows", _I), ("cols", _I), ("group", _I), ("b_min", _I),
+                ("b_max", _I), ("planes", _P), ("scales", _P), ("zeros", _P)]
+
+
+class _Routing(ctypes.Structure):
+    _fields_ = [("logits", _P), ("topk_idx", _P), ("topk_w", _P), ("topk_bits", _P),
+                ("hist", _P), ("offsets", _P), ("perm", _P), ("slot_of", _P),
+                ("expert_maxbit", _P), ("flags", _P)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"HIP library not built: {LIB_PATH} is missing "
+                               "(call paper_2504_15299_amd.build.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        sz = ctypes.POINTER(ctypes.c_size_t)
+        L.d2moe_status_string.argtypes = [_I]
+        L.d2moe_status_string.restype = ctypes.c_char_p
+        L.d2moe_mwq_size.argtypes = [_I, _I, _I, _I, _I, _I, sz, sz, sz]
+        L.d2moe_pack_mwq.argtypes = [_P, _I, ctypes.POINTER(_Mwq), _P]
+        L.d2moe_debug_unpack.argtypes = [ctypes.POINTER(_Mwq), _I, _I, _P, _P, _P]
+        L.d2moe_route.argtypes = [_P, _I, _I, _I, _P, _P, _I, _I, _P, _P, _I, _I, _I,
+                                  ctypes.POINTER(_Routing), _P]
+        L.d2moe_moe_forward_workspace.argtypes = [_I, _I, _I, _I, _I, _I, sz]
+        L.d2moe_moe_forward.argtypes = [_P, _I, _I, _I, _I, _I, _I, ctypes.POINTER(_Mwq),
+                                        ctypes.POINTER(_Mwq), ctypes.POINTER(_Routing),
+                                        ctypes.POINTER(_Mwq), ctypes.POINTER(_Mwq), _I, _I, _P,
+                                        _P, ctypes.c_size_t, _P]
+        L.d2moe_moe_forward_profiled.argtypes = L.d2moe_moe_forward.argtypes + [_P]
+        for name in ("d2moe_mwq_size", "d2moe_pack_mwq", "d2moe_debug_unpack", "d2moe_route",
+                     "d2moe_moe_forward_workspace", "d2moe_moe_forward",
+                     "d2moe_moe_forward_profiled"):
+            getattr(L, name).restype = _I
+        _lib = L
+    return _lib
+
+
+class D2MoEError(RuntimeError):
+    def __init__(self, fn, status):
+        super().__init__(f"{fn} failed: {status} ({status_string(status)})")
+        self.status = status
+
+
+def status_string(s: int) -> str:
+    return lib().d2moe_status_string(int(s)).decode()
+
+
+def _check(fn, rc):
+    if rc != OK:
+        raise D2MoEError(fn, rc)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return D2MOE_F32
+    if t.dtype == torch.bfloat16:
+        return D2MOE_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+# ---- packed weights ---------------------------------------------------------
+
+def mwq_size(n_experts, rows, cols, group, b_min=2, b_max=8):
+    a, b, c = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+    _check("d2moe_mwq_size", lib().d2moe_mwq_size(n_experts, rows, cols, group, b_min, b_max,
+                                                  ctypes.byref(a), ctypes.byref(b),
+                                                  ctypes.byref(c)))
+    return a.value, b.value, c.value
+
+
+@dataclass
+class MWQ:
+    """Device buffers of packed MWQ weights (canonical tiled bit-plane layout)."""
+    n_experts: int
+    rows: int
+    cols: int
+    group: int
+    b_min: int
+    b_max: int
+    planes: torch.Tensor   # uint32 words, stored as int32
+    scales: torch.Tensor   # binary16 bit patterns, stored as int16
+    zeros: torch.Tensor    # uint8
+
+    @staticmethod
+    def empty(n_experts, rows, cols, group, b_min=2, b_max=8, device="cuda"):
+        pb, sb, zb = mwq_size(n_experts, rows, cols, group, b_min, b_max)
+        return MWQ(n_experts, rows, cols, group, b_min, b_max,
+                   torch.empty(pb // 4, dtype=torch.int32, device=device),
+                   torch.empty(sb // 2, dtype=torch.int16, device=device),
+                   torch.empty(zb, dtype=torch.uint8, device=device))
+
+    def _c(self) -> _Mwq:
+        return _Mwq(self.n_experts, self.rows, self.cols, self.group, self.b_min, self.b_max,
+                    self.planes.data_ptr(), self.scales.data_ptr(), self.zeros.data_ptr())
+
+    def nbytes(self):
+        return self.planes.numel() * 4 + self.scales.numel() * 2 + self.zeros.numel()
+
+    def expert(self, e: int) -> "MWQ":
+        """View of expert e as a one-expert MWQ (experts are outermost)."""
+        np_, ns, nz = (t.numel() // self.n_experts for t in (self.planes, self.scales, self.zeros))
+        return MWQ(1, self.rows, self.cols, self.group, self.b_min, self.b_max,
+                   self.planes.narrow(0, e * np_, np_), self.scales.narrow(0, e * ns, ns),
+                   self.zeros.narrow(0, e * nz, nz))
+
+
+def pack_mwq(W: torch.Tensor, out: MWQ, stream=None) -> MWQ:
+    """Quantize + pack W [n_experts][rows][cols] (fp32, device) into ``out``."""
+    assert W.is_cuda and W.is_contiguous()
+    c = out._c()
+    _check("d2moe_pack_mwq", lib().d2moe_pack_mwq(_ptr(W), _dtype_code(W), ctypes.byref(c),
+                                                  _stream(stream)))
+    return out
+
+
+def debug_unpack(w: MWQ, expert: int, bits: int, stream=None):
+    """(q1 [rows][cols] uint8, signs [bits-b_min][rows][cols] int8 or None)."""
+    dev = w.planes.device
+    q1 = torch.empty((w.rows, w.cols), dtype=torch.uint8, device=dev)
+    signs = (torch.empty((bits - w.b_min, w.rows, w.cols), dtype=torch.int8, device=dev)
+             if bits > w.b_min else None)
+    c = w._c()
+    _check("d2moe_debug_unpack", lib().d2moe_debug_unpack(ctypes.byref(c), expert, bits,
+                                                          _ptr(q1), _ptr(signs),
+                                                          _stream(stream)))
+    return q1, signs
+
+
+# ---- routing ----------------------------------------------------------------
+
+@dataclass
+class Routing:
+    logits: torch.Tensor
+    topk_idx: torch.Tensor
+    topk_w: torch.Tensor
+    topk_bits: torch.Tensor
+    hist: torch.Tensor
+    offsets: torch.Tensor
+    perm: torch.Tensor
+    slot_of: torch.Tensor
+    expert_maxbit: torch.Tensor
+    flags: torch.Tensor
+
+    @staticmethod
+    def empty(T, E, k, b_min=2, b_max=8, device="cuda"):
+        L = b_max - b_min + 1
+        i32, dev = torch.int32, device
+        return Routing(torch.empty((T, E), dtype=torch.float32, device=dev),
+                       torch.empty((T, k), dtype=i32, device=dev),
+                       torch.empty((T, k), dtype=torch.float32, device=dev),
+                       torch.empty((T, k), dtype=torch.uint8, device=dev),
+                       torch.empty((E, L), dtype=i32, device=dev),
+                       torch.empty(E * L + 1, dtype=i32, device=dev),
+                       torch.empty(T * k, dtype=i32, device=dev),
+                       torch.empty(T * k, dtype=i32, device=dev),
+                       torch.empty(E, dtype=torch.uint8, device=dev),
+                       torch.empty(1, dtype=i32, device=dev))
+
+    def _c(self) -> _Routing:
+        return _Routing(*[getattr(self, f).data_ptr() for f, _ in _Routing._fields_])
+
+
+def route(x: torch.Tensor, Wg: torch.Tensor, bias, k: int, token_req, bit_table: torch.Tensor,
+          b_min=2, b_max=8, out: Routing | None = None, stream=None) -> Routing:
+    T, d = x.shape
+    E = Wg.shape[0]
+    if out is None:
+        out = Routing.empty(T, E, k, b_min, b_max, device=x.device)
+    c = out._c()
+    _check("d2moe_route", lib().d2moe_route(_ptr(x), _dtype_code(x), T, d, _ptr(Wg), _ptr(bias),
+                                            E, k, _ptr(token_req), _ptr(bit_table),
+                                            bit_table.shape[0], b_min, b_max, ctypes.byref(c),
+                                            _stream(stream)))
+    return out
+
+
+# ---- forward ----------------------------------------------------------------
+
+def moe_forward_workspace(T, d, d_ff, E, k, shared_d_ff=0) -> int:
+    n = ctypes.c_size_t()
+    _check("d2moe_moe_forward_workspace",
+           lib().d2moe_moe_forward_workspace(T, d, d_ff, E, k, shared_d_ff, ctypes.byref(n)))
+    return n.value
+
+
+def moe_forward(x: torch.Tensor, w13: MWQ, w2: MWQ, r: Routing, k: int, shared=None,
+                out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                stream=None, events=None) -> torch.Tensor:
+    """``shared`` is None or (shared_w13: MWQ, shared_w2: MWQ, shared_bits).
+    ``events``: optional 4 torch.cuda.Event (created with enable_timing) that
+    are recorded around the W1/W3 and the W2 expert kernels."""
+    T, d = x.shape
+    E = w13.n_experts
+    d_ff = w2.cols
+    sw13 = sw2 = None
+    sbits = sff = 0
+    if shared is not None:
+        sw13, sw2, sbits = shared
+        sff = sw2.cols
+    if out is None:
+        out = torch.empty_like(x)
+    need = moe_forward_workspace(T, d, d_ff, E, k, sff)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    c13, c2, cr = w13._c(), w2._c(), r._c()
+    cs13 = ctypes.byref(sw13._c()) if sw13 is not None else None
+    cs2 = ctypes.byref(sw2._c()) if sw2 is not None else None
+    args = (_ptr(x), _dtype_code(x), T, d, d_ff, E, k, ctypes.byref(c13), ctypes.byref(c2),
+            ctypes.byref(cr), cs13, cs2, sbits, sff, _ptr(out), _ptr(workspace),
+            workspace.numel(), _stream(stream))
+    if events is None:
+        _check("d2moe_moe_forward", lib().d2moe_moe_forward(*args))
+    else:
+        arr = (ctypes.c_void_p * 4)(*[ev.cuda_event for ev in events])
+        _check("d2moe_moe_forward_profiled", lib().d2moe_moe_forward_profiled(*args, arr))
+    return out

@@ -1,0 +1,155 @@
+// C ABI of libd2moe: argument validation on the host, then asynchronous
+// launches on the caller's stream.  No allocation, no global state.
+#include "internal.h"
+
+using namespace d2moe;
+
+namespace {
+
+bool ladder_ok(int b_min, int b_max) { return b_min >= 1 && b_min <= b_max && b_max <= 8; }
+
+bool shape_ok(int rows, int cols, int group) {
+  if (group != 64 && group != 128) return false;
+  if (rows <= 0 || cols <= 0 || cols % group != 0) return false;
+  return rows % (2048 / group) == 0;
+}
+
+bool mwq_ok(const d2moe_mwq* m) {
+  return m && m->n_experts >= 1 && shape_ok(m->rows, m->cols, m->group) &&
+         ladder_ok(m->b_min, m->b_max) && m->planes && m->scales && m->zeros;
+}
+
+d2moe_status from_hip(hipError_t e) { return e == hipSuccess ? D2MOE_OK : D2MOE_EHIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* d2moe_status_string(d2moe_status s) {
+  switch (s) {
+    case D2MOE_OK: return "ok";
+    case D2MOE_EINVAL: return "invalid argument";
+    case D2MOE_EUNSUPPORTED: return "unsupported";
+    case D2MOE_EHIP: return "HIP error";
+    case D2MOE_EWORKSPACE: return "workspace too small";
+    default: return "unknown status";
+  }
+}
+
+d2moe_status d2moe_mwq_size(int32_t n_experts, int32_t rows, int32_t cols, int32_t group,
+                            int32_t b_min, int32_t b_max, size_t* planes_bytes,
+                            size_t* scales_bytes, size_t* zeros_bytes) {
+  if (n_experts < 1 || !shape_ok(rows, cols, group) || !ladder_ok(b_min, b_max))
+    return D2MOE_EINVAL;
+  const size_t E = (size_t)n_experts, N = (size_t)rows, K = (size_t)cols;
+  if (planes_bytes) *planes_bytes = E * N * K / 32 * (size_t)b_max * 4;
+  if (scales_bytes) *scales_bytes = E * N * (K / group) * (size_t)(b_max - b_min + 1) * 2;
+  if (zeros_bytes) *zeros_bytes = E * N * (K / group);
+  return D2MOE_OK;
+}
+
+d2moe_status d2moe_pack_mwq(const void* W, d2moe_dtype w_dtype, const d2moe_mwq* out,
+                            void* stream) {
+  if (!W || !mwq_ok(out)) return D2MOE_EINVAL;
+  if (w_dtype != D2MOE_F32) return D2MOE_EUNSUPPORTED;
+  return from_hip(launch_pack((const float*)W, out, (hipStream_t)stream));
+}
+
+d2moe_status d2moe_debug_unpack(const d2moe_mwq* w, int32_t expert, int32_t bits, uint8_t* q1,
+                                int8_t* signs, void* stream) {
+  if (!mwq_ok(w) || expert < 0 || expert >= w->n_experts || bits < w->b_min ||
+      bits > w->b_max || !q1 || (bits > w->b_min && !signs))
+    return D2MOE_EINVAL;
+  return from_hip(launch_debug_unpack(w, expert, bits, q1, signs, (hipStream_t)stream));
+}
+
+d2moe_status d2moe_route(const void* x, d2moe_dtype x_dtype, int32_t T, int32_t d,
+                         const float* Wg, const float* bias, int32_t E, int32_t k,
+                         const int32_t* token_req, const uint8_t* bit_table, int32_t R,
+                         int32_t b_min, int32_t b_max, const d2moe_routing* out, void* stream) {
+  if (T < 0 || d < 1 || E < 1 || E > 64 || k < 1 || k > E || R < 1 || !ladder_ok(b_min, b_max))
+    return D2MOE_EINVAL;
+  if (x_dtype != D2MOE_F32 && x_dtype != D2MOE_BF16) return D2MOE_EUNSUPPORTED;
+  if (!out || !out->hist || !out->offsets || !out->expert_maxbit || !out->flags)
+    return D2MOE_EINVAL;
+  if (T > 0 && (!out->topk_idx || !out->topk_w || !out->topk_bits || !out->perm ||
+                !out->slot_of || !out->logits))
+    return D2MOE_EINVAL;
+  if (T > 0 && (!x || !Wg || !bit_table)) return D2MOE_EINVAL;
+  if ((long long)T * k > (1ll << 30)) return D2MOE_EINVAL;
+  return from_hip(launch_route(x, x_dtype, T, d, Wg, bias, E, k, token_req, bit_table, R, b_min,
+                               b_max, out, (hipStream_t)stream));
+}
+
+d2moe_status d2moe_moe_forward_workspace(int32_t T, int32_t d, int32_t d_ff, int32_t E,
+                                         int32_t k, int32_t shared_d_ff, size_t* bytes) {
+  if (T < 0 || d < 1 || d_ff < 1 || E < 1 || E > 64 || k < 1 || k > E || shared_d_ff < 0 ||
+      !bytes)
+    return D2MOE_EINVAL;
+  *bytes = fwd_workspace_layout(T, d, d_ff, E, k, shared_d_ff).total;
+  return D2MOE_OK;
+}
+
+static d2moe_status forward_impl(const void* x, d2moe_dtype x_dtype, int32_t T, int32_t d,
+                                 int32_t d_ff, int32_t E, int32_t k, const d2moe_mwq* w13,
+                                 const d2moe_mwq* w2, const d2moe_routing* r,
+                                 const d2moe_mwq* shared_w13, const d2moe_mwq* shared_w2,
+                                 int32_t shared_bits, int32_t shared_d_ff, void* out,
+                                 void* workspace, size_t ws_bytes, void* stream,
+                                 void* const* events) {
+  if (T < 0 || d < 1 || d_ff < 1 || E < 1 || E > 64 || k < 1 || k > E) return D2MOE_EINVAL;
+  if (x_dtype != D2MOE_F32 && x_dtype != D2MOE_BF16) return D2MOE_EUNSUPPORTED;
+  if (!mwq_ok(w13) || !mwq_ok(w2) || !r) return D2MOE_EINVAL;
+  if (w13->n_experts != E || w13->rows != 2 * d_ff || w13->cols != d) return D2MOE_EINVAL;
+  if (w2->n_experts != E || w2->rows != d || w2->cols != d_ff) return D2MOE_EINVAL;
+  if (w13->b_min != w2->b_min || w13->b_max != w2->b_max) return D2MOE_EINVAL;
+  // output tiling: 32-row slices of W1/W3, 64-row slices of W2
+  if (d_ff % 32 != 0 || d % 64 != 0) return D2MOE_EUNSUPPORTED;
+  if (!r->hist || !r->offsets || !r->expert_maxbit) return D2MOE_EINVAL;
+  if (T > 0 && (!r->topk_w || !r->topk_bits || !r->perm || !r->slot_of)) return D2MOE_EINVAL;
+  const bool has_shared = shared_w13 || shared_w2;
+  if (has_shared) {
+    if (!mwq_ok(shared_w13) || !mwq_ok(shared_w2) || shared_d_ff < 1) return D2MOE_EINVAL;
+    if (shared_w13->n_experts != 1 || shared_w13->rows != 2 * shared_d_ff ||
+        shared_w13->cols != d || shared_w2->n_experts != 1 || shared_w2->rows != d ||
+        shared_w2->cols != shared_d_ff)
+      return D2MOE_EINVAL;
+    if (shared_w13->b_min != shared_w2->b_min || shared_w13->b_max != shared_w2->b_max ||
+        shared_bits < shared_w13->b_min || shared_bits > shared_w13->b_max)
+      return D2MOE_EINVAL;
+    if (shared_d_ff % 32 != 0) return D2MOE_EUNSUPPORTED;
+  }
+  if (T > 0 && (!x || !out)) return D2MOE_EINVAL;
+  const size_t need = fwd_workspace_layout(T, d, d_ff, E, k, has_shared ? shared_d_ff : 0).total;
+  if (T > 0 && (!workspace || ws_bytes < need || ((uintptr_t)workspace & 255u) != 0))
+    return D2MOE_EWORKSPACE;
+  return from_hip(launch_forward(x, x_dtype, T, d, d_ff, E, k, w13, w2, r,
+                                 has_shared ? shared_w13 : nullptr,
+                                 has_shared ? shared_w2 : nullptr, shared_bits,
+                                 has_shared ? shared_d_ff : 0, out, workspace,
+                                 (hipStream_t)stream, (hipEvent_t const*)events));
+}
+
+d2moe_status d2moe_moe_forward(const void* x, d2moe_dtype x_dtype, int32_t T, int32_t d,
+                               int32_t d_ff, int32_t E, int32_t k, const d2moe_mwq* w13,
+                               const d2moe_mwq* w2, const d2moe_routing* r,
+                               const d2moe_mwq* shared_w13, const d2moe_mwq* shared_w2,
+                               int32_t shared_bits, int32_t shared_d_ff, void* out,
+                               void* workspace, size_t ws_bytes, void* stream) {
+  return forward_impl(x, x_dtype, T, d, d_ff, E, k, w13, w2, r, shared_w13, shared_w2,
+                      shared_bits, shared_d_ff, out, workspace, ws_bytes, stream, nullptr);
+}
+
+d2moe_status d2moe_moe_forward_profiled(const void* x, d2moe_dtype x_dtype, int32_t T,
+                                        int32_t d, int32_t d_ff, int32_t E, int32_t k,
+                                        const d2moe_mwq* w13, const d2moe_mwq* w2,
+                                        const d2moe_routing* r, const d2moe_mwq* shared_w13,
+                                        const d2moe_mwq* shared_w2, int32_t shared_bits,
+                                        int32_t shared_d_ff, void* out, void* workspace,
+                                        size_t ws_bytes, void* stream, void* const* events) {
+  if (!events || !events[0] || !events[1] || !events[2] || !events[3]) return D2MOE_EINVAL;
+  return forward_impl(x, x_dtype, T, d, d_ff, E, k, w13, w2, r, shared_w13, shared_w2,
+                      shared_bits, shared_d_ff, out, workspace, ws_bytes, stream, events);
+}
+
+}  // extern "C"

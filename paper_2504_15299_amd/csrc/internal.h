@@ -1,0 +1,85 @@
+// Internal declarations shared by the HIP translation units of libd2moe.
+// Layout helpers for the canonical tiled bit-plane MWQ format and the
+// host-side launchers each kernel file provides.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/d2moe.h"
+
+namespace d2moe {
+
+// ---- canonical layout -----------------------------------------------------
+// A block is BR = 2048/group rows x group columns; per (block, plane) there are
+// 64 uint32 words; word w covers row w % BR and columns 32*(w/BR) .. +31.
+__host__ __device__ inline int block_rows(int group) { return 2048 / group; }
+
+struct MwqView {
+  int E, rows, cols, group, b_min, b_max;
+  const uint32_t* planes;
+  const uint16_t* scales;
+  const uint8_t* zeros;
+  __host__ __device__ int BR() const { return 2048 / group; }
+  __host__ __device__ int KB() const { return cols / group; }
+  __host__ __device__ int levels() const { return b_max - b_min + 1; }
+  // index of block (row-block rb, column-block kb) of expert e
+  __host__ __device__ size_t block(int e, int rb, int kb) const {
+    return ((size_t)e * (rows / BR()) + rb) * KB() + kb;
+  }
+  __host__ __device__ size_t plane_word(size_t blk, int p, int w) const {
+    return (blk * b_max + p) * 64 + w;
+  }
+  __host__ __device__ size_t scale_idx(size_t blk, int lev, int i) const {
+    return (blk * levels() + lev) * BR() + i;
+  }
+  __host__ __device__ size_t zero_idx(size_t blk, int i) const {
+    return blk * BR() + i;
+  }
+};
+
+inline MwqView view_of(const d2moe_mwq* m) {
+  MwqView v;
+  v.E = m->n_experts; v.rows = m->rows; v.cols = m->cols; v.group = m->group;
+  v.b_min = m->b_min; v.b_max = m->b_max;
+  v.planes = m->planes; v.scales = m->scales; v.zeros = m->zeros;
+  return v;
+}
+
+// Binary16 bit pattern <-> float (hardware conversions; float -> binary16
+// rounds to nearest even, subnormals kept).
+__device__ inline float h2f(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
+__device__ inline uint16_t f2h(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
+
+// bf16 helpers (round to nearest even).
+__device__ inline uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+__device__ inline float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// ---- launchers (return hipError_t of the launch) ---------------------------
+hipError_t launch_pack(const float* W, const d2moe_mwq* out, hipStream_t s);
+hipError_t launch_debug_unpack(const d2moe_mwq* w, int expert, int bits, uint8_t* q1,
+                               int8_t* signs, hipStream_t s);
+hipError_t launch_route(const void* x, d2moe_dtype xd, int T, int d, const float* Wg,
+                        const float* bias, int E, int k, const int32_t* token_req,
+                        const uint8_t* bit_table, int R, int b_min, int b_max,
+                        const d2moe_routing* out, hipStream_t s);
+
+// Forward workspace layout (256-byte aligned sub-buffers).
+struct FwdWorkspace {
+  size_t sched_off, h_off, hs_off, y_off, ys_off, total;
+};
+FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shared_d_ff);
+
+hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff, int E, int k,
+                          const d2moe_mwq* w13, const d2moe_mwq* w2, const d2moe_routing* r,
+                          const d2moe_mwq* sw13, const d2moe_mwq* sw2, int shared_bits,
+                          int shared_d_ff, void* out, void* ws, hipStream_t s,
+                          const hipEvent_t* events);
+
+}  // namespace d2moe

@@ -1,0 +1,188 @@
+// Dual routing (Fig. 1): gate logits, top-k expert IDs with a softmax over the
+// selected logits, the bit-width of every activated expert from the
+// per-(request, expert) table, and the (expert, bit-width) selection counts
+// B_{j,k} of Sec. 3.4.3 with their exclusive scan and the stable permutation
+// of (token, slot) pairs that the grouped expert kernels consume.
+//
+// Everything stays on the device; nothing synchronizes with the host.
+#include "internal.h"
+
+namespace d2moe {
+namespace {
+
+constexpr int kGateThreads = 256;
+
+template <typename XT>
+__device__ inline float load_x(const XT* p);
+template <>
+__device__ inline float load_x<float>(const float* p) { return *p; }
+template <>
+__device__ inline float load_x<uint16_t>(const uint16_t* p) { return bf2f(*p); }
+
+// logits[t][e] = x[t] . Wg[e] (+ bias[e]); one workgroup per token, one wave
+// per expert at a time, lanes stride the model dimension, fp32 accumulation.
+template <typename XT>
+__global__ __launch_bounds__(kGateThreads) void gate_kernel(const XT* __restrict__ x, int d,
+                                                            const float* __restrict__ Wg,
+                                                            const float* __restrict__ bias, int E,
+                                                            float* __restrict__ logits,
+                                                            int32_t* __restrict__ flags) {
+  const int t = blockIdx.x;
+  // the flag word is cleared here (a fill by a kernel rather than a memset
+  // node, so that a captured graph replays correctly)
+  if (t == 0 && threadIdx.x == 0) *flags = 0;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const XT* xt = x + (size_t)t * d;
+  for (int e = wave; e < E; e += kGateThreads / 64) {
+    const float* we = Wg + (size_t)e * d;
+    float acc = 0.0f;
+    for (int c = lane; c < d; c += 64) acc += load_x<XT>(xt + c) * we[c];
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    if (lane == 0) logits[(size_t)t * E + e] = acc + (bias ? bias[e] : 0.0f);
+  }
+}
+
+// Per token: top-k by (logit desc, index asc), softmax over the selected
+// logits, bit-width lookup with range checks.
+__global__ void topk_kernel(const float* __restrict__ logits, int T, int E, int k,
+                            const int32_t* __restrict__ token_req,
+                            const uint8_t* __restrict__ bit_table, int R, int b_min, int b_max,
+                            int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
+                            uint8_t* __restrict__ topk_bits, int32_t* __restrict__ flags) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= T) return;
+  const float* l = logits + (size_t)t * E;
+  uint64_t taken = 0;
+  int sel[64];
+  for (int i = 0; i < k; ++i) {
+    int best = -1;
+    for (int e = 0; e < E; ++e) {
+      if ((taken >> e) & 1ull) continue;
+      if (best < 0 || l[e] > l[best]) best = e;
+    }
+    taken |= 1ull << best;
+    sel[i] = best;
+  }
+  const float lmax = l[sel[0]];
+  float den = 0.0f;
+  for (int i = 0; i < k; ++i) den += expf(l[sel[i]] - lmax);
+  int r = token_req ? token_req[t] : 0;
+  int flag = 0;
+  if (r < 0 || r >= R) {
+    flag |= 2;
+    r = r < 0 ? 0 : R - 1;
+  }
+  for (int i = 0; i < k; ++i) {
+    topk_idx[t * k + i] = sel[i];
+    topk_w[t * k + i] = expf(l[sel[i]] - lmax) / den;
+    int b = bit_table[(size_t)r * E + sel[i]];
+    if (b < b_min || b > b_max) {
+      flag |= 1;
+      b = b < b_min ? b_min : b_max;
+    }
+    topk_bits[t * k + i] = (uint8_t)b;
+  }
+  if (flag) atomicOr(flags, flag);
+}
+
+constexpr int kHistThreads = 1024;
+constexpr int kHistWaves = kHistThreads / 64;
+constexpr int kMaxKeys = 64 * 8;  // E <= 64, L <= 8
+
+// Single workgroup: histogram of keys (expert * L + bit - b_min), exclusive
+// scan, stable placement of slots in ascending slot order within each key,
+// inverse permutation and largest requested bit per expert.  Slots are taken
+// 1024 at a time; within a chunk the rank of a slot among earlier slots with
+// the same key comes from wave ballots (equal-key lane masks) plus per-wave
+// counts of earlier waves.
+__global__ __launch_bounds__(kHistThreads) void hist_perm_kernel(
+    const int32_t* __restrict__ topk_idx, const uint8_t* __restrict__ topk_bits, int n, int E,
+    int L, int b_min, int32_t* __restrict__ flags, int32_t* __restrict__ hist, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ perm, int32_t* __restrict__ slot_of, uint8_t* __restrict__ maxbit) {
+  __shared__ int cnt[kMaxKeys];
+  __shared__ int off[kMaxKeys + 1];
+  __shared__ int run[kMaxKeys];
+  __shared__ int wave_cnt[kHistWaves][kMaxKeys];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nkeys = E * L;
+  if (n == 0 && tid == 0) *flags = 0;  // no gate launch cleared it
+  for (int j = tid; j < nkeys; j += kHistThreads) { cnt[j] = 0; run[j] = 0; }
+  __syncthreads();
+  for (int s = tid; s < n; s += kHistThreads)
+    atomicAdd(&cnt[topk_idx[s] * L + (topk_bits[s] - b_min)], 1);
+  __syncthreads();
+  if (tid == 0) {
+    int acc = 0;
+    for (int j = 0; j < nkeys; ++j) { off[j] = acc; acc += cnt[j]; }
+    off[nkeys] = acc;
+  }
+  __syncthreads();
+  for (int j = tid; j < nkeys; j += kHistThreads) hist[j] = cnt[j];
+  for (int j = tid; j <= nkeys; j += kHistThreads) offsets[j] = off[j];
+  for (int e = tid; e < E; e += kHistThreads) {
+    int mb = 0;
+    for (int j = 0; j < L; ++j) if (cnt[e * L + j] > 0) mb = b_min + j;
+    maxbit[e] = (uint8_t)mb;
+  }
+
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int base = 0; base < n; base += kHistThreads) {
+    for (int j = tid; j < kHistWaves * nkeys; j += kHistThreads)
+      wave_cnt[j / nkeys][j % nkeys] = 0;
+    __syncthreads();
+    const int s = base + tid;
+    const bool valid = s < n;
+    const int key = valid ? topk_idx[s] * L + (topk_bits[s] - b_min) : 0;
+    uint64_t same = __ballot(valid);
+    for (int bit = 0; bit < 10; ++bit) {
+      const bool b = (key >> bit) & 1;
+      const uint64_t mb = __ballot(b);
+      same &= b ? mb : ~mb;
+    }
+    const int rank_in_wave = __popcll(same & lt_mask);
+    if (valid && rank_in_wave == 0) wave_cnt[wave][key] = __popcll(same);
+    __syncthreads();
+    if (valid) {
+      int pos = off[key] + run[key] + rank_in_wave;
+      for (int w = 0; w < wave; ++w) pos += wave_cnt[w][key];
+      perm[pos] = s;
+      slot_of[s] = pos;
+    }
+    __syncthreads();
+    for (int j = tid; j < nkeys; j += kHistThreads) {
+      int acc = 0;
+      for (int w = 0; w < kHistWaves; ++w) acc += wave_cnt[w][j];
+      run[j] += acc;
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+hipError_t launch_route(const void* x, d2moe_dtype xd, int T, int d, const float* Wg,
+                        const float* bias, int E, int k, const int32_t* token_req,
+                        const uint8_t* bit_table, int R, int b_min, int b_max,
+                        const d2moe_routing* out, hipStream_t s) {
+  hipError_t err;
+  const int L = b_max - b_min + 1;
+  if (T > 0) {
+    if (xd == D2MOE_BF16)
+      gate_kernel<uint16_t><<<T, kGateThreads, 0, s>>>((const uint16_t*)x, d, Wg, bias, E,
+                                                       out->logits, out->flags);
+    else
+      gate_kernel<float><<<T, kGateThreads, 0, s>>>((const float*)x, d, Wg, bias, E,
+                                                    out->logits, out->flags);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    topk_kernel<<<(T + 63) / 64, 64, 0, s>>>(out->logits, T, E, k, token_req, bit_table, R,
+                                             b_min, b_max, out->topk_idx, out->topk_w,
+                                             out->topk_bits, out->flags);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+  }
+  hist_perm_kernel<<<1, kHistThreads, 0, s>>>(out->topk_idx, out->topk_bits, T * k, E, L, b_min,
+                                              out->flags, out->hist, out->offsets, out->perm, out->slot_of,
+                                              out->expert_maxbit);
+  return hipGetLastError();
+}
+
+}  // namespace d2moe

@@ -1,0 +1,112 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads and
+exports every entry point declared in include/d2moe.h, size queries follow the
+packed-format definition, and invalid arguments are rejected on the host
+before anything is launched."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2504_15299_amd import api
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "d2moe.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(d2moe_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = api.lib()
+    syms = declared_symbols()
+    assert len(syms) >= 7
+    for name in syms:
+        assert hasattr(lib, name), f"{name} not exported"
+
+
+def test_status_strings():
+    assert api.status_string(0) == "ok"
+    assert api.status_string(-4) == "workspace too small"
+    assert api.status_string(123) == "unknown status"
+
+
+@pytest.mark.parametrize("E,rows,cols,group,b_min,b_max", [
+    (8, 28672, 4096, 128, 2, 8), (64, 2816, 2048, 64, 2, 8), (1, 32, 64, 64, 1, 1)])
+def test_mwq_size_matches_layout(E, rows, cols, group, b_min, b_max):
+    pb, sb, zb = api.mwq_size(E, rows, cols, group, b_min, b_max)
+    assert pb == E * rows * cols * b_max // 8
+    assert sb == E * rows * (cols // group) * (b_max - b_min + 1) * 2
+    assert zb == E * rows * (cols // group)
+
+
+@pytest.mark.parametrize("args", [
+    (0, 32, 128, 128, 2, 8), (1, 30, 128, 128, 2, 8), (1, 32, 100, 128, 2, 8),
+    (1, 32, 128, 96, 2, 8), (1, 32, 128, 128, 0, 8), (1, 32, 128, 128, 5, 4),
+    (1, 32, 128, 128, 2, 9), (1, 16, 128, 64, 2, 8)])
+def test_mwq_size_rejects_bad_shapes(args):
+    with pytest.raises(api.D2MoEError) as ei:
+        api.mwq_size(*args)
+    assert ei.value.status == api.EINVAL
+
+
+def _mwq(**kw):
+    d = dict(n_experts=1, rows=32, cols=128, group=128, b_min=2, b_max=8,
+             planes=1 << 20, scales=1 << 21, zeros=1 << 22)
+    d.update(kw)
+    return api._Mwq(**d)
+
+
+def test_validation_before_launch():
+    """Every call below is invalid and must return before any HIP call (the
+    pointers are fake and would fault if used)."""
+    L = api.lib()
+    fake = ctypes.c_void_p(1 << 20)
+    # pack: null W, bad group, bad ladder, unsupported dtype
+    assert L.d2moe_pack_mwq(None, 0, ctypes.byref(_mwq()), None) == api.EINVAL
+    assert L.d2moe_pack_mwq(fake, 0, ctypes.byref(_mwq(group=32)), None) == api.EINVAL
+    assert L.d2moe_pack_mwq(fake, 0, ctypes.byref(_mwq(b_min=3, b_max=2)), None) == api.EINVAL
+    assert L.d2moe_pack_mwq(fake, 1, ctypes.byref(_mwq()), None) == api.EUNSUPPORTED
+    assert L.d2moe_pack_mwq(fake, 0, ctypes.byref(_mwq(planes=0)), None) == api.EINVAL
+    # debug unpack: expert / bits out of range, missing signs
+    assert L.d2moe_debug_unpack(ctypes.byref(_mwq()), 1, 4, fake, fake, None) == api.EINVAL
+    assert L.d2moe_debug_unpack(ctypes.byref(_mwq()), 0, 9, fake, fake, None) == api.EINVAL
+    assert L.d2moe_debug_unpack(ctypes.byref(_mwq()), 0, 4, fake, None, None) == api.EINVAL
+    # route: k > E, E > 64, missing outputs
+    r = api._Routing(*([1 << 20] * 10))
+    rb = ctypes.byref(r)
+    assert L.d2moe_route(fake, 1, 4, 64, fake, None, 8, 9, None, fake, 1, 2, 8, rb, None) == api.EINVAL
+    assert L.d2moe_route(fake, 1, 4, 64, fake, None, 65, 2, None, fake, 1, 2, 8, rb, None) == api.EINVAL
+    assert L.d2moe_route(fake, 1, 4, 64, fake, None, 8, 2, None, fake, 1, 2, 9, rb, None) == api.EINVAL
+    assert L.d2moe_route(fake, 7, 4, 64, fake, None, 8, 2, None, fake, 1, 2, 8, rb, None) == api.EUNSUPPORTED
+    r0 = api._Routing(*([1 << 20] * 9 + [0]))
+    assert L.d2moe_route(fake, 1, 4, 64, fake, None, 8, 2, None, fake, 1, 2, 8, ctypes.byref(r0),
+                         None) == api.EINVAL
+    # forward: shape mismatches and workspace
+    w13 = _mwq(n_experts=8, rows=2 * 256, cols=128)
+    w2 = _mwq(n_experts=8, rows=128, cols=256)
+    fwd = L.d2moe_moe_forward
+    assert fwd(fake, 1, 4, 128, 256, 8, 2, ctypes.byref(w13), ctypes.byref(w2), rb, None, None,
+               0, 0, fake, fake, 0, None) == api.EWORKSPACE
+    assert fwd(fake, 1, 4, 128, 256, 8, 2, ctypes.byref(w2), ctypes.byref(w13), rb, None, None,
+               0, 0, fake, fake, 1 << 30, None) == api.EINVAL
+    bad2 = _mwq(n_experts=8, rows=128, cols=256, b_max=7)
+    assert fwd(fake, 1, 4, 128, 256, 8, 2, ctypes.byref(w13), ctypes.byref(bad2), rb, None, None,
+               0, 0, fake, fake, 1 << 30, None) == api.EINVAL
+    s13 = _mwq(rows=2 * 128, cols=128)
+    s2 = _mwq(rows=128, cols=128)
+    assert fwd(fake, 1, 4, 128, 256, 8, 2, ctypes.byref(w13), ctypes.byref(w2), rb,
+               ctypes.byref(s13), ctypes.byref(s2), 9, 128, fake, fake, 1 << 30, None) == api.EINVAL
+    # misaligned workspace
+    assert fwd(fake, 1, 4, 128, 256, 8, 2, ctypes.byref(w13), ctypes.byref(w2), rb, None, None,
+               0, 0, fake, ctypes.c_void_p((1 << 20) + 8), 1 << 30, None) == api.EWORKSPACE
+
+
+def test_workspace_size_grows_with_tokens():
+    a = api.moe_forward_workspace(1, 4096, 14336, 8, 2)
+    b = api.moe_forward_workspace(16, 4096, 14336, 8, 2)
+    c = api.moe_forward_workspace(16, 4096, 14336, 8, 2, 5632)
+    assert 0 < a < b < c
