@@ -284,6 +284,13 @@ FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shar
   L.hs_off = off;     off += align256(sizeof(uint16_t) * (size_t)T * shared_d_ff);
   L.y_off = off;      off += align256(sizeof(float) * (size_t)T * k * d);
   L.ys_off = off;     off += align256(sizeof(float) * (size_t)T * (shared_d_ff > 0 ? d : 0));
+  const size_t nd = T <= kDecodeMaxTokens ? (size_t)T * k : 0;  // decode positions
+  L.elist_off = off;  off += align256(sizeof(int32_t) * ((size_t)E * 4 + 4));
+  L.xq13_off = off;   off += align256(nd * d * 2);
+  L.xs13_off = off;   off += align256(nd * (d / 32) * 2);
+  L.h32_off = off;    off += align256(nd * d_ff * sizeof(float));
+  L.xq2_off = off;    off += align256(nd * d_ff * 2);
+  L.xs2_off = off;    off += align256(nd * (d_ff / 32) * 2);
   L.total = off;
   return L;
 }
@@ -308,25 +315,39 @@ hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff,
   float* ys = (float*)(base + L.ys_off);
 
   hipError_t err;
-  schedule_kernel<<<1, 64, 0, s>>>(r->hist, r->offsets, nb, tstart, bstart, bcnt);
-  if ((err = hipGetLastError()) != hipSuccess) return err;
-
-  Sched sc{tstart, bstart, bcnt, nb, 0, 0, Lv, w13->b_min};
-  const int n = T * k;
-  const int ub = (n + BM - 1) / BM + (nb < n ? nb : n);
-  const MwqView W13 = view_of(w13), W2 = view_of(w2);
-  if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
-  if (xd == D2MOE_BF16)
-    err = run_gemm<true, uint16_t>((const uint16_t*)x, d, r->perm, k, W13, 0, sc, ub, d_ff, h,
-                                   d_ff, s);
-  else
-    err = run_gemm<true, float>((const float*)x, d, r->perm, k, W13, 0, sc, ub, d_ff, h, d_ff, s);
-  if (err != hipSuccess) return err;
-  if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
-  if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
-  err = run_gemm<false, uint16_t>(h, d_ff, nullptr, 1, W2, 0, sc, ub, d_ff, y, d, s);
-  if (err != hipSuccess) return err;
-  if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
+  if (decode_path_ok(w13, w2, T)) {
+    DecodeBuffers db;
+    db.elist = (int32_t*)(base + L.elist_off);
+    db.ecount = db.elist + (size_t)E * 4;
+    db.xq13 = (uint8_t*)(base + L.xq13_off);
+    db.xs13 = (uint8_t*)(base + L.xs13_off);
+    db.h32 = (float*)(base + L.h32_off);
+    db.xq2 = (uint8_t*)(base + L.xq2_off);
+    db.xs2 = (uint8_t*)(base + L.xs2_off);
+    db.y = y;
+    err = launch_decode_ffn(x, xd, T, d, d_ff, E, k, w13, w2, r, db, s, events);
+    if (err != hipSuccess) return err;
+  } else {
+    schedule_kernel<<<1, 64, 0, s>>>(r->hist, r->offsets, nb, tstart, bstart, bcnt);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    Sched sc{tstart, bstart, bcnt, nb, 0, 0, Lv, w13->b_min};
+    const int n = T * k;
+    const int ub = (n + BM - 1) / BM + (nb < n ? nb : n);
+    const MwqView W13 = view_of(w13), W2 = view_of(w2);
+    if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
+    if (xd == D2MOE_BF16)
+      err = run_gemm<true, uint16_t>((const uint16_t*)x, d, r->perm, k, W13, 0, sc, ub, d_ff, h,
+                                     d_ff, s);
+    else
+      err = run_gemm<true, float>((const float*)x, d, r->perm, k, W13, 0, sc, ub, d_ff, h, d_ff,
+                                  s);
+    if (err != hipSuccess) return err;
+    if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
+    if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
+    err = run_gemm<false, uint16_t>(h, d_ff, nullptr, 1, W2, 0, sc, ub, d_ff, y, d, s);
+    if (err != hipSuccess) return err;
+    if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
+  }
 
   if (has_shared) {
     Sched one{nullptr, nullptr, nullptr, 0, T, shared_bits, 1, sw13->b_min};

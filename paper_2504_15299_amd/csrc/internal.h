@@ -70,10 +70,27 @@ hipError_t launch_route(const void* x, d2moe_dtype xd, int T, int d, const float
                         const uint8_t* bit_table, int R, int b_min, int b_max,
                         const d2moe_routing* out, hipStream_t s);
 
-// Forward workspace layout (256-byte aligned sub-buffers).
+// Forward workspace layout (256-byte aligned sub-buffers).  The decode
+// buffers exist only when T <= kDecodeMaxTokens.
+constexpr int kDecodeMaxTokens = 16;
 struct FwdWorkspace {
-  size_t sched_off, h_off, hs_off, y_off, ys_off, total;
+  size_t sched_off, h_off, hs_off, y_off, ys_off;
+  size_t elist_off, xq13_off, xs13_off, h32_off, xq2_off, xs2_off;
+  size_t total;
 };
+
+struct DecodeBuffers {
+  int32_t* elist;   // [E][4]
+  int32_t* ecount;  // [1]
+  uint8_t *xq13, *xs13, *xq2, *xs2;
+  float* h32;       // [T*k][d_ff]
+  float* y;         // [T*k][d]
+};
+
+bool decode_path_ok(const d2moe_mwq* w13, const d2moe_mwq* w2, int T);
+hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_ff, int E, int k,
+                             const d2moe_mwq* w13, const d2moe_mwq* w2, const d2moe_routing* r,
+                             const DecodeBuffers& b, hipStream_t s, const hipEvent_t* events);
 FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shared_d_ff);
 
 hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff, int E, int k,

@@ -218,6 +218,23 @@ def test_forward_all_tokens_one_expert():
     assert err.max() <= FWD_TOL
 
 
+@pytest.mark.parametrize("T", [9, 16])
+def test_forward_decode_hot_experts(T):
+    """Decode batch where two experts receive every token (more than 8 tokens
+    per expert: two MFMA column blocks) with mixed bit-widths per token."""
+    spec = wl.scaled(wl.mixtral_decode(T=T), d=512, f=256)
+    L = Layer(spec)
+    L.bias = np.array([30.0, 20.0] + [0.0] * (spec.E - 2), np.float32)
+    L.ref_logits = O.gate_logits(L.x, L.Wg, L.bias)
+    L.ref_route = O.route_from_logits(L.ref_logits, spec.k, L.req, L.table)
+    L.pack()
+    r = L.route()
+    torch.cuda.synchronize()
+    assert r.hist.cpu().numpy()[0].sum() == T
+    err = row_max_abs_rel(L.forward(), L.reference())
+    assert err.max() <= FWD_TOL, f"worst row {err.max():.3e}"
+
+
 def test_forward_empty_batch():
     spec = wl.scaled(wl.mixtral_decode(T=1), d=256, f=128)
     L = Layer(spec).pack()
