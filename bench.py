@@ -48,6 +48,9 @@ def main():
     ap.add_argument("--layers", type=int, default=8)
     ap.add_argument("--sweep", default="1,4", help="extra batch sizes reported alongside")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 256 MiB device copy three times (reference for "
+                         "hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build runs the MoE layer on a single "
@@ -60,6 +63,13 @@ def main():
     from paper_2504_15299_amd import api
 
     dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     d, f, E, k, g, b_min, b_max = 4096, 14336, 8, 2, 128, 2, 8
     NL = args.layers
 

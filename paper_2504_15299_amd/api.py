@@ -2,8 +2,9 @@
 of the MoE layer runs in the HIP library; torch provides device memory and the
 current stream.  The names mirror the C ABI in include/d2moe.h.
 
-The library is loaded from this package directory; if it is missing the call
-fails loudly (run ``paper_2504_15299_amd.build.build()`` first).
+The library is loaded from this package directory (or from the path in the
+D2MOE_LIB environment variable); if it is missing the call fails loudly (run
+``paper_2504_15299_amd.build.build()`` first).
 """
 from __future__ import annotations
 
@@ -14,7 +15,7 @@ from dataclasses import dataclass
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libd2moe.so")
+LIB_PATH = os.environ.get("D2MOE_LIB") or os.path.join(_HERE, "libd2moe.so")
 
 D2MOE_F32, D2MOE_BF16 = 0, 1
 OK, EINVAL, EUNSUPPORTED, EHIP, EWORKSPACE = 0, -1, -2, -3, -4

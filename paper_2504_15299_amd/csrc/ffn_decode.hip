@@ -16,13 +16,14 @@
 // fold into three chained MFMAs (planes 0 and 1 with A scales 1 and 2, plus a
 // constant fp4 operand z - 1.5), so (Q - z) . x = -D as well.  Every plane
 // thus costs one MFMA and one fp16-scaled FMA per output, and no weight is
-// ever materialised as a number.  Tokens whose bit-width is below a plane
-// skip its FMA (exec mask); they share the loads.
+// ever materialised as a number.  Tokens whose bit-width is below a plane get
+// a zero coefficient for it; they share the loads.
 //
-// Work split: a workgroup owns one 16-row block (W1 and the matching W3 block
-// for the SwiGLU variant) of one active expert; its waves split the groups of
-// the reduction dimension and reduce through LDS.  Requirements: group 128,
-// b_min 2, at most 16 tokens per expert.
+// Work split: a workgroup owns one 16-row block (for SwiGLU, half its waves
+// take the W1 block and half the matching W3 block) of one active expert; the
+// waves of each half split the groups of the reduction dimension and reduce
+// through LDS.  Requirements: group 128, b_min 2, at most 16 tokens per
+// expert.
 #include "internal.h"
 
 namespace d2moe {
@@ -74,23 +75,30 @@ __device__ inline float ld_act<uint16_t>(const uint16_t* p) { return bf2f(*p); }
 // E8M0 block scales.  Logical column 32q + 4n + d sits at hardware k
 // 32q + 8d + n, matching the nibble order of the expanded plane words.
 //   Xq [pos][K/128][piece][128] bytes, Xs [pos][K/128][piece][4] bytes
+// Position npos is an all-zero slot that decode lanes without a token read,
+// so that every load in the decode loop is unconditional.
 template <typename TIN>
 __global__ void xprep_kernel(const TIN* __restrict__ in, int in_ld,
                              const int32_t* __restrict__ perm, int kdiv, int npos, int K,
                              uint8_t* __restrict__ Xq, uint8_t* __restrict__ Xs) {
   const int nb32 = K / 32;
   const int tid = blockIdx.x * blockDim.x + threadIdx.x;
-  if (tid >= npos * nb32) return;
+  if (tid >= (npos + 1) * nb32) return;
   const int pos = tid / nb32, kb = tid % nb32;
   const int g = kb >> 2, q = kb & 3, NG = K / G;
-  const long row = perm ? (long)(perm[pos] / kdiv) : (long)pos;
-  const TIN* src = in + row * in_ld + (long)kb * 32;
   float v[32];
   float amax = 0.0f;
+  if (pos < npos) {
+    const long row = perm ? (long)(perm[pos] / kdiv) : (long)pos;
+    const TIN* src = in + row * in_ld + (long)kb * 32;
 #pragma unroll
-  for (int e = 0; e < 32; ++e) {
-    v[e] = ld_act<TIN>(src + e);
-    amax = fmaxf(amax, fabsf(v[e]));
+    for (int e = 0; e < 32; ++e) {
+      v[e] = ld_act<TIN>(src + e);
+      amax = fmaxf(amax, fabsf(v[e]));
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 32; ++e) v[e] = 0.0f;
   }
   int s = 0;
   if (amax > 0.0f) {
@@ -139,132 +147,216 @@ __device__ inline v8i zero_operand(uint32_t z) {
   return a;
 }
 
+// Cross-lane product: every call sits in wave-uniform control flow (no
+// per-lane condition guards an MFMA or the use of its result in this file;
+// per-token predication is done by selecting coefficients), and every call
+// passes a zero accumulator.
 __device__ inline v4f mfma_fp4_fp8(const v8i& a, const v8i& b, v4f c, int sa, int sb) {
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 4, 0, 0, sa, 0, sb);
 }
 
 __device__ inline float silu(float a) { return a / (1.0f + __expf(-a)); }
 
-// elist[4*i]: expert, first position, end position, largest bit-width
+// Four binary16 scales (rows 4q..4q+3) as floats, or zeros when off.
+__device__ inline void scales4(uint2 s, bool on, float (&out)[4]) {
+  const uint32_t lo = on ? s.x : 0u, hi = on ? s.y : 0u;
+  out[0] = h2f((uint16_t)(lo & 0xffff));
+  out[1] = h2f((uint16_t)(lo >> 16));
+  out[2] = h2f((uint16_t)(hi & 0xffff));
+  out[3] = h2f((uint16_t)(hi >> 16));
+}
+
+template <int MB>
+struct GroupData {
+  uint32_t w[MB];      // plane words
+  uint2 s[MB - 1];     // four binary16 scales per level (rows 4q..4q+3)
+  uint32_t z;          // zero point of row j
+  v8i b[2];            // activation pieces per column block
+  int bs[2];           // their E8M0 block scales
+};
+
+struct WaveCtx {
+  const uint32_t* pl;  // plane words of group 0 of this row-block
+  const uint16_t* sc;  // scales of group 0
+  const uint8_t* zp;   // zero points of group 0
+  int pl_step, sc_step;
+  int lane, q, j, ncb;
+  bool valid[2];
+  int bit[2];
+  const uint8_t* xq[2];  // activation pieces of group 0, this lane
+  const uint8_t* xs[2];  // their scales
+};
+
+template <int MB>
+__device__ inline void load_group(GroupData<MB>& t, const WaveCtx& c, int g) {
+  const uint32_t* pp = c.pl + (size_t)g * c.pl_step + c.lane;
+#pragma unroll
+  for (int p = 0; p < MB; ++p) t.w[p] = __builtin_nontemporal_load(pp + p * 64);
+  const uint16_t* sp = c.sc + (size_t)g * c.sc_step + 4 * c.q;
+#pragma unroll
+  for (int lv = 0; lv < MB - 1; ++lv) t.s[lv] = *(const uint2*)(sp + lv * 16);
+  t.z = c.zp[(size_t)g * 16 + c.j];
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb) {
+    if (cb >= c.ncb) continue;  // wave-uniform; lanes without a token read the zero slot
+    const uint4* src = (const uint4*)(c.xq[cb] + (size_t)g * 256);
+    const uint4 u0 = src[0], u1 = src[1];
+    t.b[cb] = v8i{(int)u0.x, (int)u0.y, (int)u0.z, (int)u0.w,
+                  (int)u1.x, (int)u1.y, (int)u1.z, (int)u1.w};
+    t.bs[cb] = c.xs[cb][(size_t)g * 8];
+  }
+}
+
+template <int MB>
+__device__ inline void compute_group(const GroupData<MB>& t, const WaveCtx& c,
+                                     v4f (&acc)[2]) {
+  const v8i a0 = expand_sigma(t.w[0]), a1 = expand_sigma(t.w[1]);
+  const v8i au = zero_operand(t.z);
+  float s1[4];
+  scales4(t.s[0], true, s1);
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb) {
+    if (cb >= c.ncb) continue;  // wave-uniform
+    // three products with a zero accumulator, summed on the VALU: chaining
+    // them through the accumulator operand let the register allocator give
+    // the result a range that partially overlaps the accumulator input
+    const v4f z4 = v4f{0.f, 0.f, 0.f, 0.f};
+    const v4f d0 = mfma_fp4_fp8(a0, t.b[cb], z4, 127, t.bs[cb]);
+    const v4f d1 = mfma_fp4_fp8(a1, t.b[cb], z4, 128, t.bs[cb]);
+    const v4f du = mfma_fp4_fp8(au, t.b[cb], z4, 127, t.bs[cb]);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-s1[r], (d0[r] + d1[r]) + du[r], acc[cb][r]);
+  }
+#pragma unroll
+  for (int p = 2; p < MB; ++p) {
+    const v8i ap = expand_sigma(t.w[p]);
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) {
+      if (cb >= c.ncb) continue;  // wave-uniform
+      const v4f d = mfma_fp4_fp8(ap, t.b[cb], v4f{0.f, 0.f, 0.f, 0.f}, 128, t.bs[cb]);
+      float sp[4];
+      scales4(t.s[p - 1], p < c.bit[cb], sp);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-sp[r], d[r], acc[cb][r]);
+    }
+  }
+}
+
+// One wave's share: groups [g0, g1) at MB planes.  Everything a group needs
+// (planes, scales, zero points, activation pieces) is requested one group
+// ahead of its arithmetic, into two register sets used in turn (no copies,
+// so the wait before a group's arithmetic covers only the older loads).
+template <int MB>
+__device__ inline void decode_groups(const WaveCtx& c, int g0, int g1, v4f (&acc)[2]) {
+  if (g0 >= g1) return;
+  GroupData<MB> ga, gb;
+  load_group<MB>(ga, c, g0);
+  int g = g0;
+  for (; g + 1 < g1; g += 2) {
+    load_group<MB>(gb, c, g + 1);
+    compute_group<MB>(ga, c, acc);
+    if (g + 2 < g1) load_group<MB>(ga, c, g + 2);
+    compute_group<MB>(gb, c, acc);
+  }
+  if (g < g1) compute_group<MB>(ga, c, acc);
+}
+
+// elist[4*i]: expert, first position, end position, largest bit-width.
+// SwiGLU variant: waves [0, NW/2) stream the W1 row-block, waves [NW/2, NW)
+// the matching W3 row-block, each half splitting the groups; the epilogue
+// combines them through LDS.
 template <bool SWIGLU, int NW>
 __global__ __launch_bounds__(64 * NW) void decode_kernel(
     MwqView W, const int32_t* __restrict__ elist, const int32_t* __restrict__ ecount,
     const int32_t* __restrict__ perm, const uint8_t* __restrict__ topk_bits,
-    const uint8_t* __restrict__ Xq, const uint8_t* __restrict__ Xs, int f,
+    const uint8_t* __restrict__ Xq, const uint8_t* __restrict__ Xs, int npos, int f,
     float* __restrict__ out, int out_ld) {
-  __shared__ float red[NW][64][16];
+  __shared__ float red[NW][64][8];
   const int ei = blockIdx.y;
   if (ei >= *ecount) return;
   const int e = elist[4 * ei], p0 = elist[4 * ei + 1], p1 = elist[4 * ei + 2];
   const int mb = elist[4 * ei + 3];
   const int rb = blockIdx.x;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int q = lane >> 4, j = lane & 15, piece = lane & 1;
+  const int lane = threadIdx.x & 63;
+  // wave-uniform by construction; readfirstlane lets the compiler keep the
+  // group loop in scalar control flow
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int NG = W.cols / G;
-  const int g0 = wave * NG / NW, g1 = (wave + 1) * NG / NW;
+  constexpr int KS = SWIGLU ? NW / 2 : NW;  // waves splitting the groups
+  const int rr = SWIGLU ? wave / KS : 0;
+  const int wk = wave % KS;
+  const int g0 = wk * NG / KS, g1 = (wk + 1) * NG / KS;
   const int ncol = p1 - p0;
-  const int ncb = ncol > 8 ? 2 : 1;
 
-  int posj[2], bitj[2];
-  bool validj[2];
+  WaveCtx c;
+  c.lane = lane;
+  c.q = lane >> 4;
+  c.j = lane & 15;
+  c.ncb = ncol > 8 ? 2 : 1;
+  const int piece = lane & 1;
+  int posj[2];
 #pragma unroll
   for (int cb = 0; cb < 2; ++cb) {
-    const int t = cb * 8 + (j >> 1);
-    validj[cb] = t < ncol;
+    const int t = cb * 8 + (c.j >> 1);
+    c.valid[cb] = t < ncol;
     posj[cb] = p0 + t;
-    bitj[cb] = validj[cb] ? (int)topk_bits[perm[posj[cb]]] : 0;
+    c.bit[cb] = c.valid[cb] ? (int)topk_bits[perm[posj[cb]]] : 0;
+    const int src = c.valid[cb] ? posj[cb] : npos;  // zero slot when no token
+    const size_t base = ((size_t)src * NG) * 2 + piece;  // group 0
+    c.xq[cb] = Xq + base * 128 + c.q * 32;
+    c.xs[cb] = Xs + base * 4 + c.q;
+  }
+  const int rowblock = rr == 0 ? rb : rb + f / 16;
+  const size_t blk0 = W.block(e, rowblock, 0);
+  c.pl = W.planes + W.plane_word(blk0, 0, 0);
+  c.sc = W.scales + W.scale_idx(blk0, 0, 0);
+  c.zp = W.zeros + W.zero_idx(blk0, 0);
+  c.pl_step = W.b_max * 64;
+  c.sc_step = W.levels() * 16;
+
+  // An AGPR clobber keeps the accumulation registers allocated, which makes the
+  // compiler emit the AGPR-destination form of the MFMAs: their results can
+  // then never share registers with the VGPR operands they read.
+  asm volatile("" ::: "a0");
+  v4f acc[2];
+  acc[0] = acc[1] = v4f{0.f, 0.f, 0.f, 0.f};
+  switch (mb) {
+    case 2: decode_groups<2>(c, g0, g1, acc); break;
+    case 3: decode_groups<3>(c, g0, g1, acc); break;
+    case 4: decode_groups<4>(c, g0, g1, acc); break;
+    case 5: decode_groups<5>(c, g0, g1, acc); break;
+    case 6: decode_groups<6>(c, g0, g1, acc); break;
+    case 7: decode_groups<7>(c, g0, g1, acc); break;
+    case 8: decode_groups<8>(c, g0, g1, acc); break;
+    default: break;
   }
 
-  constexpr int NR = SWIGLU ? 2 : 1;
-  v4f acc[NR][2];
 #pragma unroll
-  for (int rr = 0; rr < NR; ++rr)
+  for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) acc[rr][cb] = v4f{0.f, 0.f, 0.f, 0.f};
-
-  for (int g = g0; g < g1; ++g) {
-    v8i bop[2];
-    int bsc[2];
-#pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
-      bsc[cb] = 127;
-      bop[cb] = v8i{0, 0, 0, 0, 0, 0, 0, 0};
-      if (cb < ncb && validj[cb]) {
-        const size_t base = ((size_t)posj[cb] * NG + g) * 2 + piece;
-        const uint4* src = (const uint4*)(Xq + base * 128 + q * 32);
-        const uint4 u0 = src[0], u1 = src[1];
-        bop[cb] = v8i{(int)u0.x, (int)u0.y, (int)u0.z, (int)u0.w,
-                      (int)u1.x, (int)u1.y, (int)u1.z, (int)u1.w};
-        bsc[cb] = Xs[base * 4 + q];
-      }
-    }
-#pragma unroll
-    for (int rr = 0; rr < NR; ++rr) {
-      const int rowblock = rr == 0 ? rb : rb + f / 16;
-      const size_t blk = W.block(e, rowblock, g);
-      const uint32_t z = W.zeros[W.zero_idx(blk, j)];
-      const uint2 s1 = *(const uint2*)(W.scales + W.scale_idx(blk, 0, 4 * q));
-      const uint32_t w0 = W.planes[W.plane_word(blk, 0, lane)];
-      const uint32_t w1 = W.planes[W.plane_word(blk, 1, lane)];
-      const v8i a0 = expand_sigma(w0), a1 = expand_sigma(w1), au = zero_operand(z);
-      const float sc[4] = {h2f((uint16_t)(s1.x & 0xffff)), h2f((uint16_t)(s1.x >> 16)),
-                           h2f((uint16_t)(s1.y & 0xffff)), h2f((uint16_t)(s1.y >> 16))};
-#pragma unroll
-      for (int cb = 0; cb < 2; ++cb) {
-        if (cb >= ncb) continue;
-        v4f d = v4f{0.f, 0.f, 0.f, 0.f};
-        d = mfma_fp4_fp8(a0, bop[cb], d, 127, bsc[cb]);
-        d = mfma_fp4_fp8(a1, bop[cb], d, 128, bsc[cb]);
-        d = mfma_fp4_fp8(au, bop[cb], d, 127, bsc[cb]);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc[rr][cb][r] = fmaf(-sc[r], d[r], acc[rr][cb][r]);
-      }
-      for (int p = 2; p < mb; ++p) {
-        const uint32_t wp = W.planes[W.plane_word(blk, p, lane)];
-        const uint2 sp2 = *(const uint2*)(W.scales + W.scale_idx(blk, p - 1, 4 * q));
-        const v8i ap = expand_sigma(wp);
-        const float sp[4] = {h2f((uint16_t)(sp2.x & 0xffff)), h2f((uint16_t)(sp2.x >> 16)),
-                             h2f((uint16_t)(sp2.y & 0xffff)), h2f((uint16_t)(sp2.y >> 16))};
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb) {
-          if (cb >= ncb) continue;
-          const v4f d = mfma_fp4_fp8(ap, bop[cb], v4f{0.f, 0.f, 0.f, 0.f}, 128, bsc[cb]);
-          if (p < bitj[cb]) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) acc[rr][cb][r] = fmaf(-sp[r], d[r], acc[rr][cb][r]);
-          }
-        }
-      }
-    }
-  }
-
-  // reduce the groups split over the waves
-#pragma unroll
-  for (int rr = 0; rr < NR; ++rr)
-#pragma unroll
-    for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) red[wave][lane][rr * 8 + cb * 4 + r] = acc[rr][cb][r];
+    for (int r = 0; r < 4; ++r) red[wave][lane][cb * 4 + r] = acc[cb][r];
   __syncthreads();
   if (wave != 0) return;
-  float v[NR][2][4];
+  constexpr int NRR = SWIGLU ? 2 : 1;
+  float v[NRR][2][4];
 #pragma unroll
-  for (int rr = 0; rr < NR; ++rr)
+  for (int h = 0; h < NRR; ++h)
 #pragma unroll
     for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        float s = 0.0f;
-        for (int w = 0; w < NW; ++w) s += red[w][lane][rr * 8 + cb * 4 + r];
-        v[rr][cb][r] = s + __shfl_xor(s, 1, 64);  // hi + lo pieces
+        float sum = 0.0f;
+        for (int w = 0; w < KS; ++w) sum += red[h * KS + w][lane][cb * 4 + r];
+        v[h][cb][r] = sum + __shfl_xor(sum, 1, 64);  // hi + lo pieces
       }
 #pragma unroll
   for (int cb = 0; cb < 2; ++cb) {
-    if (cb >= ncb || !validj[cb] || piece != 0) continue;
-    float* dst = out + (size_t)posj[cb] * out_ld + rb * 16 + 4 * q;
+    if (cb >= c.ncb || !c.valid[cb] || piece != 0) continue;
+    float* dst = out + (size_t)posj[cb] * out_ld + rb * 16 + 4 * c.q;
     float o[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) o[r] = SWIGLU ? silu(v[0][cb][r]) * v[NR - 1][cb][r] : v[0][cb][r];
+    for (int r = 0; r < 4; ++r)
+      o[r] = SWIGLU ? silu(v[0][cb][r]) * v[NRR - 1][cb][r] : v[0][cb][r];
     *(float4*)dst = float4{o[0], o[1], o[2], o[3]};
   }
 }
@@ -289,7 +381,7 @@ __global__ void expert_list_kernel(const int32_t* __restrict__ offsets,
 template <typename TIN>
 hipError_t run_xprep(const TIN* in, int in_ld, const int32_t* perm, int kdiv, int npos, int K,
                      uint8_t* Xq, uint8_t* Xs, hipStream_t s) {
-  const int n = npos * (K / 32);
+  const int n = (npos + 1) * (K / 32);
   xprep_kernel<TIN><<<(n + 255) / 256, 256, 0, s>>>(in, in_ld, perm, kdiv, npos, K, Xq, Xs);
   return hipGetLastError();
 }
@@ -317,15 +409,15 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   const int ny = E < npos ? E : npos;
   const MwqView W13 = view_of(w13), W2 = view_of(w2);
   if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
-  decode_kernel<true, 4><<<dim3(d_ff / 16, ny), 256, 0, s>>>(
-      W13, b.elist, b.ecount, r->perm, r->topk_bits, b.xq13, b.xs13, d_ff, b.h32, d_ff);
+  decode_kernel<true, 8><<<dim3(d_ff / 16, ny), 512, 0, s>>>(
+      W13, b.elist, b.ecount, r->perm, r->topk_bits, b.xq13, b.xs13, npos, d_ff, b.h32, d_ff);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
   err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.xq2, b.xs2, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
   decode_kernel<false, 8><<<dim3(d / 16, ny), 512, 0, s>>>(
-      W2, b.elist, b.ecount, r->perm, r->topk_bits, b.xq2, b.xs2, 0, b.y, d);
+      W2, b.elist, b.ecount, r->perm, r->topk_bits, b.xq2, b.xs2, npos, 0, b.y, d);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
   return hipSuccess;

@@ -286,11 +286,12 @@ FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shar
   L.ys_off = off;     off += align256(sizeof(float) * (size_t)T * (shared_d_ff > 0 ? d : 0));
   const size_t nd = T <= kDecodeMaxTokens ? (size_t)T * k : 0;  // decode positions
   L.elist_off = off;  off += align256(sizeof(int32_t) * ((size_t)E * 4 + 4));
-  L.xq13_off = off;   off += align256(nd * d * 2);
-  L.xs13_off = off;   off += align256(nd * (d / 32) * 2);
+  const size_t nz = nd ? nd + 1 : 0;  // plus one all-zero activation slot
+  L.xq13_off = off;   off += align256(nz * d * 2);
+  L.xs13_off = off;   off += align256(nz * (d / 32) * 2);
   L.h32_off = off;    off += align256(nd * d_ff * sizeof(float));
-  L.xq2_off = off;    off += align256(nd * d_ff * 2);
-  L.xs2_off = off;    off += align256(nd * (d_ff / 32) * 2);
+  L.xq2_off = off;    off += align256(nz * d_ff * 2);
+  L.xs2_off = off;    off += align256(nz * (d_ff / 32) * 2);
   L.total = off;
   return L;
 }

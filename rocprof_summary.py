@@ -1,0 +1,68 @@
+"""Summarise rocprofv3 result databases (rocpd SQLite) of bench.py runs.
+
+  python rocprof_summary.py trace <kt_results.db>
+      per-kernel call count, total and average duration (kernel-trace run)
+  python rocprof_summary.py counter <results.db> <COUNTER> [<kernel substring> ...]
+      per-kernel average of a per-dispatch counter (e.g. FETCH_SIZE, WRITE_SIZE,
+      in KiB), and the same counter for the plain 256 MiB copy that
+      `bench.py --copy-calibration` runs first, as the calibration factor
+      measured KiB / 262144 KiB.
+"""
+import sqlite3
+import sys
+from collections import defaultdict
+
+
+def _short(name: str) -> str:
+    for key in ("decode_kernel<true", "decode_kernel<false", "xprep_kernel", "gemm_kernel",
+                "combine_kernel", "gate_kernel", "topk_kernel", "hist_perm_kernel",
+                "expert_list_kernel", "schedule_kernel", "pack_kernel"):
+        if key in name:
+            return name[name.find(key):][:90]
+    return name[:90]
+
+
+def trace(db):
+    con = sqlite3.connect(db)
+    rows = con.execute("select name, duration from kernels").fetchall()
+    agg = defaultdict(list)
+    for name, dur in rows:
+        agg[_short(name)].append(dur)
+    print(f"{'kernel':92s} {'calls':>6s} {'total_us':>10s} {'avg_us':>9s}")
+    for name, durs in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
+        print(f"{name:92s} {len(durs):6d} {sum(durs) / 1e3:10.1f} {sum(durs) / len(durs) / 1e3:9.2f}")
+
+
+def counter(db, cname, subs):
+    con = sqlite3.connect(db)
+    cols = [r[1] for r in con.execute("pragma table_info('counters_collection')")]
+    rows = con.execute("select * from counters_collection").fetchall()
+    ix = {c: i for i, c in enumerate(cols)}
+    name_col = "kernel_name" if "kernel_name" in ix else "name"
+    per_disp = defaultdict(float)
+    names = {}
+    for r in rows:
+        if r[ix["counter_name"]] != cname:
+            continue
+        key = r[ix["dispatch_id"]]
+        per_disp[key] += float(r[ix["value"]])
+        names[key] = r[ix[name_col]]
+    agg = defaultdict(list)
+    for key, v in per_disp.items():
+        agg[_short(names[key])].append(v)
+    print(f"{'kernel':92s} {'dispatches':>10s} {cname + '_KiB_avg':>16s}")
+    for name, vals in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
+        if subs and not any(s in name for s in subs + ["elementwise", "copy"]):
+            continue
+        print(f"{name:92s} {len(vals):10d} {sum(vals) / len(vals):16.1f}")
+    cal = [v for n, vs in agg.items() for v in vs if ("copy" in n.lower() or "elementwise" in n.lower())]
+    if cal:
+        print(f"calibration: first copy-like kernel {cal[0]:.1f} KiB for a 262144 KiB copy "
+              f"-> factor {cal[0] / 262144.0:.4f}")
+
+
+if __name__ == "__main__":
+    if sys.argv[1] == "trace":
+        trace(sys.argv[2])
+    else:
+        counter(sys.argv[2], sys.argv[3], sys.argv[4:])
