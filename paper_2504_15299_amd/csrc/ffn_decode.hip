@@ -127,12 +127,27 @@ __global__ void xprep_kernel(const TIN* __restrict__ in, int in_ld,
   Xs[(base + 1) * 4 + q] = (uint8_t)(s - 4 + 127);
 }
 
-__device__ inline v8i expand_sigma(uint32_t w) {
+// Opaque copies of the two masks used by expand_sigma: held in VGPRs, they
+// let each output dword be one shift plus one v_and_or_b32 (the three-operand
+// form takes no literal on this target).
+struct SigmaConsts {
+  uint32_t m8, c1;
+};
+__device__ inline SigmaConsts sigma_consts() {
+  SigmaConsts k;
+  asm volatile("" : "=v"(k.m8) : "0"(0x88888888u));
+  asm volatile("" : "=v"(k.c1) : "0"(0x11111111u));
+  return k;
+}
+
+// fp4 e2m1 operand of one plane word: bit 4n+d of w becomes the sign of
+// nibble n of dword d, magnitude 0.5, so a set bit reads as -0.5.
+__device__ inline v8i expand_sigma(uint32_t w, const SigmaConsts& k) {
   v8i a;
-  a[0] = (int)(((w << 3) & 0x88888888u) | 0x11111111u);
-  a[1] = (int)(((w << 2) & 0x88888888u) | 0x11111111u);
-  a[2] = (int)(((w << 1) & 0x88888888u) | 0x11111111u);
-  a[3] = (int)((w & 0x88888888u) | 0x11111111u);
+  a[0] = (int)(((w << 3) & k.m8) | k.c1);
+  a[1] = (int)(((w << 2) & k.m8) | k.c1);
+  a[2] = (int)(((w << 1) & k.m8) | k.c1);
+  a[3] = (int)((w & k.m8) | k.c1);
   a[4] = a[5] = a[6] = a[7] = 0;
   return a;
 }
@@ -149,56 +164,75 @@ __device__ inline v8i zero_operand(uint32_t z) {
 
 // Cross-lane product: every call sits in wave-uniform control flow (no
 // per-lane condition guards an MFMA or the use of its result in this file;
-// per-token predication is done by selecting coefficients), and every call
-// passes a zero accumulator.
+// per-token predication is done through the activation block scale).
 __device__ inline v4f mfma_fp4_fp8(const v8i& a, const v8i& b, v4f c, int sa, int sb) {
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 4, 0, 0, sa, 0, sb);
 }
 
 __device__ inline float silu(float a) { return a / (1.0f + __expf(-a)); }
 
-// Four binary16 scales (rows 4q..4q+3) as floats, or zeros when off.
-__device__ inline void scales4(uint2 s, bool on, float (&out)[4]) {
-  const uint32_t lo = on ? s.x : 0u, hi = on ? s.y : 0u;
-  out[0] = h2f((uint16_t)(lo & 0xffff));
-  out[1] = h2f((uint16_t)(lo >> 16));
-  out[2] = h2f((uint16_t)(hi & 0xffff));
-  out[3] = h2f((uint16_t)(hi >> 16));
+// Four binary16 scales (rows 4q..4q+3) as floats.
+__device__ inline void scales4(uint2 s, float (&out)[4]) {
+  out[0] = h2f((uint16_t)(s.x & 0xffff));
+  out[1] = h2f((uint16_t)(s.x >> 16));
+  out[2] = h2f((uint16_t)(s.y & 0xffff));
+  out[3] = h2f((uint16_t)(s.y >> 16));
 }
 
-template <int MB>
-struct GroupData {
-  uint32_t w[MB];      // plane words
-  uint2 s[MB - 1];     // four binary16 scales per level (rows 4q..4q+3)
-  uint32_t z;          // zero point of row j
-  v8i b[2];            // activation pieces per column block
-  int bs[2];           // their E8M0 block scales
-};
+// Per-wave LDS ring for the weight stream: one stage holds one group's
+// planes (up to 8 x 256 B), its scales (up to 7 levels x 16 rows x 2 B) and
+// its 16 zero points, copied from global memory by the LDS DMA engine so that
+// data in flight costs no registers.
+constexpr int kStage = 2304;            // bytes per stage
+// ring depth 3 (two groups in flight), one LDS array per stage
+constexpr int kScaleOff = 2048, kZeroOff = 2272;
+
+#define D2MOE_GPTR(p) ((__attribute__((address_space(1))) void*)(p))
+#define D2MOE_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
 
 struct WaveCtx {
-  const uint32_t* pl;  // plane words of group 0 of this row-block
-  const uint16_t* sc;  // scales of group 0
+  const uint8_t* pl;   // plane words of group 0 of this row-block (bytes)
+  const uint8_t* sc;   // scales of group 0 (bytes)
   const uint8_t* zp;   // zero points of group 0
-  int pl_step, sc_step;
+  int pl_step, sc_step;  // bytes per group
   int lane, q, j, ncb;
-  bool valid[2];
   int bit[2];
   const uint8_t* xq[2];  // activation pieces of group 0, this lane
   const uint8_t* xs[2];  // their scales
+  SigmaConsts k;
 };
 
+// Number of memory instructions one group's DMA issues (planes, scales, zeros).
 template <int MB>
-__device__ inline void load_group(GroupData<MB>& t, const WaveCtx& c, int g) {
-  const uint32_t* pp = c.pl + (size_t)g * c.pl_step + c.lane;
-#pragma unroll
-  for (int p = 0; p < MB; ++p) t.w[p] = __builtin_nontemporal_load(pp + p * 64);
-  const uint16_t* sp = c.sc + (size_t)g * c.sc_step + 4 * c.q;
-#pragma unroll
-  for (int lv = 0; lv < MB - 1; ++lv) t.s[lv] = *(const uint2*)(sp + lv * 16);
-  t.z = c.zp[(size_t)g * 16 + c.j];
+constexpr int dma_ops() { return (MB > 4 ? 2 : 1) + 2; }
+
+template <int MB>
+__device__ inline void dma_group(const WaveCtx& c, int g, uint8_t* st) {
+  const uint8_t* gp = c.pl + (size_t)g * c.pl_step;
+  if (c.lane < (MB > 4 ? 4 : MB) * 16)
+    __builtin_amdgcn_global_load_lds(D2MOE_GPTR(gp + 16 * c.lane), D2MOE_LPTR(st), 16, 0, 0);
+  if (MB > 4 && c.lane < (MB - 4) * 16)
+    __builtin_amdgcn_global_load_lds(D2MOE_GPTR(gp + 1024 + 16 * c.lane),
+                                     D2MOE_LPTR(st + 1024), 16, 0, 0);
+  if (c.lane < 2 * (MB - 1))
+    __builtin_amdgcn_global_load_lds(D2MOE_GPTR(c.sc + (size_t)g * c.sc_step + 16 * c.lane),
+                                     D2MOE_LPTR(st + kScaleOff), 16, 0, 0);
+  if (c.lane == 0)
+    __builtin_amdgcn_global_load_lds(D2MOE_GPTR(c.zp + (size_t)g * 16), D2MOE_LPTR(st + kZeroOff),
+                                     16, 0, 0);
+}
+
+struct BData {
+  v8i b[2];   // activation pieces per column block
+  int bs[2];  // their E8M0 block scales
+};
+
+// Three memory instructions per column block; lanes without a token read the
+// all-zero activation slot, so the count never depends on the lane.
+__device__ inline void load_b(BData& t, const WaveCtx& c, int g) {
 #pragma unroll
   for (int cb = 0; cb < 2; ++cb) {
-    if (cb >= c.ncb) continue;  // wave-uniform; lanes without a token read the zero slot
+    if (cb >= c.ncb) continue;  // wave-uniform
     const uint4* src = (const uint4*)(c.xq[cb] + (size_t)g * 256);
     const uint4 u0 = src[0], u1 = src[1];
     t.b[cb] = v8i{(int)u0.x, (int)u0.y, (int)u0.z, (int)u0.w,
@@ -207,58 +241,164 @@ __device__ inline void load_group(GroupData<MB>& t, const WaveCtx& c, int g) {
   }
 }
 
+// LDS reads of a ring stage are issued as inline assembly: the compiler's
+// wait insertion would otherwise treat every LDS read as possibly reading a
+// DMA still in flight and drain all of them.  The explicit vmcnt wait before
+// the stage is consumed (wait_vm) orders the DMA, and one lgkmcnt wait after
+// the reads orders the reads; each value is then re-bound by an empty asm so
+// no use can move above that wait.
+__device__ inline uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+template <int OFF>
+__device__ inline uint32_t lds_rd32(uint32_t a) {
+  uint32_t v;
+  asm volatile("ds_read_b32 %0, %1 offset:%2" : "=v"(v) : "v"(a), "n"(OFF));
+  return v;
+}
+template <int OFF>
+__device__ inline uint2 lds_rd64(uint32_t a) {
+  uint2 v;
+  asm volatile("ds_read_b64 %0, %1 offset:%2" : "=v"(v) : "v"(a), "n"(OFF));
+  return v;
+}
+__device__ inline uint32_t lds_rdu8(uint32_t a) {
+  uint32_t v;
+  asm volatile("ds_read_u8 %0, %1" : "=v"(v) : "v"(a));
+  return v;
+}
+template <int P, int MB>
+struct StageReader {
+  static __device__ inline void run(uint32_t pa, uint32_t sa, uint32_t (&w)[MB],
+                                    uint2 (&sc)[MB - 1]) {
+    w[P] = lds_rd32<P * 256>(pa);
+    if constexpr (P + 1 < MB) sc[P] = lds_rd64<P * 32>(sa);
+    StageReader<P + 1, MB>::run(pa, sa, w, sc);
+  }
+};
 template <int MB>
-__device__ inline void compute_group(const GroupData<MB>& t, const WaveCtx& c,
+struct StageReader<MB, MB> {
+  static __device__ inline void run(uint32_t, uint32_t, uint32_t (&)[MB], uint2 (&)[MB - 1]) {}
+};
+
+template <int MB>
+__device__ inline void read_stage(const uint8_t* st, const WaveCtx& c, uint32_t (&w)[MB],
+                                  uint2 (&sc)[MB - 1], uint32_t& z) {
+  const uint32_t base = lds_addr(st);
+  StageReader<0, MB>::run(base + 4 * c.lane, base + kScaleOff + 8 * c.q, w, sc);
+  z = lds_rdu8(base + kZeroOff + c.j);
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int p = 0; p < MB; ++p) asm volatile("" : "+v"(w[p]));
+#pragma unroll
+  for (int p = 0; p < MB - 1; ++p) asm volatile("" : "+v"(sc[p]));
+  asm volatile("" : "+v"(z));
+}
+
+// Planes a token does not request are switched off through its activation
+// block scale: E8M0 code 0 scales that column's products by 2^-127, which
+// leaves at most ~1e-33 (|x| < 2^9 per fp8 piece, 128 terms) in place of an
+// exact zero.
+template <int MB>
+__device__ inline void compute_group(const uint8_t* st, const BData& t, const WaveCtx& c,
                                      v4f (&acc)[2]) {
-  const v8i a0 = expand_sigma(t.w[0]), a1 = expand_sigma(t.w[1]);
-  const v8i au = zero_operand(t.z);
+  const SigmaConsts& k = c.k;
+  uint32_t w[MB];
+  uint2 sw[MB - 1];
+  uint32_t z;
+  read_stage<MB>(st, c, w, sw, z);
+  const v8i a0 = expand_sigma(w[0], k), a1 = expand_sigma(w[1], k);
+  const v8i au = zero_operand(z);
   float s1[4];
-  scales4(t.s[0], true, s1);
+  scales4(sw[0], s1);
 #pragma unroll
   for (int cb = 0; cb < 2; ++cb) {
     if (cb >= c.ncb) continue;  // wave-uniform
-    // three products with a zero accumulator, summed on the VALU: chaining
-    // them through the accumulator operand let the register allocator give
-    // the result a range that partially overlaps the accumulator input
-    const v4f z4 = v4f{0.f, 0.f, 0.f, 0.f};
-    const v4f d0 = mfma_fp4_fp8(a0, t.b[cb], z4, 127, t.bs[cb]);
-    const v4f d1 = mfma_fp4_fp8(a1, t.b[cb], z4, 128, t.bs[cb]);
-    const v4f du = mfma_fp4_fp8(au, t.b[cb], z4, 127, t.bs[cb]);
+    // base: sum_k x_k (1.5 - Q_k) + sum_k x_k (z - 1.5), accumulated in place
+    v4f m = mfma_fp4_fp8(au, t.b[cb], v4f{0.f, 0.f, 0.f, 0.f}, 127, t.bs[cb]);
+    m = mfma_fp4_fp8(a0, t.b[cb], m, 127, t.bs[cb]);
+    m = mfma_fp4_fp8(a1, t.b[cb], m, 128, t.bs[cb]);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-s1[r], (d0[r] + d1[r]) + du[r], acc[cb][r]);
+    for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-s1[r], m[r], acc[cb][r]);
   }
 #pragma unroll
   for (int p = 2; p < MB; ++p) {
-    const v8i ap = expand_sigma(t.w[p]);
+    const v8i ap = expand_sigma(w[p], k);
+    float sp[4];
+    scales4(sw[p - 1], sp);
 #pragma unroll
     for (int cb = 0; cb < 2; ++cb) {
       if (cb >= c.ncb) continue;  // wave-uniform
-      const v4f d = mfma_fp4_fp8(ap, t.b[cb], v4f{0.f, 0.f, 0.f, 0.f}, 128, t.bs[cb]);
-      float sp[4];
-      scales4(t.s[p - 1], p < c.bit[cb], sp);
+      const int bs = p < c.bit[cb] ? t.bs[cb] : 0;
+      const v4f d = mfma_fp4_fp8(ap, t.b[cb], v4f{0.f, 0.f, 0.f, 0.f}, 128, bs);
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-sp[r], d[r], acc[cb][r]);
     }
   }
 }
 
-// One wave's share: groups [g0, g1) at MB planes.  Everything a group needs
-// (planes, scales, zero points, activation pieces) is requested one group
-// ahead of its arithmetic, into two register sets used in turn (no copies,
-// so the wait before a group's arithmetic covers only the older loads).
-template <int MB>
-__device__ inline void decode_groups(const WaveCtx& c, int g0, int g1, v4f (&acc)[2]) {
+// Wait until at most N memory instructions of this wave are outstanding, and
+// keep every later LDS read below the wait.
+template <int N>
+__device__ inline void wait_vm() {
+  if constexpr (N == 0)
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// One wave's share: groups [g0, g1) at MB planes.  Order of issue: at the
+// step that computes group g, the activations of g+1 and then the DMA of
+// g+2 go out; the DMA of g was issued two steps and the activations of g one
+// step earlier, so waiting until the instructions issued after the
+// activations of g are the only ones outstanding covers both.  The three
+// ring stages are distinct LDS arrays and the loop is unrolled by six (ring
+// depth times the two activation register sets) so that every LDS access
+// names its stage statically; the compiler then never has to assume an LDS
+// read overlaps a DMA still in flight.
+template <int MB, int NCB>
+__device__ inline void decode_groups(const WaveCtx& c, uint8_t* st0, uint8_t* st1, uint8_t* st2,
+                                     int g0, int g1, v4f (&acc)[2]) {
   if (g0 >= g1) return;
-  GroupData<MB> ga, gb;
-  load_group<MB>(ga, c, g0);
-  int g = g0;
-  for (; g + 1 < g1; g += 2) {
-    load_group<MB>(gb, c, g + 1);
-    compute_group<MB>(ga, c, acc);
-    if (g + 2 < g1) load_group<MB>(ga, c, g + 2);
-    compute_group<MB>(gb, c, acc);
+  constexpr int ND = dma_ops<MB>(), NB = 3 * NCB;
+  uint8_t* const ST[3] = {st0, st1, st2};
+  BData B[2];
+  dma_group<MB>(c, g0, ST[0]);
+  load_b(B[0], c, g0);
+  if (g0 + 1 < g1) dma_group<MB>(c, g0 + 1, ST[1]);
+#define D2MOE_STEP(K)                                                        \
+  {                                                                          \
+    const int gg = g + (K);                                                  \
+    if (gg >= g1) break;                                                     \
+    if (gg + 1 < g1) load_b(B[((K) + 1) & 1], c, gg + 1);                    \
+    if (gg + 2 < g1) {                                                       \
+      dma_group<MB>(c, gg + 2, ST[((K) + 2) % 3]);                           \
+      wait_vm<2 * ND + NB>();                                                \
+    } else if (gg + 1 < g1) {                                                \
+      wait_vm<ND + NB>();                                                    \
+    } else {                                                                 \
+      wait_vm<0>();                                                          \
+    }                                                                        \
+    compute_group<MB>(ST[(K) % 3], B[(K) & 1], c, acc);                      \
   }
-  if (g < g1) compute_group<MB>(ga, c, acc);
+  for (int g = g0; g < g1; g += 6) {
+    D2MOE_STEP(0)
+    D2MOE_STEP(1)
+    D2MOE_STEP(2)
+    D2MOE_STEP(3)
+    D2MOE_STEP(4)
+    D2MOE_STEP(5)
+  }
+#undef D2MOE_STEP
+}
+
+template <int MB>
+__device__ inline void decode_groups_ncb(const WaveCtx& c, uint8_t* st0, uint8_t* st1,
+                                         uint8_t* st2, int g0, int g1, v4f (&acc)[2]) {
+  if (c.ncb == 2)
+    decode_groups<MB, 2>(c, st0, st1, st2, g0, g1, acc);
+  else
+    decode_groups<MB, 1>(c, st0, st1, st2, g0, g1, acc);
 }
 
 // elist[4*i]: expert, first position, end position, largest bit-width.
@@ -271,6 +411,9 @@ __global__ __launch_bounds__(64 * NW) void decode_kernel(
     const int32_t* __restrict__ perm, const uint8_t* __restrict__ topk_bits,
     const uint8_t* __restrict__ Xq, const uint8_t* __restrict__ Xs, int npos, int f,
     float* __restrict__ out, int out_ld) {
+  __shared__ __attribute__((aligned(16))) uint8_t ring0[NW][kStage];
+  __shared__ __attribute__((aligned(16))) uint8_t ring1[NW][kStage];
+  __shared__ __attribute__((aligned(16))) uint8_t ring2[NW][kStage];
   __shared__ float red[NW][64][8];
   const int ei = blockIdx.y;
   if (ei >= *ecount) return;
@@ -295,24 +438,26 @@ __global__ __launch_bounds__(64 * NW) void decode_kernel(
   c.ncb = ncol > 8 ? 2 : 1;
   const int piece = lane & 1;
   int posj[2];
+  bool validj[2];
 #pragma unroll
   for (int cb = 0; cb < 2; ++cb) {
     const int t = cb * 8 + (c.j >> 1);
-    c.valid[cb] = t < ncol;
+    validj[cb] = t < ncol;
     posj[cb] = p0 + t;
-    c.bit[cb] = c.valid[cb] ? (int)topk_bits[perm[posj[cb]]] : 0;
-    const int src = c.valid[cb] ? posj[cb] : npos;  // zero slot when no token
+    c.bit[cb] = validj[cb] ? (int)topk_bits[perm[posj[cb]]] : 0;
+    const int src = validj[cb] ? posj[cb] : npos;  // zero slot when no token
     const size_t base = ((size_t)src * NG) * 2 + piece;  // group 0
     c.xq[cb] = Xq + base * 128 + c.q * 32;
     c.xs[cb] = Xs + base * 4 + c.q;
   }
   const int rowblock = rr == 0 ? rb : rb + f / 16;
   const size_t blk0 = W.block(e, rowblock, 0);
-  c.pl = W.planes + W.plane_word(blk0, 0, 0);
-  c.sc = W.scales + W.scale_idx(blk0, 0, 0);
+  c.pl = (const uint8_t*)(W.planes + W.plane_word(blk0, 0, 0));
+  c.sc = (const uint8_t*)(W.scales + W.scale_idx(blk0, 0, 0));
   c.zp = W.zeros + W.zero_idx(blk0, 0);
-  c.pl_step = W.b_max * 64;
-  c.sc_step = W.levels() * 16;
+  c.pl_step = W.b_max * 64 * 4;
+  c.sc_step = W.levels() * 16 * 2;
+  c.k = sigma_consts();
 
   // An AGPR clobber keeps the accumulation registers allocated, which makes the
   // compiler emit the AGPR-destination form of the MFMAs: their results can
@@ -321,13 +466,13 @@ __global__ __launch_bounds__(64 * NW) void decode_kernel(
   v4f acc[2];
   acc[0] = acc[1] = v4f{0.f, 0.f, 0.f, 0.f};
   switch (mb) {
-    case 2: decode_groups<2>(c, g0, g1, acc); break;
-    case 3: decode_groups<3>(c, g0, g1, acc); break;
-    case 4: decode_groups<4>(c, g0, g1, acc); break;
-    case 5: decode_groups<5>(c, g0, g1, acc); break;
-    case 6: decode_groups<6>(c, g0, g1, acc); break;
-    case 7: decode_groups<7>(c, g0, g1, acc); break;
-    case 8: decode_groups<8>(c, g0, g1, acc); break;
+    case 2: decode_groups_ncb<2>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
+    case 3: decode_groups_ncb<3>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
+    case 4: decode_groups_ncb<4>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
+    case 5: decode_groups_ncb<5>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
+    case 6: decode_groups_ncb<6>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
+    case 7: decode_groups_ncb<7>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
+    case 8: decode_groups_ncb<8>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
     default: break;
   }
 
@@ -351,7 +496,7 @@ __global__ __launch_bounds__(64 * NW) void decode_kernel(
       }
 #pragma unroll
   for (int cb = 0; cb < 2; ++cb) {
-    if (cb >= c.ncb || !c.valid[cb] || piece != 0) continue;
+    if (cb >= c.ncb || !validj[cb] || piece != 0) continue;
     float* dst = out + (size_t)posj[cb] * out_ld + rb * 16 + 4 * c.q;
     float o[4];
 #pragma unroll
