@@ -5,11 +5,16 @@ Every HIP source is compiled to an object file (in parallel) and linked into
 disabled for all device code; the MWQ pack kernel is also compiled without
 floating-point contraction because its integer codes must match the CPU
 definition bit for bit.
+
+The build fails if a decode kernel needs per-lane scratch memory: those
+kernels place their own vmcnt waits around the LDS DMA ring, which assume
+that no other vector-memory traffic (such as register spills) is interleaved.
 """
 from __future__ import annotations
 
 import concurrent.futures as cf
 import os
+import re
 import shutil
 import subprocess
 
@@ -24,6 +29,7 @@ COMMON = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}", "-I", INCLUDE,
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wno-unused-command-line-argument"]
 EXTRA = {"pack.hip": ["-ffp-contract=off"]}
+NO_SCRATCH = ("decode_kernel",)  # kernels that must not spill
 
 
 def _hipcc() -> str:
@@ -40,11 +46,31 @@ def sources() -> list[str]:
 def _compile(src: str) -> str:
     os.makedirs(OBJ_DIR, exist_ok=True)
     obj = os.path.join(OBJ_DIR, src.replace(".hip", ".o"))
-    cmd = [_hipcc(), *COMMON, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [_hipcc(), *COMMON, *EXTRA.get(src, []), "-Rpass-analysis=kernel-resource-usage",
+           "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
+    spills = {k: v for k, v in scratch_users(r.stderr).items()
+              if any(n in k for n in NO_SCRATCH)}
+    if spills:
+        raise RuntimeError(f"{src}: kernels use scratch memory (register spills): {spills}")
     return obj
+
+
+def scratch_users(remarks: str) -> dict[str, int]:
+    """Kernels with a non-zero per-lane scratch size in the compiler's
+    resource-usage remarks."""
+    out, name = {}, None
+    for line in remarks.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            continue
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and name is not None and int(m.group(1)) > 0:
+            out[name] = int(m.group(1))
+    return out
 
 
 def build(jobs: int | None = None) -> str:

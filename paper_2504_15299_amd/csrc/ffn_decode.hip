@@ -538,6 +538,10 @@ bool decode_path_ok(const d2moe_mwq* w13, const d2moe_mwq* w2, int T) {
          w2->b_min == 2;
 }
 
+// Waves per workgroup: one per SIMD, so that the per-SIMD register budget,
+// not the workgroup size, sets how many workgroups share a compute unit.
+constexpr int kDecodeWaves = 4;
+
 hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_ff, int E, int k,
                              const d2moe_mwq* w13, const d2moe_mwq* w2, const d2moe_routing* r,
                              const DecodeBuffers& b, hipStream_t s, const hipEvent_t* events) {
@@ -554,14 +558,14 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   const int ny = E < npos ? E : npos;
   const MwqView W13 = view_of(w13), W2 = view_of(w2);
   if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
-  decode_kernel<true, 8><<<dim3(d_ff / 16, ny), 512, 0, s>>>(
+  decode_kernel<true, kDecodeWaves><<<dim3(d_ff / 16, ny), 64 * kDecodeWaves, 0, s>>>(
       W13, b.elist, b.ecount, r->perm, r->topk_bits, b.xq13, b.xs13, npos, d_ff, b.h32, d_ff);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
   err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.xq2, b.xs2, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
-  decode_kernel<false, 8><<<dim3(d / 16, ny), 512, 0, s>>>(
+  decode_kernel<false, kDecodeWaves><<<dim3(d / 16, ny), 64 * kDecodeWaves, 0, s>>>(
       W2, b.elist, b.ecount, r->perm, r->topk_bits, b.xq2, b.xs2, npos, 0, b.y, d);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
