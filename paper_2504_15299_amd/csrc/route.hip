@@ -11,34 +11,87 @@ namespace d2moe {
 namespace {
 
 constexpr int kGateThreads = 256;
+constexpr int kGateE = 8;  // experts per pass over the token's row
 
-template <typename XT>
-__device__ inline float load_x(const XT* p);
-template <>
-__device__ inline float load_x<float>(const float* p) { return *p; }
-template <>
-__device__ inline float load_x<uint16_t>(const uint16_t* p) { return bf2f(*p); }
+__device__ inline void load8(const float* p, float (&v)[8]) {
+  const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ inline void load8(const uint16_t* p, float (&v)[8]) {
+  const uint4 u = *(const uint4*)p;
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = bf2f((uint16_t)(w[i] & 0xffff));
+    v[2 * i + 1] = bf2f((uint16_t)(w[i] >> 16));
+  }
+}
+__device__ inline float load1(const float* p) { return *p; }
+__device__ inline float load1(const uint16_t* p) { return bf2f(*p); }
 
-// logits[t][e] = x[t] . Wg[e] (+ bias[e]); one workgroup per token, one wave
-// per expert at a time, lanes stride the model dimension, fp32 accumulation.
+// logits[t][e] = x[t] . Wg[e] (+ bias[e]); one workgroup per token.  Each
+// thread takes 8 consecutive columns per step (one 16-byte load of x, two of
+// each gate row) for up to kGateE experts per pass, with one fp32 fma chain
+// per expert; the partial sums are reduced across the wave with shuffles and
+// across the waves through LDS.  A term passes through at most
+// ceil(d/256) + 11 roundings.
 template <typename XT>
 __global__ __launch_bounds__(kGateThreads) void gate_kernel(const XT* __restrict__ x, int d,
                                                             const float* __restrict__ Wg,
                                                             const float* __restrict__ bias, int E,
                                                             float* __restrict__ logits,
                                                             int32_t* __restrict__ flags) {
+  constexpr int NWAVE = kGateThreads / 64;
+  __shared__ float part[NWAVE][kGateE];
   const int t = blockIdx.x;
   // the flag word is cleared here (a fill by a kernel rather than a memset
   // node, so that a captured graph replays correctly)
   if (t == 0 && threadIdx.x == 0) *flags = 0;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const XT* xt = x + (size_t)t * d;
-  for (int e = wave; e < E; e += kGateThreads / 64) {
-    const float* we = Wg + (size_t)e * d;
-    float acc = 0.0f;
-    for (int c = lane; c < d; c += 64) acc += load_x<XT>(xt + c) * we[c];
-    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-    if (lane == 0) logits[(size_t)t * E + e] = acc + (bias ? bias[e] : 0.0f);
+  const bool vec = (d & 7) == 0 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)Wg & 15) == 0;
+  for (int e0 = 0; e0 < E; e0 += kGateE) {
+    const int ne = E - e0 < kGateE ? E - e0 : kGateE;
+    const float* w0 = Wg + (size_t)e0 * d;
+    float acc[kGateE];
+#pragma unroll
+    for (int j = 0; j < kGateE; ++j) acc[j] = 0.0f;
+    if (vec) {
+      for (int c = 8 * tid; c < d; c += 8 * kGateThreads) {
+        float xv[8];
+        load8(xt + c, xv);
+#pragma unroll
+        for (int j = 0; j < kGateE; ++j) {
+          if (j >= ne) continue;  // uniform
+          float wv[8];
+          load8(w0 + (size_t)j * d + c, wv);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc[j] = fmaf(xv[i], wv[i], acc[j]);
+        }
+      }
+    } else {
+      for (int c = tid; c < d; c += kGateThreads) {
+        const float xv = load1(xt + c);
+#pragma unroll
+        for (int j = 0; j < kGateE; ++j)
+          if (j < ne) acc[j] = fmaf(xv, w0[(size_t)j * d + c], acc[j]);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kGateE; ++j)
+      for (int off = 32; off > 0; off >>= 1) acc[j] += __shfl_xor(acc[j], off, 64);
+    if (lane == 0) {
+#pragma unroll
+      for (int j = 0; j < kGateE; ++j) part[wave][j] = acc[j];
+    }
+    __syncthreads();
+    if (tid < ne) {
+      float sum = 0.0f;
+      for (int w = 0; w < NWAVE; ++w) sum += part[w][tid];
+      logits[(size_t)t * E + e0 + tid] = sum + (bias ? bias[e0 + tid] : 0.0f);
+    }
+    __syncthreads();
   }
 }
 
@@ -53,7 +106,14 @@ __global__ void topk_kernel(const float* __restrict__ logits, int T, int E, int 
   if (t >= T) return;
   const float* l = logits + (size_t)t * E;
   uint64_t taken = 0;
-  int sel[64];
+  int r = token_req ? token_req[t] : 0;
+  int flag = 0;
+  if (r < 0 || r >= R) {
+    flag |= 2;
+    r = r < 0 ? 0 : R - 1;
+  }
+  // selection in descending order: the first pick holds the largest logit
+  float lmax = 0.0f, den = 0.0f;
   for (int i = 0; i < k; ++i) {
     int best = -1;
     for (int e = 0; e < E; ++e) {
@@ -61,27 +121,17 @@ __global__ void topk_kernel(const float* __restrict__ logits, int T, int E, int 
       if (best < 0 || l[e] > l[best]) best = e;
     }
     taken |= 1ull << best;
-    sel[i] = best;
-  }
-  const float lmax = l[sel[0]];
-  float den = 0.0f;
-  for (int i = 0; i < k; ++i) den += expf(l[sel[i]] - lmax);
-  int r = token_req ? token_req[t] : 0;
-  int flag = 0;
-  if (r < 0 || r >= R) {
-    flag |= 2;
-    r = r < 0 ? 0 : R - 1;
-  }
-  for (int i = 0; i < k; ++i) {
-    topk_idx[t * k + i] = sel[i];
-    topk_w[t * k + i] = expf(l[sel[i]] - lmax) / den;
-    int b = bit_table[(size_t)r * E + sel[i]];
+    if (i == 0) lmax = l[best];
+    den += expf(l[best] - lmax);
+    topk_idx[t * k + i] = best;
+    int b = bit_table[(size_t)r * E + best];
     if (b < b_min || b > b_max) {
       flag |= 1;
       b = b < b_min ? b_min : b_max;
     }
     topk_bits[t * k + i] = (uint8_t)b;
   }
+  for (int i = 0; i < k; ++i) topk_w[t * k + i] = expf(l[topk_idx[t * k + i]] - lmax) / den;
   if (flag) atomicOr(flags, flag);
 }
 

@@ -22,13 +22,15 @@ def row_max_abs_rel(got: np.ndarray, ref: np.ndarray) -> np.ndarray:
 
 def logit_error_bound(x: np.ndarray, Wg: np.ndarray, bias) -> np.ndarray:
     """Bound on |fp32 GPU logit - exact| for the gate kernel's summation
-    (64 strided partial sums of d/64 terms, then a 6-level tree), per token:
-    (d/64 + 8) * 2^-24 * max_e sum_c |x_c Wg_ec| (+ |bias|)."""
+    (256 per-thread fma chains of ceil(d/256) terms, a 6-level shuffle tree,
+    a sequential sum over 4 waves and the bias: at most ceil(d/256) + 11
+    roundings per term), per token, with one rounding of slack:
+    (ceil(d/256) + 12) * 2^-24 * max_e sum_c |x_c Wg_ec| (+ |bias|)."""
     d = x.shape[1]
     mag = np.abs(x.astype(np.float64)) @ np.abs(Wg.astype(np.float64)).T
     if bias is not None:
         mag = mag + np.abs(bias)[None, :]
-    return (d / 64 + 8) * 2.0 ** -24 * mag.max(axis=1)
+    return (-(-d // 256) + 12) * 2.0 ** -24 * mag.max(axis=1)
 
 
 def ambiguous_tokens(logits: np.ndarray, k: int, bound: np.ndarray) -> np.ndarray:
