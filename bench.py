@@ -46,7 +46,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--batch", type=int, default=16)
     ap.add_argument("--layers", type=int, default=8)
-    ap.add_argument("--sweep", default="1,4", help="extra batch sizes reported alongside")
+    ap.add_argument("--sweep", default="", help="extra batch sizes reported alongside, e.g. 1,4")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 256 MiB device copy three times (reference for "
@@ -157,6 +157,7 @@ def main():
     if not args.no_cpu:
         cpu = cpu_baseline(d, f, E, k, g)
 
+    traffic = profiled_traffic()
     line = {
         "metric": METRIC,
         "value": round(main_res["tokens_per_s"], 2),
@@ -181,15 +182,43 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "W1/W3 expert kernel",
                      "achieved": round(main_res["w13_GBps"], 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(main_res["w13_GBps"] / HBM_PEAK_GBPS, 4),
-                     "traffic": None,
+                     "traffic": traffic[0],
+                     "traffic_unit": "bytes/launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                      "alg_bytes_per_launch": main_res["w13_bytes"],
                      "avg_ms": round(main_res["w13_ms"], 5)},
-        "w2_kernel": {"achieved": round(main_res["w2_GBps"], 1), "avg_ms": round(main_res["w2_ms"], 5)},
+        "w2_kernel": {"achieved": round(main_res["w2_GBps"], 1), "avg_ms": round(main_res["w2_ms"], 5),
+                      "traffic": traffic[1]},
         "sweep": sweep,
         "cpu_baseline": cpu,
         "pack_seconds": round(pack_s, 2),
     }
     print(json.dumps(line), flush=True)
+
+
+PROFILE = os.path.join(ROOT, "profiles", "decode_step_mixtral_T16_hbm_bytes.txt")
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for name in ("ffn_decode.hip", "internal.h"):
+        with open(os.path.join(ROOT, "paper_2504_15299_amd", "csrc", name), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def profiled_traffic():
+    """HBM bytes per launch of the W1/W3 and W2 decode kernels from the
+    committed rocprofv3 counter summary, or None when the kernel source has
+    changed since the counters were taken (or no summary exists)."""
+    try:
+        with open(PROFILE) as fh:
+            kv = dict(line.split(": ", 1) for line in fh.read().splitlines() if ": " in line)
+    except OSError:
+        return None, None
+    if kv.get("kernel_source_sha256_16", "").strip() != kernel_source_hash():
+        return None, None
+    return int(kv["traffic_w13_bytes"]), int(kv["traffic_w2_bytes"])
 
 
 def cpu_baseline(d, f, E, k, g):

@@ -47,18 +47,24 @@ def counter(db, cname, subs):
         key = r[ix["dispatch_id"]]
         per_disp[key] += float(r[ix["value"]])
         names[key] = r[ix[name_col]]
+    # the three 256 MiB device-to-device copies of `bench.py --copy-calibration`
+    # run as the runtime's copy kernel; each reads and writes 262144 KiB
+    cal = sorted(v for d, v in per_disp.items()
+                 if "copyBuffer" in names[d] and v > 0.25 * 262144)
+    factor = cal[len(cal) // 2] / 262144.0 if cal else None
+    if cal:
+        print(f"calibration: {len(cal)} copies of 262144 KiB read and written, median "
+              f"{cname} {cal[len(cal) // 2]:.1f} KiB -> factor {factor:.4f} (counter / bytes)")
     agg = defaultdict(list)
     for key, v in per_disp.items():
         agg[_short(names[key])].append(v)
-    print(f"{'kernel':92s} {'dispatches':>10s} {cname + '_KiB_avg':>16s}")
+    print(f"{'kernel':92s} {'dispatches':>10s} {'KiB_avg':>12s} {'MB_avg_calibrated':>18s}")
     for name, vals in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
-        if subs and not any(s in name for s in subs + ["elementwise", "copy"]):
+        if subs and not any(s in name for s in subs):
             continue
-        print(f"{name:92s} {len(vals):10d} {sum(vals) / len(vals):16.1f}")
-    cal = [v for n, vs in agg.items() for v in vs if ("copy" in n.lower() or "elementwise" in n.lower())]
-    if cal:
-        print(f"calibration: first copy-like kernel {cal[0]:.1f} KiB for a 262144 KiB copy "
-              f"-> factor {cal[0] / 262144.0:.4f}")
+        avg = sum(vals) / len(vals)
+        calib = f"{avg / factor * 1024 / 1e6:18.2f}" if factor else f"{'-':>18s}"
+        print(f"{name:92s} {len(vals):10d} {avg:12.1f} {calib}")
 
 
 if __name__ == "__main__":
