@@ -352,15 +352,15 @@ static double dequant_elem(int rows, int cols, int group, int b_min, int b,
 
 static double silu(double a) { return a / (1.0 + exp(-a)); }
 
-int oracle_expert_ffn(int d, int f, int group13, int group2, int b_min,
+int oracle_expert_ffn(int d, int f, int d_out, int group13, int group2, int b_min,
                       int b_max, int b,
                       const uint8_t* q1_13, const uint8_t* zeros_13,
                       const uint16_t* scales_13, const uint8_t* signs_13,
                       const uint8_t* q1_2, const uint8_t* zeros_2,
                       const uint16_t* scales_2, const uint8_t* signs_2,
                       const double* x, int n, double* y) {
-  if (d <= 0 || f <= 0 || n < 0 || !check_ladder(b_min, b_max) || b < b_min ||
-      b > b_max || d % group13 != 0 || f % group2 != 0)
+  if (d <= 0 || f <= 0 || d_out <= 0 || n < 0 || !check_ladder(b_min, b_max) ||
+      b < b_min || b > b_max || d % group13 != 0 || f % group2 != 0)
     return -1;
   double* h = (double*)malloc(sizeof(double) * (size_t)f * (n > 0 ? n : 1));
   double* wa = (double*)malloc(sizeof(double) * (size_t)d);
@@ -387,15 +387,15 @@ int oracle_expert_ffn(int d, int f, int group13, int group2, int b_min,
     }
   }
   /* y = W2_b h */
-  for (int r = 0; r < d; ++r) {
+  for (int r = 0; r < d_out; ++r) {
     for (int c = 0; c < f; ++c)
-      w2[c] = dequant_elem(d, f, group2, b_min, b, q1_2, zeros_2, scales_2,
+      w2[c] = dequant_elem(d_out, f, group2, b_min, b, q1_2, zeros_2, scales_2,
                            signs_2, r, c);
     for (int j = 0; j < n; ++j) {
       const double* hj = h + (size_t)j * f;
       double acc = 0.0;
       for (int c = 0; c < f; ++c) acc += w2[c] * hj[c];
-      y[(size_t)j * d + r] = acc;
+      y[(size_t)j * d_out + r] = acc;
     }
   }
   free(h); free(wa); free(wc); free(w2);

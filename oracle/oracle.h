@@ -91,8 +91,10 @@ int oracle_route_from_logits(const double* logits, int T, int E, int k,
 /* One SwiGLU expert at bit-width b from logical codes, for n input vectors:
  *   a = W1_b x, c = W3_b x, h = silu(a) * c, y = W2_b h     (binary64)
  * w13 codes describe a [2f][d] matrix (W1 rows then W3 rows); w2 codes a
- * [d][f] matrix.  x is [n][d] binary64, y is [n][d]. */
-int oracle_expert_ffn(int d, int f, int group13, int group2, int b_min,
+ * [d_out][f] matrix: all d rows of W2, or any subset of its rows, since MWQ
+ * codes of a row depend on that row alone.  x is [n][d] binary64, y is
+ * [n][d_out]. */
+int oracle_expert_ffn(int d, int f, int d_out, int group13, int group2, int b_min,
                       int b_max, int b,
                       const uint8_t* q1_13, const uint8_t* zeros_13,
                       const uint16_t* scales_13, const uint8_t* signs_13,

@@ -61,7 +61,7 @@ def _L():
         lib.oracle_mwq_pack.argtypes = [I, I, I, I, I, P, P, P, P, P, P, P]
         lib.oracle_gate_logits.argtypes = [P, I, I, P, P, I, P]
         lib.oracle_route_from_logits.argtypes = [P, I, I, I, P, P, I, I, I, P, P, P, P, P, P, P, P]
-        lib.oracle_expert_ffn.argtypes = [I, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P, I, P]
+        lib.oracle_expert_ffn.argtypes = [I, I, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P, I, P]
         lib.oracle_combine.argtypes = [I, I, I, P, P, P]
         for name in ("oracle_mwq_quantize", "oracle_mwq_dequant", "oracle_mwq_pack",
                      "oracle_gate_logits", "oracle_route_from_logits", "oracle_expert_ffn",
@@ -198,14 +198,18 @@ def route_from_logits(logits: np.ndarray, k: int, token_req: np.ndarray | None,
 # ---- expert FFN, combine, whole layer --------------------------------------
 
 def expert_ffn(c13: MWQCodes, c2: MWQCodes, b: int, x: np.ndarray) -> np.ndarray:
+    """y = W2_b (silu(W1_b x) * W3_b x) for each row of x, binary64.  ``c2``
+    may hold a subset of W2's rows (codes are per row); y has c2.rows
+    columns."""
     x = np.ascontiguousarray(x, dtype=np.float64)
     n, d = x.shape
     f = c2.cols
-    assert c13.rows == 2 * f and c13.cols == d and c2.rows == d
-    y = np.zeros((n, d), np.float64)
+    assert c13.rows == 2 * f and c13.cols == d
+    y = np.zeros((n, c2.rows), np.float64)
     s13 = c13.signs if c13.signs.size else np.zeros((1, c13.rows, c13.cols), np.uint8)
     s2 = c2.signs if c2.signs.size else np.zeros((1, c2.rows, c2.cols), np.uint8)
-    _ok(_L().oracle_expert_ffn(d, f, c13.group, c2.group, c13.b_min, c13.b_max, b, _p(c13.q1),
+    _ok(_L().oracle_expert_ffn(d, f, c2.rows, c13.group, c2.group, c13.b_min, c13.b_max, b,
+                               _p(c13.q1),
                                _p(c13.zeros), _p(c13.scales), _p(np.ascontiguousarray(s13)),
                                _p(c2.q1), _p(c2.zeros), _p(c2.scales),
                                _p(np.ascontiguousarray(s2)), _p(x), n, _p(y)), "expert_ffn")

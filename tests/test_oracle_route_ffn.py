@@ -99,6 +99,27 @@ def test_expert_ffn_is_dense_swiglu(b):
     np.testing.assert_allclose(O.expert_ffn(c13, c2, b, x), ref, rtol=1e-11, atol=1e-14)
 
 
+def test_expert_ffn_on_a_subset_of_w2_rows():
+    """MWQ codes of a row depend on that row alone, so quantizing a subset of
+    W2's rows gives the same codes as quantizing all of W2, and the expert
+    output on those rows equals the matching columns of the full output."""
+    d, f, g, b = 128, 192, 64, 5
+    rng = np.random.default_rng(41)
+    W13 = (rng.standard_normal((2 * f, d)) * 0.02).astype(np.float32)
+    W2 = (rng.standard_normal((d, f)) * 0.02).astype(np.float32)
+    rows = np.array([0, 5, 6, 77, d - 1])
+    c13 = O.mwq_quantize(W13, g)
+    c2 = O.mwq_quantize(W2, g)
+    c2s = O.mwq_quantize(np.ascontiguousarray(W2[rows]), g)
+    assert np.array_equal(c2s.q1, c2.q1[rows]) and np.array_equal(c2s.signs, c2.signs[:, rows])
+    assert np.array_equal(c2s.scales, c2.scales[:, rows]) and np.array_equal(c2s.zeros, c2.zeros[rows])
+    x = rng.standard_normal((3, d))
+    full = O.expert_ffn(c13, c2, b, x)
+    sub = O.expert_ffn(c13, c2s, b, x)
+    assert sub.shape == (3, len(rows))
+    assert np.array_equal(sub, full[:, rows])
+
+
 def test_layer_equivariance_and_linearity():
     """Permuting tokens permutes the layer output exactly; the combine is
     linear in the routing weights; a top-1 layer with one bit-width equals the
