@@ -6,6 +6,11 @@ disabled for all device code; the MWQ pack kernel is also compiled without
 floating-point contraction because its integer codes must match the CPU
 definition bit for bit.
 
+The build also fails if any MFMA in the device assembly writes registers
+that overlap its own source operands: multi-pass MFMAs read their sources
+while they write, and the compiler does not always keep a 4-register result
+apart from them (the decode kernels pin their operands to prevent it).
+
 The build fails if any kernel needs per-lane scratch memory: the decode
 kernels place their own vmcnt waits around the LDS DMA ring, which assume
 that no other vector-memory traffic (such as register spills) is
@@ -54,7 +59,52 @@ def _compile(src: str) -> str:
     spills = scratch_users(r.stderr)
     if spills:
         raise RuntimeError(f"{src}: kernels use scratch memory (register spills): {spills}")
+    _check_mfma(src)
     return obj
+
+
+_REG = re.compile(r"([va])\[(\d+):(\d+)\]|([va])(\d+)$")
+
+
+def _reg_range(tok: str):
+    m = _REG.match(tok)
+    if not m:
+        return None
+    if m.group(1):
+        return m.group(1), int(m.group(2)), int(m.group(3))
+    return m.group(4), int(m.group(5)), int(m.group(5))
+
+
+def mfma_overlaps(asm: str) -> list[str]:
+    """MFMA instructions whose destination overlaps srcA, srcB, a scale
+    operand, or srcC other than exactly (in-place accumulation is allowed)."""
+    bad = []
+    for line in asm.splitlines():
+        line = line.strip()
+        if not line.startswith("v_mfma"):
+            continue
+        ops = [o.strip().split()[0] for o in line.split(None, 1)[1].split(",")]
+        rs = [_reg_range(o) for o in ops]
+        d = rs[0]
+        srcs = rs[1:3] + (rs[4:6] if "scale" in line.split()[0] else [])
+        if rs[3] != d:
+            srcs.append(rs[3])
+        for r in srcs:
+            if d and r and d[0] == r[0] and not (d[2] < r[1] or r[2] < d[1]):
+                bad.append(line)
+                break
+    return bad
+
+
+def _check_mfma(src: str) -> None:
+    cmd = [_hipcc(), *COMMON, *EXTRA.get(src, []), "--cuda-device-only", "-S", "-o", "-",
+           os.path.join(CSRC, src)]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc -S failed for {src}:\n{r.stderr}")
+    bad = mfma_overlaps(r.stdout)
+    if bad:
+        raise RuntimeError(f"{src}: {len(bad)} MFMAs write over their own operands, e.g. {bad[0]}")
 
 
 def scratch_users(remarks: str) -> dict[str, int]:

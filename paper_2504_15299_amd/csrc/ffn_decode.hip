@@ -32,6 +32,7 @@ namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef int v4i __attribute__((ext_vector_type(4)));
 
 constexpr int G = 128;  // group size served by this path (one MFMA K)
 
@@ -165,8 +166,23 @@ __device__ inline v8i zero_operand(uint32_t z) {
 // Cross-lane product: every call sits in wave-uniform control flow (no
 // per-lane condition guards an MFMA or the use of its result in this file;
 // per-token predication is done through the activation block scale).
+//
+// This 8-pass MFMA must not write registers it is still reading, but the
+// compiler treats a 4-register result as free to overlap the operands.  Each
+// call therefore keeps its operands live past the instruction (an empty asm
+// that reads them), so the result is always given registers of its own.
+__device__ inline v4i lo4(const v8i& a) { return v4i{a[0], a[1], a[2], a[3]}; }
+
+__device__ inline v4f mfma_fp4_fp8(const v8i& a, const v8i& b, int sa, int sb) {
+  const v4f d = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
+      a, b, v4f{0.f, 0.f, 0.f, 0.f}, 4, 0, 0, sa, 0, sb);
+  asm volatile("" ::"v"(lo4(a)), "v"(b), "v"(sa), "v"(sb));
+  return d;
+}
 __device__ inline v4f mfma_fp4_fp8(const v8i& a, const v8i& b, v4f c, int sa, int sb) {
-  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 4, 0, 0, sa, 0, sb);
+  const v4f d = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 4, 0, 0, sa, 0, sb);
+  asm volatile("" ::"v"(lo4(a)), "v"(b), "v"(c), "v"(sa), "v"(sb));
+  return d;
 }
 
 __device__ inline float silu(float a) { return a / (1.0f + __expf(-a)); }
@@ -184,7 +200,7 @@ __device__ inline void scales4(uint2 s, float (&out)[4]) {
 // its 16 zero points, copied from global memory by the LDS DMA engine so that
 // data in flight costs no registers.
 constexpr int kStage = 2304;            // bytes per stage
-// ring depth 3 (two groups in flight), one LDS array per stage
+constexpr int kDepth = 4;               // stages: the DMA runs kDepth-1 groups ahead
 constexpr int kScaleOff = 2048, kZeroOff = 2272;
 
 #define D2MOE_GPTR(p) ((__attribute__((address_space(1))) void*)(p))
@@ -200,6 +216,7 @@ struct WaveCtx {
   const uint8_t* xq[2];  // activation pieces of group 0, this lane
   const uint8_t* xs[2];  // their scales
   SigmaConsts k;
+  uint32_t lds_pl, lds_sc, lds_z;  // this lane's LDS read addresses in stage 0
 };
 
 // Number of memory instructions one group's DMA issues (planes, scales, zeros).
@@ -262,31 +279,31 @@ __device__ inline uint2 lds_rd64(uint32_t a) {
   asm volatile("ds_read_b64 %0, %1 offset:%2" : "=v"(v) : "v"(a), "n"(OFF));
   return v;
 }
+template <int OFF>
 __device__ inline uint32_t lds_rdu8(uint32_t a) {
   uint32_t v;
-  asm volatile("ds_read_u8 %0, %1" : "=v"(v) : "v"(a));
+  asm volatile("ds_read_u8 %0, %1 offset:%2" : "=v"(v) : "v"(a), "n"(OFF));
   return v;
 }
-template <int P, int MB>
+template <int P, int MB, int SOFF>
 struct StageReader {
   static __device__ inline void run(uint32_t pa, uint32_t sa, uint32_t (&w)[MB],
                                     uint2 (&sc)[MB - 1]) {
-    w[P] = lds_rd32<P * 256>(pa);
-    if constexpr (P + 1 < MB) sc[P] = lds_rd64<P * 32>(sa);
-    StageReader<P + 1, MB>::run(pa, sa, w, sc);
+    w[P] = lds_rd32<SOFF + P * 256>(pa);
+    if constexpr (P + 1 < MB) sc[P] = lds_rd64<SOFF + P * 32>(sa);
+    StageReader<P + 1, MB, SOFF>::run(pa, sa, w, sc);
   }
 };
-template <int MB>
-struct StageReader<MB, MB> {
+template <int MB, int SOFF>
+struct StageReader<MB, MB, SOFF> {
   static __device__ inline void run(uint32_t, uint32_t, uint32_t (&)[MB], uint2 (&)[MB - 1]) {}
 };
 
-template <int MB>
-__device__ inline void read_stage(const uint8_t* st, const WaveCtx& c, uint32_t (&w)[MB],
-                                  uint2 (&sc)[MB - 1], uint32_t& z) {
-  const uint32_t base = lds_addr(st);
-  StageReader<0, MB>::run(base + 4 * c.lane, base + kScaleOff + 8 * c.q, w, sc);
-  z = lds_rdu8(base + kZeroOff + c.j);
+template <int MB, int SOFF>
+__device__ inline void read_stage(const WaveCtx& c, uint32_t (&w)[MB], uint2 (&sc)[MB - 1],
+                                  uint32_t& z) {
+  StageReader<0, MB, SOFF>::run(c.lds_pl, c.lds_sc, w, sc);
+  z = lds_rdu8<SOFF>(c.lds_z);
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
   for (int p = 0; p < MB; ++p) asm volatile("" : "+v"(w[p]));
@@ -299,14 +316,13 @@ __device__ inline void read_stage(const uint8_t* st, const WaveCtx& c, uint32_t 
 // block scale: E8M0 code 0 scales that column's products by 2^-127, which
 // leaves at most ~1e-33 (|x| < 2^9 per fp8 piece, 128 terms) in place of an
 // exact zero.
-template <int MB>
-__device__ inline void compute_group(const uint8_t* st, const BData& t, const WaveCtx& c,
-                                     v4f (&acc)[2]) {
+template <int MB, int SOFF>
+__device__ inline void compute_group(const BData& t, const WaveCtx& c, v4f (&acc)[2]) {
   const SigmaConsts& k = c.k;
   uint32_t w[MB];
   uint2 sw[MB - 1];
   uint32_t z;
-  read_stage<MB>(st, c, w, sw, z);
+  read_stage<MB, SOFF>(c, w, sw, z);
   const v8i a0 = expand_sigma(w[0], k), a1 = expand_sigma(w[1], k);
   const v8i au = zero_operand(z);
   float s1[4];
@@ -315,7 +331,7 @@ __device__ inline void compute_group(const uint8_t* st, const BData& t, const Wa
   for (int cb = 0; cb < 2; ++cb) {
     if (cb >= c.ncb) continue;  // wave-uniform
     // base: sum_k x_k (1.5 - Q_k) + sum_k x_k (z - 1.5), accumulated in place
-    v4f m = mfma_fp4_fp8(au, t.b[cb], v4f{0.f, 0.f, 0.f, 0.f}, 127, t.bs[cb]);
+    v4f m = mfma_fp4_fp8(au, t.b[cb], 127, t.bs[cb]);
     m = mfma_fp4_fp8(a0, t.b[cb], m, 127, t.bs[cb]);
     m = mfma_fp4_fp8(a1, t.b[cb], m, 128, t.bs[cb]);
 #pragma unroll
@@ -330,7 +346,7 @@ __device__ inline void compute_group(const uint8_t* st, const BData& t, const Wa
     for (int cb = 0; cb < 2; ++cb) {
       if (cb >= c.ncb) continue;  // wave-uniform
       const int bs = p < c.bit[cb] ? t.bs[cb] : 0;
-      const v4f d = mfma_fp4_fp8(ap, t.b[cb], v4f{0.f, 0.f, 0.f, 0.f}, 128, bs);
+      const v4f d = mfma_fp4_fp8(ap, t.b[cb], 128, bs);
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-sp[r], d[r], acc[cb][r]);
     }
@@ -347,58 +363,62 @@ __device__ inline void wait_vm() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// One wave's share: groups [g0, g1) at MB planes.  Order of issue: at the
-// step that computes group g, the activations of g+1 and then the DMA of
-// g+2 go out; the DMA of g was issued two steps and the activations of g one
-// step earlier, so waiting until the instructions issued after the
-// activations of g are the only ones outstanding covers both.  The three
-// ring stages are distinct LDS arrays and the loop is unrolled by six (ring
-// depth times the two activation register sets) so that every LDS access
-// names its stage statically; the compiler then never has to assume an LDS
-// read overlaps a DMA still in flight.
+// One wave's share: groups [g0, g1) at MB planes, through this wave's ring
+// of kDepth stages (kStage bytes apart, starting at `ring`).  Order of issue:
+// the prologue sends the DMA of g0 and g0+1, the activations of g0, then the
+// DMA of g0+2; the step that computes group g sends the activations of g+1
+// and the DMA of g+3, then waits.  Before that wait, the memory instructions
+// issued after the activations of g are the DMA of g+2, the activations of
+// g+1 and the DMA of g+3 (those that exist), and every earlier one covers
+// group g; vector-memory instructions of a wave complete in order, so
+// waiting until only those remain outstanding makes the stage and the
+// activations of g ready.  The DMA of g+3 overwrites the stage of g-1, whose
+// LDS reads completed in the previous step.  The loop is unrolled by kDepth
+// so every stage offset is a constant.
 template <int MB, int NCB>
-__device__ inline void decode_groups(const WaveCtx& c, uint8_t* st0, uint8_t* st1, uint8_t* st2,
-                                     int g0, int g1, v4f (&acc)[2]) {
+__device__ inline void decode_groups(const WaveCtx& c, uint8_t* ring, int g0, int g1,
+                                     v4f (&acc)[2]) {
+  static_assert(kDepth == 4, "the unrolled step below assumes four stages");
   if (g0 >= g1) return;
   constexpr int ND = dma_ops<MB>(), NB = 3 * NCB;
-  uint8_t* const ST[3] = {st0, st1, st2};
   BData B[2];
-  dma_group<MB>(c, g0, ST[0]);
+  dma_group<MB>(c, g0, ring);
+  if (g0 + 1 < g1) dma_group<MB>(c, g0 + 1, ring + kStage);
   load_b(B[0], c, g0);
-  if (g0 + 1 < g1) dma_group<MB>(c, g0 + 1, ST[1]);
+  if (g0 + 2 < g1) dma_group<MB>(c, g0 + 2, ring + 2 * kStage);
 #define D2MOE_STEP(K)                                                        \
   {                                                                          \
     const int gg = g + (K);                                                  \
     if (gg >= g1) break;                                                     \
     if (gg + 1 < g1) load_b(B[((K) + 1) & 1], c, gg + 1);                    \
-    if (gg + 2 < g1) {                                                       \
-      dma_group<MB>(c, gg + 2, ST[((K) + 2) % 3]);                           \
+    if (gg + 3 < g1) {                                                       \
+      dma_group<MB>(c, gg + 3, ring + (((K) + 3) % kDepth) * kStage);        \
       wait_vm<2 * ND + NB>();                                                \
-    } else if (gg + 1 < g1) {                                                \
+    } else if (gg + 2 < g1) {                                                \
       wait_vm<ND + NB>();                                                    \
+    } else if (gg + 1 < g1) {                                                \
+      wait_vm<NB>();                                                         \
     } else {                                                                 \
       wait_vm<0>();                                                          \
     }                                                                        \
-    compute_group<MB>(ST[(K) % 3], B[(K) & 1], c, acc);                      \
+    compute_group<MB, ((K) % kDepth) * kStage>(B[(K) & 1], c, acc);          \
   }
-  for (int g = g0; g < g1; g += 6) {
+  for (int g = g0; g < g1; g += kDepth) {
     D2MOE_STEP(0)
     D2MOE_STEP(1)
     D2MOE_STEP(2)
     D2MOE_STEP(3)
-    D2MOE_STEP(4)
-    D2MOE_STEP(5)
   }
 #undef D2MOE_STEP
 }
 
 template <int MB>
-__device__ inline void decode_groups_ncb(const WaveCtx& c, uint8_t* st0, uint8_t* st1,
-                                         uint8_t* st2, int g0, int g1, v4f (&acc)[2]) {
+__device__ inline void decode_groups_ncb(const WaveCtx& c, uint8_t* ring, int g0, int g1,
+                                         v4f (&acc)[2]) {
   if (c.ncb == 2)
-    decode_groups<MB, 2>(c, st0, st1, st2, g0, g1, acc);
+    decode_groups<MB, 2>(c, ring, g0, g1, acc);
   else
-    decode_groups<MB, 1>(c, st0, st1, st2, g0, g1, acc);
+    decode_groups<MB, 1>(c, ring, g0, g1, acc);
 }
 
 // elist[4*i]: expert, first position, end position, largest bit-width.
@@ -406,14 +426,12 @@ __device__ inline void decode_groups_ncb(const WaveCtx& c, uint8_t* st0, uint8_t
 // the matching W3 row-block, each half splitting the groups; the epilogue
 // combines them through LDS.
 template <bool SWIGLU, int NW>
-__global__ __launch_bounds__(64 * NW) void decode_kernel(
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(3))) void decode_kernel(
     MwqView W, const int32_t* __restrict__ elist, const int32_t* __restrict__ ecount,
     const int32_t* __restrict__ perm, const uint8_t* __restrict__ topk_bits,
     const uint8_t* __restrict__ Xq, const uint8_t* __restrict__ Xs, int npos, int f,
     float* __restrict__ out, int out_ld) {
-  __shared__ __attribute__((aligned(16))) uint8_t ring0[NW][kStage];
-  __shared__ __attribute__((aligned(16))) uint8_t ring1[NW][kStage];
-  __shared__ __attribute__((aligned(16))) uint8_t ring2[NW][kStage];
+  __shared__ __attribute__((aligned(16))) uint8_t ring[NW][kDepth * kStage];
   __shared__ float red[NW][64][8];
   const int ei = blockIdx.y;
   if (ei >= *ecount) return;
@@ -458,21 +476,23 @@ __global__ __launch_bounds__(64 * NW) void decode_kernel(
   c.pl_step = W.b_max * 64 * 4;
   c.sc_step = W.levels() * 16 * 2;
   c.k = sigma_consts();
+  {
+    const uint32_t base = lds_addr(ring[wave]);
+    c.lds_pl = base + 4 * lane;
+    c.lds_sc = base + kScaleOff + 8 * c.q;
+    c.lds_z = base + kZeroOff + c.j;
+  }
 
-  // An AGPR clobber keeps the accumulation registers allocated, which makes the
-  // compiler emit the AGPR-destination form of the MFMAs: their results can
-  // then never share registers with the VGPR operands they read.
-  asm volatile("" ::: "a0");
   v4f acc[2];
   acc[0] = acc[1] = v4f{0.f, 0.f, 0.f, 0.f};
   switch (mb) {
-    case 2: decode_groups_ncb<2>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
-    case 3: decode_groups_ncb<3>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
-    case 4: decode_groups_ncb<4>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
-    case 5: decode_groups_ncb<5>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
-    case 6: decode_groups_ncb<6>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
-    case 7: decode_groups_ncb<7>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
-    case 8: decode_groups_ncb<8>(c, ring0[wave], ring1[wave], ring2[wave], g0, g1, acc); break;
+    case 2: decode_groups_ncb<2>(c, ring[wave], g0, g1, acc); break;
+    case 3: decode_groups_ncb<3>(c, ring[wave], g0, g1, acc); break;
+    case 4: decode_groups_ncb<4>(c, ring[wave], g0, g1, acc); break;
+    case 5: decode_groups_ncb<5>(c, ring[wave], g0, g1, acc); break;
+    case 6: decode_groups_ncb<6>(c, ring[wave], g0, g1, acc); break;
+    case 7: decode_groups_ncb<7>(c, ring[wave], g0, g1, acc); break;
+    case 8: decode_groups_ncb<8>(c, ring[wave], g0, g1, acc); break;
     default: break;
   }
 
