@@ -240,9 +240,28 @@ __device__ inline void dma_group(const WaveCtx& c, int g, uint8_t* st) {
 }
 
 struct BData {
-  v8i b[2];   // activation pieces per column block
-  int bs[2];  // their E8M0 block scales
+  v4i lo[2], hi[2];  // activation pieces per column block (32 bytes per lane)
+  int bs[2];         // their E8M0 block scales
 };
+
+// Activation loads are issued as inline assembly for the same reason as the
+// ring reads: with LDS DMA in flight the compiler cannot tell which vector
+// loads have completed and would wait for all of them (draining the weight
+// prefetch) before the first use of these registers.  They are ordered by the
+// explicit vmcnt waits of the group loop instead; ready_b() re-binds the
+// registers after that wait so that no use can move above it.  The "memory"
+// clobber keeps their issue order fixed relative to the DMA instructions,
+// which the wait counts rely on.
+__device__ inline v4i gload16(const uint8_t* p) {
+  v4i v;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+__device__ inline int gload_u8(const uint8_t* p) {
+  int v;
+  asm volatile("global_load_ubyte %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
 
 // Three memory instructions per column block; lanes without a token read the
 // all-zero activation slot, so the count never depends on the lane.
@@ -250,12 +269,25 @@ __device__ inline void load_b(BData& t, const WaveCtx& c, int g) {
 #pragma unroll
   for (int cb = 0; cb < 2; ++cb) {
     if (cb >= c.ncb) continue;  // wave-uniform
-    const uint4* src = (const uint4*)(c.xq[cb] + (size_t)g * 256);
-    const uint4 u0 = src[0], u1 = src[1];
-    t.b[cb] = v8i{(int)u0.x, (int)u0.y, (int)u0.z, (int)u0.w,
-                  (int)u1.x, (int)u1.y, (int)u1.z, (int)u1.w};
-    t.bs[cb] = c.xs[cb][(size_t)g * 8];
+    const uint8_t* src = c.xq[cb] + (size_t)g * 256;
+    t.lo[cb] = gload16(src);
+    t.hi[cb] = gload16(src + 16);
+    t.bs[cb] = gload_u8(c.xs[cb] + (size_t)g * 8);
   }
+}
+
+// Called after the wait that covers the loads of `t`.
+__device__ inline void ready_b(BData& t, const WaveCtx& c) {
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb) {
+    if (cb >= c.ncb) continue;  // wave-uniform
+    asm volatile("" : "+v"(t.lo[cb]), "+v"(t.hi[cb]), "+v"(t.bs[cb]));
+  }
+}
+
+__device__ inline v8i b8(const BData& t, int cb) {
+  const v4i l = t.lo[cb], h = t.hi[cb];
+  return v8i{l[0], l[1], l[2], l[3], h[0], h[1], h[2], h[3]};
 }
 
 // LDS reads of a ring stage are issued as inline assembly: the compiler's
@@ -325,15 +357,19 @@ __device__ inline void compute_group(const BData& t, const WaveCtx& c, v4f (&acc
   read_stage<MB, SOFF>(c, w, sw, z);
   const v8i a0 = expand_sigma(w[0], k), a1 = expand_sigma(w[1], k);
   const v8i au = zero_operand(z);
+  v8i bb[2];
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb)
+    if (cb < c.ncb) bb[cb] = b8(t, cb);
   float s1[4];
   scales4(sw[0], s1);
 #pragma unroll
   for (int cb = 0; cb < 2; ++cb) {
     if (cb >= c.ncb) continue;  // wave-uniform
     // base: sum_k x_k (1.5 - Q_k) + sum_k x_k (z - 1.5), accumulated in place
-    v4f m = mfma_fp4_fp8(au, t.b[cb], 127, t.bs[cb]);
-    m = mfma_fp4_fp8(a0, t.b[cb], m, 127, t.bs[cb]);
-    m = mfma_fp4_fp8(a1, t.b[cb], m, 128, t.bs[cb]);
+    v4f m = mfma_fp4_fp8(au, bb[cb], 127, t.bs[cb]);
+    m = mfma_fp4_fp8(a0, bb[cb], m, 127, t.bs[cb]);
+    m = mfma_fp4_fp8(a1, bb[cb], m, 128, t.bs[cb]);
 #pragma unroll
     for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-s1[r], m[r], acc[cb][r]);
   }
@@ -346,7 +382,7 @@ __device__ inline void compute_group(const BData& t, const WaveCtx& c, v4f (&acc
     for (int cb = 0; cb < 2; ++cb) {
       if (cb >= c.ncb) continue;  // wave-uniform
       const int bs = p < c.bit[cb] ? t.bs[cb] : 0;
-      const v4f d = mfma_fp4_fp8(ap, t.b[cb], 128, bs);
+      const v4f d = mfma_fp4_fp8(ap, bb[cb], 128, bs);
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-sp[r], d[r], acc[cb][r]);
     }
@@ -401,6 +437,7 @@ __device__ inline void decode_groups(const WaveCtx& c, uint8_t* ring, int g0, in
     } else {                                                                 \
       wait_vm<0>();                                                          \
     }                                                                        \
+    ready_b(B[(K) & 1], c);                                                  \
     compute_group<MB, ((K) % kDepth) * kStage>(B[(K) & 1], c, acc);          \
   }
   for (int g = g0; g < g1; g += kDepth) {
@@ -468,6 +505,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(3))) vo
     c.xq[cb] = Xq + base * 128 + c.q * 32;
     c.xs[cb] = Xs + base * 4 + c.q;
   }
+  // the bit-widths are needed only inside the group loop; consuming them here
+  // makes the compiler's wait for their loads happen before the first DMA
+  // (a wait placed after it would drain the weight prefetch)
+  asm volatile("" : "+v"(c.bit[0]), "+v"(c.bit[1])::"memory");
+
   const int rowblock = rr == 0 ? rb : rb + f / 16;
   const size_t blk0 = W.block(e, rowblock, 0);
   c.pl = (const uint8_t*)(W.planes + W.plane_word(blk0, 0, 0));
