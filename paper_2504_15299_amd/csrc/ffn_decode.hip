@@ -70,37 +70,22 @@ __device__ inline float ld_act<float>(const float* p) { return *p; }
 template <>
 __device__ inline float ld_act<uint16_t>(const uint16_t* p) { return bf2f(*p); }
 
-// Activation prep: one thread per (position, 32-column block).  Writes the
-// hi/lo fp8 pieces in the B-operand lane order of the 16x16x128 MFMA
-// (lane group q holds hardware k 16q..16q+15 and 64+16q..64+16q+15) and the
-// E8M0 block scales.  Logical column 32q + 4n + d sits at hardware k
-// 32q + 8d + n, matching the nibble order of the expanded plane words.
-//   Xq [pos][K/128][piece][128] bytes, Xs [pos][K/128][piece][4] bytes
+// Activation prep, in two passes (below).  Each row is scaled by one
+// power of two 2^s, with s taken from its largest magnitude so that
+// |x| / 2^s < 256, and split into two fp8 e4m3 pieces, hi = rne(x / 2^s) and
+// lo = rne(16 (x / 2^s - hi)).  Together they hold a bf16 value exactly
+// while hi is a normal e4m3 number; smaller elements keep an absolute error
+// below 2^-22 of the row maximum.  The pieces are written in the B-operand
+// lane order of the 16x16x128 MFMA (lane group q holds hardware k
+// 16q..16q+15 and 64+16q..64+16q+15); logical column 32q + 4n + d sits at
+// hardware k 32q + 8d + n, matching the nibble order of the expanded plane
+// words.  Xs holds the E8M0 codes of 2^s (hi) and 2^(s-4) (lo).
+//   Xq [pos][K/128][piece][128] bytes, Xs [pos][piece] bytes
 // Position npos is an all-zero slot that decode lanes without a token read,
 // so that every load in the decode loop is unconditional.
-template <typename TIN>
-__global__ void xprep_kernel(const TIN* __restrict__ in, int in_ld,
-                             const int32_t* __restrict__ perm, int kdiv, int npos, int K,
-                             uint8_t* __restrict__ Xq, uint8_t* __restrict__ Xs) {
-  const int nb32 = K / 32;
-  const int tid = blockIdx.x * blockDim.x + threadIdx.x;
-  if (tid >= (npos + 1) * nb32) return;
-  const int pos = tid / nb32, kb = tid % nb32;
-  const int g = kb >> 2, q = kb & 3, NG = K / G;
-  float v[32];
-  float amax = 0.0f;
-  if (pos < npos) {
-    const long row = perm ? (long)(perm[pos] / kdiv) : (long)pos;
-    const TIN* src = in + row * in_ld + (long)kb * 32;
-#pragma unroll
-    for (int e = 0; e < 32; ++e) {
-      v[e] = ld_act<TIN>(src + e);
-      amax = fmaxf(amax, fabsf(v[e]));
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < 32; ++e) v[e] = 0.0f;
-  }
+constexpr int kPrepThreads = 256;
+
+__device__ inline int row_scale_exp(float amax) {
   int s = 0;
   if (amax > 0.0f) {
     int E;
@@ -108,8 +93,46 @@ __global__ void xprep_kernel(const TIN* __restrict__ in, int in_ld,
     s = E - 8;
     s = s < -120 ? -120 : (s > 120 ? 120 : s);
   }
-  const size_t base = ((size_t)pos * NG + g) * 2;
-  uint8_t* hi = Xq + base * 128;
+  return s;
+}
+
+// Pass 1: one workgroup per position: the row's scale exponent s.
+template <typename TIN>
+__global__ __launch_bounds__(kPrepThreads) void xscale_kernel(
+    const TIN* __restrict__ in, int in_ld, const int32_t* __restrict__ perm, int kdiv, int npos,
+    int K, uint8_t* __restrict__ Xs) {
+  __shared__ float wmax[kPrepThreads / 64];
+  const int pos = blockIdx.x;
+  float amax = 0.0f;
+  if (pos < npos) {
+    const TIN* src = in + (long)(perm ? perm[pos] / kdiv : pos) * in_ld;
+    for (int c = threadIdx.x; c < K; c += kPrepThreads) amax = fmaxf(amax, fabsf(ld_act<TIN>(src + c)));
+  }
+  for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, 64));
+  if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = amax;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < kPrepThreads / 64; ++w) amax = fmaxf(amax, wmax[w]);
+    const int s = row_scale_exp(amax);
+    Xs[pos * 2] = (uint8_t)(s + 127);
+    Xs[pos * 2 + 1] = (uint8_t)(s - 4 + 127);
+  }
+}
+
+// Pass 2: one thread per (position, 32-column block): the two fp8 pieces.
+template <typename TIN>
+__global__ __launch_bounds__(kPrepThreads) void xquant_kernel(
+    const TIN* __restrict__ in, int in_ld, const int32_t* __restrict__ perm, int kdiv, int npos,
+    int K, const uint8_t* __restrict__ Xs, uint8_t* __restrict__ Xq) {
+  const int nb32 = K / 32;
+  const int tid = blockIdx.x * blockDim.x + threadIdx.x;
+  if (tid >= (npos + 1) * nb32) return;
+  const int pos = tid / nb32, kb = tid % nb32;
+  const int g = kb >> 2, q = kb & 3, NG = K / G;
+  const int s = (int)Xs[pos * 2] - 127;
+  const TIN* src = nullptr;
+  if (pos < npos) src = in + (long)(perm ? perm[pos] / kdiv : pos) * in_ld + (long)kb * 32;
+  uint8_t* hi = Xq + ((size_t)pos * NG + g) * 2 * 128;
   uint8_t* lo = hi + 128;
 #pragma unroll
   for (int kl = 0; kl < 32; ++kl) {
@@ -117,15 +140,13 @@ __global__ void xprep_kernel(const TIN* __restrict__ in, int in_ld,
     const int khw = 32 * q + 8 * d + n;
     const int qq = khw < 64 ? (khw >> 4) : ((khw - 64) >> 4);
     const int ee = khw < 64 ? (khw & 15) : (16 + ((khw - 64) & 15));
-    const float x = ldexpf(v[kl], -s);
+    const float x = src ? ldexpf(ld_act<TIN>(src + kl), -s) : 0.0f;
     const uint32_t ch = e4m3_rne(x);
     const float r = x - e4m3_val(ch);
     const uint32_t cl = e4m3_rne(r * 16.0f);
     hi[qq * 32 + ee] = (uint8_t)ch;
     lo[qq * 32 + ee] = (uint8_t)cl;
   }
-  Xs[base * 4 + q] = (uint8_t)(s + 127);
-  Xs[(base + 1) * 4 + q] = (uint8_t)(s - 4 + 127);
 }
 
 // Opaque copies of the two masks used by expand_sigma: held in VGPRs, they
@@ -214,7 +235,7 @@ struct WaveCtx {
   int lane, q, j, ncb;
   int bit[2];
   const uint8_t* xq[2];  // activation pieces of group 0, this lane
-  const uint8_t* xs[2];  // their scales
+  int bsc[2];            // their E8M0 scale code
   SigmaConsts k;
   uint32_t lds_pl, lds_sc, lds_z;  // this lane's LDS read addresses in stage 0
 };
@@ -241,7 +262,6 @@ __device__ inline void dma_group(const WaveCtx& c, int g, uint8_t* st) {
 
 struct BData {
   v4i lo[2], hi[2];  // activation pieces per column block (32 bytes per lane)
-  int bs[2];         // their E8M0 block scales
 };
 
 // Activation loads are issued as inline assembly for the same reason as the
@@ -257,13 +277,8 @@ __device__ inline v4i gload16(const uint8_t* p) {
   asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
   return v;
 }
-__device__ inline int gload_u8(const uint8_t* p) {
-  int v;
-  asm volatile("global_load_ubyte %0, %1, off" : "=v"(v) : "v"(p) : "memory");
-  return v;
-}
 
-// Three memory instructions per column block; lanes without a token read the
+// Two memory instructions per column block; lanes without a token read the
 // all-zero activation slot, so the count never depends on the lane.
 __device__ inline void load_b(BData& t, const WaveCtx& c, int g) {
 #pragma unroll
@@ -272,7 +287,6 @@ __device__ inline void load_b(BData& t, const WaveCtx& c, int g) {
     const uint8_t* src = c.xq[cb] + (size_t)g * 256;
     t.lo[cb] = gload16(src);
     t.hi[cb] = gload16(src + 16);
-    t.bs[cb] = gload_u8(c.xs[cb] + (size_t)g * 8);
   }
 }
 
@@ -281,7 +295,7 @@ __device__ inline void ready_b(BData& t, const WaveCtx& c) {
 #pragma unroll
   for (int cb = 0; cb < 2; ++cb) {
     if (cb >= c.ncb) continue;  // wave-uniform
-    asm volatile("" : "+v"(t.lo[cb]), "+v"(t.hi[cb]), "+v"(t.bs[cb]));
+    asm volatile("" : "+v"(t.lo[cb]), "+v"(t.hi[cb]));
   }
 }
 
@@ -367,9 +381,9 @@ __device__ inline void compute_group(const BData& t, const WaveCtx& c, v4f (&acc
   for (int cb = 0; cb < 2; ++cb) {
     if (cb >= c.ncb) continue;  // wave-uniform
     // base: sum_k x_k (1.5 - Q_k) + sum_k x_k (z - 1.5), accumulated in place
-    v4f m = mfma_fp4_fp8(au, bb[cb], 127, t.bs[cb]);
-    m = mfma_fp4_fp8(a0, bb[cb], m, 127, t.bs[cb]);
-    m = mfma_fp4_fp8(a1, bb[cb], m, 128, t.bs[cb]);
+    v4f m = mfma_fp4_fp8(au, bb[cb], 127, c.bsc[cb]);
+    m = mfma_fp4_fp8(a0, bb[cb], m, 127, c.bsc[cb]);
+    m = mfma_fp4_fp8(a1, bb[cb], m, 128, c.bsc[cb]);
 #pragma unroll
     for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-s1[r], m[r], acc[cb][r]);
   }
@@ -381,7 +395,7 @@ __device__ inline void compute_group(const BData& t, const WaveCtx& c, v4f (&acc
 #pragma unroll
     for (int cb = 0; cb < 2; ++cb) {
       if (cb >= c.ncb) continue;  // wave-uniform
-      const int bs = p < c.bit[cb] ? t.bs[cb] : 0;
+      const int bs = p < c.bit[cb] ? c.bsc[cb] : 0;
       const v4f d = mfma_fp4_fp8(ap, bb[cb], 128, bs);
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-sp[r], d[r], acc[cb][r]);
@@ -416,7 +430,7 @@ __device__ inline void decode_groups(const WaveCtx& c, uint8_t* ring, int g0, in
                                      v4f (&acc)[2]) {
   static_assert(kDepth == 4, "the unrolled step below assumes four stages");
   if (g0 >= g1) return;
-  constexpr int ND = dma_ops<MB>(), NB = 3 * NCB;
+  constexpr int ND = dma_ops<MB>(), NB = 2 * NCB;
   BData B[2];
   dma_group<MB>(c, g0, ring);
   if (g0 + 1 < g1) dma_group<MB>(c, g0 + 1, ring + kStage);
@@ -503,12 +517,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(3))) vo
     const int src = validj[cb] ? posj[cb] : npos;  // zero slot when no token
     const size_t base = ((size_t)src * NG) * 2 + piece;  // group 0
     c.xq[cb] = Xq + base * 128 + c.q * 32;
-    c.xs[cb] = Xs + base * 4 + c.q;
+    c.bsc[cb] = Xs[src * 2 + piece];
   }
-  // the bit-widths are needed only inside the group loop; consuming them here
+  // the bit-widths and activation scale codes are needed only inside the group
+  // loop; consuming them here
   // makes the compiler's wait for their loads happen before the first DMA
   // (a wait placed after it would drain the weight prefetch)
-  asm volatile("" : "+v"(c.bit[0]), "+v"(c.bit[1])::"memory");
+  asm volatile("" : "+v"(c.bit[0]), "+v"(c.bit[1]), "+v"(c.bsc[0]), "+v"(c.bsc[1])::"memory");
 
   const int rowblock = rr == 0 ? rb : rb + f / 16;
   const size_t blk0 = W.block(e, rowblock, 0);
@@ -588,8 +603,12 @@ __global__ void expert_list_kernel(const int32_t* __restrict__ offsets,
 template <typename TIN>
 hipError_t run_xprep(const TIN* in, int in_ld, const int32_t* perm, int kdiv, int npos, int K,
                      uint8_t* Xq, uint8_t* Xs, hipStream_t s) {
+  xscale_kernel<TIN><<<npos + 1, kPrepThreads, 0, s>>>(in, in_ld, perm, kdiv, npos, K, Xs);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
   const int n = (npos + 1) * (K / 32);
-  xprep_kernel<TIN><<<(n + 255) / 256, 256, 0, s>>>(in, in_ld, perm, kdiv, npos, K, Xq, Xs);
+  xquant_kernel<TIN><<<(n + kPrepThreads - 1) / kPrepThreads, kPrepThreads, 0, s>>>(
+      in, in_ld, perm, kdiv, npos, K, Xs, Xq);
   return hipGetLastError();
 }
 
