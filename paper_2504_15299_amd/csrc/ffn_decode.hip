@@ -70,7 +70,7 @@ __device__ inline float ld_act<float>(const float* p) { return *p; }
 template <>
 __device__ inline float ld_act<uint16_t>(const uint16_t* p) { return bf2f(*p); }
 
-// Activation prep, in two passes (below).  Each row is scaled by one
+// Activation prep (xprep_kernel below).  Each row is scaled by one
 // power of two 2^s, with s taken from its largest magnitude so that
 // |x| / 2^s < 256, and split into two fp8 e4m3 pieces, hi = rne(x / 2^s) and
 // lo = rne(16 (x / 2^s - hi)).  Together they hold a bf16 value exactly
@@ -83,7 +83,7 @@ __device__ inline float ld_act<uint16_t>(const uint16_t* p) { return bf2f(*p); }
 //   Xq [pos][K/128][piece][128] bytes, Xs [pos][piece] bytes
 // Position npos is an all-zero slot that decode lanes without a token read,
 // so that every load in the decode loop is unconditional.
-constexpr int kPrepThreads = 256;
+constexpr int kPrepThreads = 1024;
 
 __device__ inline int row_scale_exp(float amax) {
   int s = 0;
@@ -96,56 +96,59 @@ __device__ inline int row_scale_exp(float amax) {
   return s;
 }
 
-// Pass 1: one workgroup per position: the row's scale exponent s.
+// One workgroup per position: the row's largest magnitude, then one element
+// per thread per step.  The workgroup of the zero slot also writes the
+// active-expert list of the decode kernels when `elist` is given:
+// elist[4 i] = expert, first position, end position, largest bit-width.
 template <typename TIN>
-__global__ __launch_bounds__(kPrepThreads) void xscale_kernel(
+__global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
     const TIN* __restrict__ in, int in_ld, const int32_t* __restrict__ perm, int kdiv, int npos,
-    int K, uint8_t* __restrict__ Xs) {
+    int K, uint8_t* __restrict__ Xq, uint8_t* __restrict__ Xs,
+    const int32_t* __restrict__ offsets, const uint8_t* __restrict__ maxbit, int E, int L,
+    int32_t* __restrict__ elist, int32_t* __restrict__ ecount) {
   __shared__ float wmax[kPrepThreads / 64];
-  const int pos = blockIdx.x;
-  float amax = 0.0f;
-  if (pos < npos) {
-    const TIN* src = in + (long)(perm ? perm[pos] / kdiv : pos) * in_ld;
-    for (int c = threadIdx.x; c < K; c += kPrepThreads) amax = fmaxf(amax, fabsf(ld_act<TIN>(src + c)));
+  const int pos = blockIdx.x, NG = K / G;
+  if (pos == npos && elist && threadIdx.x == 0) {
+    int n = 0;
+    for (int e = 0; e < E; ++e) {
+      if (maxbit[e] == 0) continue;
+      elist[4 * n] = e;
+      elist[4 * n + 1] = offsets[e * L];
+      elist[4 * n + 2] = offsets[e * L + L];
+      elist[4 * n + 3] = maxbit[e];
+      ++n;
+    }
+    *ecount = n;
   }
+  const TIN* src = nullptr;
+  if (pos < npos) src = in + (long)(perm ? perm[pos] / kdiv : pos) * in_ld;
+  float amax = 0.0f;
+  if (src)
+    for (int c = threadIdx.x; c < K; c += kPrepThreads) amax = fmaxf(amax, fabsf(ld_act<TIN>(src + c)));
   for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, 64));
   if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = amax;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int w = 1; w < kPrepThreads / 64; ++w) amax = fmaxf(amax, wmax[w]);
-    const int s = row_scale_exp(amax);
-    Xs[pos * 2] = (uint8_t)(s + 127);
-    Xs[pos * 2 + 1] = (uint8_t)(s - 4 + 127);
-  }
-}
-
-// Pass 2: one thread per (position, 32-column block): the two fp8 pieces.
-template <typename TIN>
-__global__ __launch_bounds__(kPrepThreads) void xquant_kernel(
-    const TIN* __restrict__ in, int in_ld, const int32_t* __restrict__ perm, int kdiv, int npos,
-    int K, const uint8_t* __restrict__ Xs, uint8_t* __restrict__ Xq) {
-  const int nb32 = K / 32;
-  const int tid = blockIdx.x * blockDim.x + threadIdx.x;
-  if (tid >= (npos + 1) * nb32) return;
-  const int pos = tid / nb32, kb = tid % nb32;
-  const int g = kb >> 2, q = kb & 3, NG = K / G;
-  const int s = (int)Xs[pos * 2] - 127;
-  const TIN* src = nullptr;
-  if (pos < npos) src = in + (long)(perm ? perm[pos] / kdiv : pos) * in_ld + (long)kb * 32;
-  uint8_t* hi = Xq + ((size_t)pos * NG + g) * 2 * 128;
-  uint8_t* lo = hi + 128;
-#pragma unroll
-  for (int kl = 0; kl < 32; ++kl) {
+  amax = 0.0f;
+  for (int w = 0; w < kPrepThreads / 64; ++w) amax = fmaxf(amax, wmax[w]);
+  const int s = row_scale_exp(amax);
+  uint8_t* row = Xq + (size_t)pos * NG * 256;
+  for (int c = threadIdx.x; c < K; c += kPrepThreads) {
+    const int g = c / G, kb = (c % G) >> 5, kl = c & 31;
     const int d = kl & 3, n = kl >> 2;
-    const int khw = 32 * q + 8 * d + n;
+    const int khw = 32 * kb + 8 * d + n;
     const int qq = khw < 64 ? (khw >> 4) : ((khw - 64) >> 4);
     const int ee = khw < 64 ? (khw & 15) : (16 + ((khw - 64) & 15));
-    const float x = src ? ldexpf(ld_act<TIN>(src + kl), -s) : 0.0f;
+    const float x = src ? ldexpf(ld_act<TIN>(src + c), -s) : 0.0f;
     const uint32_t ch = e4m3_rne(x);
     const float r = x - e4m3_val(ch);
     const uint32_t cl = e4m3_rne(r * 16.0f);
+    uint8_t* hi = row + (size_t)g * 256;
     hi[qq * 32 + ee] = (uint8_t)ch;
-    lo[qq * 32 + ee] = (uint8_t)cl;
+    hi[128 + qq * 32 + ee] = (uint8_t)cl;
+  }
+  if (threadIdx.x == 0) {
+    Xs[pos * 2] = (uint8_t)(s + 127);
+    Xs[pos * 2 + 1] = (uint8_t)(s - 4 + 127);
   }
 }
 
@@ -583,32 +586,14 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(3))) vo
   }
 }
 
-// Active-expert list for the decode kernels (ascending expert id).
-__global__ void expert_list_kernel(const int32_t* __restrict__ offsets,
-                                   const uint8_t* __restrict__ maxbit, int E, int L,
-                                   int32_t* __restrict__ elist, int32_t* __restrict__ ecount) {
-  if (threadIdx.x != 0) return;
-  int n = 0;
-  for (int e = 0; e < E; ++e) {
-    if (maxbit[e] == 0) continue;
-    elist[4 * n] = e;
-    elist[4 * n + 1] = offsets[e * L];
-    elist[4 * n + 2] = offsets[e * L + L];
-    elist[4 * n + 3] = maxbit[e];
-    ++n;
-  }
-  *ecount = n;
-}
 
 template <typename TIN>
 hipError_t run_xprep(const TIN* in, int in_ld, const int32_t* perm, int kdiv, int npos, int K,
-                     uint8_t* Xq, uint8_t* Xs, hipStream_t s) {
-  xscale_kernel<TIN><<<npos + 1, kPrepThreads, 0, s>>>(in, in_ld, perm, kdiv, npos, K, Xs);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
-  const int n = (npos + 1) * (K / 32);
-  xquant_kernel<TIN><<<(n + kPrepThreads - 1) / kPrepThreads, kPrepThreads, 0, s>>>(
-      in, in_ld, perm, kdiv, npos, K, Xs, Xq);
+                     uint8_t* Xq, uint8_t* Xs, const d2moe_routing* r, int E, int L,
+                     int32_t* elist, int32_t* ecount, hipStream_t s) {
+  xprep_kernel<TIN><<<npos + 1, kPrepThreads, 0, s>>>(
+      in, in_ld, perm, kdiv, npos, K, Xq, Xs, r ? r->offsets : nullptr,
+      r ? r->expert_maxbit : nullptr, E, L, elist, ecount);
   return hipGetLastError();
 }
 
@@ -629,12 +614,12 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   hipError_t err;
   const int L = w13->b_max - w13->b_min + 1;
   const int npos = T * k;
-  expert_list_kernel<<<1, 64, 0, s>>>(r->offsets, r->expert_maxbit, E, L, b.elist, b.ecount);
-  if ((err = hipGetLastError()) != hipSuccess) return err;
   if (xd == D2MOE_BF16)
-    err = run_xprep<uint16_t>((const uint16_t*)x, d, r->perm, k, npos, d, b.xq13, b.xs13, s);
+    err = run_xprep<uint16_t>((const uint16_t*)x, d, r->perm, k, npos, d, b.xq13, b.xs13, r, E, L,
+                              b.elist, b.ecount, s);
   else
-    err = run_xprep<float>((const float*)x, d, r->perm, k, npos, d, b.xq13, b.xs13, s);
+    err = run_xprep<float>((const float*)x, d, r->perm, k, npos, d, b.xq13, b.xs13, r, E, L,
+                           b.elist, b.ecount, s);
   if (err != hipSuccess) return err;
   const int ny = E < npos ? E : npos;
   const MwqView W13 = view_of(w13), W2 = view_of(w2);
@@ -643,7 +628,8 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
       W13, b.elist, b.ecount, r->perm, r->topk_bits, b.xq13, b.xs13, npos, d_ff, b.h32, d_ff);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
-  err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.xq2, b.xs2, s);
+  err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.xq2, b.xs2, nullptr, 0, 0,
+                         nullptr, nullptr, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
   decode_kernel<false, kDecodeWaves><<<dim3(d / 16, ny), 64 * kDecodeWaves, 0, s>>>(

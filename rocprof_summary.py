@@ -16,7 +16,7 @@ from collections import defaultdict
 def _short(name: str) -> str:
     for key in ("decode_kernel<true", "decode_kernel<false", "xprep_kernel", "gemm_kernel",
                 "combine_kernel", "gate_kernel", "topk_kernel", "hist_perm_kernel",
-                "expert_list_kernel", "schedule_kernel", "pack_kernel"):
+                "schedule_kernel", "pack_kernel"):
         if key in name:
             return name[name.find(key):][:90]
     return name[:90]
