@@ -83,7 +83,8 @@ __device__ inline float ld_act<uint16_t>(const uint16_t* p) { return bf2f(*p); }
 //   Xq [pos][K/128][piece][128] bytes, Xs [pos][piece] bytes
 // Position npos is an all-zero slot that decode lanes without a token read,
 // so that every load in the decode loop is unconditional.
-constexpr int kPrepThreads = 1024;
+constexpr int kPrepThreads = 256;
+constexpr int kPrepCols = 2048;  // columns per workgroup (16 groups)
 
 __device__ inline int row_scale_exp(float amax) {
   int s = 0;
@@ -96,19 +97,55 @@ __device__ inline int row_scale_exp(float amax) {
   return s;
 }
 
-// One workgroup per position: the row's largest magnitude, then one element
-// per thread per step.  The workgroup of the zero slot also writes the
-// active-expert list of the decode kernels when `elist` is given:
-// elist[4 i] = expert, first position, end position, largest bit-width.
+// Grid (position, column slice of kPrepCols).  Every workgroup of a row
+// takes the row's largest magnitude (from `rowmax`, or computed from the
+// row, which is small and cached), then converts its slice, four output bytes per thread per step: output bytes
+// 4j..4j+3 of a 16-byte run hold hardware k = 4j..4j+3, i.e. logical columns
+// 32q + 4n + d for n = 4j'..4j'+3 (fixed d), so each thread reads four
+// columns at stride 4 and stores one dword per piece.  The zero-slot
+// workgroup of slice 0 also writes the active-expert list of the decode
+// kernels when `elist` is given: elist[4 i] = expert, first position, end
+// position, largest bit-width.
+template <typename TIN>
+__device__ inline float row_absmax(const TIN* row, int K);
+template <>
+__device__ inline float row_absmax<uint16_t>(const uint16_t* row, int K) {
+  float m = 0.0f;
+  for (int c = 8 * threadIdx.x; c < K; c += 8 * kPrepThreads) {
+    const uint4 u = *(const uint4*)(row + c);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      m = fmaxf(m, fmaxf(fabsf(bf2f((uint16_t)(w[i] & 0xffff))), fabsf(bf2f((uint16_t)(w[i] >> 16)))));
+  }
+  return m;
+}
+template <>
+__device__ inline float row_absmax<float>(const float* row, int K) {
+  float m = 0.0f;
+  for (int c = 4 * threadIdx.x; c < K; c += 4 * kPrepThreads) {
+    const float4 v = *(const float4*)(row + c);
+    m = fmaxf(m, fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w))));
+  }
+  return m;
+}
+
+// rowmax: largest |value| of each position's row as binary32 bits (given by
+// the producer of the rows), or NULL to compute it here with 16-byte loads
+// (rows are K % 128 == 0 elements on 16-byte aligned bases).  zero_max: if
+// given, npos + 1 entries set to 0 for the next producer's atomicMax.
 template <typename TIN>
 __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
     const TIN* __restrict__ in, int in_ld, const int32_t* __restrict__ perm, int kdiv, int npos,
-    int K, uint8_t* __restrict__ Xq, uint8_t* __restrict__ Xs,
-    const int32_t* __restrict__ offsets, const uint8_t* __restrict__ maxbit, int E, int L,
-    int32_t* __restrict__ elist, int32_t* __restrict__ ecount) {
+    int K, const uint32_t* __restrict__ rowmax, uint8_t* __restrict__ Xq,
+    uint8_t* __restrict__ Xs, const int32_t* __restrict__ offsets,
+    const uint8_t* __restrict__ maxbit, int E, int L, int32_t* __restrict__ elist,
+    int32_t* __restrict__ ecount, uint32_t* __restrict__ zero_max) {
   __shared__ float wmax[kPrepThreads / 64];
   const int pos = blockIdx.x, NG = K / G;
-  if (pos == npos && elist && threadIdx.x == 0) {
+  if (zero_max && pos == npos && blockIdx.y == 0)
+    for (int i = threadIdx.x; i <= npos; i += kPrepThreads) zero_max[i] = 0u;
+  if (pos == npos && blockIdx.y == 0 && elist && threadIdx.x == 0) {
     int n = 0;
     for (int e = 0; e < E; ++e) {
       if (maxbit[e] == 0) continue;
@@ -123,30 +160,41 @@ __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
   const TIN* src = nullptr;
   if (pos < npos) src = in + (long)(perm ? perm[pos] / kdiv : pos) * in_ld;
   float amax = 0.0f;
-  if (src)
-    for (int c = threadIdx.x; c < K; c += kPrepThreads) amax = fmaxf(amax, fabsf(ld_act<TIN>(src + c)));
-  for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, 64));
-  if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = amax;
-  __syncthreads();
-  amax = 0.0f;
-  for (int w = 0; w < kPrepThreads / 64; ++w) amax = fmaxf(amax, wmax[w]);
-  const int s = row_scale_exp(amax);
-  uint8_t* row = Xq + (size_t)pos * NG * 256;
-  for (int c = threadIdx.x; c < K; c += kPrepThreads) {
-    const int g = c / G, kb = (c % G) >> 5, kl = c & 31;
-    const int d = kl & 3, n = kl >> 2;
-    const int khw = 32 * kb + 8 * d + n;
-    const int qq = khw < 64 ? (khw >> 4) : ((khw - 64) >> 4);
-    const int ee = khw < 64 ? (khw & 15) : (16 + ((khw - 64) & 15));
-    const float x = src ? ldexpf(ld_act<TIN>(src + c), -s) : 0.0f;
-    const uint32_t ch = e4m3_rne(x);
-    const float r = x - e4m3_val(ch);
-    const uint32_t cl = e4m3_rne(r * 16.0f);
-    uint8_t* hi = row + (size_t)g * 256;
-    hi[qq * 32 + ee] = (uint8_t)ch;
-    hi[128 + qq * 32 + ee] = (uint8_t)cl;
+  if (rowmax) {
+    if (src) amax = __uint_as_float(rowmax[pos]);
+  } else {
+    if (src) amax = row_absmax<TIN>(src, K);
+    for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, 64));
+    if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = amax;
+    __syncthreads();
+    amax = 0.0f;
+    for (int w = 0; w < kPrepThreads / 64; ++w) amax = fmaxf(amax, wmax[w]);
   }
-  if (threadIdx.x == 0) {
+  const int s = row_scale_exp(amax);
+  uint32_t* row = (uint32_t*)(Xq + (size_t)pos * NG * 256);
+  const int c0 = blockIdx.y * kPrepCols, c1 = min(K, c0 + kPrepCols);
+  // one dword per thread per step: output dword u of the row covers
+  // group u / 64, piece 0 (hi) dwords 0..31 of the group's 64
+  for (int u = c0 / 4 + threadIdx.x; u < c1 / 4; u += kPrepThreads) {
+    const int g = u >> 5, w = u & 31;                 // hi dword w of group g
+    const int qq = w >> 3, e4 = (w & 7) * 4;          // lane group, first byte
+    const int khw = e4 < 16 ? 16 * qq + e4 : 64 + 16 * qq + (e4 - 16);
+    const int kb = khw >> 5, dd = (khw & 31) >> 3, n0 = khw & 7;
+    uint32_t hi = 0, lo = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int col = g * G + 32 * kb + 4 * (n0 + i) + dd;
+      const float x = src ? ldexpf(ld_act<TIN>(src + col), -s) : 0.0f;
+      const uint32_t ch = e4m3_rne(x);
+      const float r = x - e4m3_val(ch);
+      const uint32_t cl = e4m3_rne(r * 16.0f);
+      hi |= ch << (8 * i);
+      lo |= cl << (8 * i);
+    }
+    row[g * 64 + w] = hi;
+    row[g * 64 + 32 + w] = lo;
+  }
+  if (threadIdx.x == 0 && blockIdx.y == 0) {
     Xs[pos * 2] = (uint8_t)(s + 127);
     Xs[pos * 2 + 1] = (uint8_t)(s - 4 + 127);
   }
@@ -484,7 +532,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(3))) vo
     MwqView W, const int32_t* __restrict__ elist, const int32_t* __restrict__ ecount,
     const int32_t* __restrict__ perm, const uint8_t* __restrict__ topk_bits,
     const uint8_t* __restrict__ Xq, const uint8_t* __restrict__ Xs, int npos, int f,
-    float* __restrict__ out, int out_ld) {
+    float* __restrict__ out, int out_ld, uint32_t* __restrict__ rowmax) {
   __shared__ __attribute__((aligned(16))) uint8_t ring[NW][kDepth * kStage];
   __shared__ float red[NW][64][8];
   const int ei = blockIdx.y;
@@ -584,16 +632,32 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(3))) vo
       o[r] = SWIGLU ? silu(v[0][cb][r]) * v[NRR - 1][cb][r] : v[0][cb][r];
     *(float4*)dst = float4{o[0], o[1], o[2], o[3]};
   }
+  if (rowmax) {
+    // largest |output| of each position, for the scale of its fp8 pieces:
+    // max over this lane's rows, then over the four lanes (q) of the token
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) {
+      if (cb >= c.ncb) continue;  // wave-uniform
+      float m = 0.0f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        m = fmaxf(m, fabsf(SWIGLU ? silu(v[0][cb][r]) * v[NRR - 1][cb][r] : v[0][cb][r]));
+      m = fmaxf(m, __shfl_xor(m, 16, 64));
+      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      if (validj[cb] && piece == 0 && c.q == 0) atomicMax(rowmax + posj[cb], __float_as_uint(m));
+    }
+  }
 }
 
 
 template <typename TIN>
 hipError_t run_xprep(const TIN* in, int in_ld, const int32_t* perm, int kdiv, int npos, int K,
-                     uint8_t* Xq, uint8_t* Xs, const d2moe_routing* r, int E, int L,
-                     int32_t* elist, int32_t* ecount, hipStream_t s) {
-  xprep_kernel<TIN><<<npos + 1, kPrepThreads, 0, s>>>(
-      in, in_ld, perm, kdiv, npos, K, Xq, Xs, r ? r->offsets : nullptr,
-      r ? r->expert_maxbit : nullptr, E, L, elist, ecount);
+                     const uint32_t* rowmax, uint8_t* Xq, uint8_t* Xs, const d2moe_routing* r,
+                     int E, int L, int32_t* elist, int32_t* ecount, uint32_t* zero_max,
+                     hipStream_t s) {
+  xprep_kernel<TIN><<<dim3(npos + 1, (K + kPrepCols - 1) / kPrepCols), kPrepThreads, 0, s>>>(
+      in, in_ld, perm, kdiv, npos, K, rowmax, Xq, Xs, r ? r->offsets : nullptr,
+      r ? r->expert_maxbit : nullptr, E, L, elist, ecount, zero_max);
   return hipGetLastError();
 }
 
@@ -615,25 +679,26 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   const int L = w13->b_max - w13->b_min + 1;
   const int npos = T * k;
   if (xd == D2MOE_BF16)
-    err = run_xprep<uint16_t>((const uint16_t*)x, d, r->perm, k, npos, d, b.xq13, b.xs13, r, E, L,
-                              b.elist, b.ecount, s);
+    err = run_xprep<uint16_t>((const uint16_t*)x, d, r->perm, k, npos, d, nullptr, b.xq13, b.xs13,
+                              r, E, L, b.elist, b.ecount, b.hmax, s);
   else
-    err = run_xprep<float>((const float*)x, d, r->perm, k, npos, d, b.xq13, b.xs13, r, E, L,
-                           b.elist, b.ecount, s);
+    err = run_xprep<float>((const float*)x, d, r->perm, k, npos, d, nullptr, b.xq13, b.xs13, r,
+                           E, L, b.elist, b.ecount, b.hmax, s);
   if (err != hipSuccess) return err;
   const int ny = E < npos ? E : npos;
   const MwqView W13 = view_of(w13), W2 = view_of(w2);
   if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
   decode_kernel<true, kDecodeWaves><<<dim3(d_ff / 16, ny), 64 * kDecodeWaves, 0, s>>>(
-      W13, b.elist, b.ecount, r->perm, r->topk_bits, b.xq13, b.xs13, npos, d_ff, b.h32, d_ff);
+      W13, b.elist, b.ecount, r->perm, r->topk_bits, b.xq13, b.xs13, npos, d_ff, b.h32, d_ff,
+      b.hmax);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
-  err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.xq2, b.xs2, nullptr, 0, 0,
-                         nullptr, nullptr, s);
+  err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.hmax, b.xq2, b.xs2, nullptr, 0,
+                         0, nullptr, nullptr, nullptr, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
   decode_kernel<false, kDecodeWaves><<<dim3(d / 16, ny), 64 * kDecodeWaves, 0, s>>>(
-      W2, b.elist, b.ecount, r->perm, r->topk_bits, b.xq2, b.xs2, npos, 0, b.y, d);
+      W2, b.elist, b.ecount, r->perm, r->topk_bits, b.xq2, b.xs2, npos, 0, b.y, d, nullptr);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
   return hipSuccess;

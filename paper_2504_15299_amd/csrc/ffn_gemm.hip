@@ -288,10 +288,11 @@ FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shar
   L.elist_off = off;  off += align256(sizeof(int32_t) * ((size_t)E * 4 + 4));
   const size_t nz = nd ? nd + 1 : 0;  // plus one all-zero activation slot
   L.xq13_off = off;   off += align256(nz * d * 2);
-  L.xs13_off = off;   off += align256(nz * (d / 32) * 2);
+  L.xs13_off = off;   off += align256(nz * 2);
   L.h32_off = off;    off += align256(nd * d_ff * sizeof(float));
   L.xq2_off = off;    off += align256(nz * d_ff * 2);
-  L.xs2_off = off;    off += align256(nz * (d_ff / 32) * 2);
+  L.xs2_off = off;    off += align256(nz * 2);
+  L.hmax_off = off;   off += align256(nz * sizeof(uint32_t));
   L.total = off;
   return L;
 }
@@ -325,6 +326,7 @@ hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff,
     db.h32 = (float*)(base + L.h32_off);
     db.xq2 = (uint8_t*)(base + L.xq2_off);
     db.xs2 = (uint8_t*)(base + L.xs2_off);
+    db.hmax = (uint32_t*)(base + L.hmax_off);
     db.y = y;
     err = launch_decode_ffn(x, xd, T, d, d_ff, E, k, w13, w2, r, db, s, events);
     if (err != hipSuccess) return err;

@@ -75,7 +75,7 @@ hipError_t launch_route(const void* x, d2moe_dtype xd, int T, int d, const float
 constexpr int kDecodeMaxTokens = 16;
 struct FwdWorkspace {
   size_t sched_off, h_off, hs_off, y_off, ys_off;
-  size_t elist_off, xq13_off, xs13_off, h32_off, xq2_off, xs2_off;
+  size_t elist_off, xq13_off, xs13_off, h32_off, xq2_off, xs2_off, hmax_off;
   size_t total;
 };
 
@@ -84,6 +84,7 @@ struct DecodeBuffers {
   int32_t* ecount;  // [1]
   uint8_t *xq13, *xs13, *xq2, *xs2;
   float* h32;       // [T*k][d_ff]
+  uint32_t* hmax;   // [T*k+1] largest |h| of each position (binary32 bits)
   float* y;         // [T*k][d]
 };
 
