@@ -10,11 +10,14 @@ layer call: route (gate, top-k, bit lookup, histogram/permutation) plus the
 expert forward (W1/W3 + SwiGLU, W2, combine).
 
 Prints one JSON line.  `value` = tokens per second of the whole step with
-inputs resident in HBM; `roofline` = algorithmic bytes of the dominant kernel
-(W1/W3 expert kernel: packed planes, scales and zeros of every active expert
-up to its largest requested bit-width) per launch over its average duration,
-timed with HIP events on the stream it runs on; `cpu_baseline` = the CPU
-oracle on a bounded sample of the same workload.
+inputs resident in HBM, timed over eager launches (--graph times replays of
+one captured HIP graph per layer step instead; the eager step time is always
+reported as ms_per_step_eager);
+`roofline` = algorithmic bytes of the dominant kernel (W1/W3 expert kernel:
+packed planes, scales and zeros of every active expert up to its largest
+requested bit-width) per launch over its average duration, timed with HIP
+events on the stream it runs on during the eager pass; `cpu_baseline` = the
+CPU oracle on a bounded sample of the same workload.
 """
 import argparse
 import json
@@ -48,6 +51,9 @@ def main():
     ap.add_argument("--layers", type=int, default=8)
     ap.add_argument("--sweep", default="", help="extra batch sizes reported alongside, e.g. 1,4")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of one captured HIP graph per layer step instead of "
+                         "eager launches")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 256 MiB device copy three times (reference for "
                          "hardware byte counters)")
@@ -71,6 +77,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     d, f, E, k, g, b_min, b_max = 4096, 14336, 8, 2, 128, 2, 8
+    use_graphs = args.graph
     NL = args.layers
 
     # ---- resident packed weights, one set per rotating layer ----
@@ -113,6 +120,7 @@ def main():
 
         for i in range(warmup):
             step(i)
+        # eager pass: per-kernel durations from HIP events on the launch stream
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
         for row in evs:            # torch creates the HIP event at its first record
             for ev in row:
@@ -125,7 +133,33 @@ def main():
             step(warmup + i, evs[i] if profile else None)
         t_stop.record()
         torch.cuda.synchronize()
-        ms = t_start.elapsed_time(t_stop) / steps
+        ms_eager = t_start.elapsed_time(t_stop) / steps
+        ms = ms_eager
+        if use_graphs:
+            # one captured step (route + forward) per rotating layer, replayed
+            cur = torch.cuda.current_stream()
+            side = torch.cuda.Stream()
+            side.wait_stream(cur)
+            with torch.cuda.stream(side):
+                for l in range(NL):
+                    step(l)
+            cur.wait_stream(side)
+            torch.cuda.synchronize()
+            graphs = []
+            for l in range(NL):
+                g_ = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g_):
+                    step(l)
+                graphs.append(g_)
+            for i in range(warmup):
+                graphs[i % NL].replay()
+            torch.cuda.synchronize()
+            t_start.record()
+            for i in range(steps):
+                graphs[(warmup + i) % NL].replay()
+            t_stop.record()
+            torch.cuda.synchronize()
+            ms = t_start.elapsed_time(t_stop) / steps
         # algorithmic bytes per layer call from each layer's routing
         alg13, alg2 = [], []
         for l in range(NL):
@@ -134,7 +168,7 @@ def main():
             alg2.append(sum(mwq_bytes(d, f, g, b_min, int(b)) for b in mb))
         per_step13 = [alg13[(warmup + i) % NL] for i in range(steps)]
         per_step2 = [alg2[(warmup + i) % NL] for i in range(steps)]
-        res = dict(T=T, ms_per_step=ms, tokens_per_s=T / (ms * 1e-3),
+        res = dict(T=T, ms_per_step=ms, ms_per_step_eager=ms_eager, tokens_per_s=T / (ms * 1e-3),
                    layer_bytes=float(np.mean([a + b for a, b in zip(per_step13, per_step2)])))
         res["layer_GBps"] = res["layer_bytes"] / (ms * 1e-3) / 1e9
         if profile:
@@ -166,6 +200,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(main_res["ms_per_step"], 5),
+        "ms_per_step_eager": round(main_res["ms_per_step_eager"], 5),
+        "launch": "hip graph per layer step" if use_graphs else "eager",
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
