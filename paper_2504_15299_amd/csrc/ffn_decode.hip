@@ -287,6 +287,7 @@ struct WaveCtx {
   int bit[2];
   const uint8_t* xq[2];  // activation pieces of group 0, this lane
   int bsc[2];            // their E8M0 scale code
+  uint64_t lmask[2];     // lanes holding a token, per column block
   SigmaConsts k;
   uint32_t lds_pl, lds_sc, lds_z;  // this lane's LDS read addresses in stage 0
 };
@@ -323,21 +324,30 @@ struct BData {
 // registers after that wait so that no use can move above it.  The "memory"
 // clobber keeps their issue order fixed relative to the DMA instructions,
 // which the wait counts rely on.
-__device__ inline v4i gload16(const uint8_t* p) {
-  v4i v;
-  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
-  return v;
+// Only the lanes in `m` load (EXEC is narrowed and restored inside the asm);
+// the other lanes keep `v`.  `m` always contains lane 0, so the instruction
+// is always issued and counted by vmcnt.
+__device__ inline void gload16(v4i& v, const uint8_t* p, uint64_t m) {
+  uint64_t saved;
+  asm volatile(
+      "s_and_saveexec_b64 %1, %3\n\t"
+      "global_load_dwordx4 %0, %2, off\n\t"
+      "s_mov_b64 exec, %1"
+      : "+v"(v), "=&s"(saved)
+      : "v"(p), "s"(m)
+      : "memory");
 }
 
-// Two memory instructions per column block; lanes without a token read the
-// all-zero activation slot, so the count never depends on the lane.
+// Two memory instructions per column block, issued by the lanes that hold a
+// token (lane 0 always does); the other lanes keep the zeros they were given
+// before the loop.
 __device__ inline void load_b(BData& t, const WaveCtx& c, int g) {
 #pragma unroll
   for (int cb = 0; cb < 2; ++cb) {
     if (cb >= c.ncb) continue;  // wave-uniform
     const uint8_t* src = c.xq[cb] + (size_t)g * 256;
-    t.lo[cb] = gload16(src);
-    t.hi[cb] = gload16(src + 16);
+    gload16(t.lo[cb], src, c.lmask[cb]);
+    gload16(t.hi[cb], src + 16, c.lmask[cb]);
   }
 }
 
@@ -483,6 +493,10 @@ __device__ inline void decode_groups(const WaveCtx& c, uint8_t* ring, int g0, in
   if (g0 >= g1) return;
   constexpr int ND = dma_ops<MB>(), NB = 2 * NCB;
   BData B[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) B[i].lo[cb] = B[i].hi[cb] = v4i{0, 0, 0, 0};
   dma_group<MB>(c, g0, ring);
   if (g0 + 1 < g1) dma_group<MB>(c, g0 + 1, ring + kStage);
   load_b(B[0], c, g0);
@@ -569,6 +583,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(3))) vo
     const size_t base = ((size_t)src * NG) * 2 + piece;  // group 0
     c.xq[cb] = Xq + base * 128 + c.q * 32;
     c.bsc[cb] = Xs[src * 2 + piece];
+    c.lmask[cb] = __ballot(validj[cb]);
   }
   // the bit-widths and activation scale codes are needed only inside the group
   // loop; consuming them here
