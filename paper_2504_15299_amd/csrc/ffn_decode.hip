@@ -35,6 +35,9 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 constexpr int G = 128;  // group size served by this path (one MFMA K)
+// A decode work item covers at most kDecodeCols tokens: the 16 MFMA columns
+// hold each token's hi and lo activation pieces.
+constexpr int kDecodeCols = 8;
 
 // ---- fp8 e4m3 (OCP), round to nearest even; |a| <= 448 assumed ----------
 __device__ inline uint32_t e4m3_rne(float v) {
@@ -103,9 +106,10 @@ __device__ inline int row_scale_exp(float amax) {
 // 4j..4j+3 of a 16-byte run hold hardware k = 4j..4j+3, i.e. logical columns
 // 32q + 4n + d for n = 4j'..4j'+3 (fixed d), so each thread reads four
 // columns at stride 4 and stores one dword per piece.  The zero-slot
-// workgroup of slice 0 also writes the active-expert list of the decode
-// kernels when `elist` is given: elist[4 i] = expert, first position, end
-// position, largest bit-width.
+// workgroup of slice 0 also writes the work list of the decode kernels when
+// `elist` is given: each active expert's positions in runs of at most
+// kDecodeCols, elist[4 i] = expert, first position, end position, the
+// expert's largest bit-width.
 template <typename TIN>
 __device__ inline float row_absmax(const TIN* row, int K);
 template <>
@@ -149,11 +153,14 @@ __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
     int n = 0;
     for (int e = 0; e < E; ++e) {
       if (maxbit[e] == 0) continue;
-      elist[4 * n] = e;
-      elist[4 * n + 1] = offsets[e * L];
-      elist[4 * n + 2] = offsets[e * L + L];
-      elist[4 * n + 3] = maxbit[e];
-      ++n;
+      const int lo = offsets[e * L], hi = offsets[e * L + L];
+      for (int p = lo; p < hi; p += kDecodeCols) {
+        elist[4 * n] = e;
+        elist[4 * n + 1] = p;
+        elist[4 * n + 2] = min(p + kDecodeCols, hi);
+        elist[4 * n + 3] = maxbit[e];
+        ++n;
+      }
     }
     *ecount = n;
   }
@@ -283,11 +290,11 @@ struct WaveCtx {
   const uint8_t* sc;   // scales of group 0 (bytes)
   const uint8_t* zp;   // zero points of group 0
   int pl_step, sc_step;  // bytes per group
-  int lane, q, j, ncb;
-  int bit[2];
-  const uint8_t* xq[2];  // activation pieces of group 0, this lane
-  int bsc[2];            // their E8M0 scale code
-  uint64_t lmask[2];     // lanes holding a token, per column block
+  int lane, q, j;
+  int bit;               // bit-width of this lane's token (0: no token)
+  const uint8_t* xq;     // activation pieces of group 0, this lane
+  int bsc;               // their E8M0 scale code
+  uint64_t lmask;        // lanes holding a token
   SigmaConsts k;
   uint32_t lds_pl, lds_sc, lds_z;  // this lane's LDS read addresses in stage 0
 };
@@ -313,7 +320,7 @@ __device__ inline void dma_group(const WaveCtx& c, int g, uint8_t* st) {
 }
 
 struct BData {
-  v4i lo[2], hi[2];  // activation pieces per column block (32 bytes per lane)
+  v4i lo, hi;  // this lane's 32 bytes of activation pieces
 };
 
 // Activation loads are issued as inline assembly for the same reason as the
@@ -338,31 +345,20 @@ __device__ inline void gload16(v4i& v, const uint8_t* p, uint64_t m) {
       : "memory");
 }
 
-// Two memory instructions per column block, issued by the lanes that hold a
-// token (lane 0 always does); the other lanes keep the zeros they were given
-// before the loop.
+// Two memory instructions, issued by the lanes that hold a token (lane 0
+// always does); the other lanes keep the zeros they were given before the
+// loop.
 __device__ inline void load_b(BData& t, const WaveCtx& c, int g) {
-#pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
-    if (cb >= c.ncb) continue;  // wave-uniform
-    const uint8_t* src = c.xq[cb] + (size_t)g * 256;
-    gload16(t.lo[cb], src, c.lmask[cb]);
-    gload16(t.hi[cb], src + 16, c.lmask[cb]);
-  }
+  const uint8_t* src = c.xq + (size_t)g * 256;
+  gload16(t.lo, src, c.lmask);
+  gload16(t.hi, src + 16, c.lmask);
 }
 
 // Called after the wait that covers the loads of `t`.
-__device__ inline void ready_b(BData& t, const WaveCtx& c) {
-#pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
-    if (cb >= c.ncb) continue;  // wave-uniform
-    asm volatile("" : "+v"(t.lo[cb]), "+v"(t.hi[cb]));
-  }
-}
+__device__ inline void ready_b(BData& t) { asm volatile("" : "+v"(t.lo), "+v"(t.hi)); }
 
-__device__ inline v8i b8(const BData& t, int cb) {
-  const v4i l = t.lo[cb], h = t.hi[cb];
-  return v8i{l[0], l[1], l[2], l[3], h[0], h[1], h[2], h[3]};
+__device__ inline v8i b8(const BData& t) {
+  return v8i{t.lo[0], t.lo[1], t.lo[2], t.lo[3], t.hi[0], t.hi[1], t.hi[2], t.hi[3]};
 }
 
 // LDS reads of a ring stage are issued as inline assembly: the compiler's
@@ -424,7 +420,7 @@ __device__ inline void read_stage(const WaveCtx& c, uint32_t (&w)[MB], uint2 (&s
 // leaves at most ~1e-33 (|x| < 2^9 per fp8 piece, 128 terms) in place of an
 // exact zero.
 template <int MB, int SOFF>
-__device__ inline void compute_group(const BData& t, const WaveCtx& c, v4f (&acc)[2]) {
+__device__ inline void compute_group(const BData& t, const WaveCtx& c, v4f& acc) {
   const SigmaConsts& k = c.k;
   uint32_t w[MB];
   uint2 sw[MB - 1];
@@ -432,35 +428,24 @@ __device__ inline void compute_group(const BData& t, const WaveCtx& c, v4f (&acc
   read_stage<MB, SOFF>(c, w, sw, z);
   const v8i a0 = expand_sigma(w[0], k), a1 = expand_sigma(w[1], k);
   const v8i au = zero_operand(z);
-  v8i bb[2];
-#pragma unroll
-  for (int cb = 0; cb < 2; ++cb)
-    if (cb < c.ncb) bb[cb] = b8(t, cb);
+  const v8i bb = b8(t);
   float s1[4];
   scales4(sw[0], s1);
+  // base: sum_k x_k (1.5 - Q_k) + sum_k x_k (z - 1.5), accumulated in place
+  v4f m = mfma_fp4_fp8(au, bb, 127, c.bsc);
+  m = mfma_fp4_fp8(a0, bb, m, 127, c.bsc);
+  m = mfma_fp4_fp8(a1, bb, m, 128, c.bsc);
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
-    if (cb >= c.ncb) continue;  // wave-uniform
-    // base: sum_k x_k (1.5 - Q_k) + sum_k x_k (z - 1.5), accumulated in place
-    v4f m = mfma_fp4_fp8(au, bb[cb], 127, c.bsc[cb]);
-    m = mfma_fp4_fp8(a0, bb[cb], m, 127, c.bsc[cb]);
-    m = mfma_fp4_fp8(a1, bb[cb], m, 128, c.bsc[cb]);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-s1[r], m[r], acc[cb][r]);
-  }
+  for (int r = 0; r < 4; ++r) acc[r] = fmaf(-s1[r], m[r], acc[r]);
 #pragma unroll
   for (int p = 2; p < MB; ++p) {
     const v8i ap = expand_sigma(w[p], k);
     float sp[4];
     scales4(sw[p - 1], sp);
+    const int bs = p < c.bit ? c.bsc : 0;
+    const v4f d = mfma_fp4_fp8(ap, bb, 128, bs);
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
-      if (cb >= c.ncb) continue;  // wave-uniform
-      const int bs = p < c.bit[cb] ? c.bsc[cb] : 0;
-      const v4f d = mfma_fp4_fp8(ap, bb[cb], 128, bs);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-sp[r], d[r], acc[cb][r]);
-    }
+    for (int r = 0; r < 4; ++r) acc[r] = fmaf(-sp[r], d[r], acc[r]);
   }
 }
 
@@ -486,17 +471,14 @@ __device__ inline void wait_vm() {
 // activations of g ready.  The DMA of g+3 overwrites the stage of g-1, whose
 // LDS reads completed in the previous step.  The loop is unrolled by kDepth
 // so every stage offset is a constant.
-template <int MB, int NCB>
-__device__ inline void decode_groups(const WaveCtx& c, uint8_t* ring, int g0, int g1,
-                                     v4f (&acc)[2]) {
+template <int MB>
+__device__ inline void decode_groups(const WaveCtx& c, uint8_t* ring, int g0, int g1, v4f& acc) {
   static_assert(kDepth == 4, "the unrolled step below assumes four stages");
   if (g0 >= g1) return;
-  constexpr int ND = dma_ops<MB>(), NB = 2 * NCB;
+  constexpr int ND = dma_ops<MB>(), NB = 2;
   BData B[2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int cb = 0; cb < 2; ++cb) B[i].lo[cb] = B[i].hi[cb] = v4i{0, 0, 0, 0};
+  for (int i = 0; i < 2; ++i) B[i].lo = B[i].hi = v4i{0, 0, 0, 0};
   dma_group<MB>(c, g0, ring);
   if (g0 + 1 < g1) dma_group<MB>(c, g0 + 1, ring + kStage);
   load_b(B[0], c, g0);
@@ -516,7 +498,7 @@ __device__ inline void decode_groups(const WaveCtx& c, uint8_t* ring, int g0, in
     } else {                                                                 \
       wait_vm<0>();                                                          \
     }                                                                        \
-    ready_b(B[(K) & 1], c);                                                  \
+    ready_b(B[(K) & 1]);                                                     \
     compute_group<MB, ((K) % kDepth) * kStage>(B[(K) & 1], c, acc);          \
   }
   for (int g = g0; g < g1; g += kDepth) {
@@ -528,27 +510,21 @@ __device__ inline void decode_groups(const WaveCtx& c, uint8_t* ring, int g0, in
 #undef D2MOE_STEP
 }
 
-template <int MB>
-__device__ inline void decode_groups_ncb(const WaveCtx& c, uint8_t* ring, int g0, int g1,
-                                         v4f (&acc)[2]) {
-  if (c.ncb == 2)
-    decode_groups<MB, 2>(c, ring, g0, g1, acc);
-  else
-    decode_groups<MB, 1>(c, ring, g0, g1, acc);
-}
 
-// elist[4*i]: expert, first position, end position, largest bit-width.
+// elist[4*i]: expert, first position, end position (at most kDecodeCols
+// positions), largest bit-width of the expert.
 // SwiGLU variant: waves [0, NW/2) stream the W1 row-block, waves [NW/2, NW)
 // the matching W3 row-block, each half splitting the groups; the epilogue
-// combines them through LDS.
+// combines them through LDS (each wave's partial sums go to its own ring,
+// which is idle by then).
 template <bool SWIGLU, int NW>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(3))) void decode_kernel(
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void decode_kernel(
     MwqView W, const int32_t* __restrict__ elist, const int32_t* __restrict__ ecount,
     const int32_t* __restrict__ perm, const uint8_t* __restrict__ topk_bits,
     const uint8_t* __restrict__ Xq, const uint8_t* __restrict__ Xs, int npos, int f,
     float* __restrict__ out, int out_ld, uint32_t* __restrict__ rowmax) {
   __shared__ __attribute__((aligned(16))) uint8_t ring[NW][kDepth * kStage];
-  __shared__ float red[NW][64][8];
+  static_assert(kDepth * kStage >= 64 * 4 * (int)sizeof(float), "partial sums fit the ring");
   const int ei = blockIdx.y;
   if (ei >= *ecount) return;
   const int e = elist[4 * ei], p0 = elist[4 * ei + 1], p1 = elist[4 * ei + 2];
@@ -569,27 +545,23 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(3))) vo
   c.lane = lane;
   c.q = lane >> 4;
   c.j = lane & 15;
-  c.ncb = ncol > 8 ? 2 : 1;
   const int piece = lane & 1;
-  int posj[2];
-  bool validj[2];
-#pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
-    const int t = cb * 8 + (c.j >> 1);
-    validj[cb] = t < ncol;
-    posj[cb] = p0 + t;
-    c.bit[cb] = validj[cb] ? (int)topk_bits[perm[posj[cb]]] : 0;
-    const int src = validj[cb] ? posj[cb] : npos;  // zero slot when no token
+  const int t = c.j >> 1;
+  const bool valid = t < ncol;
+  const int pos = p0 + t;
+  c.bit = valid ? (int)topk_bits[perm[pos]] : 0;
+  {
+    const int src = valid ? pos : npos;  // zero slot when no token
     const size_t base = ((size_t)src * NG) * 2 + piece;  // group 0
-    c.xq[cb] = Xq + base * 128 + c.q * 32;
-    c.bsc[cb] = Xs[src * 2 + piece];
-    c.lmask[cb] = __ballot(validj[cb]);
+    c.xq = Xq + base * 128 + c.q * 32;
+    c.bsc = Xs[src * 2 + piece];
   }
-  // the bit-widths and activation scale codes are needed only inside the group
-  // loop; consuming them here
-  // makes the compiler's wait for their loads happen before the first DMA
-  // (a wait placed after it would drain the weight prefetch)
-  asm volatile("" : "+v"(c.bit[0]), "+v"(c.bit[1]), "+v"(c.bsc[0]), "+v"(c.bsc[1])::"memory");
+  c.lmask = __ballot(valid);
+  // the bit-width and the activation scale code are needed only inside the
+  // group loop; consuming them here makes the compiler's wait for their loads
+  // happen before the first DMA (a wait placed after it would drain the
+  // weight prefetch)
+  asm volatile("" : "+v"(c.bit), "+v"(c.bsc)::"memory");
 
   const int rowblock = rr == 0 ? rb : rb + f / 16;
   const size_t blk0 = W.block(e, rowblock, 0);
@@ -606,64 +578,55 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(3))) vo
     c.lds_z = base + kZeroOff + c.j;
   }
 
-  v4f acc[2];
-  acc[0] = acc[1] = v4f{0.f, 0.f, 0.f, 0.f};
+  v4f acc = v4f{0.f, 0.f, 0.f, 0.f};
   switch (mb) {
-    case 2: decode_groups_ncb<2>(c, ring[wave], g0, g1, acc); break;
-    case 3: decode_groups_ncb<3>(c, ring[wave], g0, g1, acc); break;
-    case 4: decode_groups_ncb<4>(c, ring[wave], g0, g1, acc); break;
-    case 5: decode_groups_ncb<5>(c, ring[wave], g0, g1, acc); break;
-    case 6: decode_groups_ncb<6>(c, ring[wave], g0, g1, acc); break;
-    case 7: decode_groups_ncb<7>(c, ring[wave], g0, g1, acc); break;
-    case 8: decode_groups_ncb<8>(c, ring[wave], g0, g1, acc); break;
+    case 2: decode_groups<2>(c, ring[wave], g0, g1, acc); break;
+    case 3: decode_groups<3>(c, ring[wave], g0, g1, acc); break;
+    case 4: decode_groups<4>(c, ring[wave], g0, g1, acc); break;
+    case 5: decode_groups<5>(c, ring[wave], g0, g1, acc); break;
+    case 6: decode_groups<6>(c, ring[wave], g0, g1, acc); break;
+    case 7: decode_groups<7>(c, ring[wave], g0, g1, acc); break;
+    case 8: decode_groups<8>(c, ring[wave], g0, g1, acc); break;
     default: break;
   }
 
-#pragma unroll
-  for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) red[wave][lane][cb * 4 + r] = acc[cb][r];
+  // every DMA of this wave has completed (the last step waits for all), so
+  // its ring can hold its partial sums
+  float4* red = (float4*)ring[wave];
+  red[lane] = float4{acc[0], acc[1], acc[2], acc[3]};
   __syncthreads();
   if (wave != 0) return;
   constexpr int NRR = SWIGLU ? 2 : 1;
-  float v[NRR][2][4];
+  float v[NRR][4];
 #pragma unroll
-  for (int h = 0; h < NRR; ++h)
-#pragma unroll
-    for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float sum = 0.0f;
-        for (int w = 0; w < KS; ++w) sum += red[h * KS + w][lane][cb * 4 + r];
-        v[h][cb][r] = sum + __shfl_xor(sum, 1, 64);  // hi + lo pieces
-      }
-#pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
-    if (cb >= c.ncb || !validj[cb] || piece != 0) continue;
-    float* dst = out + (size_t)posj[cb] * out_ld + rb * 16 + 4 * c.q;
-    float o[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      o[r] = SWIGLU ? silu(v[0][cb][r]) * v[NRR - 1][cb][r] : v[0][cb][r];
-    *(float4*)dst = float4{o[0], o[1], o[2], o[3]};
+  for (int h = 0; h < NRR; ++h) {
+    float4 sum = float4{0.f, 0.f, 0.f, 0.f};
+    for (int w = 0; w < KS; ++w) {
+      const float4 part = ((const float4*)ring[h * KS + w])[lane];
+      sum.x += part.x; sum.y += part.y; sum.z += part.z; sum.w += part.w;
+    }
+    v[h][0] = sum.x + __shfl_xor(sum.x, 1, 64);  // hi + lo pieces
+    v[h][1] = sum.y + __shfl_xor(sum.y, 1, 64);
+    v[h][2] = sum.z + __shfl_xor(sum.z, 1, 64);
+    v[h][3] = sum.w + __shfl_xor(sum.w, 1, 64);
   }
+  float o[4];
+  float m = 0.0f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    o[r] = SWIGLU ? silu(v[0][r]) * v[NRR - 1][r] : v[0][r];
+    m = fmaxf(m, fabsf(o[r]));
+  }
+  if (valid && piece == 0)
+    *(float4*)(out + (size_t)pos * out_ld + rb * 16 + 4 * c.q) = float4{o[0], o[1], o[2], o[3]};
   if (rowmax) {
     // largest |output| of each position, for the scale of its fp8 pieces:
     // max over this lane's rows, then over the four lanes (q) of the token
-#pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
-      if (cb >= c.ncb) continue;  // wave-uniform
-      float m = 0.0f;
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        m = fmaxf(m, fabsf(SWIGLU ? silu(v[0][cb][r]) * v[NRR - 1][cb][r] : v[0][cb][r]));
-      m = fmaxf(m, __shfl_xor(m, 16, 64));
-      m = fmaxf(m, __shfl_xor(m, 32, 64));
-      if (validj[cb] && piece == 0 && c.q == 0) atomicMax(rowmax + posj[cb], __float_as_uint(m));
-    }
+    m = fmaxf(m, __shfl_xor(m, 16, 64));
+    m = fmaxf(m, __shfl_xor(m, 32, 64));
+    if (valid && piece == 0 && c.q == 0) atomicMax(rowmax + pos, __float_as_uint(m));
   }
 }
-
 
 template <typename TIN>
 hipError_t run_xprep(const TIN* in, int in_ld, const int32_t* perm, int kdiv, int npos, int K,
@@ -700,7 +663,8 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
     err = run_xprep<float>((const float*)x, d, r->perm, k, npos, d, nullptr, b.xq13, b.xs13, r,
                            E, L, b.elist, b.ecount, b.hmax, s);
   if (err != hipSuccess) return err;
-  const int ny = E < npos ? E : npos;
+  // work items: each active expert's positions in runs of kDecodeCols
+  const int ny = (E < npos ? E : npos) + (npos + kDecodeCols - 1) / kDecodeCols;
   const MwqView W13 = view_of(w13), W2 = view_of(w2);
   if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
   decode_kernel<true, kDecodeWaves><<<dim3(d_ff / 16, ny), 64 * kDecodeWaves, 0, s>>>(

@@ -285,7 +285,8 @@ FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shar
   L.y_off = off;      off += align256(sizeof(float) * (size_t)T * k * d);
   L.ys_off = off;     off += align256(sizeof(float) * (size_t)T * (shared_d_ff > 0 ? d : 0));
   const size_t nd = T <= kDecodeMaxTokens ? (size_t)T * k : 0;  // decode positions
-  L.elist_off = off;  off += align256(sizeof(int32_t) * ((size_t)E * 4 + 4));
+  // decode work list: at most one run per active expert plus one per 8 positions
+  L.elist_off = off;  off += align256(sizeof(int32_t) * (4 * ((size_t)E + (nd + 7) / 8) + 4));
   const size_t nz = nd ? nd + 1 : 0;  // plus one all-zero activation slot
   L.xq13_off = off;   off += align256(nz * d * 2);
   L.xs13_off = off;   off += align256(nz * 2);
@@ -320,7 +321,7 @@ hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff,
   if (decode_path_ok(w13, w2, T)) {
     DecodeBuffers db;
     db.elist = (int32_t*)(base + L.elist_off);
-    db.ecount = db.elist + (size_t)E * 4;
+    db.ecount = db.elist + 4 * ((size_t)E + ((size_t)T * k + 7) / 8);
     db.xq13 = (uint8_t*)(base + L.xq13_off);
     db.xs13 = (uint8_t*)(base + L.xs13_off);
     db.h32 = (float*)(base + L.h32_off);
