@@ -274,13 +274,24 @@ __device__ inline void scales4(uint2 s, float (&out)[4]) {
   out[3] = h2f((uint16_t)(s.y >> 16));
 }
 
-// Per-wave LDS ring for the weight stream: one stage holds one group's
-// planes (up to 8 x 256 B), its scales (up to 7 levels x 16 rows x 2 B) and
-// its 16 zero points, copied from global memory by the LDS DMA engine so that
-// data in flight costs no registers.
-constexpr int kStage = 2304;            // bytes per stage
+// Per-wave LDS ring for the weight stream.  One stage holds one group of the
+// wave's 16 rows at MB planes, packed as [planes MB x 256 B][scales
+// (MB-1) x 32 B][zero points 16 B], copied from global memory by the LDS DMA
+// engine so that data in flight costs no registers.  Each DMA instruction
+// moves 16 bytes per lane into consecutive LDS addresses; lane slot s of the
+// stage (s = 64 i + lane for instruction i) fetches plane bytes for
+// s < 16 MB, scale bytes for the next 2 (MB-1) slots and the zero points in
+// the last one, each from its own array.
+constexpr int kStage = 2304;            // bytes per stage (>= 18 x 128 - 16)
 constexpr int kDepth = 4;               // stages: the DMA runs kDepth-1 groups ahead
-constexpr int kScaleOff = 2048, kZeroOff = 2272;
+
+template <int MB>
+struct StageLayout {
+  static constexpr int scale_off = 256 * MB;
+  static constexpr int zero_off = scale_off + 32 * (MB - 1);
+  static constexpr int slots = 18 * MB - 1;
+  static constexpr int ops = (slots + 63) / 64;  // DMA instructions per group
+};
 
 #define D2MOE_GPTR(p) ((__attribute__((address_space(1))) void*)(p))
 #define D2MOE_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
@@ -296,27 +307,53 @@ struct WaveCtx {
   int bsc;               // their E8M0 scale code
   uint64_t lmask;        // lanes holding a token
   SigmaConsts k;
-  uint32_t lds_pl, lds_sc, lds_z;  // this lane's LDS read addresses in stage 0
+  uint32_t lds_pl, lds_sc, lds_z;  // this lane's LDS read bases in stage 0
 };
 
-// Number of memory instructions one group's DMA issues (planes, scales, zeros).
+// Source of each DMA instruction's 16 bytes for this lane: the address for
+// group 0 and the stride per group (0 for lanes past the last slot, which
+// do not issue).
 template <int MB>
-constexpr int dma_ops() { return (MB > 4 ? 2 : 1) + 2; }
+struct DmaPlan {
+  const uint8_t* a0[StageLayout<MB>::ops];
+  int step[StageLayout<MB>::ops];
+};
 
 template <int MB>
-__device__ inline void dma_group(const WaveCtx& c, int g, uint8_t* st) {
-  const uint8_t* gp = c.pl + (size_t)g * c.pl_step;
-  if (c.lane < (MB > 4 ? 4 : MB) * 16)
-    __builtin_amdgcn_global_load_lds(D2MOE_GPTR(gp + 16 * c.lane), D2MOE_LPTR(st), 16, 0, 0);
-  if (MB > 4 && c.lane < (MB - 4) * 16)
-    __builtin_amdgcn_global_load_lds(D2MOE_GPTR(gp + 1024 + 16 * c.lane),
-                                     D2MOE_LPTR(st + 1024), 16, 0, 0);
-  if (c.lane < 2 * (MB - 1))
-    __builtin_amdgcn_global_load_lds(D2MOE_GPTR(c.sc + (size_t)g * c.sc_step + 16 * c.lane),
-                                     D2MOE_LPTR(st + kScaleOff), 16, 0, 0);
-  if (c.lane == 0)
-    __builtin_amdgcn_global_load_lds(D2MOE_GPTR(c.zp + (size_t)g * 16), D2MOE_LPTR(st + kZeroOff),
-                                     16, 0, 0);
+__device__ inline DmaPlan<MB> dma_plan(const WaveCtx& c) {
+  using SL = StageLayout<MB>;
+  DmaPlan<MB> d;
+#pragma unroll
+  for (int i = 0; i < SL::ops; ++i) {
+    const int s = 64 * i + c.lane;
+    if (s < 16 * MB) {
+      d.a0[i] = c.pl + 16 * s;
+      d.step[i] = c.pl_step;
+    } else if (s < 16 * MB + 2 * (MB - 1)) {
+      d.a0[i] = c.sc + 16 * (s - 16 * MB);
+      d.step[i] = c.sc_step;
+    } else if (s == SL::slots - 1) {
+      d.a0[i] = c.zp;
+      d.step[i] = 16;
+    } else {
+      d.a0[i] = c.pl;
+      d.step[i] = 0;
+    }
+  }
+  return d;
+}
+
+template <int MB>
+__device__ inline void dma_group(const DmaPlan<MB>& d, const WaveCtx& c, int g, uint8_t* st) {
+  using SL = StageLayout<MB>;
+#pragma unroll
+  for (int i = 0; i < SL::ops; ++i) {
+    // every instruction has lane 0 active (slot 64 i < slots), so each one
+    // issues and is counted by vmcnt
+    if (64 * i + c.lane < SL::slots)
+      __builtin_amdgcn_global_load_lds(D2MOE_GPTR(d.a0[i] + (size_t)g * d.step[i]),
+                                       D2MOE_LPTR(st + 1024 * i), 16, 0, 0);
+  }
 }
 
 struct BData {
@@ -393,7 +430,7 @@ struct StageReader {
   static __device__ inline void run(uint32_t pa, uint32_t sa, uint32_t (&w)[MB],
                                     uint2 (&sc)[MB - 1]) {
     w[P] = lds_rd32<SOFF + P * 256>(pa);
-    if constexpr (P + 1 < MB) sc[P] = lds_rd64<SOFF + P * 32>(sa);
+    if constexpr (P + 1 < MB) sc[P] = lds_rd64<SOFF + StageLayout<MB>::scale_off + P * 32>(sa);
     StageReader<P + 1, MB, SOFF>::run(pa, sa, w, sc);
   }
 };
@@ -406,7 +443,7 @@ template <int MB, int SOFF>
 __device__ inline void read_stage(const WaveCtx& c, uint32_t (&w)[MB], uint2 (&sc)[MB - 1],
                                   uint32_t& z) {
   StageReader<0, MB, SOFF>::run(c.lds_pl, c.lds_sc, w, sc);
-  z = lds_rdu8<SOFF>(c.lds_z);
+  z = lds_rdu8<SOFF + StageLayout<MB>::zero_off>(c.lds_z);
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
   for (int p = 0; p < MB; ++p) asm volatile("" : "+v"(w[p]));
@@ -475,21 +512,22 @@ template <int MB>
 __device__ inline void decode_groups(const WaveCtx& c, uint8_t* ring, int g0, int g1, v4f& acc) {
   static_assert(kDepth == 4, "the unrolled step below assumes four stages");
   if (g0 >= g1) return;
-  constexpr int ND = dma_ops<MB>(), NB = 2;
+  constexpr int ND = StageLayout<MB>::ops, NB = 2;
+  const DmaPlan<MB> plan = dma_plan<MB>(c);
   BData B[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) B[i].lo = B[i].hi = v4i{0, 0, 0, 0};
-  dma_group<MB>(c, g0, ring);
-  if (g0 + 1 < g1) dma_group<MB>(c, g0 + 1, ring + kStage);
+  dma_group<MB>(plan, c, g0, ring);
+  if (g0 + 1 < g1) dma_group<MB>(plan, c, g0 + 1, ring + kStage);
   load_b(B[0], c, g0);
-  if (g0 + 2 < g1) dma_group<MB>(c, g0 + 2, ring + 2 * kStage);
+  if (g0 + 2 < g1) dma_group<MB>(plan, c, g0 + 2, ring + 2 * kStage);
 #define D2MOE_STEP(K)                                                        \
   {                                                                          \
     const int gg = g + (K);                                                  \
     if (gg >= g1) break;                                                     \
     if (gg + 1 < g1) load_b(B[((K) + 1) & 1], c, gg + 1);                    \
     if (gg + 3 < g1) {                                                       \
-      dma_group<MB>(c, gg + 3, ring + (((K) + 3) % kDepth) * kStage);        \
+      dma_group<MB>(plan, c, gg + 3, ring + (((K) + 3) % kDepth) * kStage);  \
       wait_vm<2 * ND + NB>();                                                \
     } else if (gg + 2 < g1) {                                                \
       wait_vm<ND + NB>();                                                    \
@@ -574,8 +612,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   {
     const uint32_t base = lds_addr(ring[wave]);
     c.lds_pl = base + 4 * lane;
-    c.lds_sc = base + kScaleOff + 8 * c.q;
-    c.lds_z = base + kZeroOff + c.j;
+    c.lds_sc = base + 8 * c.q;
+    c.lds_z = base + c.j;
   }
 
   v4f acc = v4f{0.f, 0.f, 0.f, 0.f};
