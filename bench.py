@@ -31,6 +31,7 @@ sys.path.insert(0, ROOT)
 METRIC = ("MoE-layer tokens/s + achieved HBM GB/s (fraction of peak) at mixed 2/3/4/8-bit "
           "experts")
 HBM_PEAK_GBPS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
 def mwq_bytes(rows, cols, group, b_min, bits):
@@ -51,6 +52,8 @@ def main():
     ap.add_argument("--layers", type=int, default=8)
     ap.add_argument("--sweep", default="", help="extra batch sizes reported alongside, e.g. 1,4")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--prefill-steps", type=int, default=5,
+                    help="also time the 2048-token prefill of the same layers (0: skip)")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of one captured HIP graph per layer step instead of "
                          "eager launches")
@@ -181,11 +184,68 @@ def main():
             res["w13_bytes"] = float(np.mean(per_step13))
         return res
 
+    def run_prefill(steps, warmup):
+        """Prefill of the same layers: 2048 tokens from 4 requests of 512,
+        per-request bit tables from {2,4,8}, gate bias ln p_e with
+        p_e ~ (e+1)^-1.1 so that expert load follows Zipf(1.1).  Returns the
+        step time and the expert GEMMs' rate in algorithmic TFLOP/s
+        (2 * 3 * d * d_ff per routed token, the W1/W3 and W2 kernels timed
+        with HIP events)."""
+        T, R = 2048, 4
+        rng = np.random.default_rng(3)
+        x = torch.from_numpy(rng.standard_normal((T, d), dtype=np.float32)).to(dev).to(torch.bfloat16)
+        req = torch.from_numpy((np.arange(T) // (T // R)).astype(np.int32)).to(dev)
+        p = (np.arange(E) + 1.0) ** -1.1
+        bias = torch.from_numpy(np.log(p / p.sum()).astype(np.float32)).to(dev)
+        tables = [torch.from_numpy(rng.choice(np.array([2, 4, 8], np.uint8), size=(R, E))).to(dev)
+                  for _ in range(NL)]
+        routs = [api.Routing.empty(T, E, k, b_min, b_max, device=dev) for _ in range(NL)]
+        out = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+        ws = torch.empty(api.moe_forward_workspace(T, d, f, E, k), dtype=torch.uint8, device=dev)
+
+        def step(i, events=None):
+            l = i % NL
+            w13, w2, Wg = layers[l]
+            api.route(x, Wg, bias, k, req, tables[l], b_min, b_max, out=routs[l])
+            api.moe_forward(x, w13, w2, routs[l], k, out=out, workspace=ws, events=events)
+
+        for i in range(warmup):
+            step(i)
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+        for row in evs:
+            for ev in row:
+                ev.record()
+        torch.cuda.synchronize()
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_stop = torch.cuda.Event(enable_timing=True)
+        t_start.record()
+        for i in range(steps):
+            step(warmup + i, evs[i])
+        t_stop.record()
+        torch.cuda.synchronize()
+        ms = t_start.elapsed_time(t_stop) / steps
+        d13 = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+        d2 = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+        flop13 = 2.0 * 2 * d * f * T * k
+        flop2 = 2.0 * d * f * T * k
+        hist = routs[(warmup + steps - 1) % NL].hist.cpu().numpy().sum(axis=1)
+        return {"tokens": T, "ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms * 1e-3), 1),
+                "w13_ms": round(d13, 4), "w2_ms": round(d2, 4),
+                "w13_TFLOPs": round(flop13 / (d13 * 1e-3) / 1e12, 1),
+                "w2_TFLOPs": round(flop2 / (d2 * 1e-3) / 1e12, 1),
+                "expert_TFLOPs": round((flop13 + flop2) / ((d13 + d2) * 1e-3) / 1e12, 1),
+                "mfma_peak_TFLOPs": MFMA_BF16_PEAK_TFLOPS,
+                "mfma_frac": round((flop13 + flop2) / ((d13 + d2) * 1e-3) / 1e12
+                                   / MFMA_BF16_PEAK_TFLOPS, 4),
+                "expert_load": [int(v) for v in hist]}
+
     main_res = run_batch(args.batch, args.steps, args.warmup, profile=True)
     sweep = []
     for T in [int(v) for v in args.sweep.split(",") if v.strip()]:
         r = run_batch(T, max(args.steps // 2, 5), args.warmup, profile=True)
         sweep.append({kk: (round(v, 4) if isinstance(v, float) else v) for kk, v in r.items()})
+
+    prefill = run_prefill(args.prefill_steps, 2) if args.prefill_steps > 0 else None
 
     cpu = None
     if not args.no_cpu:
@@ -225,6 +285,7 @@ def main():
         "w2_kernel": {"achieved": round(main_res["w2_GBps"], 1), "avg_ms": round(main_res["w2_ms"], 5),
                       "traffic": traffic[1]},
         "sweep": sweep,
+        "prefill": prefill,
         "cpu_baseline": cpu,
         "pack_seconds": round(pack_s, 2),
     }
