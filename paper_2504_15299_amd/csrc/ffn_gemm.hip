@@ -3,8 +3,8 @@
 // weighted combine (Fig. 1: outputs of the activated experts weighted by the
 // gate).
 //
-// Work is cut into tiles of (expert, bit-width bucket, 64 positions, 64
-// output rows).  Positions are the (token, slot) pairs sorted by (expert,
+// Work is cut into tiles of (expert, bit-width bucket, 256 positions, 128
+// output rows), one 512-thread workgroup each.  Positions are the (token, slot) pairs sorted by (expert,
 // bit-width), so every tile reads its expert's planes 0..b-1 only.  Per K step
 // (one quantization group) the workgroup stages the gathered activations and
 // the dequantized weight tile as bf16 in LDS and runs v_mfma_f32_16x16x32_bf16
@@ -19,7 +19,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int BM = 64, BN = 64, kThreads = 256;
+constexpr int BM = 256, BN = 128, KS = 64, kThreads = 512;
 
 // Bucket table produced on the device from the routing histogram.
 struct Sched {
@@ -48,26 +48,52 @@ __global__ void schedule_kernel(const int32_t* __restrict__ hist,
 
 __device__ inline float silu(float a) { return a / (1.0f + __expf(-a)); }
 
-template <typename T>
-__device__ inline float ld_in(const T* p);
-template <>
-__device__ inline float ld_in<float>(const float* p) { return *p; }
-template <>
-__device__ inline float ld_in<uint16_t>(const uint16_t* p) { return bf2f(*p); }
 
-// in:  activations, row r of the tile reads in[src_row(pos) * in_ld + k]
-//      with src_row = perm ? perm[pos] / kdiv : pos
-// SWIGLU: W is [2f][K] (w13), output h[pos][n] bf16, n in [0, f)
-// else:   W is [N][K], output y[pos][n] f32
-template <int G, bool SWIGLU, typename TIN>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(const TIN* __restrict__ in, int in_ld,
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef float f2 __attribute__((ext_vector_type(2)));
+typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+
+__device__ inline h2 as_h2(uint32_t v) { return __builtin_bit_cast(h2, v); }
+__device__ inline uint32_t as_u(h2 v) { return __builtin_bit_cast(uint32_t, v); }
+__device__ inline uint32_t h2_to_bf2(h2 v) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(__builtin_convertvector(v, f2), b2));
+}
+__device__ inline uint32_t h2_splat(float v) {
+  const _Float16 h = (_Float16)v;
+  return as_u(h2{h, h});
+}
+
+// Tiles in LDS are [rows][KS] bf16 (128 bytes per row) with the 16-byte
+// chunks of a row stored at chunk ^ (row & 7), so that the 16 rows an MFMA
+// operand reads spread over the banks.
+__device__ inline int swz(int row, int chunk) { return row * KS + ((chunk ^ (row & 7)) << 3); }
+
+// Grouped expert GEMM: one workgroup computes BM positions x BN weight rows
+// of one (expert, bit-width) bucket.
+//   in:  bf16 activations, position p reads in[src_row(p) * in_ld + k] with
+//        src_row = perm ? perm[p] / kdiv : p
+//   SWIGLU: W is [2f][K] (w13); the tile holds 64 rows of W1 and the same 64
+//           rows of W3 interleaved in 16-row slices, out = h [pos][f] bf16
+//   else:   W is [N][K], out = y [pos][N] fp32
+// Per K step (KS columns): the activations and the plane words, scales and
+// zero points of the next step are loaded into registers while the MFMAs of
+// the current step run; then each thread dequantizes 16 weights of one row
+// into LDS.  Dequantization works on pairs of weights (j, j + 16) of a plane
+// word in packed fp16: shifting the word left by 15 - j puts bit j at bit 15
+// and bit j + 16 at bit 31, the sign positions of the two halves, and v_bfi
+// turns the pair into (+-c_p, +-c_p).  With every plane read as a sign,
+//   W^_b = s1 (Q - z) + sum_{p>=b_min} s_p sigma_p
+//        = C + sum_{p<b} c_p (2 bit_p - 1),  c_p = s1 2^(p-1) for p < b_min,
+//          c_p = s_p for p >= b_min,  C = s1 ((2^b_min - 1) / 2 - z),
+// accumulated in fp16 from C, then rounded to bf16 for the MFMA.
+template <int G, bool SWIGLU>
+__global__ __launch_bounds__(kThreads) void gemm_kernel(const uint16_t* __restrict__ in, int in_ld,
                                                         const int32_t* __restrict__ perm, int kdiv,
                                                         MwqView W, int expert_fixed, Sched sc,
-                                                        int f, void* __restrict__ out,
+                                                        int f, int N, void* __restrict__ out,
                                                         int out_ld) {
-  constexpr int LDK = G + 8;  // padded LDS row (bf16 elements)
-  __shared__ __attribute__((aligned(16))) uint16_t xs[BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t ws[BN * LDK];
+  __shared__ __attribute__((aligned(16))) uint16_t xs[BM * KS];
+  __shared__ __attribute__((aligned(16))) uint16_t ws[BN * KS];
   __shared__ int s_info[4];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -105,133 +131,165 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const TIN* __restrict__ 
   const int expert = sc.nb == 0 ? expert_fixed : (s_info[0] >> 1);
   const int pos0 = s_info[1], cnt = s_info[2], bits = s_info[3];
   const int n0 = blockIdx.y * (SWIGLU ? BN / 2 : BN);  // first output row
-  const int K = W.cols, BR = W.BR();
+  const int K = W.cols, BR = W.BR(), b_min = W.b_min;
 
-  f32x4 acc[2][2];
-  for (int a = 0; a < 2; ++a)
-    for (int b = 0; b < 2; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // source row of each staged activation row (fixed over K)
-  const int xm = tid >> 2, xpart = tid & 3;  // 64 rows x 4 parts
-  long src_row = -1;
-  if (xm < cnt) {
-    const int pos = pos0 + xm;
-    src_row = perm ? (long)(perm[pos] / kdiv) : (long)pos;
+  // ---- activation loader: row xr, 16-byte chunks 4 xh .. 4 xh + 3 ----
+  const int xr = tid >> 1, xh = tid & 1;
+  const uint16_t* xsrc = nullptr;
+  if (xr < cnt) {
+    const int pos = pos0 + xr;
+    xsrc = in + (size_t)(perm ? perm[pos] / kdiv : pos) * in_ld + 32 * xh;
   }
+  // ---- dequantizer: tile row dc, 32-column word dsub, pairs 8 dh .. 8 dh + 7 ----
+  const int item = tid >> 1, dh = tid & 1;
+  const int dc = item >> 1, dsub = item & 1;
+  int mrow;  // matrix row of tile row dc
+  bool drow_ok;
+  if (SWIGLU) {
+    const int dwn = dc >> 6, cc = dc & 63, sl = cc >> 4;
+    const int hrow = n0 + 32 * dwn + 16 * (sl >> 1) + (cc & 15);
+    drow_ok = hrow < f;
+    mrow = ((sl & 1) ? f : 0) + hrow;
+  } else {
+    mrow = n0 + dc;
+    drow_ok = mrow < N;
+  }
+  const int drb = drow_ok ? mrow / BR : 0, dib = drow_ok ? mrow % BR : 0;
+  uint32_t sh_m;  // opaque copy of the sign mask: keeps v_bfi on registers
+  asm volatile("" : "=v"(sh_m) : "0"(0x80008000u));
 
-  // tile column c (0..63) -> matrix row of W
-  auto tile_row = [&](int c) -> int {
-    if (SWIGLU) {
-      const int w_n = c >> 5, h = (c >> 4) & 1, r = c & 15;
-      return (h ? f : 0) + n0 + 16 * w_n + r;
+  uint4 xreg[4];
+  uint32_t preg[8];
+  uint16_t sreg[8];
+  uint32_t zreg = 0;
+  auto load_step = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      xreg[i] = xsrc ? *(const uint4*)(xsrc + k0 + 8 * i) : uint4{0u, 0u, 0u, 0u};
+    if (drow_ok) {
+      const size_t blk = W.block(expert, drb, k0 / G);
+      const int wq = ((k0 % G) / 32 + dsub) * BR + dib;
+#pragma unroll
+      for (int p = 0; p < 8; ++p)
+        if (p < bits) preg[p] = W.planes[W.plane_word(blk, p, wq)];
+#pragma unroll
+      for (int l = 0; l < 8; ++l)
+        if (l < bits - b_min + 1) sreg[l] = W.scales[W.scale_idx(blk, l, dib)];
+      zreg = W.zeros[W.zero_idx(blk, dib)];
     }
-    return n0 + c;
+  };
+  auto store_step = [&]() {
+    // activations
+    uint4* xd = (uint4*)xs;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) xd[swz(xr, 4 * xh + i) >> 3] = xreg[i];
+    // weights
+    uint32_t lo[4], hi[4];
+    if (drow_ok) {
+      const float s1 = h2f(sreg[0]);
+      uint32_t cp[8];
+#pragma unroll
+      for (int p = 0; p < 8; ++p) {
+        const float c = p < b_min ? s1 * (float)(1 << p) * 0.5f : (p < bits ? h2f(sreg[p - b_min + 1]) : 0.0f);
+        cp[p] = h2_splat(c) & 0x7fff7fffu;
+      }
+      const uint32_t C = h2_splat(s1 * ((float)((1 << b_min) - 1) * 0.5f - (float)zreg));
+      h2 acc[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] = as_h2(C);
+#pragma unroll
+      for (int p = 0; p < 8; ++p) {
+        if (p >= bits) break;  // uniform
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const uint32_t t = preg[p] << (15 - (8 * dh + j));
+          const uint32_t v = (sh_m & t) | (~sh_m & cp[p]);  // bit set -> -c_p
+          acc[j] = acc[j] - as_h2(v);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t a = h2_to_bf2(acc[2 * j]), b = h2_to_bf2(acc[2 * j + 1]);
+        lo[j] = (a & 0xffffu) | (b << 16);          // weights 8 dh + 2j, +1
+        hi[j] = (a >> 16) | (b & 0xffff0000u);      // weights 16 + 8 dh + 2j, +1
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) lo[j] = hi[j] = 0u;
+    }
+    uint4* wd = (uint4*)ws;
+    wd[swz(dc, 4 * dsub + dh) >> 3] = uint4{lo[0], lo[1], lo[2], lo[3]};
+    wd[swz(dc, 4 * dsub + 2 + dh) >> 3] = uint4{hi[0], hi[1], hi[2], hi[3]};
   };
 
-  for (int kb = 0; kb < K / G; ++kb) {
-    // ---- stage activations (bf16) ----
-    {
-      constexpr int PER = G / 4;
-      uint16_t* dst = xs + xm * LDK + xpart * PER;
-      if (src_row >= 0) {
-        const TIN* s = in + (size_t)src_row * in_ld + (size_t)kb * G + xpart * PER;
+  f32x4 acc[4][4];
 #pragma unroll
-        for (int j = 0; j < PER; ++j) dst[j] = f2bf(ld_in<TIN>(s + j));
-      } else {
+  for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int j = 0; j < PER; ++j) dst[j] = 0;
+    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int nsteps = K / KS;
+  load_step(0);
+  store_step();
+  __syncthreads();
+  for (int st = 0; st < nsteps; ++st) {
+    if (st + 1 < nsteps) load_step((st + 1) * KS);
+#pragma unroll
+    for (int kk = 0; kk < KS / 32; ++kk) {
+      bf16x8 bfr[4];
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        const int col = 64 * wn + 16 * nt + (lane & 15);
+        bfr[nt] = *(const bf16x8*)(ws + swz(col, 4 * kk + (lane >> 4)));
       }
-    }
-    // ---- dequantize the weight tile (bf16) ----
-    {
-      const int words = BN * G / 32;  // words per plane in the tile
-      for (int wi = tid; wi < words; wi += kThreads) {
-        // wi enumerates (tile row block, word) ; each word = one row, 32 cols
-        const int rbl = wi / 64, w = wi % 64;
-        const int i = w % BR, sub = w / BR;
-        const int c_first = rbl * BR;           // tile column of row-block start
-        const int c = c_first + i;              // tile column of this row
-        const int n = tile_row(c);
-        const size_t blk = W.block(expert, n / BR, kb);
-        const int ib = n % BR;                  // row within the matrix block
-        const int wq = sub * BR + ib;
-        const float s1 = h2f(W.scales[W.scale_idx(blk, 0, ib)]);
-        const float z = (float)W.zeros[W.zero_idx(blk, ib)];
-        uint32_t pw[8];
 #pragma unroll
-        for (int p = 0; p < 8; ++p) pw[p] = p < bits ? W.planes[W.plane_word(blk, p, wq)] : 0u;
-        float sl[8];
+      for (int mt = 0; mt < 4; ++mt) {
+        const int row = 64 * wm + 16 * mt + (lane & 15);
+        const bf16x8 afr = *(const bf16x8*)(xs + swz(row, 4 * kk + (lane >> 4)));
 #pragma unroll
-        for (int p = 0; p < 8; ++p)
-          sl[p] = (p >= W.b_min && p < bits) ? h2f(W.scales[W.scale_idx(blk, p - W.b_min + 1, ib)])
-                                             : 0.0f;
-        uint32_t packed[16];
-#pragma unroll
-        for (int j = 0; j < 32; j += 2) {
-          float v2[2];
-#pragma unroll
-          for (int u = 0; u < 2; ++u) {
-            const int jj = j + u;
-            int q = 0;
-#pragma unroll
-            for (int p = 0; p < 8; ++p)
-              if (p < W.b_min) q |= (int)((pw[p] >> jj) & 1u) << p;
-            float v = ((float)q - z) * s1;
-#pragma unroll
-            for (int p = 0; p < 8; ++p)
-              if (p >= W.b_min && p < bits) v += ((pw[p] >> jj) & 1u) ? sl[p] : -sl[p];
-            v2[u] = v;
-          }
-          packed[j / 2] = (uint32_t)f2bf(v2[0]) | ((uint32_t)f2bf(v2[1]) << 16);
-        }
-        uint4* dst = (uint4*)(ws + c * LDK + sub * 32);
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4)
-          dst[q4] = uint4{packed[4 * q4], packed[4 * q4 + 1], packed[4 * q4 + 2], packed[4 * q4 + 3]};
+        for (int nt = 0; nt < 4; ++nt)
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afr, bfr[nt], acc[mt][nt], 0, 0, 0);
       }
     }
     __syncthreads();
-    // ---- MFMA over the group ----
-#pragma unroll
-    for (int kk = 0; kk < G / 32; ++kk) {
-      bf16x8 a[2], b[2];
-#pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2) {
-        const int row = wm * 32 + t2 * 16 + (lane & 15);
-        a[t2] = *(const bf16x8*)(xs + row * LDK + kk * 32 + 8 * (lane >> 4));
-        const int col = wn * 32 + t2 * 16 + (lane & 15);
-        b[t2] = *(const bf16x8*)(ws + col * LDK + kk * 32 + 8 * (lane >> 4));
-      }
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mt], b[nt], acc[mt][nt], 0, 0, 0);
+    if (st + 1 < nsteps) {
+      store_step();
+      __syncthreads();
     }
-    __syncthreads();
   }
 
   // ---- epilogue ----
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt) {
+  for (int mt = 0; mt < 4; ++mt) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int m = wm * 32 + mt * 16 + 4 * (lane >> 4) + r;
+      const int m = 64 * wm + 16 * mt + 4 * (lane >> 4) + r;
       if (m >= cnt) continue;
       const size_t pos = (size_t)(pos0 + m);
       if (SWIGLU) {
-        const float a = acc[mt][0][r], c = acc[mt][1][r];
-        const int n = n0 + 16 * wn + (lane & 15);
-        ((uint16_t*)out)[pos * out_ld + n] = f2bf(silu(a) * c);
+#pragma unroll
+        for (int sp = 0; sp < 2; ++sp) {
+          const int n = n0 + 32 * wn + 16 * sp + (lane & 15);
+          if (n >= f) continue;
+          const float a = acc[mt][2 * sp][r], c = acc[mt][2 * sp + 1][r];
+          ((uint16_t*)out)[pos * out_ld + n] = f2bf(silu(a) * c);
+        }
       } else {
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-          const int n = n0 + wn * 32 + nt * 16 + (lane & 15);
+        for (int nt = 0; nt < 4; ++nt) {
+          const int n = n0 + 64 * wn + 16 * nt + (lane & 15);
+          if (n >= N) continue;
           ((float*)out)[pos * out_ld + n] = acc[mt][nt][r];
         }
       }
     }
   }
+}
+
+// fp32 activations are rounded to bf16 once for the GEMM's operand tiles.
+__global__ void to_bf16_kernel(const float* __restrict__ in, size_t n, uint16_t* __restrict__ out) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) out[i] = f2bf(in[i]);
 }
 
 // out[t][c] = sum_i w[t][i] * y[slot_of[t*k+i]][c] (+ ys[t][c]), i ascending.
@@ -257,19 +315,20 @@ __global__ void combine_kernel(const float* __restrict__ y, const float* __restr
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
-template <bool SWIGLU, typename TIN>
-hipError_t run_gemm(const TIN* in, int in_ld, const int32_t* perm, int kdiv, const MwqView& W,
+template <bool SWIGLU>
+hipError_t run_gemm(const uint16_t* in, int in_ld, const int32_t* perm, int kdiv, const MwqView& W,
                     int expert_fixed, const Sched& sc, int mtiles_ub, int f, void* out, int out_ld,
                     hipStream_t s) {
   const int N = SWIGLU ? W.rows / 2 : W.rows;
-  dim3 grid(mtiles_ub, SWIGLU ? N / (BN / 2) : N / BN);
+  const int per = SWIGLU ? BN / 2 : BN;
+  dim3 grid(mtiles_ub, (N + per - 1) / per);
   if (mtiles_ub <= 0) return hipSuccess;
   if (W.group == 128)
-    gemm_kernel<128, SWIGLU, TIN><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, expert_fixed,
-                                                            sc, f, out, out_ld);
+    gemm_kernel<128, SWIGLU><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, expert_fixed, sc,
+                                                       f, N, out, out_ld);
   else
-    gemm_kernel<64, SWIGLU, TIN><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, expert_fixed,
-                                                           sc, f, out, out_ld);
+    gemm_kernel<64, SWIGLU><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, expert_fixed, sc,
+                                                      f, N, out, out_ld);
   return hipGetLastError();
 }
 
@@ -284,6 +343,7 @@ FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shar
   L.hs_off = off;     off += align256(sizeof(uint16_t) * (size_t)T * shared_d_ff);
   L.y_off = off;      off += align256(sizeof(float) * (size_t)T * k * d);
   L.ys_off = off;     off += align256(sizeof(float) * (size_t)T * (shared_d_ff > 0 ? d : 0));
+  L.xb_off = off;     off += align256(sizeof(uint16_t) * (size_t)T * d);
   const size_t nd = T <= kDecodeMaxTokens ? (size_t)T * k : 0;  // decode positions
   // decode work list: at most one run per active expert plus one per 8 positions
   L.elist_off = off;  off += align256(sizeof(int32_t) * (4 * ((size_t)E + (nd + 7) / 8) + 4));
@@ -316,6 +376,17 @@ hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff,
   uint16_t* hs = (uint16_t*)(base + L.hs_off);
   float* y = (float*)(base + L.y_off);
   float* ys = (float*)(base + L.ys_off);
+  // bf16 activations for the grouped GEMM (fp32 inputs are rounded once)
+  const uint16_t* xb = (const uint16_t*)x;
+  const bool gemm_needed = has_shared || !decode_path_ok(w13, w2, T);
+  if (xd == D2MOE_F32 && gemm_needed) {
+    uint16_t* xw = (uint16_t*)(base + L.xb_off);
+    const size_t n = (size_t)T * d;
+    to_bf16_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>((const float*)x, n, xw);
+    hipError_t e0 = hipGetLastError();
+    if (e0 != hipSuccess) return e0;
+    xb = xw;
+  }
 
   hipError_t err;
   if (decode_path_ok(w13, w2, T)) {
@@ -339,16 +410,11 @@ hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff,
     const int ub = (n + BM - 1) / BM + (nb < n ? nb : n);
     const MwqView W13 = view_of(w13), W2 = view_of(w2);
     if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
-    if (xd == D2MOE_BF16)
-      err = run_gemm<true, uint16_t>((const uint16_t*)x, d, r->perm, k, W13, 0, sc, ub, d_ff, h,
-                                     d_ff, s);
-    else
-      err = run_gemm<true, float>((const float*)x, d, r->perm, k, W13, 0, sc, ub, d_ff, h, d_ff,
-                                  s);
+    err = run_gemm<true>(xb, d, r->perm, k, W13, 0, sc, ub, d_ff, h, d_ff, s);
     if (err != hipSuccess) return err;
     if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
     if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
-    err = run_gemm<false, uint16_t>(h, d_ff, nullptr, 1, W2, 0, sc, ub, d_ff, y, d, s);
+    err = run_gemm<false>(h, d_ff, nullptr, 1, W2, 0, sc, ub, d_ff, y, d, s);
     if (err != hipSuccess) return err;
     if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
   }
@@ -357,15 +423,9 @@ hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff,
     Sched one{nullptr, nullptr, nullptr, 0, T, shared_bits, 1, sw13->b_min};
     const int ubs = (T + BM - 1) / BM;
     const MwqView S13 = view_of(sw13), S2 = view_of(sw2);
-    if (xd == D2MOE_BF16)
-      err = run_gemm<true, uint16_t>((const uint16_t*)x, d, nullptr, 1, S13, 0, one, ubs,
-                                     shared_d_ff, hs, shared_d_ff, s);
-    else
-      err = run_gemm<true, float>((const float*)x, d, nullptr, 1, S13, 0, one, ubs, shared_d_ff,
-                                  hs, shared_d_ff, s);
+    err = run_gemm<true>(xb, d, nullptr, 1, S13, 0, one, ubs, shared_d_ff, hs, shared_d_ff, s);
     if (err != hipSuccess) return err;
-    err = run_gemm<false, uint16_t>(hs, shared_d_ff, nullptr, 1, S2, 0, one, ubs, shared_d_ff, ys,
-                                    d, s);
+    err = run_gemm<false>(hs, shared_d_ff, nullptr, 1, S2, 0, one, ubs, shared_d_ff, ys, d, s);
     if (err != hipSuccess) return err;
   }
 

@@ -74,7 +74,7 @@ hipError_t launch_route(const void* x, d2moe_dtype xd, int T, int d, const float
 // buffers exist only when T <= kDecodeMaxTokens.
 constexpr int kDecodeMaxTokens = 16;
 struct FwdWorkspace {
-  size_t sched_off, h_off, hs_off, y_off, ys_off;
+  size_t sched_off, h_off, hs_off, y_off, ys_off, xb_off;
   size_t elist_off, xq13_off, xs13_off, h32_off, xq2_off, xs2_off, hmax_off;
   size_t total;
 };
