@@ -134,21 +134,20 @@ __device__ inline float row_absmax<float>(const float* row, int K) {
   return m;
 }
 
-// rowmax: largest |value| of each position's row as binary32 bits (given by
-// the producer of the rows), or NULL to compute it here with 16-byte loads
-// (rows are K % 128 == 0 elements on 16-byte aligned bases).  zero_max: if
-// given, npos + 1 entries set to 0 for the next producer's atomicMax.
+// rowmax: partial maxima of |value| of each position's row as binary32 bits,
+// rowmax[pos * rowmax_parts + i] (written by the producer of the rows, one
+// entry per producing workgroup, so that no two producers update the same
+// word), or NULL to compute the maximum here with 16-byte loads (rows are
+// K % 128 == 0 elements on 16-byte aligned bases).
 template <typename TIN>
 __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
     const TIN* __restrict__ in, int in_ld, const int32_t* __restrict__ perm, int kdiv, int npos,
-    int K, const uint32_t* __restrict__ rowmax, uint8_t* __restrict__ Xq,
+    int K, const uint32_t* __restrict__ rowmax, int rowmax_parts, uint8_t* __restrict__ Xq,
     uint8_t* __restrict__ Xs, const int32_t* __restrict__ offsets,
     const uint8_t* __restrict__ maxbit, int E, int L, int32_t* __restrict__ elist,
-    int32_t* __restrict__ ecount, uint32_t* __restrict__ zero_max) {
+    int32_t* __restrict__ ecount) {
   __shared__ float wmax[kPrepThreads / 64];
   const int pos = blockIdx.x, NG = K / G;
-  if (zero_max && pos == npos && blockIdx.y == 0)
-    for (int i = threadIdx.x; i <= npos; i += kPrepThreads) zero_max[i] = 0u;
   if (pos == npos && blockIdx.y == 0 && elist && threadIdx.x == 0) {
     int n = 0;
     for (int e = 0; e < E; ++e) {
@@ -167,16 +166,19 @@ __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
   const TIN* src = nullptr;
   if (pos < npos) src = in + (long)(perm ? perm[pos] / kdiv : pos) * in_ld;
   float amax = 0.0f;
-  if (rowmax) {
-    if (src) amax = __uint_as_float(rowmax[pos]);
-  } else {
-    if (src) amax = row_absmax<TIN>(src, K);
-    for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, 64));
-    if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = amax;
-    __syncthreads();
-    amax = 0.0f;
-    for (int w = 0; w < kPrepThreads / 64; ++w) amax = fmaxf(amax, wmax[w]);
+  if (src) {
+    if (rowmax) {
+      for (int i = threadIdx.x; i < rowmax_parts; i += kPrepThreads)
+        amax = fmaxf(amax, __uint_as_float(rowmax[(size_t)pos * rowmax_parts + i]));
+    } else {
+      amax = row_absmax<TIN>(src, K);
+    }
   }
+  for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, 64));
+  if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = amax;
+  __syncthreads();
+  amax = 0.0f;
+  for (int w = 0; w < kPrepThreads / 64; ++w) amax = fmaxf(amax, wmax[w]);
   const int s = row_scale_exp(amax);
   uint32_t* row = (uint32_t*)(Xq + (size_t)pos * NG * 256);
   const int c0 = blockIdx.y * kPrepCols, c1 = min(K, c0 + kPrepCols);
@@ -284,6 +286,7 @@ __device__ inline void scales4(uint2 s, float (&out)[4]) {
 // the last one, each from its own array.
 constexpr int kStage = 2304;            // bytes per stage (>= 18 x 128 - 16)
 constexpr int kDepth = 4;               // stages: the DMA runs kDepth-1 groups ahead
+constexpr int kCpolNT = 2;              // cache-policy operand of the DMA: nt
 
 template <int MB>
 struct StageLayout {
@@ -349,10 +352,12 @@ __device__ inline void dma_group(const DmaPlan<MB>& d, const WaveCtx& c, int g, 
 #pragma unroll
   for (int i = 0; i < SL::ops; ++i) {
     // every instruction has lane 0 active (slot 64 i < slots), so each one
-    // issues and is counted by vmcnt
+    // issues and is counted by vmcnt.  Weights are read once per call, so the
+    // loads are marked nontemporal (cache policy nt): streaming them past the
+    // caches reads HBM markedly faster on this chip than default-policy loads.
     if (64 * i + c.lane < SL::slots)
       __builtin_amdgcn_global_load_lds(D2MOE_GPTR(d.a0[i] + (size_t)g * d.step[i]),
-                                       D2MOE_LPTR(st + 1024 * i), 16, 0, 0);
+                                       D2MOE_LPTR(st + 1024 * i), 16, 0, kCpolNT);
   }
 }
 
@@ -658,22 +663,24 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   if (valid && piece == 0)
     *(float4*)(out + (size_t)pos * out_ld + rb * 16 + 4 * c.q) = float4{o[0], o[1], o[2], o[3]};
   if (rowmax) {
-    // largest |output| of each position, for the scale of its fp8 pieces:
-    // max over this lane's rows, then over the four lanes (q) of the token
+    // largest |output| of each position over this row-block, for the scale
+    // of its fp8 pieces: max over this lane's rows, then over the four lanes
+    // (q) of the token; one word per (position, row-block), so the
+    // workgroups of a position never contend for one address
     m = fmaxf(m, __shfl_xor(m, 16, 64));
     m = fmaxf(m, __shfl_xor(m, 32, 64));
-    if (valid && piece == 0 && c.q == 0) atomicMax(rowmax + pos, __float_as_uint(m));
+    if (valid && piece == 0 && c.q == 0) rowmax[(size_t)pos * gridDim.x + rb] = __float_as_uint(m);
   }
 }
 
 template <typename TIN>
 hipError_t run_xprep(const TIN* in, int in_ld, const int32_t* perm, int kdiv, int npos, int K,
-                     const uint32_t* rowmax, uint8_t* Xq, uint8_t* Xs, const d2moe_routing* r,
-                     int E, int L, int32_t* elist, int32_t* ecount, uint32_t* zero_max,
+                     const uint32_t* rowmax, int rowmax_parts, uint8_t* Xq, uint8_t* Xs,
+                     const d2moe_routing* r, int E, int L, int32_t* elist, int32_t* ecount,
                      hipStream_t s) {
   xprep_kernel<TIN><<<dim3(npos + 1, (K + kPrepCols - 1) / kPrepCols), kPrepThreads, 0, s>>>(
-      in, in_ld, perm, kdiv, npos, K, rowmax, Xq, Xs, r ? r->offsets : nullptr,
-      r ? r->expert_maxbit : nullptr, E, L, elist, ecount, zero_max);
+      in, in_ld, perm, kdiv, npos, K, rowmax, rowmax_parts, Xq, Xs, r ? r->offsets : nullptr,
+      r ? r->expert_maxbit : nullptr, E, L, elist, ecount);
   return hipGetLastError();
 }
 
@@ -695,11 +702,11 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   const int L = w13->b_max - w13->b_min + 1;
   const int npos = T * k;
   if (xd == D2MOE_BF16)
-    err = run_xprep<uint16_t>((const uint16_t*)x, d, r->perm, k, npos, d, nullptr, b.xq13, b.xs13,
-                              r, E, L, b.elist, b.ecount, b.hmax, s);
+    err = run_xprep<uint16_t>((const uint16_t*)x, d, r->perm, k, npos, d, nullptr, 0, b.xq13,
+                              b.xs13, r, E, L, b.elist, b.ecount, s);
   else
-    err = run_xprep<float>((const float*)x, d, r->perm, k, npos, d, nullptr, b.xq13, b.xs13, r,
-                           E, L, b.elist, b.ecount, b.hmax, s);
+    err = run_xprep<float>((const float*)x, d, r->perm, k, npos, d, nullptr, 0, b.xq13, b.xs13,
+                           r, E, L, b.elist, b.ecount, s);
   if (err != hipSuccess) return err;
   // work items: each active expert's positions in runs of kDecodeCols
   const int ny = (E < npos ? E : npos) + (npos + kDecodeCols - 1) / kDecodeCols;
@@ -710,8 +717,8 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
       b.hmax);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
-  err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.hmax, b.xq2, b.xs2, nullptr, 0,
-                         0, nullptr, nullptr, nullptr, s);
+  err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.hmax, d_ff / 16, b.xq2, b.xs2,
+                         nullptr, 0, 0, nullptr, nullptr, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
   decode_kernel<false, kDecodeWaves><<<dim3(d / 16, ny), 64 * kDecodeWaves, 0, s>>>(

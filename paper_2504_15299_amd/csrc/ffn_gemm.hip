@@ -353,7 +353,8 @@ FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shar
   L.h32_off = off;    off += align256(nd * d_ff * sizeof(float));
   L.xq2_off = off;    off += align256(nz * d_ff * 2);
   L.xs2_off = off;    off += align256(nz * 2);
-  L.hmax_off = off;   off += align256(nz * sizeof(uint32_t));
+  // partial maxima of |h|: one word per (position, 16-row block of d_ff)
+  L.hmax_off = off;   off += align256(nd * ((size_t)(d_ff + 15) / 16) * sizeof(uint32_t));
   L.total = off;
   return L;
 }

@@ -84,7 +84,7 @@ struct DecodeBuffers {
   int32_t* ecount;  // [1]
   uint8_t *xq13, *xs13, *xq2, *xs2;
   float* h32;       // [T*k][d_ff]
-  uint32_t* hmax;   // [T*k+1] largest |h| of each position (binary32 bits)
+  uint32_t* hmax;   // [T*k][d_ff/16] largest |h| of each position per 16-row block (binary32 bits)
   float* y;         // [T*k][d]
 };
 
