@@ -82,8 +82,9 @@ __device__ inline float ld_act<uint16_t>(const uint16_t* p) { return bf2f(*p); }
 // lane order of the 16x16x128 MFMA (lane group q holds hardware k
 // 16q..16q+15 and 64+16q..64+16q+15); logical column 32q + 4n + d sits at
 // hardware k 32q + 8d + n, matching the nibble order of the expanded plane
-// words.  Xs holds the E8M0 codes of 2^s (hi) and 2^(s-4) (lo).
-//   Xq [pos][K/128][piece][128] bytes, Xs [pos][piece] bytes
+// words.  The position's info word Xs holds the E8M0 codes of 2^s (hi) and
+// 2^(s-4) (lo) next to its token's bit-width.
+//   Xq [pos][K/128][piece][128] bytes, Xs [pos] 32-bit words
 // Position npos is an all-zero slot that decode lanes without a token read,
 // so that every load in the decode loop is unconditional.
 constexpr int kPrepThreads = 256;
@@ -102,14 +103,16 @@ __device__ inline int row_scale_exp(float amax) {
 
 // Grid (position, column slice of kPrepCols).  Every workgroup of a row
 // takes the row's largest magnitude (from `rowmax`, or computed from the
-// row, which is small and cached), then converts its slice, four output bytes per thread per step: output bytes
-// 4j..4j+3 of a 16-byte run hold hardware k = 4j..4j+3, i.e. logical columns
-// 32q + 4n + d for n = 4j'..4j'+3 (fixed d), so each thread reads four
-// columns at stride 4 and stores one dword per piece.  The zero-slot
-// workgroup of slice 0 also writes the work list of the decode kernels when
-// `elist` is given: each active expert's positions in runs of at most
-// kDecodeCols, elist[4 i] = expert, first position, end position, the
-// expert's largest bit-width.
+// row, which is small and cached), then converts its slice, four output
+// bytes per thread per step: output bytes 4j..4j+3 of a 16-byte run hold
+// hardware k = 4j..4j+3, i.e. logical columns 32q + 4n + d for
+// n = 4j'..4j'+3 (fixed d), so each thread reads four columns at stride 4 and
+// stores one dword per piece.  The zero-slot workgroup of slice 0 also writes
+// the work list of the decode kernels when `elist` is given: each active
+// expert's positions in runs of at most kDecodeCols, elist[4 i] = expert,
+// first position, end position, the expert's largest bit-width, and entries
+// with bit-width 0 (no work) up to `nitems`, the grid's work-item count, so
+// that a decode workgroup needs one load to learn its work.
 template <typename TIN>
 __device__ inline float row_absmax(const TIN* row, int K);
 template <>
@@ -139,13 +142,19 @@ __device__ inline float row_absmax<float>(const float* row, int K) {
 // entry per producing workgroup, so that no two producers update the same
 // word), or NULL to compute the maximum here with 16-byte loads (rows are
 // K % 128 == 0 elements on 16-byte aligned bases).
+// Xs[pos] is the position's info word for the decode kernels: its token's
+// bit-width (0 for the zero slot) in bits 0-7 and the E8M0 codes of the hi
+// and lo activation pieces in bits 8-15 and 16-23.  Xs has kDecodeCols - 1
+// entries of padding past the zero slot, so a decode workgroup can read the
+// words of kDecodeCols positions from any first position.  bperm / tbits give the bit-width of
+// position p as tbits[bperm[p]].
 template <typename TIN>
 __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
     const TIN* __restrict__ in, int in_ld, const int32_t* __restrict__ perm, int kdiv, int npos,
     int K, const uint32_t* __restrict__ rowmax, int rowmax_parts, uint8_t* __restrict__ Xq,
-    uint8_t* __restrict__ Xs, const int32_t* __restrict__ offsets,
-    const uint8_t* __restrict__ maxbit, int E, int L, int32_t* __restrict__ elist,
-    int32_t* __restrict__ ecount) {
+    uint32_t* __restrict__ Xs, const int32_t* __restrict__ bperm,
+    const uint8_t* __restrict__ tbits, const int32_t* __restrict__ offsets,
+    const uint8_t* __restrict__ maxbit, int E, int L, int32_t* __restrict__ elist, int nitems) {
   __shared__ float wmax[kPrepThreads / 64];
   const int pos = blockIdx.x, NG = K / G;
   if (pos == npos && blockIdx.y == 0 && elist && threadIdx.x == 0) {
@@ -161,7 +170,8 @@ __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
         ++n;
       }
     }
-    *ecount = n;
+    // the remaining slots of the grid get no work (largest bit-width 0)
+    for (; n < nitems; ++n) elist[4 * n] = elist[4 * n + 1] = elist[4 * n + 2] = elist[4 * n + 3] = 0;
   }
   const TIN* src = nullptr;
   if (pos < npos) src = in + (long)(perm ? perm[pos] / kdiv : pos) * in_ld;
@@ -204,8 +214,8 @@ __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
     row[g * 64 + 32 + w] = lo;
   }
   if (threadIdx.x == 0 && blockIdx.y == 0) {
-    Xs[pos * 2] = (uint8_t)(s + 127);
-    Xs[pos * 2 + 1] = (uint8_t)(s - 4 + 127);
+    const uint32_t bits = pos < npos ? tbits[bperm[pos]] : 0u;
+    Xs[pos] = bits | ((uint32_t)(s + 127) << 8) | ((uint32_t)(s - 4 + 127) << 16);
   }
 }
 
@@ -305,9 +315,9 @@ struct WaveCtx {
   const uint8_t* zp;   // zero points of group 0
   int pl_step, sc_step;  // bytes per group
   int lane, q, j;
-  int bit;               // bit-width of this lane's token (0: no token)
+  uint32_t info;         // position info word (bit-width, activation scale codes)
+  int info_shift;        // bit offset of this lane's piece's scale code in `info`
   const uint8_t* xq;     // activation pieces of group 0, this lane
-  int bsc;               // their E8M0 scale code
   uint64_t lmask;        // lanes holding a token
   SigmaConsts k;
   uint32_t lds_pl, lds_sc, lds_z;  // this lane's LDS read bases in stage 0
@@ -463,6 +473,8 @@ __device__ inline void read_stage(const WaveCtx& c, uint32_t (&w)[MB], uint2 (&s
 // exact zero.
 template <int MB, int SOFF>
 __device__ inline void compute_group(const BData& t, const WaveCtx& c, v4f& acc) {
+  const int bit = (int)(c.info & 0xffu);                      // token's bit-width
+  const int bsc = (int)((c.info >> c.info_shift) & 0xffu);    // its activation scale code
   const SigmaConsts& k = c.k;
   uint32_t w[MB];
   uint2 sw[MB - 1];
@@ -474,9 +486,9 @@ __device__ inline void compute_group(const BData& t, const WaveCtx& c, v4f& acc)
   float s1[4];
   scales4(sw[0], s1);
   // base: sum_k x_k (1.5 - Q_k) + sum_k x_k (z - 1.5), accumulated in place
-  v4f m = mfma_fp4_fp8(au, bb, 127, c.bsc);
-  m = mfma_fp4_fp8(a0, bb, m, 127, c.bsc);
-  m = mfma_fp4_fp8(a1, bb, m, 128, c.bsc);
+  v4f m = mfma_fp4_fp8(au, bb, 127, bsc);
+  m = mfma_fp4_fp8(a0, bb, m, 127, bsc);
+  m = mfma_fp4_fp8(a1, bb, m, 128, bsc);
 #pragma unroll
   for (int r = 0; r < 4; ++r) acc[r] = fmaf(-s1[r], m[r], acc[r]);
 #pragma unroll
@@ -484,7 +496,7 @@ __device__ inline void compute_group(const BData& t, const WaveCtx& c, v4f& acc)
     const v8i ap = expand_sigma(w[p], k);
     float sp[4];
     scales4(sw[p - 1], sp);
-    const int bs = p < c.bit ? c.bsc : 0;
+    const int bs = p < bit ? bsc : 0;
     const v4f d = mfma_fp4_fp8(ap, bb, 128, bs);
 #pragma unroll
     for (int r = 0; r < 4; ++r) acc[r] = fmaf(-sp[r], d[r], acc[r]);
@@ -555,23 +567,23 @@ __device__ inline void decode_groups(const WaveCtx& c, uint8_t* ring, int g0, in
 
 
 // elist[4*i]: expert, first position, end position (at most kDecodeCols
-// positions), largest bit-width of the expert.
+// positions), largest bit-width of the expert (0: no work).  Xs: position
+// info words (bit-width, activation scale codes) from the activation prep.
 // SwiGLU variant: waves [0, NW/2) stream the W1 row-block, waves [NW/2, NW)
 // the matching W3 row-block, each half splitting the groups; the epilogue
 // combines them through LDS (each wave's partial sums go to its own ring,
 // which is idle by then).
 template <bool SWIGLU, int NW>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void decode_kernel(
-    MwqView W, const int32_t* __restrict__ elist, const int32_t* __restrict__ ecount,
-    const int32_t* __restrict__ perm, const uint8_t* __restrict__ topk_bits,
-    const uint8_t* __restrict__ Xq, const uint8_t* __restrict__ Xs, int npos, int f,
-    float* __restrict__ out, int out_ld, uint32_t* __restrict__ rowmax) {
+    MwqView W, const int32_t* __restrict__ elist, const uint8_t* __restrict__ Xq,
+    const uint32_t* __restrict__ Xs, int npos, int f, float* __restrict__ out, int out_ld,
+    uint32_t* __restrict__ rowmax) {
   __shared__ __attribute__((aligned(16))) uint8_t ring[NW][kDepth * kStage];
   static_assert(kDepth * kStage >= 64 * 4 * (int)sizeof(float), "partial sums fit the ring");
   const int ei = blockIdx.y;
-  if (ei >= *ecount) return;
   const int e = elist[4 * ei], p0 = elist[4 * ei + 1], p1 = elist[4 * ei + 2];
   const int mb = elist[4 * ei + 3];
+  if (mb == 0) return;
   const int rb = blockIdx.x;
   const int lane = threadIdx.x & 63;
   // wave-uniform by construction; readfirstlane lets the compiler keep the
@@ -592,19 +604,25 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   const int t = c.j >> 1;
   const bool valid = t < ncol;
   const int pos = p0 + t;
-  c.bit = valid ? (int)topk_bits[perm[pos]] : 0;
+  const int src = valid ? pos : npos;  // zero slot when no token
   {
-    const int src = valid ? pos : npos;  // zero slot when no token
     const size_t base = ((size_t)src * NG) * 2 + piece;  // group 0
     c.xq = Xq + base * 128 + c.q * 32;
-    c.bsc = Xs[src * 2 + piece];
   }
+  c.info_shift = 8 + 8 * piece;
   c.lmask = __ballot(valid);
-  // the bit-width and the activation scale code are needed only inside the
-  // group loop; consuming them here makes the compiler's wait for their loads
-  // happen before the first DMA (a wait placed after it would drain the
-  // weight prefetch)
-  asm volatile("" : "+v"(c.bit), "+v"(c.bsc)::"memory");
+  {
+    // the info words of the item's positions are wave-uniform reads (scalar
+    // cache, ordered by lgkmcnt), so waiting for them never holds back the
+    // weight DMA; each lane then picks its token's word
+    uint32_t iw[kDecodeCols];
+#pragma unroll
+    for (int i = 0; i < kDecodeCols; ++i) iw[i] = Xs[p0 + i];
+    uint32_t info = 0u;
+#pragma unroll
+    for (int i = 0; i < kDecodeCols; ++i) info = t == i ? iw[i] : info;
+    c.info = valid ? info : 0u;  // no token: bit-width 0, zero activations
+  }
 
   const int rowblock = rr == 0 ? rb : rb + f / 16;
   const size_t blk0 = W.block(e, rowblock, 0);
@@ -675,12 +693,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
 
 template <typename TIN>
 hipError_t run_xprep(const TIN* in, int in_ld, const int32_t* perm, int kdiv, int npos, int K,
-                     const uint32_t* rowmax, int rowmax_parts, uint8_t* Xq, uint8_t* Xs,
-                     const d2moe_routing* r, int E, int L, int32_t* elist, int32_t* ecount,
-                     hipStream_t s) {
+                     const uint32_t* rowmax, int rowmax_parts, uint8_t* Xq, uint32_t* Xs,
+                     const d2moe_routing* r, bool work_list, int E, int L, int32_t* elist,
+                     int nitems, hipStream_t s) {
   xprep_kernel<TIN><<<dim3(npos + 1, (K + kPrepCols - 1) / kPrepCols), kPrepThreads, 0, s>>>(
-      in, in_ld, perm, kdiv, npos, K, rowmax, rowmax_parts, Xq, Xs, r ? r->offsets : nullptr,
-      r ? r->expert_maxbit : nullptr, E, L, elist, ecount);
+      in, in_ld, perm, kdiv, npos, K, rowmax, rowmax_parts, Xq, Xs, r->perm, r->topk_bits,
+      work_list ? r->offsets : nullptr, work_list ? r->expert_maxbit : nullptr, E, L, elist,
+      nitems);
   return hipGetLastError();
 }
 
@@ -701,28 +720,27 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   hipError_t err;
   const int L = w13->b_max - w13->b_min + 1;
   const int npos = T * k;
-  if (xd == D2MOE_BF16)
-    err = run_xprep<uint16_t>((const uint16_t*)x, d, r->perm, k, npos, d, nullptr, 0, b.xq13,
-                              b.xs13, r, E, L, b.elist, b.ecount, s);
-  else
-    err = run_xprep<float>((const float*)x, d, r->perm, k, npos, d, nullptr, 0, b.xq13, b.xs13,
-                           r, E, L, b.elist, b.ecount, s);
-  if (err != hipSuccess) return err;
   // work items: each active expert's positions in runs of kDecodeCols
   const int ny = (E < npos ? E : npos) + (npos + kDecodeCols - 1) / kDecodeCols;
+  if (xd == D2MOE_BF16)
+    err = run_xprep<uint16_t>((const uint16_t*)x, d, r->perm, k, npos, d, nullptr, 0, b.xq13,
+                              b.xs13, r, true, E, L, b.elist, ny, s);
+  else
+    err = run_xprep<float>((const float*)x, d, r->perm, k, npos, d, nullptr, 0, b.xq13, b.xs13,
+                           r, true, E, L, b.elist, ny, s);
+  if (err != hipSuccess) return err;
   const MwqView W13 = view_of(w13), W2 = view_of(w2);
   if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
   decode_kernel<true, kDecodeWaves><<<dim3(d_ff / 16, ny), 64 * kDecodeWaves, 0, s>>>(
-      W13, b.elist, b.ecount, r->perm, r->topk_bits, b.xq13, b.xs13, npos, d_ff, b.h32, d_ff,
-      b.hmax);
+      W13, b.elist, b.xq13, b.xs13, npos, d_ff, b.h32, d_ff, b.hmax);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
-  err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.hmax, d_ff / 16, b.xq2, b.xs2,
-                         nullptr, 0, 0, nullptr, nullptr, s);
+  err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.hmax, d_ff / 16, b.xq2, b.xs2, r,
+                         false, E, L, nullptr, 0, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
   decode_kernel<false, kDecodeWaves><<<dim3(d / 16, ny), 64 * kDecodeWaves, 0, s>>>(
-      W2, b.elist, b.ecount, r->perm, r->topk_bits, b.xq2, b.xs2, npos, 0, b.y, d, nullptr);
+      W2, b.elist, b.xq2, b.xs2, npos, 0, b.y, d, nullptr);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
   return hipSuccess;

@@ -349,10 +349,11 @@ FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shar
   L.elist_off = off;  off += align256(sizeof(int32_t) * (4 * ((size_t)E + (nd + 7) / 8) + 4));
   const size_t nz = nd ? nd + 1 : 0;  // plus one all-zero activation slot
   L.xq13_off = off;   off += align256(nz * d * 2);
-  L.xs13_off = off;   off += align256(nz * 2);
+  const size_t nxs = nz ? nz + 8 : 0;  // info words, padded for 8-position reads
+  L.xs13_off = off;   off += align256(nxs * sizeof(uint32_t));
   L.h32_off = off;    off += align256(nd * d_ff * sizeof(float));
   L.xq2_off = off;    off += align256(nz * d_ff * 2);
-  L.xs2_off = off;    off += align256(nz * 2);
+  L.xs2_off = off;    off += align256(nxs * sizeof(uint32_t));
   // partial maxima of |h|: one word per (position, 16-row block of d_ff)
   L.hmax_off = off;   off += align256(nd * ((size_t)(d_ff + 15) / 16) * sizeof(uint32_t));
   L.total = off;
@@ -393,12 +394,11 @@ hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff,
   if (decode_path_ok(w13, w2, T)) {
     DecodeBuffers db;
     db.elist = (int32_t*)(base + L.elist_off);
-    db.ecount = db.elist + 4 * ((size_t)E + ((size_t)T * k + 7) / 8);
     db.xq13 = (uint8_t*)(base + L.xq13_off);
-    db.xs13 = (uint8_t*)(base + L.xs13_off);
+    db.xs13 = (uint32_t*)(base + L.xs13_off);
     db.h32 = (float*)(base + L.h32_off);
     db.xq2 = (uint8_t*)(base + L.xq2_off);
-    db.xs2 = (uint8_t*)(base + L.xs2_off);
+    db.xs2 = (uint32_t*)(base + L.xs2_off);
     db.hmax = (uint32_t*)(base + L.hmax_off);
     db.y = y;
     err = launch_decode_ffn(x, xd, T, d, d_ff, E, k, w13, w2, r, db, s, events);

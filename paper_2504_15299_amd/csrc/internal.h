@@ -80,9 +80,9 @@ struct FwdWorkspace {
 };
 
 struct DecodeBuffers {
-  int32_t* elist;   // [E][4]
-  int32_t* ecount;  // [1]
-  uint8_t *xq13, *xs13, *xq2, *xs2;
+  int32_t* elist;   // [work items][4]
+  uint8_t *xq13, *xq2;
+  uint32_t *xs13, *xs2;  // [T*k+1] position info words
   float* h32;       // [T*k][d_ff]
   uint32_t* hmax;   // [T*k][d_ff/16] largest |h| of each position per 16-row block (binary32 bits)
   float* y;         // [T*k][d]
