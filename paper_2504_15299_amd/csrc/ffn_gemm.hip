@@ -102,7 +102,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint16_t* __restri
   // ---- which bucket / tile ----
   if (tid == 0) {
     int j = 0, nb = sc.nb;
-    int mt = blockIdx.x;
+    int mt = blockIdx.y;
     if (nb == 0) {
       const int ntiles = (sc.one_cnt + BM - 1) / BM;
       s_info[0] = mt < ntiles ? 1 : 0;
@@ -130,7 +130,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint16_t* __restri
   if (!(s_info[0] & 1)) return;
   const int expert = sc.nb == 0 ? expert_fixed : (s_info[0] >> 1);
   const int pos0 = s_info[1], cnt = s_info[2], bits = s_info[3];
-  const int n0 = blockIdx.y * (SWIGLU ? BN / 2 : BN);  // first output row
+  const int n0 = blockIdx.x * (SWIGLU ? BN / 2 : BN);  // first output row
   const int K = W.cols, BR = W.BR(), b_min = W.b_min;
 
   // ---- activation loader: row xr, 16-byte chunks 4 xh .. 4 xh + 3 ----
@@ -321,7 +321,11 @@ hipError_t run_gemm(const uint16_t* in, int in_ld, const int32_t* perm, int kdiv
                     hipStream_t s) {
   const int N = SWIGLU ? W.rows / 2 : W.rows;
   const int per = SWIGLU ? BN / 2 : BN;
-  dim3 grid(mtiles_ub, (N + per - 1) / per);
+  // output-row tiles vary fastest: consecutive workgroups, which the
+  // dispatcher deals round-robin to the 8 XCDs, share one M-tile, so every
+  // XCD's L2 holds the activations of the one or two M-tiles in flight
+  // rather than of all of them
+  dim3 grid((N + per - 1) / per, mtiles_ub);
   if (mtiles_ub <= 0) return hipSuccess;
   if (W.group == 128)
     gemm_kernel<128, SWIGLU><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, expert_fixed, sc,
