@@ -18,7 +18,7 @@ import numpy as np
 import pytest
 import torch
 
-from layer_cases import DEV, FWD_TOL, ambiguous_tokens, logit_error_bound, row_max_abs_rel
+from layer_cases import DEV, FWD_TOL, Layer, ambiguous_tokens, logit_error_bound, row_max_abs_rel
 from oracle import oracle as O
 from paper_2504_15299_amd import api
 from paper_2504_15299_amd import workloads as wl
@@ -113,3 +113,103 @@ def test_mixtral_decode_full_size_sampled():
     err = row_max_abs_rel(got[tokens][:, rows], want)
     print(f"full-size decode: tokens {tokens} worst row {err.max():.3e}", flush=True)
     assert err.max() <= FWD_TOL
+
+
+def _bucket_cover(idx, bits, candidates, per_group=None, groups=None):
+    """Tokens from `candidates` chosen greedily so that every (expert, bit)
+    bucket that any candidate uses holds at least one chosen slot; with
+    `groups` (a group id per token) at least `per_group` tokens per group."""
+    need = {(int(e), int(b)) for t in candidates for e, b in zip(idx[t], bits[t])}
+    chosen, have = [], set()
+    while need - have:
+        t = max(candidates, key=lambda u: (len({(int(e), int(b)) for e, b in zip(idx[u], bits[u])}
+                                               - have), -u))
+        chosen.append(t)
+        have |= {(int(e), int(b)) for e, b in zip(idx[t], bits[t])}
+        candidates = [u for u in candidates if u != t]
+    if groups is not None:
+        for gid in np.unique(groups):
+            mine = [t for t in chosen if groups[t] == gid]
+            extra = [t for t in candidates if groups[t] == gid][:max(0, per_group - len(mine))]
+            chosen += extra
+    return sorted(set(chosen))
+
+
+def _sampled_full_layer(spec, t0, rows, per_group=None):
+    """Route + forward the full layer on the device; compare routing on every
+    token and the output on a sample of tokens (every (expert, bit) bucket
+    covered) and of output columns against the oracle."""
+    L = Layer(spec)
+    _say(t0, "inputs drawn")
+    L.pack()
+    L.route()
+    got = L.forward()
+    _say(t0, "route + forward done on the device")
+    amb = ambiguous_tokens(L.ref_logits, spec.k, logit_error_bound(L.x, L.Wg, L.bias))
+    gi, gb = L.r.topk_idx.cpu().numpy(), L.r.topk_bits.cpu().numpy()
+    assert np.array_equal(gi[~amb], L.ref_route["topk_idx"][~amb])
+    assert np.array_equal(gb[~amb], L.ref_route["topk_bits"][~amb])
+    assert amb.sum() <= max(1, spec.T // 50)
+    assert np.isfinite(got).all()
+    decided = [t for t in range(spec.T) if not amb[t]]
+    groups = L.req if per_group else None
+    toks = _bucket_cover(L.ref_route["topk_idx"], L.ref_route["topk_bits"], decided,
+                         per_group, groups)
+    idx, bits = L.ref_route["topk_idx"], L.ref_route["topk_bits"]
+    need = sorted({int(e) for t in toks for e in idx[t]})
+    _say(t0, f"{len(toks)} sampled tokens, {len(need)} experts, near-tied {int(amb.sum())}")
+
+    def codes(e):
+        return (O.mwq_quantize(L.W13[e], spec.group, spec.b_min, spec.b_max),
+                O.mwq_quantize(np.ascontiguousarray(L.W2[e][rows]), spec.group, spec.b_min,
+                               spec.b_max))
+
+    with ThreadPoolExecutor(16) as ex:
+        cs = dict(zip(need, ex.map(codes, need)))
+        work = [(e, b) for e in need for b in sorted({int(bits[t, i]) for t in toks
+                                                      for i in range(spec.k) if idx[t, i] == e})]
+
+        def ffn(eb):
+            e, b = eb
+            sel = [(j, i) for j, t in enumerate(toks) for i in range(spec.k)
+                   if idx[t, i] == e and bits[t, i] == b]
+            xs = np.stack([L.x[toks[j]] for j, _ in sel]).astype(np.float64)
+            return sel, O.expert_ffn(cs[e][0], cs[e][1], b, xs)
+
+        y_slot = np.zeros((len(toks), spec.k, len(rows)), np.float64)
+        for sel, ys in ex.map(ffn, work):
+            for (j, i), yv in zip(sel, ys):
+                y_slot[j, i] = yv
+        want = O.combine(L.ref_route["topk_w"][toks], y_slot)
+        if spec.shared_f:
+            sc13 = O.mwq_quantize(L.SW13, spec.group, spec.b_min, spec.b_max)
+            sc2 = O.mwq_quantize(np.ascontiguousarray(L.SW2[rows]), spec.group, spec.b_min,
+                                 spec.b_max)
+            want = want + O.expert_ffn(sc13, sc2, spec.shared_bits,
+                                       L.x[toks].astype(np.float64))
+    _say(t0, "oracle done")
+    err = row_max_abs_rel(got[toks][:, rows], want)
+    print(f"{spec.name} full size: {len(toks)} tokens, worst row {err.max():.3e}, "
+          f"median {np.median(err):.3e}", flush=True)
+    assert err.max() <= FWD_TOL
+
+
+def test_mixtral_prefill_full_size_sampled():
+    """2048 tokens from 4 requests (Zipf(1.1) expert load, bits from {2,4,8}
+    per request and expert): routing on every token, the output on at least
+    16 tokens per request covering every (expert, bit) bucket, 256 of the
+    4096 output columns (one per 16-row block, every offset within a block)."""
+    t0 = time.time()
+    s = wl.mixtral_prefill()
+    rows = np.arange(0, s.d, 16) + np.arange(s.d // 16) % 16
+    _sampled_full_layer(s, t0, rows, per_group=16)
+
+
+def test_fine_grained_full_size_sampled():
+    """512 tokens, 64 routed experts (top-6, bits hottest-first 8/4/3/2) plus
+    the shared expert at 8 bits: routing on every token, the output on tokens
+    covering every (expert, bit) bucket, 256 of the 2048 output columns."""
+    t0 = time.time()
+    s = wl.fine_grained()
+    rows = np.arange(0, s.d, 8) + np.arange(s.d // 8) % 8
+    _sampled_full_layer(s, t0, rows)
