@@ -54,6 +54,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--prefill-steps", type=int, default=5,
                     help="also time the 2048-token prefill of the same layers (0: skip)")
+    ap.add_argument("--fine-steps", type=int, default=10,
+                    help="also time the 512-token fine-grained layer (64 routed experts top-6 "
+                         "plus a shared expert; 0: skip)")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of one captured HIP graph per layer step instead of "
                          "eager launches")
@@ -239,6 +242,79 @@ def main():
                                    / MFMA_BF16_PEAK_TFLOPS, 4),
                 "expert_load": [int(v) for v in hist]}
 
+    def run_fine(steps, warmup, copies=4):
+        """Fine-grained MoE layer: d_model 2048, 64 routed SwiGLU experts d_ff
+        1408 (top-6) plus one shared expert d_ff 5632 at 8 bits, 512 tokens,
+        MWQ group 64 nested to 8 bits.  Bit-widths hottest-first: a first
+        routing pass (untimed) counts each expert's tokens; the 16 most routed
+        get 8 bits, the next 16 get 4, the next 16 get 3, the rest 2.  Four
+        independently drawn copies rotate.  Reports tokens/s, the algorithmic
+        HBM bytes (active experts at their largest bit-width plus the shared
+        expert) and flops of the step, and both roofline fractions."""
+        dF, fF, EF, kF, gF, fS, T = 2048, 1408, 64, 6, 64, 5632, 512
+        rng = np.random.default_rng(4)
+        x = torch.from_numpy(rng.standard_normal((T, dF), dtype=np.float32)).to(dev).to(torch.bfloat16)
+        sets = []
+        for c in range(copies):
+            w13 = api.MWQ.empty(EF, 2 * fF, dF, gF, b_min, b_max, device=dev)
+            w2 = api.MWQ.empty(EF, dF, fF, gF, b_min, b_max, device=dev)
+            gen.manual_seed(9_000_000 + c)
+            api.pack_mwq(torch.randn((EF, 2 * fF, dF), generator=gen, device=dev) * 0.02, w13)
+            api.pack_mwq(torch.randn((EF, dF, fF), generator=gen, device=dev) * 0.02, w2)
+            s13 = api.MWQ.empty(1, 2 * fS, dF, gF, b_min, b_max, device=dev)
+            s2 = api.MWQ.empty(1, dF, fS, gF, b_min, b_max, device=dev)
+            api.pack_mwq(torch.randn((1, 2 * fS, dF), generator=gen, device=dev) * 0.02, s13)
+            api.pack_mwq(torch.randn((1, dF, fS), generator=gen, device=dev) * 0.02, s2)
+            Wg = torch.randn((EF, dF), generator=gen, device=dev) * 0.02
+            probe = api.route(x, Wg, None, kF, None, torch.full((1, EF), 8, dtype=torch.uint8,
+                                                               device=dev), b_min, b_max)
+            counts = probe.hist.sum(dim=1).cpu().numpy()
+            order = sorted(range(EF), key=lambda e: (-int(counts[e]), e))
+            tb = np.full((1, EF), 2, np.uint8)
+            for rank, e in enumerate(order[:48]):
+                tb[0, e] = (8, 4, 3)[rank // 16]
+            table = torch.from_numpy(tb).to(dev)
+            r = api.Routing.empty(T, EF, kF, b_min, b_max, device=dev)
+            sets.append((w13, w2, s13, s2, Wg, table, r))
+            torch.cuda.synchronize()
+        out = torch.empty((T, dF), dtype=torch.bfloat16, device=dev)
+        ws = torch.empty(api.moe_forward_workspace(T, dF, fF, EF, kF, shared_d_ff=fS),
+                         dtype=torch.uint8, device=dev)
+
+        def step(i):
+            w13, w2, s13, s2, Wg, table, r = sets[i % copies]
+            api.route(x, Wg, None, kF, None, table, b_min, b_max, out=r)
+            api.moe_forward(x, w13, w2, r, kF, shared=(s13, s2, 8), out=out, workspace=ws)
+
+        for i in range(warmup):
+            step(i)
+        torch.cuda.synchronize()
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_stop = torch.cuda.Event(enable_timing=True)
+        t_start.record()
+        for i in range(steps):
+            step(warmup + i)
+        t_stop.record()
+        torch.cuda.synchronize()
+        ms = t_start.elapsed_time(t_stop) / steps
+        byts = []
+        for c in range(copies):
+            mb = sets[c][6].expert_maxbit.cpu().numpy()
+            byts.append(sum(mwq_bytes(2 * fF, dF, gF, b_min, int(b)) + mwq_bytes(dF, fF, gF, b_min, int(b))
+                            for b in mb)
+                        + mwq_bytes(2 * fS, dF, gF, b_min, 8) + mwq_bytes(dF, fS, gF, b_min, 8))
+        nbytes = float(np.mean([byts[(warmup + i) % copies] for i in range(steps)]))
+        flop = 2.0 * 3 * dF * fF * T * kF + 2.0 * 3 * dF * fS * T
+        gbps = nbytes / (ms * 1e-3) / 1e9
+        tflops = flop / (ms * 1e-3) / 1e12
+        return {"workload": "fine-grained MoE layer (d_model 2048, 64 routed SwiGLU experts "
+                            "d_ff 1408 top-6, shared expert d_ff 5632 at 8 bits, 512 tokens, "
+                            "group 64, bits hottest-first 8/4/3/2), 4 rotating copies",
+                "tokens": T, "ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms * 1e-3), 1),
+                "alg_bytes": nbytes, "hbm_GBps": round(gbps, 1),
+                "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4), "alg_GFLOP": round(flop / 1e9, 2),
+                "TFLOPs": round(tflops, 1), "mfma_frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4)}
+
     main_res = run_batch(args.batch, args.steps, args.warmup, profile=True)
     sweep = []
     for T in [int(v) for v in args.sweep.split(",") if v.strip()]:
@@ -246,6 +322,7 @@ def main():
         sweep.append({kk: (round(v, 4) if isinstance(v, float) else v) for kk, v in r.items()})
 
     prefill = run_prefill(args.prefill_steps, 2) if args.prefill_steps > 0 else None
+    fine = run_fine(args.fine_steps, 2) if args.fine_steps > 0 else None
 
     cpu = None
     if not args.no_cpu:
@@ -286,6 +363,7 @@ def main():
                       "traffic": traffic[1]},
         "sweep": sweep,
         "prefill": prefill,
+        "fine_grained": fine,
         "cpu_baseline": cpu,
         "pack_seconds": round(pack_s, 2),
     }
