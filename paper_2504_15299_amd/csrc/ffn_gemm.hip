@@ -3,14 +3,26 @@
 // weighted combine (Fig. 1: outputs of the activated experts weighted by the
 // gate).
 //
-// Work is cut into tiles of (expert, bit-width bucket, 256 positions, 128
-// output rows), one 512-thread workgroup each.  Positions are the (token, slot) pairs sorted by (expert,
-// bit-width), so every tile reads its expert's planes 0..b-1 only.  Per K step
-// (one quantization group) the workgroup stages the gathered activations and
-// the dequantized weight tile as bf16 in LDS and runs v_mfma_f32_16x16x32_bf16
-// with fp32 accumulation.  The W1/W3 variant interleaves 16-row slices of W1
-// and W3 so each lane holds a and c of the same output and applies SwiGLU in
-// registers.
+// Positions are the (token, slot) pairs sorted by (expert, bit-width), so an
+// (expert, bit-width) bucket is a contiguous run of positions that all read
+// the same b-bit prefix of the expert's planes.  Buckets are cut into chunks
+// of at most kChunk positions; one 512-thread workgroup computes one chunk
+// against 128 weight rows.  Each of its 8 waves owns 64 positions, and all 8
+// share one dequantized weight tile, so a weight is dequantized once per
+// chunk however many positions the chunk holds.
+//
+// Per reduction step of 32 columns (one plane word per row):
+//   * the LDS DMA engine brings the raw planes, scales and zero points of a
+//     later step into a 4-stage ring shared by the workgroup (each wave moves
+//     one 1 KB slice), and each wave's gathered activation rows of a later
+//     step into its own 3-stage ring;
+//   * the workgroup dequantizes the next step's 128 x 32 tile into bf16 (one
+//     quarter plane word per thread) while each wave runs the current step's
+//     v_mfma_f32_16x16x32_bf16 products (64 positions x 128 rows, fp32
+//     accumulation) from the other tile buffer;
+//   * one barrier per step orders the shared buffers.
+// The W1/W3 variant puts 64 rows of W1 and the same 64 rows of W3 in one tile,
+// so a lane holds a and c of the same output and applies SwiGLU in registers.
 #include "internal.h"
 
 namespace d2moe {
@@ -18,36 +30,76 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int BM = 256, BN = 128, KS = 64, kThreads = 512;
+constexpr int kThreads = 512;               // 8 waves
+constexpr int kWaveM = 64;                  // positions per wave
+constexpr int kChunk = 8 * kWaveM;          // positions per chunk
+constexpr int kTileRows = 128;              // weight rows per workgroup
+constexpr int kStepK = 32;                  // reduction columns per step
+constexpr int kRawRing = 4;                 // raw stages: DMA 3 steps ahead of dequantization
+constexpr int kXRing = 3;                   // activation stages: DMA 2 steps ahead of use
+constexpr int kXStage = kWaveM * kStepK * 2;  // bytes per wave and stage
+// Raw stage layout (bytes): plane p at 512 p (one word per tile row), scales
+// of level l at 4096 + 256 l (one binary16 per tile row, up to 8 levels),
+// zero points at 6144 (one byte per tile row).  16-byte DMA slots 0..391
+// carry them; waves 0..6 move slots 64 w .. 64 w + 63.
+constexpr int kRawScaleOff = 4096, kRawZeroOff = 6144, kRawStage = 7168;
+constexpr int kRawSlots = 392, kRawWaves = 7;
+constexpr int kWTile = kTileRows * kStepK * 2;  // dequantized bf16 tile bytes
 
-// Bucket table produced on the device from the routing histogram.
-struct Sched {
-  const int32_t* tstart;  // [nb+1] first M-tile of each bucket (prefix sums)
-  const int32_t* bstart;  // [nb] first position of each bucket
-  const int32_t* bcnt;    // [nb] positions in the bucket
-  int nb;                 // buckets; 0 = one bucket given by the scalars below
-  int one_cnt, one_bit;   // single-bucket mode (shared expert: all tokens)
-  int L, b_min;
-};
+#define D2MOE_GPTR(p) ((__attribute__((address_space(1))) void*)(p))
+#define D2MOE_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
 
-__global__ void schedule_kernel(const int32_t* __restrict__ hist,
-                                const int32_t* __restrict__ offsets, int nb,
-                                int32_t* __restrict__ tstart, int32_t* __restrict__ bstart,
-                                int32_t* __restrict__ bcnt) {
-  if (threadIdx.x != 0) return;
-  int acc = 0;
-  for (int j = 0; j < nb; ++j) {
-    tstart[j] = acc;
-    bstart[j] = offsets[j];
-    bcnt[j] = hist[j];
-    acc += (hist[j] + BM - 1) / BM;
+// Chunk table, written on the device from the routing histogram:
+// chunks[4 c] = first position, positions (0: no work), bit-width, expert.
+// Buckets are taken in order of size (largest first, ties in bucket order)
+// so that the longest workgroups start first.  One workgroup of kChunkThreads
+// threads, one bucket per thread (nb <= kChunkThreads).
+constexpr int kChunkThreads = 512;
+__global__ __launch_bounds__(kChunkThreads) void chunk_kernel(
+    const int32_t* __restrict__ hist, const int32_t* __restrict__ offsets, int nb, int L, int b_min,
+    int one_cnt, int one_bit, int n_ub, int32_t* __restrict__ chunks) {
+  __shared__ int cnt[kChunkThreads], nch[kChunkThreads], first[kChunkThreads];
+  const int j = threadIdx.x;
+  if (hist == nullptr) {  // one bucket: every position, expert 0
+    for (int c = j; c < n_ub; c += kChunkThreads) {
+      const int m0 = c * kChunk;
+      chunks[4 * c] = m0;
+      chunks[4 * c + 1] = m0 < one_cnt ? min(kChunk, one_cnt - m0) : 0;
+      chunks[4 * c + 2] = one_bit;
+      chunks[4 * c + 3] = 0;
+    }
+    return;
   }
-  tstart[nb] = acc;
+  const int cj = j < nb ? hist[j] : 0;
+  cnt[j] = cj;
+  nch[j] = (cj + kChunk - 1) / kChunk;
+  __syncthreads();
+  // chunks of the buckets that come before this one in size order
+  int before = 0;
+  for (int i = 0; i < nb; ++i)
+    if (cnt[i] > cj || (cnt[i] == cj && i < j)) before += nch[i];
+  first[j] = before;
+  __syncthreads();
+  int total = 0;
+  for (int i = 0; i < nb; ++i) total += nch[i];
+  if (j < nb) {
+    const int b0 = offsets[j];
+    for (int q = 0; q < nch[j]; ++q) {
+      const int c = first[j] + q;
+      if (c >= n_ub) break;
+      chunks[4 * c] = b0 + q * kChunk;
+      chunks[4 * c + 1] = min(kChunk, cj - q * kChunk);
+      chunks[4 * c + 2] = b_min + j % L;
+      chunks[4 * c + 3] = j / L;
+    }
+  }
+  for (int c = total + j; c < n_ub; c += kChunkThreads) chunks[4 * c + 1] = 0;
 }
 
 __device__ inline float silu(float a) { return a / (1.0f + __expf(-a)); }
-
 
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef float f2 __attribute__((ext_vector_type(2)));
@@ -63,221 +115,320 @@ __device__ inline uint32_t h2_splat(float v) {
   return as_u(h2{h, h});
 }
 
-// Tiles in LDS are [rows][KS] bf16 (128 bytes per row) with the 16-byte
-// chunks of a row stored at chunk ^ (row & 7), so that the 16 rows an MFMA
-// operand reads spread over the banks.
-__device__ inline int swz(int row, int chunk) { return row * KS + ((chunk ^ (row & 7)) << 3); }
+// LDS accesses to the DMA-filled rings and to the shared tile are inline
+// assembly: with LDS DMA in flight the compiler would otherwise wait for every
+// outstanding vector-memory instruction (draining the prefetch) before each
+// LDS access it cannot prove independent.  Reads are ordered by an explicit
+// lgkmcnt wait and re-bound after it.
+__device__ inline uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+__device__ inline void ld128(u32x4& v, uint32_t a) {
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
+}
+__device__ inline void ld32(uint32_t& v, uint32_t a) {
+  asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(a) : "memory");
+}
+__device__ inline void ldu16(uint32_t& v, uint32_t a) {
+  asm volatile("ds_read_u16 %0, %1" : "=v"(v) : "v"(a) : "memory");
+}
+__device__ inline void ldu8(uint32_t& v, uint32_t a) {
+  asm volatile("ds_read_u8 %0, %1" : "=v"(v) : "v"(a) : "memory");
+}
+__device__ inline void st64(uint32_t a, uint32_t lo, uint32_t hi) {
+  asm volatile("ds_write_b64 %0, %1" ::"v"(a), "v"(u32x2{lo, hi}) : "memory");
+}
+__device__ inline void wait_lgkm() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+template <int N>
+__device__ inline void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ inline void bar() { __builtin_amdgcn_s_barrier(); }
 
-// Grouped expert GEMM: one workgroup computes BM positions x BN weight rows
-// of one (expert, bit-width) bucket.
-//   in:  bf16 activations, position p reads in[src_row(p) * in_ld + k] with
-//        src_row = perm ? perm[p] / kdiv : p
-//   SWIGLU: W is [2f][K] (w13); the tile holds 64 rows of W1 and the same 64
-//           rows of W3 interleaved in 16-row slices, out = h [pos][f] bf16
-//   else:   W is [N][K], out = y [pos][N] fp32
-// Per K step (KS columns): the activations and the plane words, scales and
-// zero points of the next step are loaded into registers while the MFMAs of
-// the current step run; then each thread dequantizes 16 weights of one row
-// into LDS.  Dequantization works on pairs of weights (j, j + 16) of a plane
-// word in packed fp16: shifting the word left by 15 - j puts bit j at bit 15
-// and bit j + 16 at bit 31, the sign positions of the two halves, and v_bfi
-// turns the pair into (+-c_p, +-c_p).  With every plane read as a sign,
+// 16-byte chunk q of tile row r sits at chunk q ^ ((r >> 2) & 3), so that the
+// 16 rows one MFMA operand read touches fall in distinct banks.
+__device__ inline uint32_t swz(int r, int q) { return (uint32_t)(r * 64 + ((q ^ ((r >> 2) & 3)) << 4)); }
+
+// Registers of one step: raw words, scales and zero point of the tile row a
+// thread dequantizes, and the MFMA operands of its wave.
+struct StepRegs {
+  uint32_t w[8];   // plane words
+  uint32_t sp[8];  // binary16 scale of plane p (p >= b_min); register index = plane
+  uint32_t s1, z;  // base scale and zero point
+  u32x4 A[4], B[4];  // B: the weight operands of 64 of the tile's 128 rows
+  __device__ __attribute__((always_inline)) inline void rebind() {
+#pragma unroll
+    for (int p = 0; p < 8; ++p) asm volatile("" : "+v"(w[p]));
+#pragma unroll
+    for (int p = 0; p < 8; ++p) asm volatile("" : "+v"(sp[p]));
+    asm volatile("" : "+v"(s1));
+    asm volatile("" : "+v"(z));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(A[i]));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(B[i]));
+  }
+};
+
+// Dequantization of four weight pairs (columns j, j + 16 for
+// j = 4 dq .. 4 dq + 3) of a tile row at MB planes into bf16 pairs for the
+// tile (o[0..1] columns 4 dq .. 4 dq + 3, o[2..3] columns 16 + 4 dq ..).
+// It works on pairs in packed fp16: shifting a plane word left by 15 - j puts
+// bit j at bit 15 and bit j + 16 at bit 31, the sign positions of the two
+// halves, and v_bfi turns the pair into (+-c_p, +-c_p).  With every plane read
+// as a sign,
 //   W^_b = s1 (Q - z) + sum_{p>=b_min} s_p sigma_p
 //        = C + sum_{p<b} c_p (2 bit_p - 1),  c_p = s1 2^(p-1) for p < b_min,
 //          c_p = s_p for p >= b_min,  C = s1 ((2^b_min - 1) / 2 - z),
 // accumulated in fp16 from C, then rounded to bf16 for the MFMA.
-template <int G, bool SWIGLU>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(const uint16_t* __restrict__ in, int in_ld,
-                                                        const int32_t* __restrict__ perm, int kdiv,
-                                                        MwqView W, int expert_fixed, Sched sc,
-                                                        int f, int N, void* __restrict__ out,
-                                                        int out_ld) {
-  __shared__ __attribute__((aligned(16))) uint16_t xs[BM * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t ws[BN * KS];
-  __shared__ int s_info[4];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-
-  // ---- which bucket / tile ----
-  if (tid == 0) {
-    int j = 0, nb = sc.nb;
-    int mt = blockIdx.y;
-    if (nb == 0) {
-      const int ntiles = (sc.one_cnt + BM - 1) / BM;
-      s_info[0] = mt < ntiles ? 1 : 0;
-      s_info[1] = mt * BM;
-      s_info[2] = min(BM, sc.one_cnt - mt * BM);
-      s_info[3] = sc.one_bit;
-    } else if (mt >= sc.tstart[nb]) {
-      s_info[0] = 0;
-    } else {
-      int lo = 0, hi = nb - 1;  // largest j with tstart[j] <= mt
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (sc.tstart[mid] <= mt) lo = mid; else hi = mid - 1;
-      }
-      j = lo;
-      const int local = mt - sc.tstart[j];
-      s_info[0] = 1;
-      s_info[1] = sc.bstart[j] + local * BM;
-      s_info[2] = min(BM, sc.bcnt[j] - local * BM);
-      s_info[3] = sc.b_min + (j % sc.L);
-      s_info[0] |= (j / sc.L) << 1;  // expert in the upper bits
+template <int MB>
+__device__ __attribute__((always_inline)) inline void dequant_pairs(
+    const StepRegs& R, int b_min, uint32_t sh_m, int dq, bool d_ok, uint32_t (&o)[4]) {
+  const float s1 = h2f((uint16_t)R.s1);
+  const uint32_t C = h2_splat(s1 * ((float)((1 << b_min) - 1) * 0.5f - (float)R.z));
+  h2 a[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) a[j] = as_h2(C);
+#pragma unroll
+  for (int p = 0; p < MB; ++p) {
+    const float c = p < b_min ? s1 * (float)(1 << p) * 0.5f : h2f((uint16_t)R.sp[p]);
+    const uint32_t cp = h2_splat(c) & 0x7fff7fffu;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t t = R.w[p] << (15 - (4 * dq + j));
+      const uint32_t v = (sh_m & t) | (~sh_m & cp);  // bit set -> -c_p
+      a[j] = a[j] - as_h2(v);
     }
   }
-  __syncthreads();
-  if (!(s_info[0] & 1)) return;
-  const int expert = sc.nb == 0 ? expert_fixed : (s_info[0] >> 1);
-  const int pos0 = s_info[1], cnt = s_info[2], bits = s_info[3];
-  const int n0 = blockIdx.x * (SWIGLU ? BN / 2 : BN);  // first output row
-  const int K = W.cols, BR = W.BR(), b_min = W.b_min;
+  const uint32_t a0 = h2_to_bf2(a[0]), a1 = h2_to_bf2(a[1]);
+  const uint32_t a2 = h2_to_bf2(a[2]), a3 = h2_to_bf2(a[3]);
+  o[0] = (a0 & 0xffffu) | (a1 << 16);          // columns 4 dq, 4 dq + 1
+  o[1] = (a2 & 0xffffu) | (a3 << 16);          // 4 dq + 2, 4 dq + 3
+  o[2] = (a0 >> 16) | (a1 & 0xffff0000u);      // 16 + 4 dq, ...
+  o[3] = (a2 >> 16) | (a3 & 0xffff0000u);
+  if (!d_ok) o[0] = o[1] = o[2] = o[3] = 0u;
+}
 
-  // ---- activation loader: row xr, 16-byte chunks 4 xh .. 4 xh + 3 ----
-  const int xr = tid >> 1, xh = tid & 1;
-  const uint16_t* xsrc = nullptr;
-  if (xr < cnt) {
-    const int pos = pos0 + xr;
-    xsrc = in + (size_t)(perm ? perm[pos] / kdiv : pos) * in_ld + 32 * xh;
-  }
-  // ---- dequantizer: tile row dc, 32-column word dsub, pairs 8 dh .. 8 dh + 7 ----
-  const int item = tid >> 1, dh = tid & 1;
-  const int dc = item >> 1, dsub = item & 1;
-  int mrow;  // matrix row of tile row dc
-  bool drow_ok;
-  if (SWIGLU) {
-    const int dwn = dc >> 6, cc = dc & 63, sl = cc >> 4;
-    const int hrow = n0 + 32 * dwn + 16 * (sl >> 1) + (cc & 15);
-    drow_ok = hrow < f;
-    mrow = ((sl & 1) ? f : 0) + hrow;
-  } else {
-    mrow = n0 + dc;
-    drow_ok = mrow < N;
-  }
-  const int drb = drow_ok ? mrow / BR : 0, dib = drow_ok ? mrow % BR : 0;
-  uint32_t sh_m;  // opaque copy of the sign mask: keeps v_bfi on registers
-  asm volatile("" : "=v"(sh_m) : "0"(0x80008000u));
+// One workgroup: chunk blockIdx.y of the chunk table against weight-row tile
+// blockIdx.x.
+//   in:  bf16 activations; position p reads row (perm ? perm[p] / kdiv : p)
+//   SWIGLU: W is [2f][K] (w13); the tile holds W1 rows n0..n0+63 (tile rows
+//           0..63) and W3 rows f+n0.. (tile rows 64..127); out = h [pos][f] bf16
+//   else:   W is [N][K], out = y [pos][N] fp32
+// `expert_fixed` >= 0 overrides the chunk's expert (the shared expert).
+template <int G, bool SWIGLU>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void bgemm_kernel(
+    const uint16_t* __restrict__ in, int in_ld, const int32_t* __restrict__ perm, int kdiv,
+    MwqView W, const int32_t* __restrict__ chunks, int f, int N, void* __restrict__ out,
+    int out_ld) {
+  __shared__ __attribute__((aligned(16))) uint8_t xring[kXRing][8][kXStage];
+  __shared__ __attribute__((aligned(16))) uint8_t rraw[kRawRing][kRawStage];
+  __shared__ __attribute__((aligned(16))) uint8_t wtile[2][kWTile];
+  __shared__ __attribute__((aligned(16))) uint8_t dummy[1][16];
+  constexpr int BR = 2048 / G, SPG = G / kStepK;  // rows per block, steps per group
 
-  uint4 xreg[4];
-  uint32_t preg[8];
-  uint16_t sreg[8];
-  uint32_t zreg = 0;
-  auto load_step = [&](int k0) {
+  const int ci = blockIdx.y;
+  const int m_first = chunks[4 * ci], m_cnt = chunks[4 * ci + 1];
+  const int bits = chunks[4 * ci + 2], expert = chunks[4 * ci + 3];
+  if (m_cnt == 0) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n0 = blockIdx.x * (SWIGLU ? kTileRows / 2 : kTileRows);
+  const int K = W.cols, nsteps = K / kStepK, b_min = W.b_min;
+  const int nlev = bits - b_min + 1;
+  const int nout = SWIGLU ? f : N;
+  const bool active = kWaveM * wave < m_cnt;  // wave-uniform
+
+  // ---- raw weight DMA: this lane's 16-byte slot u of the stage ----
+  // global row of tile row r
+  auto grow = [&](int r) { return SWIGLU ? (r < 64 ? n0 + r : f + n0 + r - 64) : n0 + r; };
+  auto row_ok = [&](int r) { return SWIGLU ? n0 + (r & 63) < f : n0 + r < N; };
+  const int u = 64 * wave + lane;
+  const uint8_t* rsrc = (const uint8_t*)W.planes;  // address at step 0
+  int rstride_b = 0, rstride_c = 0;                 // per group, per 32-column step
+  bool rreal = false;
+  if (u < 256) {  // plane p = u / 32, tile rows 4 v .. 4 v + 3 of it
+    const int p = u >> 5, v = u & 31;
+    const int r = 4 * v;  // first tile row of the slot
+    if (p < bits && row_ok(r)) {
+      const int gr = grow(r);
+      const size_t blk = W.block(expert, gr / BR, 0);
+      rsrc = (const uint8_t*)(W.planes + W.plane_word(blk, p, gr % BR));
+      rstride_b = W.b_max * 64 * 4;
+      rstride_c = BR * 4;
+      rreal = true;
+    }
+  } else if (u < 256 + 16 * 8) {  // level l, tile rows 8 v .. 8 v + 7
+    const int l = (u - 256) >> 4, v = (u - 256) & 15;
+    const int r = 8 * v;
+    if (l < nlev && row_ok(r)) {
+      const int gr = grow(r);
+      const size_t blk = W.block(expert, gr / BR, 0);
+      rsrc = (const uint8_t*)(W.scales + W.scale_idx(blk, l, gr % BR));
+      rstride_b = W.levels() * BR * 2;
+      rreal = true;
+    }
+  } else if (u < kRawSlots) {  // zero points, tile rows 16 z .. 16 z + 15
+    const int z = u - 256 - 16 * 8;
+    const int r = 16 * z;
+    if (row_ok(r)) {
+      const int gr = grow(r);
+      const size_t blk = W.block(expert, gr / BR, 0);
+      rsrc = W.zeros + W.zero_idx(blk, gr % BR);
+      rstride_b = BR;
+      rreal = true;
+    }
+  }
+  // every wave issues one raw DMA per step (lane 0 at least), so that all
+  // waves count the same memory instructions; idle slots write a dummy area
+  const bool rissue = rreal || lane == 0;
+  const uint32_t rdst_off = wave < kRawWaves ? 1024u * wave : 0u;
+  auto raw_dma = [&](int step) {
+    const int st = step < nsteps ? step : nsteps - 1;  // past the end: reload, unused
+    const uint8_t* src = rsrc + (size_t)(st / SPG) * rstride_b + (st % SPG) * rstride_c;
+    uint8_t* dst = wave < kRawWaves ? &rraw[step % kRawRing][rdst_off] : dummy[0];
+    if (rissue)
+      __builtin_amdgcn_global_load_lds(D2MOE_GPTR(src), D2MOE_LPTR(dst), 16, 0, 0);
+  };
+
+  // ---- activation DMA: instruction i moves tile rows 16 i .. 16 i + 15 ----
+  const uint16_t* xsrc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int rl = 16 * i + (lane >> 2);
+    int pos = m_first + kWaveM * wave + rl;
+    pos = pos < m_first + m_cnt ? pos : m_first + m_cnt - 1;
+    const int src = perm ? perm[pos] / kdiv : pos;
+    const int q = (lane & 3) ^ ((rl >> 2) & 3);
+    xsrc[i] = in + (size_t)src * in_ld + 8 * q;
+  }
+  auto x_dma = [&](int step) {
+    const int st = step < nsteps ? step : nsteps - 1;
+    uint8_t* dst = xring[step % kXRing][wave];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      xreg[i] = xsrc ? *(const uint4*)(xsrc + k0 + 8 * i) : uint4{0u, 0u, 0u, 0u};
-    if (drow_ok) {
-      const size_t blk = W.block(expert, drb, k0 / G);
-      const int wq = ((k0 % G) / 32 + dsub) * BR + dib;
-#pragma unroll
-      for (int p = 0; p < 8; ++p)
-        if (p < bits) preg[p] = W.planes[W.plane_word(blk, p, wq)];
-#pragma unroll
-      for (int l = 0; l < 8; ++l)
-        if (l < bits - b_min + 1) sreg[l] = W.scales[W.scale_idx(blk, l, dib)];
-      zreg = W.zeros[W.zero_idx(blk, dib)];
-    }
-  };
-  auto store_step = [&]() {
-    // activations
-    uint4* xd = (uint4*)xs;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) xd[swz(xr, 4 * xh + i) >> 3] = xreg[i];
-    // weights
-    uint32_t lo[4], hi[4];
-    if (drow_ok) {
-      const float s1 = h2f(sreg[0]);
-      uint32_t cp[8];
-#pragma unroll
-      for (int p = 0; p < 8; ++p) {
-        const float c = p < b_min ? s1 * (float)(1 << p) * 0.5f : (p < bits ? h2f(sreg[p - b_min + 1]) : 0.0f);
-        cp[p] = h2_splat(c) & 0x7fff7fffu;
-      }
-      const uint32_t C = h2_splat(s1 * ((float)((1 << b_min) - 1) * 0.5f - (float)zreg));
-      h2 acc[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) acc[j] = as_h2(C);
-#pragma unroll
-      for (int p = 0; p < 8; ++p) {
-        if (p >= bits) break;  // uniform
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const uint32_t t = preg[p] << (15 - (8 * dh + j));
-          const uint32_t v = (sh_m & t) | (~sh_m & cp[p]);  // bit set -> -c_p
-          acc[j] = acc[j] - as_h2(v);
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t a = h2_to_bf2(acc[2 * j]), b = h2_to_bf2(acc[2 * j + 1]);
-        lo[j] = (a & 0xffffu) | (b << 16);          // weights 8 dh + 2j, +1
-        hi[j] = (a >> 16) | (b & 0xffff0000u);      // weights 16 + 8 dh + 2j, +1
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) lo[j] = hi[j] = 0u;
-    }
-    uint4* wd = (uint4*)ws;
-    wd[swz(dc, 4 * dsub + dh) >> 3] = uint4{lo[0], lo[1], lo[2], lo[3]};
-    wd[swz(dc, 4 * dsub + 2 + dh) >> 3] = uint4{hi[0], hi[1], hi[2], hi[3]};
+      if (active || lane == 0)
+        __builtin_amdgcn_global_load_lds(D2MOE_GPTR(xsrc[i] + kStepK * st),
+                                         D2MOE_LPTR(dst + 1024 * i), 16, 0, 0);
   };
 
-  f32x4 acc[4][4];
+  // ---- dequantization: tile row dr, columns 4 dq .. 4 dq + 3 and +16 ----
+  const int dr = tid >> 2, dq = tid & 3;
+  uint32_t sh_m;  // opaque copy of the sign mask: keeps v_bfi on registers
+  asm volatile("" : "=v"(sh_m) : "0"(0x80008000u));
+  const bool d_ok = row_ok(dr);
+  const int fr = lane & 15, fq = lane >> 4;
+
+  f32x4 acc[4][8];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int b = 0; b < 8; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int nsteps = K / KS;
-  load_step(0);
-  store_step();
-  __syncthreads();
-  for (int st = 0; st < nsteps; ++st) {
-    if (st + 1 < nsteps) load_step((st + 1) * KS);
+  // One step: dequantize tile `dstep` from its raw stage into the other tile
+  // buffer, then (if `mma`) the products of `mstep`, the weight operands read
+  // in two halves of 64 rows.
+  StepRegs R;
+  auto step = [&](int dstep, int mstep, bool mma) {
+    const uint32_t rb = lds_addr(rraw[dstep % kRawRing]);
 #pragma unroll
-    for (int kk = 0; kk < KS / 32; ++kk) {
-      bf16x8 bfr[4];
+    for (int p = 0; p < 8; ++p)
+      if (p < bits) ld32(R.w[p], rb + 512 * p + 4 * dr);
+    ldu16(R.s1, rb + kRawScaleOff + 2 * dr);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const int col = 64 * wn + 16 * nt + (lane & 15);
-        bfr[nt] = *(const bf16x8*)(ws + swz(col, 4 * kk + (lane >> 4)));
-      }
+    for (int p = 0; p < 8; ++p)  // level p - b_min + 1 holds the scale of plane p
+      if (p >= b_min && p < bits) ldu16(R.sp[p], rb + kRawScaleOff + 256 * (p - b_min + 1) + 2 * dr);
+    ldu8(R.z, rb + kRawZeroOff + dr);
+    wait_lgkm();
+    R.rebind();
+    uint32_t o[4];
+    switch (bits) {
+#define D2MOE_CASE(MB) \
+  case MB: dequant_pairs<MB>(R, b_min, sh_m, dq, d_ok, o); break;
+      D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4)
+      D2MOE_CASE(5) D2MOE_CASE(6) D2MOE_CASE(7) D2MOE_CASE(8)
+#undef D2MOE_CASE
+      default: o[0] = o[1] = o[2] = o[3] = 0u; break;
+    }
+    const uint32_t wd = lds_addr(wtile[dstep & 1]);
+    st64(wd + swz(dr, dq >> 1) + 8 * (dq & 1), o[0], o[1]);
+    st64(wd + swz(dr, 2 + (dq >> 1)) + 8 * (dq & 1), o[2], o[3]);
+    if (mma) {
+      const uint32_t xb = lds_addr(xring[mstep % kXRing][wave]);
+      const uint32_t wb = lds_addr(wtile[mstep & 1]);
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-        const int row = 64 * wm + 16 * mt + (lane & 15);
-        const bf16x8 afr = *(const bf16x8*)(xs + swz(row, 4 * kk + (lane >> 4)));
+      for (int half = 0; half < 2; ++half) {
+        if (half == 0)
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt)
-          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afr, bfr[nt], acc[mt][nt], 0, 0, 0);
+          for (int mt = 0; mt < 4; ++mt) ld128(R.A[mt], xb + swz(16 * mt + fr, fq));
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) ld128(R.B[nt], wb + swz(16 * (4 * half + nt) + fr, fq));
+        wait_lgkm();
+        R.rebind();
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt)
+            acc[mt][4 * half + nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, R.A[mt]), __builtin_bit_cast(bf16x8, R.B[nt]),
+                acc[mt][4 * half + nt], 0, 0, 0);
       }
     }
-    __syncthreads();
-    if (st + 1 < nsteps) {
-      store_step();
-      __syncthreads();
-    }
+    wait_lgkm();
+  };
+
+  // ---- prologue: raw 0..3 and activations 0..1 in flight, tile 0 ready ----
+  // issue order: raw 0, raw 1, [raw 2, x 0], [raw 3, x 1]; the wait leaves the
+  // last 11 instructions outstanding, i.e. raw 0 has landed
+  raw_dma(0);
+  raw_dma(1);
+  raw_dma(2);
+  x_dma(0);
+  raw_dma(3);
+  x_dma(1);
+  wait_vm<11>();
+  bar();
+  step(0, 0, false);
+
+  // ---- main loop: step s issues raw s+4 and activations s+2, dequantizes
+  // s+1 and multiplies s.  At the top of step s the instructions issued after
+  // the activations of s are the 5 of step s-1 (raw s+3, activations s+1), and
+  // raw s+1 was issued before the activations of s, so vmcnt(5) makes both
+  // this wave's raw s+1 and its activations of s ready; the barrier then
+  // makes every wave's raw s+1 and tile s visible, and retires all reads of
+  // the stages and the tile buffer that this step overwrites.  In the last
+  // step the dequantization works on a reloaded stage and its tile is never
+  // read.
+  for (int s = 0; s < nsteps; ++s) {
+    wait_vm<5>();
+    bar();
+    raw_dma(s + 4);
+    x_dma(s + 2);
+    step(s + 1, s, active);
   }
+  wait_vm<0>();  // no DMA may still be writing this workgroup's LDS at exit
 
   // ---- epilogue ----
+  if (!active) return;
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int m = 64 * wm + 16 * mt + 4 * (lane >> 4) + r;
-      if (m >= cnt) continue;
-      const size_t pos = (size_t)(pos0 + m);
+      const int m = kWaveM * wave + 16 * mt + 4 * (lane >> 4) + r;
+      if (m >= m_cnt) continue;
+      const size_t pos = (size_t)(m_first + m);
       if (SWIGLU) {
 #pragma unroll
-        for (int sp = 0; sp < 2; ++sp) {
-          const int n = n0 + 32 * wn + 16 * sp + (lane & 15);
+        for (int nt = 0; nt < 4; ++nt) {
+          const int n = n0 + 16 * nt + (lane & 15);
           if (n >= f) continue;
-          const float a = acc[mt][2 * sp][r], c = acc[mt][2 * sp + 1][r];
+          const float a = acc[mt][nt][r], c = acc[mt][nt + 4][r];
           ((uint16_t*)out)[pos * out_ld + n] = f2bf(silu(a) * c);
         }
       } else {
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-          const int n = n0 + 64 * wn + 16 * nt + (lane & 15);
+        for (int nt = 0; nt < 8; ++nt) {
+          const int n = n0 + 16 * nt + (lane & 15);
           if (n >= N) continue;
           ((float*)out)[pos * out_ld + n] = acc[mt][nt][r];
         }
@@ -315,24 +466,28 @@ __global__ void combine_kernel(const float* __restrict__ y, const float* __restr
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
+// Chunk-table bound for n positions in nb buckets: every nonempty bucket
+// contributes one chunk plus one per kChunk positions.
+int chunk_bound(int n, int nb) { return (nb < n ? nb : n) + (n + kChunk - 1) / kChunk; }
+
 template <bool SWIGLU>
 hipError_t run_gemm(const uint16_t* in, int in_ld, const int32_t* perm, int kdiv, const MwqView& W,
-                    int expert_fixed, const Sched& sc, int mtiles_ub, int f, void* out, int out_ld,
+                    const int32_t* chunks, int n_ub, int f, void* out, int out_ld,
                     hipStream_t s) {
   const int N = SWIGLU ? W.rows / 2 : W.rows;
-  const int per = SWIGLU ? BN / 2 : BN;
-  // output-row tiles vary fastest: consecutive workgroups, which the
-  // dispatcher deals round-robin to the 8 XCDs, share one M-tile, so every
-  // XCD's L2 holds the activations of the one or two M-tiles in flight
+  const int per = SWIGLU ? kTileRows / 2 : kTileRows;
+  // weight-row tiles vary fastest: consecutive workgroups, which the
+  // dispatcher deals round-robin to the 8 XCDs, share one chunk, so every
+  // XCD's L2 holds the activations of the one or two chunks in flight
   // rather than of all of them
-  dim3 grid((N + per - 1) / per, mtiles_ub);
-  if (mtiles_ub <= 0) return hipSuccess;
+  dim3 grid((N + per - 1) / per, n_ub);
+  if (n_ub <= 0) return hipSuccess;
   if (W.group == 128)
-    gemm_kernel<128, SWIGLU><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, expert_fixed, sc,
-                                                       f, N, out, out_ld);
+    bgemm_kernel<128, SWIGLU><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f, N,
+                                                        out, out_ld);
   else
-    gemm_kernel<64, SWIGLU><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, expert_fixed, sc,
-                                                      f, N, out, out_ld);
+    bgemm_kernel<64, SWIGLU><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f, N,
+                                                       out, out_ld);
   return hipGetLastError();
 }
 
@@ -340,9 +495,12 @@ hipError_t run_gemm(const uint16_t* in, int in_ld, const int32_t* perm, int kdiv
 
 FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shared_d_ff) {
   FwdWorkspace L;
-  const size_t nb = (size_t)E * 8 + 1;
   size_t off = 0;
-  L.sched_off = off;  off += align256(sizeof(int32_t) * (4 * nb + 4));
+  // chunk tables of the routed experts (at most 8 bit-widths per expert) and
+  // of the shared expert
+  L.chunk_n = chunk_bound(T * k, E * 8);
+  L.schunk_n = shared_d_ff > 0 ? chunk_bound(T, 1) : 0;
+  L.sched_off = off;  off += align256(sizeof(int32_t) * 4 * (size_t)(L.chunk_n + L.schunk_n));
   L.h_off = off;      off += align256(sizeof(uint16_t) * (size_t)T * k * d_ff);
   L.hs_off = off;     off += align256(sizeof(uint16_t) * (size_t)T * shared_d_ff);
   L.y_off = off;      off += align256(sizeof(float) * (size_t)T * k * d);
@@ -375,9 +533,8 @@ hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff,
   char* base = (char*)ws;
   const int Lv = w13->b_max - w13->b_min + 1;
   const int nb = E * Lv;
-  int32_t* tstart = (int32_t*)(base + L.sched_off);
-  int32_t* bstart = tstart + (nb + 1);
-  int32_t* bcnt = bstart + nb;
+  int32_t* chunks = (int32_t*)(base + L.sched_off);
+  int32_t* schunks = chunks + 4 * (size_t)L.chunk_n;
   uint16_t* h = (uint16_t*)(base + L.h_off);
   uint16_t* hs = (uint16_t*)(base + L.hs_off);
   float* y = (float*)(base + L.y_off);
@@ -408,29 +565,30 @@ hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff,
     err = launch_decode_ffn(x, xd, T, d, d_ff, E, k, w13, w2, r, db, s, events);
     if (err != hipSuccess) return err;
   } else {
-    schedule_kernel<<<1, 64, 0, s>>>(r->hist, r->offsets, nb, tstart, bstart, bcnt);
+    const int n_ub = chunk_bound(T * k, nb);
+    chunk_kernel<<<1, kChunkThreads, 0, s>>>(r->hist, r->offsets, nb, Lv, w13->b_min, 0, 0, n_ub,
+                                            chunks);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    Sched sc{tstart, bstart, bcnt, nb, 0, 0, Lv, w13->b_min};
-    const int n = T * k;
-    const int ub = (n + BM - 1) / BM + (nb < n ? nb : n);
     const MwqView W13 = view_of(w13), W2 = view_of(w2);
     if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
-    err = run_gemm<true>(xb, d, r->perm, k, W13, 0, sc, ub, d_ff, h, d_ff, s);
+    err = run_gemm<true>(xb, d, r->perm, k, W13, chunks, n_ub, d_ff, h, d_ff, s);
     if (err != hipSuccess) return err;
     if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
     if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
-    err = run_gemm<false>(h, d_ff, nullptr, 1, W2, 0, sc, ub, d_ff, y, d, s);
+    err = run_gemm<false>(h, d_ff, nullptr, 1, W2, chunks, n_ub, d_ff, y, d, s);
     if (err != hipSuccess) return err;
     if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
   }
 
   if (has_shared) {
-    Sched one{nullptr, nullptr, nullptr, 0, T, shared_bits, 1, sw13->b_min};
-    const int ubs = (T + BM - 1) / BM;
+    const int ns_ub = chunk_bound(T, 1);
+    chunk_kernel<<<1, kChunkThreads, 0, s>>>(nullptr, nullptr, 0, 1, sw13->b_min, T, shared_bits,
+                                            ns_ub, schunks);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
     const MwqView S13 = view_of(sw13), S2 = view_of(sw2);
-    err = run_gemm<true>(xb, d, nullptr, 1, S13, 0, one, ubs, shared_d_ff, hs, shared_d_ff, s);
+    err = run_gemm<true>(xb, d, nullptr, 1, S13, schunks, ns_ub, shared_d_ff, hs, shared_d_ff, s);
     if (err != hipSuccess) return err;
-    err = run_gemm<false>(hs, shared_d_ff, nullptr, 1, S2, 0, one, ubs, shared_d_ff, ys, d, s);
+    err = run_gemm<false>(hs, shared_d_ff, nullptr, 1, S2, schunks, ns_ub, shared_d_ff, ys, d, s);
     if (err != hipSuccess) return err;
   }
 

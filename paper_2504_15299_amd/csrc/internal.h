@@ -77,6 +77,7 @@ struct FwdWorkspace {
   size_t sched_off, h_off, hs_off, y_off, ys_off, xb_off;
   size_t elist_off, xq13_off, xs13_off, h32_off, xq2_off, xs2_off, hmax_off;
   size_t total;
+  int chunk_n, schunk_n;  // grouped-GEMM chunk-table entries (routed, shared)
 };
 
 struct DecodeBuffers {
