@@ -181,18 +181,25 @@ struct StepRegs {
 //        = C + sum_{p<b} c_p (2 bit_p - 1),  c_p = s1 2^(p-1) for p < b_min,
 //          c_p = s_p for p >= b_min,  C = s1 ((2^b_min - 1) / 2 - z),
 // accumulated in fp16 from C, then rounded to bf16 for the MFMA.
-template <int MB>
+// BMIN > 0 fixes b_min at compile time (the common ladder starts at 2 bits);
+// BMIN == 0 takes it from `b_min_rt`.
+template <int MB, int BMIN>
 __device__ __attribute__((always_inline)) inline void dequant_pairs(
-    const StepRegs& R, int b_min, uint32_t sh_m, int dq, bool d_ok, uint32_t (&o)[4]) {
+    const StepRegs& R, int b_min_rt, uint32_t sh_m, int dq, bool d_ok, uint32_t (&o)[4]) {
+  const int b_min = BMIN > 0 ? BMIN : b_min_rt;
   const float s1 = h2f((uint16_t)R.s1);
   const uint32_t C = h2_splat(s1 * ((float)((1 << b_min) - 1) * 0.5f - (float)R.z));
+  // base scale as a binary16 pair; every scale is >= 0, so the pair of a
+  // residual plane is its scale bits duplicated, and that of a base plane
+  // p < b_min is s1 2^(p-1), a power-of-two multiple in binary16
+  const h2 s1p = as_h2(R.s1 | (R.s1 << 16));
   h2 a[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) a[j] = as_h2(C);
 #pragma unroll
   for (int p = 0; p < MB; ++p) {
-    const float c = p < b_min ? s1 * (float)(1 << p) * 0.5f : h2f((uint16_t)R.sp[p]);
-    const uint32_t cp = h2_splat(c) & 0x7fff7fffu;
+    const _Float16 k = (_Float16)((float)(1 << p) * 0.5f);
+    const uint32_t cp = p < b_min ? as_u(s1p * h2{k, k}) : (R.sp[p] | (R.sp[p] << 16));
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const uint32_t t = R.w[p] << (15 - (4 * dq + j));
@@ -342,13 +349,25 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     wait_lgkm();
     R.rebind();
     uint32_t o[4];
-    switch (bits) {
+    o[0] = o[1] = o[2] = o[3] = 0u;
+    if (b_min == 2) {
+      switch (bits) {
 #define D2MOE_CASE(MB) \
-  case MB: dequant_pairs<MB>(R, b_min, sh_m, dq, d_ok, o); break;
-      D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4)
-      D2MOE_CASE(5) D2MOE_CASE(6) D2MOE_CASE(7) D2MOE_CASE(8)
+  case MB: dequant_pairs<MB, 2>(R, b_min, sh_m, dq, d_ok, o); break;
+        D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6) D2MOE_CASE(7)
+        D2MOE_CASE(8)
 #undef D2MOE_CASE
-      default: o[0] = o[1] = o[2] = o[3] = 0u; break;
+        default: break;
+      }
+    } else {
+      switch (bits) {
+#define D2MOE_CASE(MB) \
+  case MB: dequant_pairs<MB, 0>(R, b_min, sh_m, dq, d_ok, o); break;
+        D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
+        D2MOE_CASE(7) D2MOE_CASE(8)
+#undef D2MOE_CASE
+        default: break;
+      }
     }
     const uint32_t wd = lds_addr(wtile[dstep & 1]);
     st64(wd + swz(dr, dq >> 1) + 8 * (dq & 1), o[0], o[1]);

@@ -14,9 +14,9 @@ from collections import defaultdict
 
 
 def _short(name: str) -> str:
-    for key in ("decode_kernel<true", "decode_kernel<false", "xprep_kernel", "gemm_kernel",
+    for key in ("decode_kernel<true", "decode_kernel<false", "xprep_kernel", "bgemm_kernel", "gemm_kernel",
                 "combine_kernel", "gate_kernel", "topk_kernel", "hist_perm_kernel",
-                "schedule_kernel", "pack_kernel"):
+                "schedule_kernel", "pack_kernel", "chunk_kernel", "route_kernel", "to_bf16_kernel"):
         if key in name:
             return name[name.find(key):][:90]
     return name[:90]
