@@ -57,6 +57,9 @@ def main():
     ap.add_argument("--fine-steps", type=int, default=10,
                     help="also time the 512-token fine-grained layer (64 routed experts top-6 "
                          "plus a shared expert; 0: skip)")
+    ap.add_argument("--stack-steps", type=int, default=128,
+                    help="also run the 32-layer decoder stack of MoE layers, 64 sequences, "
+                         "this many decode steps (0: skip)")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of one captured HIP graph per layer step instead of "
                          "eager launches")
@@ -315,6 +318,77 @@ def main():
                 "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4), "alg_GFLOP": round(flop / 1e9, 2),
                 "TFLOPs": round(tflops, 1), "mfma_frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4)}
 
+    def run_stack(steps, n_layers=32, T=64, eps=1e-5):
+        """Decoder stack: n_layers Mixtral-8x7B-shaped MoE layers, each block
+        x <- x + MoE_l(rmsnorm(x)) (attention absent), all layers resident,
+        MWQ group 128 nested to 8 bits; 64 sequences, each a request with one
+        bit-width tier from {2,4,8} for every expert and layer; each decode
+        step feeds the previous step's final hidden state.  Reports tokens/s
+        over all steps and the algorithmic HBM bytes of a step (every layer's
+        active experts at their largest bit-width, from the last step's
+        routing)."""
+        stack = []
+        for l in range(n_layers):
+            w13 = api.MWQ.empty(E, 2 * f, d, g, b_min, b_max, device=dev)
+            w2 = api.MWQ.empty(E, d, f, g, b_min, b_max, device=dev)
+            for e in range(E):
+                gen.manual_seed(50_000_017 * (l + 1) + 2 * e)
+                api.pack_mwq(torch.randn((1, 2 * f, d), generator=gen, device=dev) * 0.02,
+                             w13.expert(e))
+                gen.manual_seed(50_000_017 * (l + 1) + 2 * e + 1)
+                api.pack_mwq(torch.randn((1, d, f), generator=gen, device=dev) * 0.02,
+                             w2.expert(e))
+            gen.manual_seed(5000 + l)
+            Wg = torch.randn((E, d), generator=gen, device=dev) * 0.02
+            stack.append((w13, w2, Wg, api.Routing.empty(T, E, k, b_min, b_max, device=dev)))
+        torch.cuda.synchronize()
+        rng = np.random.default_rng(5)
+        tiers = rng.choice(np.array([2, 4, 8], np.uint8), size=(T, 1))
+        table = torch.from_numpy(np.repeat(tiers, E, axis=1)).to(dev)
+        req = torch.arange(T, dtype=torch.int32, device=dev)
+        x0 = torch.from_numpy(rng.standard_normal((T, d), dtype=np.float32)).to(dev)
+        x = x0.clone()
+        h = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+        y = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+        ws = torch.empty(api.moe_forward_workspace(T, d, f, E, k), dtype=torch.uint8, device=dev)
+
+        def decode_step():
+            for w13, w2, Wg, r in stack:
+                api.route(h, Wg, None, k, req, table, b_min, b_max, out=r)
+                api.moe_forward(h, w13, w2, r, k, out=y, workspace=ws)
+                api.residual_rmsnorm(x, y, eps, h=h)
+
+        api.residual_rmsnorm(x, None, eps, h=h)
+        decode_step()                      # warm-up step, then restart from x0
+        x.copy_(x0)
+        api.residual_rmsnorm(x, None, eps, h=h)
+        torch.cuda.synchronize()
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_stop = torch.cuda.Event(enable_timing=True)
+        t_start.record()
+        for _ in range(steps):
+            decode_step()
+        t_stop.record()
+        torch.cuda.synchronize()
+        ms = t_start.elapsed_time(t_stop)
+        step_bytes = 0
+        for w13, w2, Wg, r in stack:
+            for b in r.expert_maxbit.cpu().numpy():
+                step_bytes += mwq_bytes(2 * f, d, g, b_min, int(b)) + mwq_bytes(d, f, g, b_min, int(b))
+        gbps = step_bytes * steps / (ms * 1e-3) / 1e9
+        finite = bool(torch.isfinite(x).all().item())
+        del stack
+        torch.cuda.empty_cache()
+        return {"workload": f"{n_layers}-layer decoder stack of Mixtral-8x7B-shaped MoE layers "
+                            f"(x <- x + MoE(rmsnorm(x)), attention absent), {T} sequences x "
+                            f"{steps} decode steps, per-sequence bit tier from {{2,4,8}}, "
+                            f"group 128, 8-bit nest, all layers resident",
+                "layers": n_layers, "sequences": T, "steps": steps,
+                "ms_total": round(ms, 2), "ms_per_step": round(ms / steps, 4),
+                "tokens_per_s": round(T * steps / (ms * 1e-3), 1),
+                "alg_bytes_per_step": step_bytes, "hbm_GBps": round(gbps, 1),
+                "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4), "hidden_state_finite": finite}
+
     main_res = run_batch(args.batch, args.steps, args.warmup, profile=True)
     sweep = []
     for T in [int(v) for v in args.sweep.split(",") if v.strip()]:
@@ -323,6 +397,7 @@ def main():
 
     prefill = run_prefill(args.prefill_steps, 2) if args.prefill_steps > 0 else None
     fine = run_fine(args.fine_steps, 2) if args.fine_steps > 0 else None
+    stack_res = run_stack(args.stack_steps) if args.stack_steps > 0 else None
 
     cpu = None
     if not args.no_cpu:
@@ -364,6 +439,7 @@ def main():
         "sweep": sweep,
         "prefill": prefill,
         "fine_grained": fine,
+        "stack": stack_res,
         "cpu_baseline": cpu,
         "pack_seconds": round(pack_s, 2),
     }

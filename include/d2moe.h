@@ -196,6 +196,23 @@ d2moe_status d2moe_moe_forward_profiled(const void* x, d2moe_dtype x_dtype, int3
                                         size_t ws_bytes, void* stream,
                                         void* const* events);
 
+/*
+ * Residual update and normalisation between the MoE layers of a decoder
+ * stack.  The decoders the paper evaluates (Mixtral-8x7B, LLaMA-MoE,
+ * Sec. 5.1) feed every MoE layer the RMS-normalised hidden state and add the
+ * layer's output to the residual stream; the normalisation weight is taken
+ * as all ones:
+ *     x[t] += y[t]                          (skipped when y is NULL)
+ *     h[t]  = x[t] / sqrt(mean_c x[t][c]^2 + eps)
+ *   x: device [T][d] float, the residual stream, updated in place
+ *   y: device [T][d] (y_dtype, bf16 or f32) or NULL
+ *   h: device [T][d] (h_dtype); bf16 is rounded to nearest even
+ * 1 <= d <= 16384, T >= 0, eps >= 0.  Accumulation is fp32.
+ */
+d2moe_status d2moe_residual_rmsnorm(float* x, const void* y, d2moe_dtype y_dtype,
+                                    int32_t T, int32_t d, float eps, void* h,
+                                    d2moe_dtype h_dtype, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

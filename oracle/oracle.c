@@ -403,6 +403,20 @@ int oracle_expert_ffn(int d, int f, int d_out, int group13, int group2, int b_mi
   return 0;
 }
 
+/* ---- decoder stack: normalisation before each MoE layer -------------- */
+
+int oracle_rmsnorm(int T, int d, double eps, const double* x, double* h) {
+  if (T < 0 || d <= 0 || !(eps >= 0.0)) return -1;
+  for (int t = 0; t < T; ++t) {
+    const double* row = x + (size_t)t * d;
+    double ss = 0.0;
+    for (int c = 0; c < d; ++c) ss += row[c] * row[c];
+    const double inv = 1.0 / sqrt(ss / (double)d + eps);
+    for (int c = 0; c < d; ++c) h[(size_t)t * d + c] = row[c] * inv;
+  }
+  return 0;
+}
+
 int oracle_combine(int T, int k, int d, const double* topk_w,
                    const double* y_slot, double* out) {
   if (T < 0 || k <= 0 || d <= 0) return -1;

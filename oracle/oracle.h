@@ -106,6 +106,11 @@ int oracle_expert_ffn(int d, int f, int d_out, int group13, int group2, int b_mi
 int oracle_combine(int T, int k, int d, const double* topk_w,
                    const double* y_slot, double* out);
 
+/* RMS normalisation with unit weight, binary64, as applied to the hidden
+ * state before each MoE layer of the decoders of Sec. 5.1:
+ * h[t][c] = x[t][c] / sqrt(mean_c x[t][c]^2 + eps), sums in ascending c. */
+int oracle_rmsnorm(int T, int d, double eps, const double* x, double* h);
+
 #ifdef __cplusplus
 }
 #endif

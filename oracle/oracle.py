@@ -63,9 +63,10 @@ def _L():
         lib.oracle_route_from_logits.argtypes = [P, I, I, I, P, P, I, I, I, P, P, P, P, P, P, P, P]
         lib.oracle_expert_ffn.argtypes = [I, I, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P, I, P]
         lib.oracle_combine.argtypes = [I, I, I, P, P, P]
+        lib.oracle_rmsnorm.argtypes = [I, I, ctypes.c_double, P, P]
         for name in ("oracle_mwq_quantize", "oracle_mwq_dequant", "oracle_mwq_pack",
                      "oracle_gate_logits", "oracle_route_from_logits", "oracle_expert_ffn",
-                     "oracle_combine"):
+                     "oracle_combine", "oracle_rmsnorm"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -255,3 +256,33 @@ def moe_layer(x: np.ndarray, route: dict, codes13: list, codes2: list, tokens=No
         s13, s2, sb = shared
         out = out + expert_ffn(s13, s2, sb, x[toks].astype(np.float64))
     return out
+
+
+# ---- decoder stack of MoE layers ---------------------------------------------
+
+def rmsnorm(x: np.ndarray, eps: float = 1e-5) -> np.ndarray:
+    """x / sqrt(mean(x^2) + eps) per row, binary64 (unit normalisation weight)."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    T, d = x.shape
+    h = np.zeros_like(x)
+    _ok(_L().oracle_rmsnorm(T, d, float(eps), _p(x), _p(h)), "rmsnorm")
+    return h
+
+
+def moe_stack(x0: np.ndarray, layers: list, k: int, token_req, bit_table, eps: float = 1e-5,
+              b_min: int = 2, b_max: int = 8):
+    """A stack of MoE blocks x <- x + MoE_l(rmsnorm(x)) (attention absent).
+    The MoE layer sees bf16 activations and returns bf16 outputs, as the
+    layer does for bf16 inputs; the residual stream is binary64.
+    ``layers[l]`` = (Wg, codes13, codes2).  Returns the final stream and, per
+    layer, the layer's binary64 logits (to tell near-tied tokens)."""
+    x = np.asarray(x0, dtype=np.float64).copy()
+    logits_per_layer = []
+    for Wg, c13, c2 in layers:
+        h = round_bf16(rmsnorm(x, eps).astype(np.float32)).reshape(x.shape)
+        logits = gate_logits(h, Wg)
+        logits_per_layer.append(logits)
+        route = route_from_logits(logits, k, token_req, bit_table, b_min, b_max)
+        y = moe_layer(h, route, c13, c2)
+        x = x + round_bf16(y.astype(np.float32)).reshape(y.shape).astype(np.float64)
+    return x, logits_per_layer

@@ -59,9 +59,10 @@ def lib():
                                         ctypes.POINTER(_Mwq), ctypes.POINTER(_Mwq), _I, _I, _P,
                                         _P, ctypes.c_size_t, _P]
         L.d2moe_moe_forward_profiled.argtypes = L.d2moe_moe_forward.argtypes + [_P]
+        L.d2moe_residual_rmsnorm.argtypes = [_P, _P, _I, _I, _I, ctypes.c_float, _P, _I, _P]
         for name in ("d2moe_mwq_size", "d2moe_pack_mwq", "d2moe_debug_unpack", "d2moe_route",
                      "d2moe_moe_forward_workspace", "d2moe_moe_forward",
-                     "d2moe_moe_forward_profiled"):
+                     "d2moe_moe_forward_profiled", "d2moe_residual_rmsnorm"):
             getattr(L, name).restype = _I
         _lib = L
     return _lib
@@ -256,3 +257,22 @@ def moe_forward(x: torch.Tensor, w13: MWQ, w2: MWQ, r: Routing, k: int, shared=N
         arr = (ctypes.c_void_p * 4)(*[ev.cuda_event for ev in events])
         _check("d2moe_moe_forward_profiled", lib().d2moe_moe_forward_profiled(*args, arr))
     return out
+
+
+def residual_rmsnorm(x: torch.Tensor, y: torch.Tensor | None, eps: float = 1e-5,
+                     h: torch.Tensor | None = None, h_dtype=torch.bfloat16,
+                     stream=None) -> torch.Tensor:
+    """x [T][d] float32 (updated in place: x += y); returns h = x / rms(x)
+    (h_dtype).  y is None or [T][d] bfloat16 / float32."""
+    T, d = x.shape
+    if x.dtype != torch.float32 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous float32 tensor")
+    if y is not None and (y.shape != x.shape or not y.is_contiguous()):
+        raise ValueError("y must match x")
+    if h is None:
+        h = torch.empty((T, d), dtype=h_dtype, device=x.device)
+    _check("d2moe_residual_rmsnorm",
+           lib().d2moe_residual_rmsnorm(_ptr(x), _ptr(y) if y is not None else None,
+                                        _dtype_code(y) if y is not None else D2MOE_F32, T, d,
+                                        float(eps), _ptr(h), _dtype_code(h), _stream(stream)))
+    return h

@@ -152,4 +152,16 @@ d2moe_status d2moe_moe_forward_profiled(const void* x, d2moe_dtype x_dtype, int3
                       shared_bits, shared_d_ff, out, workspace, ws_bytes, stream, events);
 }
 
+d2moe_status d2moe_residual_rmsnorm(float* x, const void* y, d2moe_dtype y_dtype, int32_t T,
+                                    int32_t d, float eps, void* h, d2moe_dtype h_dtype,
+                                    void* stream) {
+  if (T < 0 || d < 1 || d > norm_max_cols() || !(eps >= 0.0f)) return D2MOE_EINVAL;
+  if ((y_dtype != D2MOE_F32 && y_dtype != D2MOE_BF16) ||
+      (h_dtype != D2MOE_F32 && h_dtype != D2MOE_BF16))
+    return D2MOE_EINVAL;
+  if (T > 0 && (!x || !h)) return D2MOE_EINVAL;
+  return from_hip(launch_residual_rmsnorm(x, y, y_dtype, T, d, eps, h, h_dtype,
+                                          (hipStream_t)stream));
+}
+
 }  // extern "C"

@@ -22,8 +22,9 @@
 // Work split: a workgroup owns one 16-row block (for SwiGLU, half its waves
 // take the W1 block and half the matching W3 block) of one active expert; the
 // waves of each half split the groups of the reduction dimension and reduce
-// through LDS.  Requirements: group 128, b_min 2, at most 16 tokens per
-// expert.
+// through LDS.  Requirements: group 128, b_min 2.  An expert's positions
+// are cut into work items of at most 8, each of which streams the expert's
+// planes; the forward takes this path up to 64 tokens.
 #include "internal.h"
 
 namespace d2moe {

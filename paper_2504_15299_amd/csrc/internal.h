@@ -72,7 +72,7 @@ hipError_t launch_route(const void* x, d2moe_dtype xd, int T, int d, const float
 
 // Forward workspace layout (256-byte aligned sub-buffers).  The decode
 // buffers exist only when T <= kDecodeMaxTokens.
-constexpr int kDecodeMaxTokens = 16;
+constexpr int kDecodeMaxTokens = 64;
 struct FwdWorkspace {
   size_t sched_off, h_off, hs_off, y_off, ys_off, xb_off;
   size_t elist_off, xq13_off, xs13_off, h32_off, xq2_off, xs2_off, hmax_off;
@@ -94,6 +94,10 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
                              const d2moe_mwq* w13, const d2moe_mwq* w2, const d2moe_routing* r,
                              const DecodeBuffers& b, hipStream_t s, const hipEvent_t* events);
 FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shared_d_ff);
+
+int norm_max_cols();
+hipError_t launch_residual_rmsnorm(float* x, const void* y, d2moe_dtype yd, int T, int d,
+                                   float eps, void* h, d2moe_dtype hd, hipStream_t s);
 
 hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff, int E, int k,
                           const d2moe_mwq* w13, const d2moe_mwq* w2, const d2moe_routing* r,

@@ -1,0 +1,82 @@
+// Residual update and RMS normalisation between the MoE layers of a decoder
+// stack.  The models the paper evaluates (Mixtral-8x7B, LLaMA-MoE, Sec. 5.1)
+// feed each MoE layer the RMS-normalised hidden state and add its output back
+// to the residual stream; here the normalisation's scale vector is all ones
+// (synthetic weights) and attention is absent.
+//   x[t] += y[t];  h[t] = x[t] / sqrt(mean_c x[t][c]^2 + eps)
+// One workgroup per row; the row is read once into registers (d <= 16384).
+#include "internal.h"
+
+namespace d2moe {
+namespace {
+
+constexpr int kNormThreads = 256;
+constexpr int kNormPer = 64;  // values per thread: d <= 256 * 64
+
+template <typename TY, typename TH>
+__global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
+    float* __restrict__ x, const TY* __restrict__ y, int d, float eps, TH* __restrict__ h) {
+  __shared__ float part[kNormThreads / 64];
+  const size_t row = (size_t)blockIdx.x * d;
+  float v[kNormPer];
+  float ss = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kNormPer; ++i) {
+    const int c = threadIdx.x + i * kNormThreads;
+    v[i] = 0.0f;
+    if (c < d) {
+      float a = x[row + c];
+      if (y) {
+        if constexpr (sizeof(TY) == 2)
+          a += bf2f(((const uint16_t*)y)[row + c]);
+        else
+          a += ((const float*)y)[row + c];
+        x[row + c] = a;
+      }
+      v[i] = a;
+      ss = fmaf(a, a, ss);
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  ss = 0.0f;
+  for (int w = 0; w < kNormThreads / 64; ++w) ss += part[w];
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+  for (int i = 0; i < kNormPer; ++i) {
+    const int c = threadIdx.x + i * kNormThreads;
+    if (c < d) {
+      const float o = v[i] * inv;
+      if constexpr (sizeof(TH) == 2)
+        ((uint16_t*)h)[row + c] = f2bf(o);
+      else
+        ((float*)h)[row + c] = o;
+    }
+  }
+}
+
+template <typename TY>
+hipError_t run_norm(float* x, const void* y, int T, int d, float eps, void* h, d2moe_dtype hd,
+                    hipStream_t s) {
+  if (hd == D2MOE_BF16)
+    residual_rmsnorm_kernel<TY, uint16_t><<<T, kNormThreads, 0, s>>>(x, (const TY*)y, d, eps,
+                                                                    (uint16_t*)h);
+  else
+    residual_rmsnorm_kernel<TY, float><<<T, kNormThreads, 0, s>>>(x, (const TY*)y, d, eps,
+                                                                 (float*)h);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int norm_max_cols() { return kNormThreads * kNormPer; }
+
+hipError_t launch_residual_rmsnorm(float* x, const void* y, d2moe_dtype yd, int T, int d,
+                                   float eps, void* h, d2moe_dtype hd, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  if (yd == D2MOE_BF16) return run_norm<uint16_t>(x, y, T, d, eps, h, hd, s);
+  return run_norm<float>(x, y, T, d, eps, h, hd, s);
+}
+
+}  // namespace d2moe

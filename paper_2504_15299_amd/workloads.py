@@ -96,6 +96,18 @@ def fine_grained(seed: int = 4) -> LayerSpec:
                      bits_mode="hottest_first")
 
 
+def mixtral_stack(seed: int = 5) -> LayerSpec:
+    """32 Mixtral-8x7B-shaped MoE layers stacked as decoder blocks
+    x <- x + MoE_l(rmsnorm(x)) (attention absent, unit normalisation weight,
+    eps 1e-5), 64 sequences decoding 128 steps; every sequence is a request
+    with one bit-width tier from {2,4,8} for all experts and layers; gate,
+    experts and activations drawn per layer from the layer's own streams."""
+    return LayerSpec("mixtral_stack", d=4096, f=14336, E=8, k=2, T=64, group=128,
+                     x_dtype="bf16", n_requests=64, seed=seed, bits_choices=(2, 4, 8),
+                     bits_mode="per_request",
+                     extra={"layers": 32, "steps": 128, "eps": 1e-5})
+
+
 def scaled(spec: LayerSpec, **kw) -> LayerSpec:
     """A copy of ``spec`` with some fields replaced (smaller test shapes)."""
     d = dict(spec.__dict__)

@@ -171,6 +171,8 @@ FWD_SPECS = {
     "decode_T1": wl.scaled(wl.mixtral_decode(T=1), d=512, f=384),
     "decode_T4": wl.scaled(wl.mixtral_decode(T=4), d=512, f=384),
     "decode_T16": wl.scaled(wl.mixtral_decode(T=16), d=512, f=384),
+    "decode_T40": wl.scaled(wl.mixtral_decode(T=40), d=512, f=384),
+    "decode_T64": wl.scaled(wl.mixtral_decode(T=64), d=256, f=256),
     "prefill_small": wl.scaled(wl.mixtral_prefill(), d=256, f=384, T=600),
     "fine_small": wl.scaled(wl.fine_grained(), d=256, f=128, T=200, shared_f=192),
 }
