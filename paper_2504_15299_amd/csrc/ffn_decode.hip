@@ -363,12 +363,20 @@ __device__ inline void dma_group(const DmaPlan<MB>& d, const WaveCtx& c, int g, 
 #pragma unroll
   for (int i = 0; i < SL::ops; ++i) {
     // every instruction has lane 0 active (slot 64 i < slots), so each one
-    // issues and is counted by vmcnt.  Weights are read once per call, so the
-    // loads are marked nontemporal (cache policy nt): streaming them past the
-    // caches reads HBM markedly faster on this chip than default-policy loads.
-    if (64 * i + c.lane < SL::slots)
-      __builtin_amdgcn_global_load_lds(D2MOE_GPTR(d.a0[i] + (size_t)g * d.step[i]),
-                                       D2MOE_LPTR(st + 1024 * i), 16, 0, kCpolNT);
+    // issues and is counted by vmcnt.  Plane words are read once per call, so
+    // instructions that carry only plane words are marked nontemporal (cache
+    // policy nt): streaming them past the caches reads HBM markedly faster on
+    // this chip than default-policy loads.  Scales and zero points are short
+    // runs that share cache lines with the next group's, so they keep the
+    // default policy.
+    if (64 * i + c.lane < SL::slots) {
+      if (64 * (i + 1) <= 16 * MB)  // constant once the loop is unrolled
+        __builtin_amdgcn_global_load_lds(D2MOE_GPTR(d.a0[i] + (size_t)g * d.step[i]),
+                                         D2MOE_LPTR(st + 1024 * i), 16, 0, kCpolNT);
+      else
+        __builtin_amdgcn_global_load_lds(D2MOE_GPTR(d.a0[i] + (size_t)g * d.step[i]),
+                                         D2MOE_LPTR(st + 1024 * i), 16, 0, 0);
+    }
   }
 }
 
