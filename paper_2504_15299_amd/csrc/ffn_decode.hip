@@ -110,7 +110,7 @@ __device__ inline int row_scale_exp(float amax) {
 // n = 4j'..4j'+3 (fixed d), so each thread reads four columns at stride 4 and
 // stores one dword per piece.  The zero-slot workgroup of slice 0 also writes
 // the work list of the decode kernels when `elist` is given: each active
-// expert's positions in runs of at most kDecodeCols, elist[4 i] = expert,
+// expert's positions in runs of at most `item`, elist[4 i] = expert,
 // first position, end position, the expert's largest bit-width, and entries
 // with bit-width 0 (no work) up to `nitems`, the grid's work-item count, so
 // that a decode workgroup needs one load to learn its work.
@@ -145,17 +145,18 @@ __device__ inline float row_absmax<float>(const float* row, int K) {
 // K % 128 == 0 elements on 16-byte aligned bases).
 // Xs[pos] is the position's info word for the decode kernels: its token's
 // bit-width (0 for the zero slot) in bits 0-7 and the E8M0 codes of the hi
-// and lo activation pieces in bits 8-15 and 16-23.  Xs has kDecodeCols - 1
+// and lo activation pieces in bits 8-15 and 16-23.  Xs has 2 kDecodeCols - 1
 // entries of padding past the zero slot, so a decode workgroup can read the
-// words of kDecodeCols positions from any first position.  bperm / tbits give the bit-width of
-// position p as tbits[bperm[p]].
+// words of 2 kDecodeCols positions from any first position.  bperm / tbits
+// give the bit-width of position p as tbits[bperm[p]].
 template <typename TIN>
 __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
     const TIN* __restrict__ in, int in_ld, const int32_t* __restrict__ perm, int kdiv, int npos,
     int K, const uint32_t* __restrict__ rowmax, int rowmax_parts, uint8_t* __restrict__ Xq,
     uint32_t* __restrict__ Xs, const int32_t* __restrict__ bperm,
     const uint8_t* __restrict__ tbits, const int32_t* __restrict__ offsets,
-    const uint8_t* __restrict__ maxbit, int E, int L, int32_t* __restrict__ elist, int nitems) {
+    const uint8_t* __restrict__ maxbit, int E, int L, int32_t* __restrict__ elist, int nitems,
+    int item) {
   __shared__ float wmax[kPrepThreads / 64];
   const int pos = blockIdx.x, NG = K / G;
   if (pos == npos && blockIdx.y == 0 && elist && threadIdx.x == 0) {
@@ -163,10 +164,10 @@ __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
     for (int e = 0; e < E; ++e) {
       if (maxbit[e] == 0) continue;
       const int lo = offsets[e * L], hi = offsets[e * L + L];
-      for (int p = lo; p < hi; p += kDecodeCols) {
+      for (int p = lo; p < hi; p += item) {
         elist[4 * n] = e;
         elist[4 * n + 1] = p;
-        elist[4 * n + 2] = min(p + kDecodeCols, hi);
+        elist[4 * n + 2] = min(p + item, hi);
         elist[4 * n + 3] = maxbit[e];
         ++n;
       }
@@ -310,16 +311,19 @@ struct StageLayout {
 #define D2MOE_GPTR(p) ((__attribute__((address_space(1))) void*)(p))
 #define D2MOE_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
 
+// NCB column blocks of kDecodeCols tokens share every plane operand; block c
+// holds the work item's positions 8 c .. 8 c + 7.
+template <int NCB>
 struct WaveCtx {
   const uint8_t* pl;   // plane words of group 0 of this row-block (bytes)
   const uint8_t* sc;   // scales of group 0 (bytes)
   const uint8_t* zp;   // zero points of group 0
   int pl_step, sc_step;  // bytes per group
   int lane, q, j;
-  uint32_t info;         // position info word (bit-width, activation scale codes)
-  int info_shift;        // bit offset of this lane's piece's scale code in `info`
-  const uint8_t* xq;     // activation pieces of group 0, this lane
-  uint64_t lmask;        // lanes holding a token
+  uint32_t info[NCB];      // position info words (bit-width, activation scale codes)
+  int info_shift;          // bit offset of this lane's piece's scale code in `info`
+  const uint8_t* xq[NCB];  // activation pieces of group 0, this lane
+  uint64_t lmask[NCB];     // lanes holding a token (lane 0 always included)
   SigmaConsts k;
   uint32_t lds_pl, lds_sc, lds_z;  // this lane's LDS read bases in stage 0
 };
@@ -333,8 +337,8 @@ struct DmaPlan {
   int step[StageLayout<MB>::ops];
 };
 
-template <int MB>
-__device__ inline DmaPlan<MB> dma_plan(const WaveCtx& c) {
+template <int MB, typename Ctx>
+__device__ inline DmaPlan<MB> dma_plan(const Ctx& c) {
   using SL = StageLayout<MB>;
   DmaPlan<MB> d;
 #pragma unroll
@@ -357,8 +361,8 @@ __device__ inline DmaPlan<MB> dma_plan(const WaveCtx& c) {
   return d;
 }
 
-template <int MB>
-__device__ inline void dma_group(const DmaPlan<MB>& d, const WaveCtx& c, int g, uint8_t* st) {
+template <int MB, typename Ctx>
+__device__ inline void dma_group(const DmaPlan<MB>& d, const Ctx& c, int g, uint8_t* st) {
   using SL = StageLayout<MB>;
 #pragma unroll
   for (int i = 0; i < SL::ops; ++i) {
@@ -380,8 +384,9 @@ __device__ inline void dma_group(const DmaPlan<MB>& d, const WaveCtx& c, int g, 
   }
 }
 
+template <int NCB>
 struct BData {
-  v4i lo, hi;  // this lane's 32 bytes of activation pieces
+  v4i lo[NCB], hi[NCB];  // this lane's 32 bytes of activation pieces per column block
 };
 
 // Activation loads are issued as inline assembly for the same reason as the
@@ -406,20 +411,30 @@ __device__ inline void gload16(v4i& v, const uint8_t* p, uint64_t m) {
       : "memory");
 }
 
-// Two memory instructions, issued by the lanes that hold a token (lane 0
-// always does); the other lanes keep the zeros they were given before the
-// loop.
-__device__ inline void load_b(BData& t, const WaveCtx& c, int g) {
-  const uint8_t* src = c.xq + (size_t)g * 256;
-  gload16(t.lo, src, c.lmask);
-  gload16(t.hi, src + 16, c.lmask);
+// Two memory instructions per column block, issued by the lanes that hold a
+// token (lane 0 always does); the other lanes keep the zeros they were given
+// before the loop.
+template <int NCB>
+__device__ inline void load_b(BData<NCB>& t, const WaveCtx<NCB>& c, int g) {
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    const uint8_t* src = c.xq[cb] + (size_t)g * 256;
+    gload16(t.lo[cb], src, c.lmask[cb]);
+    gload16(t.hi[cb], src + 16, c.lmask[cb]);
+  }
 }
 
 // Called after the wait that covers the loads of `t`.
-__device__ inline void ready_b(BData& t) { asm volatile("" : "+v"(t.lo), "+v"(t.hi)); }
+template <int NCB>
+__device__ inline void ready_b(BData<NCB>& t) {
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) asm volatile("" : "+v"(t.lo[cb]), "+v"(t.hi[cb]));
+}
 
-__device__ inline v8i b8(const BData& t) {
-  return v8i{t.lo[0], t.lo[1], t.lo[2], t.lo[3], t.hi[0], t.hi[1], t.hi[2], t.hi[3]};
+template <int NCB>
+__device__ inline v8i b8(const BData<NCB>& t, int cb) {
+  return v8i{t.lo[cb][0], t.lo[cb][1], t.lo[cb][2], t.lo[cb][3],
+             t.hi[cb][0], t.hi[cb][1], t.hi[cb][2], t.hi[cb][3]};
 }
 
 // LDS reads of a ring stage are issued as inline assembly: the compiler's
@@ -463,8 +478,8 @@ struct StageReader<MB, MB, SOFF> {
   static __device__ inline void run(uint32_t, uint32_t, uint32_t (&)[MB], uint2 (&)[MB - 1]) {}
 };
 
-template <int MB, int SOFF>
-__device__ inline void read_stage(const WaveCtx& c, uint32_t (&w)[MB], uint2 (&sc)[MB - 1],
+template <int MB, int SOFF, typename Ctx>
+__device__ inline void read_stage(const Ctx& c, uint32_t (&w)[MB], uint2 (&sc)[MB - 1],
                                   uint32_t& z) {
   StageReader<0, MB, SOFF>::run(c.lds_pl, c.lds_sc, w, sc);
   z = lds_rdu8<SOFF + StageLayout<MB>::zero_off>(c.lds_z);
@@ -480,10 +495,15 @@ __device__ inline void read_stage(const WaveCtx& c, uint32_t (&w)[MB], uint2 (&s
 // block scale: E8M0 code 0 scales that column's products by 2^-127, which
 // leaves at most ~1e-33 (|x| < 2^9 per fp8 piece, 128 terms) in place of an
 // exact zero.
-template <int MB, int SOFF>
-__device__ inline void compute_group(const BData& t, const WaveCtx& c, v4f& acc) {
-  const int bit = (int)(c.info & 0xffu);                      // token's bit-width
-  const int bsc = (int)((c.info >> c.info_shift) & 0xffu);    // its activation scale code
+template <int MB, int SOFF, int NCB>
+__device__ inline void compute_group(const BData<NCB>& t, const WaveCtx<NCB>& c,
+                                     v4f (&acc)[NCB]) {
+  int bit[NCB], bsc[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    bit[cb] = (int)(c.info[cb] & 0xffu);                     // token's bit-width
+    bsc[cb] = (int)((c.info[cb] >> c.info_shift) & 0xffu);   // its activation scale code
+  }
   const SigmaConsts& k = c.k;
   uint32_t w[MB];
   uint2 sw[MB - 1];
@@ -491,24 +511,30 @@ __device__ inline void compute_group(const BData& t, const WaveCtx& c, v4f& acc)
   read_stage<MB, SOFF>(c, w, sw, z);
   const v8i a0 = expand_sigma(w[0], k), a1 = expand_sigma(w[1], k);
   const v8i au = zero_operand(z);
-  const v8i bb = b8(t);
   float s1[4];
   scales4(sw[0], s1);
   // base: sum_k x_k (1.5 - Q_k) + sum_k x_k (z - 1.5), accumulated in place
-  v4f m = mfma_fp4_fp8(au, bb, 127, bsc);
-  m = mfma_fp4_fp8(a0, bb, m, 127, bsc);
-  m = mfma_fp4_fp8(a1, bb, m, 128, bsc);
 #pragma unroll
-  for (int r = 0; r < 4; ++r) acc[r] = fmaf(-s1[r], m[r], acc[r]);
+  for (int cb = 0; cb < NCB; ++cb) {
+    const v8i bb = b8(t, cb);
+    v4f m = mfma_fp4_fp8(au, bb, 127, bsc[cb]);
+    m = mfma_fp4_fp8(a0, bb, m, 127, bsc[cb]);
+    m = mfma_fp4_fp8(a1, bb, m, 128, bsc[cb]);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-s1[r], m[r], acc[cb][r]);
+  }
 #pragma unroll
   for (int p = 2; p < MB; ++p) {
     const v8i ap = expand_sigma(w[p], k);
     float sp[4];
     scales4(sw[p - 1], sp);
-    const int bs = p < bit ? bsc : 0;
-    const v4f d = mfma_fp4_fp8(ap, bb, 128, bs);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) acc[r] = fmaf(-sp[r], d[r], acc[r]);
+    for (int cb = 0; cb < NCB; ++cb) {
+      const int bs = p < bit[cb] ? bsc[cb] : 0;
+      const v4f d = mfma_fp4_fp8(ap, b8(t, cb), 128, bs);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-sp[r], d[r], acc[cb][r]);
+    }
   }
 }
 
@@ -534,15 +560,18 @@ __device__ inline void wait_vm() {
 // activations of g ready.  The DMA of g+3 overwrites the stage of g-1, whose
 // LDS reads completed in the previous step.  The loop is unrolled by kDepth
 // so every stage offset is a constant.
-template <int MB>
-__device__ inline void decode_groups(const WaveCtx& c, uint8_t* ring, int g0, int g1, v4f& acc) {
+template <int MB, int NCB>
+__device__ inline void decode_groups(const WaveCtx<NCB>& c, uint8_t* ring, int g0, int g1,
+                                     v4f (&acc)[NCB]) {
   static_assert(kDepth == 4, "the unrolled step below assumes four stages");
   if (g0 >= g1) return;
-  constexpr int ND = StageLayout<MB>::ops, NB = 2;
+  constexpr int ND = StageLayout<MB>::ops, NB = 2 * NCB;
   const DmaPlan<MB> plan = dma_plan<MB>(c);
-  BData B[2];
+  BData<NCB> B[2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) B[i].lo = B[i].hi = v4i{0, 0, 0, 0};
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) B[i].lo[cb] = B[i].hi[cb] = v4i{0, 0, 0, 0};
   dma_group<MB>(plan, c, g0, ring);
   if (g0 + 1 < g1) dma_group<MB>(plan, c, g0 + 1, ring + kStage);
   load_b(B[0], c, g0);
@@ -563,7 +592,7 @@ __device__ inline void decode_groups(const WaveCtx& c, uint8_t* ring, int g0, in
       wait_vm<0>();                                                          \
     }                                                                        \
     ready_b(B[(K) & 1]);                                                     \
-    compute_group<MB, ((K) % kDepth) * kStage>(B[(K) & 1], c, acc);          \
+    compute_group<MB, ((K) % kDepth) * kStage, NCB>(B[(K) & 1], c, acc);     \
   }
   for (int g = g0; g < g1; g += kDepth) {
     D2MOE_STEP(0)
@@ -575,20 +604,24 @@ __device__ inline void decode_groups(const WaveCtx& c, uint8_t* ring, int g0, in
 }
 
 
-// elist[4*i]: expert, first position, end position (at most kDecodeCols
+// elist[4*i]: expert, first position, end position (at most NCB * kDecodeCols
 // positions), largest bit-width of the expert (0: no work).  Xs: position
-// info words (bit-width, activation scale codes) from the activation prep.
+// info words (bit-width, activation scale codes) from the activation prep,
+// padded so that NCB * kDecodeCols words can be read from any position.
 // SwiGLU variant: waves [0, NW/2) stream the W1 row-block, waves [NW/2, NW)
 // the matching W3 row-block, each half splitting the groups; the epilogue
 // combines them through LDS (each wave's partial sums go to its own ring,
-// which is idle by then).
-template <bool SWIGLU, int NW>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void decode_kernel(
-    MwqView W, const int32_t* __restrict__ elist, const uint8_t* __restrict__ Xq,
-    const uint32_t* __restrict__ Xs, int npos, int f, float* __restrict__ out, int out_ld,
-    uint32_t* __restrict__ rowmax) {
+// which is idle by then).  NCB column blocks of 8 tokens share every plane
+// operand (two when experts hold more than 8 positions on average), at 4
+// waves per SIMD for one block and 3 for two.
+template <bool SWIGLU, int NW, int NCB>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NCB == 1 ? 4 : 3)))
+void decode_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* __restrict__ Xq,
+                   const uint32_t* __restrict__ Xs, int npos, int f, float* __restrict__ out,
+                   int out_ld, uint32_t* __restrict__ rowmax) {
   __shared__ __attribute__((aligned(16))) uint8_t ring[NW][kDepth * kStage];
-  static_assert(kDepth * kStage >= 64 * 4 * (int)sizeof(float), "partial sums fit the ring");
+  static_assert(kDepth * kStage >= NCB * 64 * 4 * (int)sizeof(float),
+                "partial sums fit the ring");
   const int ei = blockIdx.y;
   const int e = elist[4 * ei], p0 = elist[4 * ei + 1], p1 = elist[4 * ei + 2];
   const int mb = elist[4 * ei + 3];
@@ -605,32 +638,38 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   const int g0 = wk * NG / KS, g1 = (wk + 1) * NG / KS;
   const int ncol = p1 - p0;
 
-  WaveCtx c;
+  WaveCtx<NCB> c;
   c.lane = lane;
   c.q = lane >> 4;
   c.j = lane & 15;
   const int piece = lane & 1;
   const int t = c.j >> 1;
-  const bool valid = t < ncol;
-  const int pos = p0 + t;
-  const int src = valid ? pos : npos;  // zero slot when no token
-  {
-    const size_t base = ((size_t)src * NG) * 2 + piece;  // group 0
-    c.xq = Xq + base * 128 + c.q * 32;
-  }
   c.info_shift = 8 + 8 * piece;
-  c.lmask = __ballot(valid);
+  bool valid[NCB];
+  int pos[NCB];
   {
     // the info words of the item's positions are wave-uniform reads (scalar
     // cache, ordered by lgkmcnt), so waiting for them never holds back the
     // weight DMA; each lane then picks its token's word
-    uint32_t iw[kDecodeCols];
+    uint32_t iw[NCB * kDecodeCols];
 #pragma unroll
-    for (int i = 0; i < kDecodeCols; ++i) iw[i] = Xs[p0 + i];
-    uint32_t info = 0u;
+    for (int i = 0; i < NCB * kDecodeCols; ++i) iw[i] = Xs[p0 + i];
 #pragma unroll
-    for (int i = 0; i < kDecodeCols; ++i) info = t == i ? iw[i] : info;
-    c.info = valid ? info : 0u;  // no token: bit-width 0, zero activations
+    for (int cb = 0; cb < NCB; ++cb) {
+      const int tc = kDecodeCols * cb + t;
+      valid[cb] = tc < ncol;
+      pos[cb] = p0 + tc;
+      const int src = valid[cb] ? pos[cb] : npos;  // zero slot when no token
+      const size_t base = ((size_t)src * NG) * 2 + piece;  // group 0
+      c.xq[cb] = Xq + base * 128 + c.q * 32;
+      // lane 0 always loads (its own slot or the zero slot), so that every
+      // activation load instruction issues and is counted by vmcnt
+      c.lmask[cb] = __ballot(valid[cb]) | 1ull;
+      uint32_t info = 0u;
+#pragma unroll
+      for (int i = 0; i < kDecodeCols; ++i) info = t == i ? iw[kDecodeCols * cb + i] : info;
+      c.info[cb] = valid[cb] ? info : 0u;  // no token: bit-width 0, zero activations
+    }
   }
 
   const int rowblock = rr == 0 ? rb : rb + f / 16;
@@ -648,55 +687,64 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     c.lds_z = base + c.j;
   }
 
-  v4f acc = v4f{0.f, 0.f, 0.f, 0.f};
+  v4f acc[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) acc[cb] = v4f{0.f, 0.f, 0.f, 0.f};
   switch (mb) {
-    case 2: decode_groups<2>(c, ring[wave], g0, g1, acc); break;
-    case 3: decode_groups<3>(c, ring[wave], g0, g1, acc); break;
-    case 4: decode_groups<4>(c, ring[wave], g0, g1, acc); break;
-    case 5: decode_groups<5>(c, ring[wave], g0, g1, acc); break;
-    case 6: decode_groups<6>(c, ring[wave], g0, g1, acc); break;
-    case 7: decode_groups<7>(c, ring[wave], g0, g1, acc); break;
-    case 8: decode_groups<8>(c, ring[wave], g0, g1, acc); break;
+    case 2: decode_groups<2, NCB>(c, ring[wave], g0, g1, acc); break;
+    case 3: decode_groups<3, NCB>(c, ring[wave], g0, g1, acc); break;
+    case 4: decode_groups<4, NCB>(c, ring[wave], g0, g1, acc); break;
+    case 5: decode_groups<5, NCB>(c, ring[wave], g0, g1, acc); break;
+    case 6: decode_groups<6, NCB>(c, ring[wave], g0, g1, acc); break;
+    case 7: decode_groups<7, NCB>(c, ring[wave], g0, g1, acc); break;
+    case 8: decode_groups<8, NCB>(c, ring[wave], g0, g1, acc); break;
     default: break;
   }
 
   // every DMA of this wave has completed (the last step waits for all), so
   // its ring can hold its partial sums
   float4* red = (float4*)ring[wave];
-  red[lane] = float4{acc[0], acc[1], acc[2], acc[3]};
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb)
+    red[64 * cb + lane] = float4{acc[cb][0], acc[cb][1], acc[cb][2], acc[cb][3]};
   __syncthreads();
   if (wave != 0) return;
   constexpr int NRR = SWIGLU ? 2 : 1;
-  float v[NRR][4];
 #pragma unroll
-  for (int h = 0; h < NRR; ++h) {
-    float4 sum = float4{0.f, 0.f, 0.f, 0.f};
-    for (int w = 0; w < KS; ++w) {
-      const float4 part = ((const float4*)ring[h * KS + w])[lane];
-      sum.x += part.x; sum.y += part.y; sum.z += part.z; sum.w += part.w;
+  for (int cb = 0; cb < NCB; ++cb) {
+    float v[NRR][4];
+#pragma unroll
+    for (int h = 0; h < NRR; ++h) {
+      float4 sum = float4{0.f, 0.f, 0.f, 0.f};
+      for (int w = 0; w < KS; ++w) {
+        const float4 part = ((const float4*)ring[h * KS + w])[64 * cb + lane];
+        sum.x += part.x; sum.y += part.y; sum.z += part.z; sum.w += part.w;
+      }
+      v[h][0] = sum.x + __shfl_xor(sum.x, 1, 64);  // hi + lo pieces
+      v[h][1] = sum.y + __shfl_xor(sum.y, 1, 64);
+      v[h][2] = sum.z + __shfl_xor(sum.z, 1, 64);
+      v[h][3] = sum.w + __shfl_xor(sum.w, 1, 64);
     }
-    v[h][0] = sum.x + __shfl_xor(sum.x, 1, 64);  // hi + lo pieces
-    v[h][1] = sum.y + __shfl_xor(sum.y, 1, 64);
-    v[h][2] = sum.z + __shfl_xor(sum.z, 1, 64);
-    v[h][3] = sum.w + __shfl_xor(sum.w, 1, 64);
-  }
-  float o[4];
-  float m = 0.0f;
+    float o[4];
+    float m = 0.0f;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    o[r] = SWIGLU ? silu(v[0][r]) * v[NRR - 1][r] : v[0][r];
-    m = fmaxf(m, fabsf(o[r]));
-  }
-  if (valid && piece == 0)
-    *(float4*)(out + (size_t)pos * out_ld + rb * 16 + 4 * c.q) = float4{o[0], o[1], o[2], o[3]};
-  if (rowmax) {
-    // largest |output| of each position over this row-block, for the scale
-    // of its fp8 pieces: max over this lane's rows, then over the four lanes
-    // (q) of the token; one word per (position, row-block), so the
-    // workgroups of a position never contend for one address
-    m = fmaxf(m, __shfl_xor(m, 16, 64));
-    m = fmaxf(m, __shfl_xor(m, 32, 64));
-    if (valid && piece == 0 && c.q == 0) rowmax[(size_t)pos * gridDim.x + rb] = __float_as_uint(m);
+    for (int r = 0; r < 4; ++r) {
+      o[r] = SWIGLU ? silu(v[0][r]) * v[NRR - 1][r] : v[0][r];
+      m = fmaxf(m, fabsf(o[r]));
+    }
+    if (valid[cb] && piece == 0)
+      *(float4*)(out + (size_t)pos[cb] * out_ld + rb * 16 + 4 * c.q) =
+          float4{o[0], o[1], o[2], o[3]};
+    if (rowmax) {
+      // largest |output| of each position over this row-block, for the scale
+      // of its fp8 pieces: max over this lane's rows, then over the four lanes
+      // (q) of the token; one word per (position, row-block), so the
+      // workgroups of a position never contend for one address
+      m = fmaxf(m, __shfl_xor(m, 16, 64));
+      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      if (valid[cb] && piece == 0 && c.q == 0)
+        rowmax[(size_t)pos[cb] * gridDim.x + rb] = __float_as_uint(m);
+    }
   }
 }
 
@@ -704,11 +752,11 @@ template <typename TIN>
 hipError_t run_xprep(const TIN* in, int in_ld, const int32_t* perm, int kdiv, int npos, int K,
                      const uint32_t* rowmax, int rowmax_parts, uint8_t* Xq, uint32_t* Xs,
                      const d2moe_routing* r, bool work_list, int E, int L, int32_t* elist,
-                     int nitems, hipStream_t s) {
+                     int nitems, int item, hipStream_t s) {
   xprep_kernel<TIN><<<dim3(npos + 1, (K + kPrepCols - 1) / kPrepCols), kPrepThreads, 0, s>>>(
       in, in_ld, perm, kdiv, npos, K, rowmax, rowmax_parts, Xq, Xs, r->perm, r->topk_bits,
       work_list ? r->offsets : nullptr, work_list ? r->expert_maxbit : nullptr, E, L, elist,
-      nitems);
+      nitems, item);
   return hipGetLastError();
 }
 
@@ -729,27 +777,40 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   hipError_t err;
   const int L = w13->b_max - w13->b_min + 1;
   const int npos = T * k;
-  // work items: each active expert's positions in runs of kDecodeCols
-  const int ny = (E < npos ? E : npos) + (npos + kDecodeCols - 1) / kDecodeCols;
+  // two column blocks per work item once experts hold more than 4 positions
+  // on average (an expert's planes are then streamed once for up to 16 of
+  // its positions instead of once per 8)
+  const int ncb = npos > 4 * E ? 2 : 1;
+  const int item = ncb * kDecodeCols;
+  // work items: each active expert's positions in runs of `item`
+  const int ny = (E < npos ? E : npos) + (npos + item - 1) / item;
   if (xd == D2MOE_BF16)
     err = run_xprep<uint16_t>((const uint16_t*)x, d, r->perm, k, npos, d, nullptr, 0, b.xq13,
-                              b.xs13, r, true, E, L, b.elist, ny, s);
+                              b.xs13, r, true, E, L, b.elist, ny, item, s);
   else
     err = run_xprep<float>((const float*)x, d, r->perm, k, npos, d, nullptr, 0, b.xq13, b.xs13,
-                           r, true, E, L, b.elist, ny, s);
+                           r, true, E, L, b.elist, ny, item, s);
   if (err != hipSuccess) return err;
   const MwqView W13 = view_of(w13), W2 = view_of(w2);
   if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
-  decode_kernel<true, kDecodeWaves><<<dim3(d_ff / 16, ny), 64 * kDecodeWaves, 0, s>>>(
-      W13, b.elist, b.xq13, b.xs13, npos, d_ff, b.h32, d_ff, b.hmax);
+  if (ncb == 1)
+    decode_kernel<true, kDecodeWaves, 1><<<dim3(d_ff / 16, ny), 64 * kDecodeWaves, 0, s>>>(
+        W13, b.elist, b.xq13, b.xs13, npos, d_ff, b.h32, d_ff, b.hmax);
+  else
+    decode_kernel<true, kDecodeWaves, 2><<<dim3(d_ff / 16, ny), 64 * kDecodeWaves, 0, s>>>(
+        W13, b.elist, b.xq13, b.xs13, npos, d_ff, b.h32, d_ff, b.hmax);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
   err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.hmax, d_ff / 16, b.xq2, b.xs2, r,
-                         false, E, L, nullptr, 0, s);
+                         false, E, L, nullptr, 0, item, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
-  decode_kernel<false, kDecodeWaves><<<dim3(d / 16, ny), 64 * kDecodeWaves, 0, s>>>(
-      W2, b.elist, b.xq2, b.xs2, npos, 0, b.y, d, nullptr);
+  if (ncb == 1)
+    decode_kernel<false, kDecodeWaves, 1><<<dim3(d / 16, ny), 64 * kDecodeWaves, 0, s>>>(
+        W2, b.elist, b.xq2, b.xs2, npos, 0, b.y, d, nullptr);
+  else
+    decode_kernel<false, kDecodeWaves, 2><<<dim3(d / 16, ny), 64 * kDecodeWaves, 0, s>>>(
+        W2, b.elist, b.xq2, b.xs2, npos, 0, b.y, d, nullptr);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
   return hipSuccess;

@@ -220,10 +220,11 @@ def test_forward_all_tokens_one_expert():
     assert err.max() <= FWD_TOL
 
 
-@pytest.mark.parametrize("T", [9, 16])
+@pytest.mark.parametrize("T", [9, 16, 40])
 def test_forward_decode_hot_experts(T):
     """Decode batch where two experts receive every token (more than 8 tokens
-    per expert: two MFMA column blocks) with mixed bit-widths per token."""
+    per expert: several work items, of two 8-token column blocks each at 40
+    tokens, the last one partial) with mixed bit-widths per token."""
     spec = wl.scaled(wl.mixtral_decode(T=T), d=512, f=256)
     L = Layer(spec)
     L.bias = np.array([30.0, 20.0] + [0.0] * (spec.E - 2), np.float32)
