@@ -11,7 +11,6 @@ namespace d2moe {
 namespace {
 
 constexpr int kGateThreads = 256;
-constexpr int kGateE = 8;  // experts per pass over the token's row
 constexpr int kMaxExperts = 64;
 
 __device__ inline void load8(const float* p, float (&v)[8]) {
@@ -31,130 +30,186 @@ __device__ inline void load8(const uint16_t* p, float (&v)[8]) {
 __device__ inline float load1(const float* p) { return *p; }
 __device__ inline float load1(const uint16_t* p) { return bf2f(*p); }
 
-// Top-k of one token by (logit descending, index ascending), softmax over
-// the selected logits, bit-width lookup with range checks.  The token's flag
-// bits (1: a bit-width outside [b_min, b_max] was clamped, 2: a request id
-// outside [0, R) was clamped) go to tflags[t]; the histogram kernel combines
-// them into the routing flag word.
-__device__ inline void select_topk(const float* l, int t, int E, int k,
-                                   const int32_t* __restrict__ token_req,
-                                   const uint8_t* __restrict__ bit_table, int R, int b_min,
-                                   int b_max, int32_t* __restrict__ topk_idx,
-                                   float* __restrict__ topk_w, uint8_t* __restrict__ topk_bits,
-                                   int32_t* __restrict__ tflags) {
-  uint64_t taken = 0;
-  int r = token_req ? token_req[t] : 0;
-  int flag = 0;
-  if (r < 0 || r >= R) {
-    flag |= 2;
-    r = r < 0 ? 0 : R - 1;
-  }
-  // selection in descending order: the first pick holds the largest logit
-  float lmax = 0.0f, den = 0.0f;
-  for (int i = 0; i < k; ++i) {
-    int best = -1;
-    for (int e = 0; e < E; ++e) {
-      if ((taken >> e) & 1ull) continue;
-      if (best < 0 || l[e] > l[best]) best = e;
-    }
-    taken |= 1ull << best;
-    if (i == 0) lmax = l[best];
-    den += expf(l[best] - lmax);
-    topk_idx[t * k + i] = best;
-    int b = bit_table[(size_t)r * E + best];
-    if (b < b_min || b > b_max) {
-      flag |= 1;
-      b = b < b_min ? b_min : b_max;
-    }
-    topk_bits[t * k + i] = (uint8_t)b;
-  }
-  for (int i = 0; i < k; ++i) topk_w[t * k + i] = expf(l[topk_idx[t * k + i]] - lmax) / den;
-  tflags[t] = flag;
-}
-
-// logits[t][e] = x[t] . Wg[e] (+ bias[e]); one workgroup per token, which
-// then also takes the token's top-k (select_topk below).  Each
-// thread takes 8 consecutive columns per step (one 16-byte load of x, two of
-// each gate row) for up to kGateE experts per pass, with one fp32 fma chain
-// per expert; the partial sums are reduced across the wave with shuffles and
-// across the waves through LDS.  A term passes through at most
-// ceil(d/256) + 11 roundings.
-template <typename XT>
+// logits[t][e] = x[t] . Wg[e] (+ bias[e]) for a tile of TT tokens by EE
+// experts per workgroup.  Each thread takes 8 consecutive columns per step
+// (one 16-byte load of x per token, two of each gate row) with one fp32 fma
+// chain per (token, expert); the partial sums are reduced across the wave
+// with shuffles and across the waves through LDS.  A term passes through at
+// most ceil(d/256) + 11 roundings.  Small batches use 1 x 1 tiles, so that
+// many workgroups share the loads and every one of them is short; large
+// batches use 4 x 8 tiles, which read each gate row once per four tokens.
+template <typename XT, int TT, int EE>
 __global__ __launch_bounds__(kGateThreads) void gate_kernel(
-    const XT* __restrict__ x, int d, const float* __restrict__ Wg, const float* __restrict__ bias,
-    int E, int k, const int32_t* __restrict__ token_req, const uint8_t* __restrict__ bit_table,
-    int R, int b_min, int b_max, float* __restrict__ logits, int32_t* __restrict__ topk_idx,
-    float* __restrict__ topk_w, uint8_t* __restrict__ topk_bits, int32_t* __restrict__ tflags) {
+    const XT* __restrict__ x, int T, int d, const float* __restrict__ Wg,
+    const float* __restrict__ bias, int E, float* __restrict__ logits) {
   constexpr int NWAVE = kGateThreads / 64;
-  __shared__ float part[NWAVE][kGateE];
-  __shared__ float lg[kMaxExperts];
-  const int t = blockIdx.x;
+  __shared__ float part[NWAVE][TT * EE];
+  const int t0 = blockIdx.x * TT, e0 = blockIdx.y * EE;
+  const int nt = T - t0 < TT ? T - t0 : TT, ne = E - e0 < EE ? E - e0 : EE;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const XT* xt = x + (size_t)t * d;
+  // rows past the tile's end repeat its last row; their sums are not written
+  const XT* xr[TT];
+  const float* wr[EE];
+#pragma unroll
+  for (int i = 0; i < TT; ++i) xr[i] = x + (size_t)(t0 + (i < nt ? i : nt - 1)) * d;
+#pragma unroll
+  for (int j = 0; j < EE; ++j) wr[j] = Wg + (size_t)(e0 + (j < ne ? j : ne - 1)) * d;
   const bool vec = (d & 7) == 0 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)Wg & 15) == 0;
-  for (int e0 = 0; e0 < E; e0 += kGateE) {
-    const int ne = E - e0 < kGateE ? E - e0 : kGateE;
-    const float* w0 = Wg + (size_t)e0 * d;
-    float acc[kGateE];
+  float acc[TT][EE];
 #pragma unroll
-    for (int j = 0; j < kGateE; ++j) acc[j] = 0.0f;
-    if (vec) {
-      for (int c = 8 * tid; c < d; c += 8 * kGateThreads) {
-        float xv[8];
-        load8(xt + c, xv);
+  for (int i = 0; i < TT; ++i)
 #pragma unroll
-        for (int j = 0; j < kGateE; ++j) {
-          if (j >= ne) continue;  // uniform
-          float wv[8];
-          load8(w0 + (size_t)j * d + c, wv);
+    for (int j = 0; j < EE; ++j) acc[i][j] = 0.0f;
+  if (vec) {
+#pragma unroll 2
+    for (int c = 8 * tid; c < d; c += 8 * kGateThreads) {
+      float xv[TT][8];
 #pragma unroll
-          for (int i = 0; i < 8; ++i) acc[j] = fmaf(xv[i], wv[i], acc[j]);
-        }
-      }
-    } else {
-      for (int c = tid; c < d; c += kGateThreads) {
-        const float xv = load1(xt + c);
+      for (int i = 0; i < TT; ++i) load8(xr[i] + c, xv[i]);
 #pragma unroll
-        for (int j = 0; j < kGateE; ++j)
-          if (j < ne) acc[j] = fmaf(xv, w0[(size_t)j * d + c], acc[j]);
+      for (int j = 0; j < EE; ++j) {
+        float wv[8];
+        load8(wr[j] + c, wv);
+#pragma unroll
+        for (int i = 0; i < TT; ++i)
+#pragma unroll
+          for (int q = 0; q < 8; ++q) acc[i][j] = fmaf(xv[i][q], wv[q], acc[i][j]);
       }
     }
+  } else {
+    for (int c = tid; c < d; c += kGateThreads) {
+      float xv[TT];
 #pragma unroll
-    for (int j = 0; j < kGateE; ++j)
-      for (int off = 32; off > 0; off >>= 1) acc[j] += __shfl_xor(acc[j], off, 64);
-    if (lane == 0) {
+      for (int i = 0; i < TT; ++i) xv[i] = load1(xr[i] + c);
 #pragma unroll
-      for (int j = 0; j < kGateE; ++j) part[wave][j] = acc[j];
+      for (int j = 0; j < EE; ++j) {
+        const float wv = wr[j][c];
+#pragma unroll
+        for (int i = 0; i < TT; ++i) acc[i][j] = fmaf(xv[i], wv, acc[i][j]);
+      }
     }
-    __syncthreads();
-    if (tid < ne) {
+  }
+#pragma unroll
+  for (int i = 0; i < TT; ++i)
+#pragma unroll
+    for (int j = 0; j < EE; ++j) {
+      float v = acc[i][j];
+      for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+      if (lane == 0) part[wave][i * EE + j] = v;
+    }
+  __syncthreads();
+  if (tid < TT * EE) {
+    const int i = tid / EE, j = tid % EE;
+    if (i < nt && j < ne) {
       float sum = 0.0f;
       for (int w = 0; w < NWAVE; ++w) sum += part[w][tid];
-      const float v = sum + (bias ? bias[e0 + tid] : 0.0f);
-      logits[(size_t)t * E + e0 + tid] = v;
-      lg[e0 + tid] = v;
+      logits[(size_t)(t0 + i) * E + e0 + j] = sum + (bias ? bias[e0 + j] : 0.0f);
     }
-    __syncthreads();
   }
-  if (tid == 0)
-    select_topk(lg, t, E, k, token_req, bit_table, R, b_min, b_max, topk_idx, topk_w, topk_bits,
-                tflags);
 }
 
+// Top-k of one token by (logit descending, index ascending), softmax over
+// the selected logits and bit-width lookup with range checks, by one wave:
+// lane e holds logit e and the table's bit-width for expert e (E <= 64).
+// Each of the k rounds takes the wave maximum of the remaining logits and,
+// among the lanes that hold it, the lowest index; round i's choice is kept by
+// lane i, which writes entry i at the end.  The softmax denominator sums the
+// selected terms in selection order.  Returns the token's flag bits (1: a
+// bit-width outside [b_min, b_max] was clamped, 2: a request id outside
+// [0, R) was clamped), the same on every lane.
+struct TopkIn {
+  float v;  // this lane's logit
+  int b;    // this lane's table bit-width
+  int flag;
+};
+
+__device__ inline TopkIn topk_load(const float* __restrict__ logits, int t, int E,
+                                   const int32_t* __restrict__ token_req,
+                                   const uint8_t* __restrict__ bit_table, int R, int lane) {
+  TopkIn in;
+  int r = token_req ? token_req[t] : 0;
+  in.flag = 0;
+  if (r < 0 || r >= R) {
+    in.flag = 2;
+    r = r < 0 ? 0 : R - 1;
+  }
+  const bool have = lane < E;
+  in.v = have ? logits[(size_t)t * E + lane] : 0.0f;
+  in.b = have ? (int)bit_table[(size_t)r * E + lane] : 0;
+  return in;
+}
+
+__device__ inline int topk_wave(const TopkIn& in, int t, int E, int k, int b_min, int b_max,
+                                int lane, int32_t* __restrict__ topk_idx,
+                                float* __restrict__ topk_w, uint8_t* __restrict__ topk_bits) {
+  uint64_t avail = E >= 64 ? ~0ull : ((1ull << E) - 1);
+  float lmax = 0.0f, den = 0.0f;
+  int my_idx = 0, my_b = 0;
+  float my_v = 0.0f;
+  for (int i = 0; i < k; ++i) {
+    const bool live = (avail >> lane) & 1ull;
+    float m = live ? in.v : -INFINITY;
+    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+    uint64_t cand = __ballot(live && in.v == m);
+    if (cand == 0) cand = avail;  // only NaN left
+    const int best = __ffsll((unsigned long long)cand) - 1;
+    const float bv = __shfl(in.v, best, 64);
+    const int bb = __shfl(in.b, best, 64);
+    avail &= ~(1ull << best);
+    if (i == 0) lmax = bv;
+    den += expf(bv - lmax);
+    if (lane == i) {
+      my_idx = best;
+      my_v = bv;
+      my_b = bb;
+    }
+  }
+  int flag = in.flag;
+  const bool clamp = lane < k && (my_b < b_min || my_b > b_max);
+  if (__ballot(clamp)) flag |= 1;
+  if (lane < k) {
+    topk_idx[t * k + lane] = my_idx;
+    topk_bits[t * k + lane] = (uint8_t)(my_b < b_min ? b_min : (my_b > b_max ? b_max : my_b));
+    topk_w[t * k + lane] = expf(my_v - lmax) / den;
+  }
+  return flag;
+}
+
+// Batches above kInlineTopk tokens: one wave per token over many
+// workgroups; each token's flag bits go to perm[t] (T <= T k entries) until
+// the histogram kernel combines them and overwrites perm.
+constexpr int kInlineTopk = 64;
+constexpr int kTopkThreads = 256;
+
+__global__ __launch_bounds__(kTopkThreads) void topk_kernel(
+    const float* __restrict__ logits, int T, int E, int k, const int32_t* __restrict__ token_req,
+    const uint8_t* __restrict__ bit_table, int R, int b_min, int b_max,
+    int32_t* __restrict__ topk_idx, float* __restrict__ topk_w, uint8_t* __restrict__ topk_bits,
+    int32_t* __restrict__ tflags) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * (kTopkThreads / 64) + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const TopkIn in = topk_load(logits, t, E, token_req, bit_table, R, lane);
+  const int fl = topk_wave(in, t, E, k, b_min, b_max, lane, topk_idx, topk_w, topk_bits);
+  if (lane == 0) tflags[t] = fl;
+}
 
 constexpr int kHistThreads = 1024;
 constexpr int kHistWaves = kHistThreads / 64;
 constexpr int kMaxKeys = 64 * 8;  // E <= 64, L <= 8
 
-// Single workgroup: histogram of keys (expert * L + bit - b_min), exclusive
-// scan, stable placement of slots in ascending slot order within each key,
-// inverse permutation and largest requested bit per expert.  Slots are taken
-// 1024 at a time; within a chunk the rank of a slot among earlier slots with
-// the same key comes from wave ballots (equal-key lane masks) plus per-wave
-// counts of earlier waves.
+// Single workgroup: every token's top-k, softmax weights and bit-widths
+// (one token per thread), then the histogram of keys (expert * L + bit -
+// b_min), exclusive scan, stable placement of slots in ascending slot order
+// within each key, inverse permutation and largest requested bit per expert.
+// Slots are taken 1024 at a time; within a chunk the rank of a slot among
+// earlier slots with the same key comes from wave ballots (equal-key lane
+// masks) plus per-wave counts of earlier waves.
 __global__ __launch_bounds__(kHistThreads) void hist_perm_kernel(
-    const int32_t* __restrict__ topk_idx, const uint8_t* __restrict__ topk_bits, int T, int n,
-    int E, int L, int b_min, int32_t* __restrict__ flags, int32_t* __restrict__ hist,
+    const float* __restrict__ logits, int k, const int32_t* __restrict__ token_req,
+    const uint8_t* __restrict__ bit_table, int R, int b_max, int32_t* __restrict__ topk_idx,
+    float* __restrict__ topk_w, uint8_t* __restrict__ topk_bits, int T, int n, int E, int L,
+    int b_min, int32_t* __restrict__ flags, int32_t* __restrict__ hist,
     int32_t* __restrict__ offsets, int32_t* __restrict__ perm, int32_t* __restrict__ slot_of,
     uint8_t* __restrict__ maxbit) {
   __shared__ int cnt[kMaxKeys];
@@ -167,11 +222,30 @@ __global__ __launch_bounds__(kHistThreads) void hist_perm_kernel(
   if (tid == 0) flag_acc = 0;
   for (int j = tid; j < nkeys; j += kHistThreads) { cnt[j] = 0; run[j] = 0; }
   __syncthreads();
-  // the gate kernel left each token's flag bits in perm[t]; combine them
-  // before perm is overwritten below
   int fl = 0;
-  for (int t = tid; t < T; t += kHistThreads) fl |= perm[t];
+  if (T <= kInlineTopk) {
+    // wave w selects for tokens w, w + 16, w + 32, w + 48, all loaded first
+    constexpr int TPW = kInlineTopk / kHistWaves;
+    TopkIn in[TPW];
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) {
+      const int t = wave + kHistWaves * j;
+      if (t < T) in[j] = topk_load(logits, t, E, token_req, bit_table, R, lane);
+    }
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) {
+      const int t = wave + kHistWaves * j;
+      if (t < T) fl |= topk_wave(in[j], t, E, k, b_min, b_max, lane, topk_idx, topk_w, topk_bits);
+    }
+    if (lane != 0) fl = 0;
+  } else {
+    // topk_kernel left each token's flag bits in perm[t]; combine them
+    // before perm is overwritten below
+    for (int t = tid; t < T; t += kHistThreads) fl |= perm[t];
+  }
   if (fl) atomicOr(&flag_acc, fl);
+  // the barrier also orders this workgroup's global writes of the
+  // selections before the reads below
   __syncthreads();
   if (tid == 0) *flags = flag_acc;
   for (int s = tid; s < n; s += kHistThreads)
@@ -224,6 +298,17 @@ __global__ __launch_bounds__(kHistThreads) void hist_perm_kernel(
   }
 }
 
+template <typename XT>
+hipError_t run_gate(const XT* x, int T, int d, const float* Wg, const float* bias, int E,
+                    float* logits, hipStream_t s) {
+  if ((size_t)T * E <= 4096)
+    gate_kernel<XT, 1, 1><<<dim3(T, E), kGateThreads, 0, s>>>(x, T, d, Wg, bias, E, logits);
+  else
+    gate_kernel<XT, 4, 8><<<dim3((T + 3) / 4, (E + 7) / 8), kGateThreads, 0, s>>>(x, T, d, Wg,
+                                                                                 bias, E, logits);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_route(const void* x, d2moe_dtype xd, int T, int d, const float* Wg,
@@ -233,21 +318,23 @@ hipError_t launch_route(const void* x, d2moe_dtype xd, int T, int d, const float
   hipError_t err;
   const int L = b_max - b_min + 1;
   if (T > 0) {
-    // each token's flag bits travel in perm[t] (T <= T*k entries) until the
-    // histogram kernel overwrites perm
     if (xd == D2MOE_BF16)
-      gate_kernel<uint16_t><<<T, kGateThreads, 0, s>>>(
-          (const uint16_t*)x, d, Wg, bias, E, k, token_req, bit_table, R, b_min, b_max,
-          out->logits, out->topk_idx, out->topk_w, out->topk_bits, out->perm);
+      err = run_gate((const uint16_t*)x, T, d, Wg, bias, E, out->logits, s);
     else
-      gate_kernel<float><<<T, kGateThreads, 0, s>>>(
-          (const float*)x, d, Wg, bias, E, k, token_req, bit_table, R, b_min, b_max, out->logits,
-          out->topk_idx, out->topk_w, out->topk_bits, out->perm);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
+      err = run_gate((const float*)x, T, d, Wg, bias, E, out->logits, s);
+    if (err != hipSuccess) return err;
+    if (T > kInlineTopk) {
+      const int per = kTopkThreads / 64;
+      topk_kernel<<<(T + per - 1) / per, kTopkThreads, 0, s>>>(
+          out->logits, T, E, k, token_req, bit_table, R, b_min, b_max, out->topk_idx,
+          out->topk_w, out->topk_bits, out->perm);
+      if ((err = hipGetLastError()) != hipSuccess) return err;
+    }
   }
-  hist_perm_kernel<<<1, kHistThreads, 0, s>>>(out->topk_idx, out->topk_bits, T, T * k, E, L, b_min,
-                                              out->flags, out->hist, out->offsets, out->perm, out->slot_of,
-                                              out->expert_maxbit);
+  hist_perm_kernel<<<1, kHistThreads, 0, s>>>(
+      out->logits, k, token_req, bit_table, R, b_max, out->topk_idx, out->topk_w, out->topk_bits,
+      T, T * k, E, L, b_min, out->flags, out->hist, out->offsets, out->perm, out->slot_of,
+      out->expert_maxbit);
   return hipGetLastError();
 }
 
