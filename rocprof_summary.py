@@ -7,7 +7,12 @@
       in KiB), and the same counter for the plain 256 MiB copy that
       `bench.py --copy-calibration` runs first, as the calibration factor
       measured KiB / 262144 KiB.
+  python rocprof_summary.py decode-traffic <fetch_results.db> <write_results.db>
+      calibrated HBM bytes per launch of the W1/W3 and W2 decode kernels
+      (FETCH_SIZE + WRITE_SIZE), tagged with the hash of the kernel source
+      that bench.py checks before it reports them as roofline.traffic.
 """
+import os
 import sqlite3
 import sys
 from collections import defaultdict
@@ -31,6 +36,43 @@ def trace(db):
     print(f"{'kernel':92s} {'calls':>6s} {'total_us':>10s} {'avg_us':>9s}")
     for name, durs in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
         print(f"{name:92s} {len(durs):6d} {sum(durs) / 1e3:10.1f} {sum(durs) / len(durs) / 1e3:9.2f}")
+
+
+def _per_kernel(db, cname):
+    """Calibration factor and per-kernel average of a per-dispatch counter."""
+    con = sqlite3.connect(db)
+    cols = [r[1] for r in con.execute("pragma table_info('counters_collection')")]
+    rows = con.execute("select * from counters_collection").fetchall()
+    ix = {c: i for i, c in enumerate(cols)}
+    name_col = "kernel_name" if "kernel_name" in ix else "name"
+    per_disp = defaultdict(float)
+    names = {}
+    for r in rows:
+        if r[ix["counter_name"]] == cname:
+            per_disp[r[ix["dispatch_id"]]] += float(r[ix["value"]])
+            names[r[ix["dispatch_id"]]] = r[ix[name_col]]
+    cal = sorted(v for d, v in per_disp.items() if "copyBuffer" in names[d] and v > 0.25 * 262144)
+    factor = cal[len(cal) // 2] / 262144.0
+    agg = defaultdict(list)
+    for key, v in per_disp.items():
+        agg[_short(names[key])].append(v)
+    return factor, {k: sum(v) / len(v) for k, v in agg.items()}
+
+
+def decode_traffic(fetch_db, write_db):
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    from bench import kernel_source_hash
+    total = defaultdict(float)
+    for db, cname in ((fetch_db, "FETCH_SIZE"), (write_db, "WRITE_SIZE")):
+        factor, avg = _per_kernel(db, cname)
+        for name, kib in avg.items():
+            total[name] += kib / factor * 1024
+    w13 = [v for k, v in total.items() if k.startswith("decode_kernel<true")]
+    w2 = [v for k, v in total.items() if k.startswith("decode_kernel<false")]
+    print("traffic per launch (FETCH + WRITE, calibrated), used by bench.py as roofline.traffic:")
+    print(f"kernel_source_sha256_16: {kernel_source_hash()}")
+    print(f"traffic_w13_bytes: {int(round(sum(w13) / len(w13)))}")
+    print(f"traffic_w2_bytes: {int(round(sum(w2) / len(w2)))}")
 
 
 def counter(db, cname, subs):
@@ -70,5 +112,7 @@ def counter(db, cname, subs):
 if __name__ == "__main__":
     if sys.argv[1] == "trace":
         trace(sys.argv[2])
+    elif sys.argv[1] == "decode-traffic":
+        decode_traffic(sys.argv[2], sys.argv[3])
     else:
         counter(sys.argv[2], sys.argv[3], sys.argv[4:])
