@@ -60,6 +60,9 @@ def main():
     ap.add_argument("--stack-steps", type=int, default=128,
                     help="also run the 32-layer decoder stack of MoE layers, 64 sequences, "
                          "this many decode steps (0: skip)")
+    ap.add_argument("--variant-steps", type=int, default=40,
+                    help="also time batch-16 decode under the paper's two nests (b 2-4, b 5-8) "
+                         "and the LLaMA2-13B-shaped dense FFN (0: skip)")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of one captured HIP graph per layer step instead of "
                          "eager launches")
@@ -389,6 +392,67 @@ def main():
                 "alg_bytes_per_step": step_bytes, "hbm_GBps": round(gbps, 1),
                 "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4), "hidden_state_finite": finite}
 
+    def run_variant(label, dV, fV, EV, kV, bmin, bmax, choices, probs, copies, steps, warmup=5,
+                    T=16):
+        """Batch-T decode of a layer of another shape or nest: `copies`
+        rotating packed copies, per-(request, expert) bit tables drawn from
+        `choices` with `probs`.  Reports the step and the W1/W3 kernel's HBM
+        rate (HIP events on the launch stream) against its algorithmic bytes."""
+        sets = []
+        for c in range(copies):
+            w13 = api.MWQ.empty(EV, 2 * fV, dV, g, bmin, bmax, device=dev)
+            w2 = api.MWQ.empty(EV, dV, fV, g, bmin, bmax, device=dev)
+            for e in range(EV):
+                gen.manual_seed(90_000_049 * (c + 1) + 2 * e)
+                api.pack_mwq(torch.randn((1, 2 * fV, dV), generator=gen, device=dev) * 0.02,
+                             w13.expert(e))
+                gen.manual_seed(90_000_049 * (c + 1) + 2 * e + 1)
+                api.pack_mwq(torch.randn((1, dV, fV), generator=gen, device=dev) * 0.02,
+                             w2.expert(e))
+            gen.manual_seed(9000 + c)
+            Wg = torch.randn((EV, dV), generator=gen, device=dev) * 0.02
+            sets.append((w13, w2, Wg, api.Routing.empty(T, EV, kV, bmin, bmax, device=dev)))
+        rng = np.random.default_rng(11 + T + bmin)
+        x = torch.from_numpy(rng.standard_normal((T, dV), dtype=np.float32)).to(dev).to(torch.bfloat16)
+        req = torch.arange(T, dtype=torch.int32, device=dev)
+        tables = [torch.from_numpy(rng.choice(np.array(choices, np.uint8), size=(T, EV),
+                                              p=probs)).to(dev) for _ in range(copies)]
+        out = torch.empty((T, dV), dtype=torch.bfloat16, device=dev)
+        ws = torch.empty(api.moe_forward_workspace(T, dV, fV, EV, kV), dtype=torch.uint8,
+                         device=dev)
+
+        def step(i, events=None):
+            w13, w2, Wg, r = sets[i % copies]
+            api.route(x, Wg, None, kV, req, tables[i % copies], bmin, bmax, out=r)
+            api.moe_forward(x, w13, w2, r, kV, out=out, workspace=ws, events=events)
+
+        for i in range(warmup):
+            step(i)
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+        for row in evs:
+            for ev in row:
+                ev.record()
+        torch.cuda.synchronize()
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_stop = torch.cuda.Event(enable_timing=True)
+        t_start.record()
+        for i in range(steps):
+            step(warmup + i, evs[i])
+        t_stop.record()
+        torch.cuda.synchronize()
+        ms = t_start.elapsed_time(t_stop) / steps
+        alg13 = [sum(mwq_bytes(2 * fV, dV, g, bmin, int(b))
+                     for b in sets[c][3].expert_maxbit.cpu().numpy()) for c in range(copies)]
+        b13 = float(np.mean([alg13[(warmup + i) % copies] for i in range(steps)]))
+        d13 = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+        gbps = b13 / (d13 * 1e-3) / 1e9
+        del sets
+        torch.cuda.empty_cache()
+        return {"workload": label, "tokens": T, "ms_per_step": round(ms, 4),
+                "tokens_per_s": round(T / (ms * 1e-3), 1), "w13_ms": round(d13, 4),
+                "w13_alg_bytes": b13, "w13_GBps": round(gbps, 1),
+                "w13_hbm_frac": round(gbps / HBM_PEAK_GBPS, 4)}
+
     main_res = run_batch(args.batch, args.steps, args.warmup, profile=True)
     sweep = []
     for T in [int(v) for v in args.sweep.split(",") if v.strip()]:
@@ -398,6 +462,22 @@ def main():
     prefill = run_prefill(args.prefill_steps, 2) if args.prefill_steps > 0 else None
     fine = run_fine(args.fine_steps, 2) if args.fine_steps > 0 else None
     stack_res = run_stack(args.stack_steps) if args.stack_steps > 0 else None
+    variants = None
+    if args.variant_steps > 0:
+        vs = args.variant_steps
+        variants = {
+            "v1": run_variant("Mixtral-8x7B-shaped MoE layer decode, batch 16, the paper's first "
+                              "nest (b 2-4, bits {2,3,4} p {.3,.4,.3}), group 128, 4 rotating "
+                              "copies", d, f, E, k, 2, 4, (2, 3, 4), (0.3, 0.4, 0.3), 4, vs),
+            "v2": run_variant("Mixtral-8x7B-shaped MoE layer decode, batch 16, the paper's "
+                              "second nest (b 5-8, bits {5,6,7,8} p .25 each), group 128, 4 "
+                              "rotating copies", d, f, E, k, 5, 8, (5, 6, 7, 8),
+                              (0.25, 0.25, 0.25, 0.25), 4, vs),
+            "dense": run_variant("LLaMA2-13B-shaped dense SwiGLU FFN (d_model 5120, d_ff 13824; "
+                                 "one expert, top-1) decode, batch 16, per-request bits {2,3,4} "
+                                 "p {.3,.4,.3} of the first nest, group 128, 8 rotating copies",
+                                 5120, 13824, 1, 1, 2, 4, (2, 3, 4), (0.3, 0.4, 0.3), 8, vs),
+        }
 
     cpu = None
     if not args.no_cpu:
@@ -440,6 +520,7 @@ def main():
         "prefill": prefill,
         "fine_grained": fine,
         "stack": stack_res,
+        "variants": variants,
         "cpu_baseline": cpu,
         "pack_seconds": round(pack_s, 2),
     }

@@ -12,19 +12,20 @@
 //   B: the activations of up to 8 tokens, each as an exact pair of fp8 (e4m3)
 //      pieces hi + lo with one E8M0 scale per 32 columns (16 MFMA columns).
 // With A = -sigma/2 the residual bit-width b contributes s_b * sum sigma x =
-// -s_b * D (A scale 2).  The base code Q = bit0 + 2 bit1 and its zero point
-// fold into three chained MFMAs (planes 0 and 1 with A scales 1 and 2, plus a
-// constant fp4 operand z - 1.5), so (Q - z) . x = -D as well.  Every plane
-// thus costs one MFMA and one fp16-scaled FMA per output, and no weight is
-// ever materialised as a number.  Tokens whose bit-width is below a plane get
+// -s_b * D (A scale 2).  The base code Q (b_min planes) folds into chained
+// MFMAs with A scales 2^p; at b_min = 2 a constant fp4 operand z - 1.5 joins
+// the chain, so (Q - z) . x = -D as well (larger b_min: one more MFMA with an
+// all-ones operand gives the activation sum for the zero-point term).  Every
+// plane thus costs one MFMA and one fp16-scaled FMA per output, and no weight
+// is ever materialised as a number.  Tokens whose bit-width is below a plane get
 // a zero coefficient for it; they share the loads.
 //
 // Work split: a workgroup owns one 16-row block (for SwiGLU, half its waves
 // take the W1 block and half the matching W3 block) of one active expert; the
 // waves of each half split the groups of the reduction dimension and reduce
-// through LDS.  Requirements: group 128, b_min 2.  An expert's positions
-// are cut into work items of at most 8, each of which streams the expert's
-// planes; the forward takes this path up to 64 tokens.
+// through LDS.  Requirement: group 128 (any nest start b_min).  An expert's
+// positions are cut into work items of at most 8 or 16, each of which
+// streams the expert's planes; the forward takes this path up to 64 tokens.
 #include "internal.h"
 
 namespace d2moe {
@@ -246,16 +247,6 @@ __device__ inline v8i expand_sigma(uint32_t w, const SigmaConsts& k) {
   return a;
 }
 
-// fp4 code of (z - 1.5) replicated over a dword: z = 0..3 -> B, 9, 1, 3
-__device__ inline v8i zero_operand(uint32_t z) {
-  const uint32_t c = (0x319Bu >> (z << 2)) & 0xFu;
-  const uint32_t dw = c * 0x11111111u;
-  v8i a;
-  a[0] = a[1] = a[2] = a[3] = (int)dw;
-  a[4] = a[5] = a[6] = a[7] = 0;
-  return a;
-}
-
 // Cross-lane product: every call sits in wave-uniform control flow (no
 // per-lane condition guards an MFMA or the use of its result in this file;
 // per-token predication is done through the activation block scale).
@@ -289,24 +280,32 @@ __device__ inline void scales4(uint2 s, float (&out)[4]) {
 }
 
 // Per-wave LDS ring for the weight stream.  One stage holds one group of the
-// wave's 16 rows at MB planes, packed as [planes MB x 256 B][scales
-// (MB-1) x 32 B][zero points 16 B], copied from global memory by the LDS DMA
+// wave's 16 rows at MB planes of a nest that starts at BMIN bits, packed as
+// [planes MB x 256 B][scales LV x 32 B][zero points 16 B] with
+// LV = MB - BMIN + 1 scale levels, copied from global memory by the LDS DMA
 // engine so that data in flight costs no registers.  Each DMA instruction
 // moves 16 bytes per lane into consecutive LDS addresses; lane slot s of the
 // stage (s = 64 i + lane for instruction i) fetches plane bytes for
-// s < 16 MB, scale bytes for the next 2 (MB-1) slots and the zero points in
-// the last one, each from its own array.
-constexpr int kStage = 2304;            // bytes per stage (>= 18 x 128 - 16)
+// s < 16 MB, scale bytes for the next 2 LV slots and the zero points in the
+// last one, each from its own array.
 constexpr int kDepth = 4;               // stages: the DMA runs kDepth-1 groups ahead
 constexpr int kCpolNT = 2;              // cache-policy operand of the DMA: nt
 
-template <int MB>
+template <int MB, int BMIN>
 struct StageLayout {
+  static constexpr int levels = MB - BMIN + 1;
   static constexpr int scale_off = 256 * MB;
-  static constexpr int zero_off = scale_off + 32 * (MB - 1);
-  static constexpr int slots = 18 * MB - 1;
+  static constexpr int zero_off = scale_off + 32 * levels;
+  static constexpr int slots = 16 * MB + 2 * levels + 1;
   static constexpr int ops = (slots + 63) / 64;  // DMA instructions per group
 };
+
+// Bytes per stage: the largest stage of the nest (MB = 8), 2304 for
+// BMIN >= 2 and 2320 for BMIN = 1.
+template <int BMIN>
+constexpr int stage_bytes() {
+  return 16 * StageLayout<8, BMIN>::slots <= 2304 ? 2304 : 16 * StageLayout<8, BMIN>::slots;
+}
 
 #define D2MOE_GPTR(p) ((__attribute__((address_space(1))) void*)(p))
 #define D2MOE_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
@@ -325,29 +324,29 @@ struct WaveCtx {
   const uint8_t* xq[NCB];  // activation pieces of group 0, this lane
   uint64_t lmask[NCB];     // lanes holding a token (lane 0 always included)
   SigmaConsts k;
-  uint32_t lds_pl, lds_sc, lds_z;  // this lane's LDS read bases in stage 0
+  uint32_t lds_pl, lds_sc, lds_z, lds_zq;  // this lane's LDS read bases in stage 0
 };
 
 // Source of each DMA instruction's 16 bytes for this lane: the address for
 // group 0 and the stride per group (0 for lanes past the last slot, which
 // do not issue).
-template <int MB>
+template <int MB, int BMIN>
 struct DmaPlan {
-  const uint8_t* a0[StageLayout<MB>::ops];
-  int step[StageLayout<MB>::ops];
+  const uint8_t* a0[StageLayout<MB, BMIN>::ops];
+  int step[StageLayout<MB, BMIN>::ops];
 };
 
-template <int MB, typename Ctx>
-__device__ inline DmaPlan<MB> dma_plan(const Ctx& c) {
-  using SL = StageLayout<MB>;
-  DmaPlan<MB> d;
+template <int MB, int BMIN, typename Ctx>
+__device__ inline DmaPlan<MB, BMIN> dma_plan(const Ctx& c) {
+  using SL = StageLayout<MB, BMIN>;
+  DmaPlan<MB, BMIN> d;
 #pragma unroll
   for (int i = 0; i < SL::ops; ++i) {
     const int s = 64 * i + c.lane;
     if (s < 16 * MB) {
       d.a0[i] = c.pl + 16 * s;
       d.step[i] = c.pl_step;
-    } else if (s < 16 * MB + 2 * (MB - 1)) {
+    } else if (s < 16 * MB + 2 * SL::levels) {
       d.a0[i] = c.sc + 16 * (s - 16 * MB);
       d.step[i] = c.sc_step;
     } else if (s == SL::slots - 1) {
@@ -361,9 +360,9 @@ __device__ inline DmaPlan<MB> dma_plan(const Ctx& c) {
   return d;
 }
 
-template <int MB, typename Ctx>
-__device__ inline void dma_group(const DmaPlan<MB>& d, const Ctx& c, int g, uint8_t* st) {
-  using SL = StageLayout<MB>;
+template <int MB, int BMIN, typename Ctx>
+__device__ inline void dma_group(const DmaPlan<MB, BMIN>& d, const Ctx& c, int g, uint8_t* st) {
+  using SL = StageLayout<MB, BMIN>;
 #pragma unroll
   for (int i = 0; i < SL::ops; ++i) {
     // every instruction has lane 0 active (slot 64 i < slots), so each one
@@ -465,39 +464,86 @@ __device__ inline uint32_t lds_rdu8(uint32_t a) {
   return v;
 }
 template <int P, int MB, int SOFF>
-struct StageReader {
-  static __device__ inline void run(uint32_t pa, uint32_t sa, uint32_t (&w)[MB],
-                                    uint2 (&sc)[MB - 1]) {
-    w[P] = lds_rd32<SOFF + P * 256>(pa);
-    if constexpr (P + 1 < MB) sc[P] = lds_rd64<SOFF + StageLayout<MB>::scale_off + P * 32>(sa);
-    StageReader<P + 1, MB, SOFF>::run(pa, sa, w, sc);
+struct PlaneReader {
+  static __device__ inline void run(uint32_t a, uint32_t (&w)[MB]) {
+    w[P] = lds_rd32<SOFF + P * 256>(a);
+    PlaneReader<P + 1, MB, SOFF>::run(a, w);
   }
 };
 template <int MB, int SOFF>
-struct StageReader<MB, MB, SOFF> {
-  static __device__ inline void run(uint32_t, uint32_t, uint32_t (&)[MB], uint2 (&)[MB - 1]) {}
+struct PlaneReader<MB, MB, SOFF> {
+  static __device__ inline void run(uint32_t, uint32_t (&)[MB]) {}
+};
+template <int L, int LV, int SOFF>
+struct ScaleReader {
+  static __device__ inline void run(uint32_t a, uint2 (&sc)[LV]) {
+    sc[L] = lds_rd64<SOFF + L * 32>(a);
+    ScaleReader<L + 1, LV, SOFF>::run(a, sc);
+  }
+};
+template <int LV, int SOFF>
+struct ScaleReader<LV, LV, SOFF> {
+  static __device__ inline void run(uint32_t, uint2 (&)[LV]) {}
 };
 
-template <int MB, int SOFF, typename Ctx>
-__device__ inline void read_stage(const Ctx& c, uint32_t (&w)[MB], uint2 (&sc)[MB - 1],
-                                  uint32_t& z) {
-  StageReader<0, MB, SOFF>::run(c.lds_pl, c.lds_sc, w, sc);
-  z = lds_rdu8<SOFF + StageLayout<MB>::zero_off>(c.lds_z);
+// Plane words, the four binary16 scales per level of the lane's output rows,
+// and the zero point of the lane's operand row (BMIN <= 2) or the four zero
+// points of its output rows (BMIN >= 3).
+template <int MB, int BMIN, int SOFF, typename Ctx>
+__device__ inline void read_stage(const Ctx& c, uint32_t (&w)[MB],
+                                  uint2 (&sc)[StageLayout<MB, BMIN>::levels], uint32_t& z) {
+  using SL = StageLayout<MB, BMIN>;
+  PlaneReader<0, MB, SOFF>::run(c.lds_pl, w);
+  ScaleReader<0, SL::levels, SOFF + SL::scale_off>::run(c.lds_sc, sc);
+  if constexpr (BMIN <= 2)
+    z = lds_rdu8<SOFF + SL::zero_off>(c.lds_z);
+  else
+    z = lds_rd32<SOFF + SL::zero_off>(c.lds_zq);
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
   for (int p = 0; p < MB; ++p) asm volatile("" : "+v"(w[p]));
 #pragma unroll
-  for (int p = 0; p < MB - 1; ++p) asm volatile("" : "+v"(sc[p]));
+  for (int l = 0; l < SL::levels; ++l) asm volatile("" : "+v"(sc[l]));
   asm volatile("" : "+v"(z));
 }
 
+// fp4 operand of the constant z - (2^BMIN - 1)/2 for BMIN <= 2 (it is one of
+// +-0.5, +-1.5): BMIN = 2, z = 0..3 -> B, 9, 1, 3; BMIN = 1, z = 0..1 -> 9, 1.
+template <int BMIN>
+__device__ inline v8i zero_operand(uint32_t z) {
+  const uint32_t c = ((BMIN == 2 ? 0x319Bu : 0x19u) >> (z << 2)) & 0xFu;
+  const uint32_t dw = c * 0x11111111u;
+  v8i a;
+  a[0] = a[1] = a[2] = a[3] = (int)dw;
+  a[4] = a[5] = a[6] = a[7] = 0;
+  return a;
+}
+
+// fp4 operand of all ones (code 2 is 1.0).
+__device__ inline v8i ones_operand() {
+  v8i a;
+  a[0] = a[1] = a[2] = a[3] = 0x22222222;
+  a[4] = a[5] = a[6] = a[7] = 0;
+  return a;
+}
+
+// One group of the wave's 16 rows against the column blocks' activations.
+//   Base level: plane p < BMIN with A scale 2^p reads 2^p (1/2 - bit p), so
+//   the chained MFMAs give m = h S - Q.x with h = (2^BMIN - 1)/2 and S the
+//   column's activation sum, and s1 (Q - z).x = -s1 m + s1 (h - z) S.  For
+//   BMIN <= 2 the constant operand z - h joins the chain, leaving -s1 m; for
+//   larger BMIN, S comes from one MFMA with an all-ones operand and the
+//   second term is one FMA per output.
+//   Residual level p >= BMIN: one MFMA with A scale 2 (-sigma) and one FMA
+//   with -s_p.
 // Planes a token does not request are switched off through its activation
 // block scale: E8M0 code 0 scales that column's products by 2^-127, which
 // leaves at most ~1e-33 (|x| < 2^9 per fp8 piece, 128 terms) in place of an
 // exact zero.
-template <int MB, int SOFF, int NCB>
+template <int MB, int BMIN, int SOFF, int NCB>
 __device__ inline void compute_group(const BData<NCB>& t, const WaveCtx<NCB>& c,
                                      v4f (&acc)[NCB]) {
+  using SL = StageLayout<MB, BMIN>;
   int bit[NCB], bsc[NCB];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) {
@@ -506,28 +552,49 @@ __device__ inline void compute_group(const BData<NCB>& t, const WaveCtx<NCB>& c,
   }
   const SigmaConsts& k = c.k;
   uint32_t w[MB];
-  uint2 sw[MB - 1];
+  uint2 sw[SL::levels];
   uint32_t z;
-  read_stage<MB, SOFF>(c, w, sw, z);
-  const v8i a0 = expand_sigma(w[0], k), a1 = expand_sigma(w[1], k);
-  const v8i au = zero_operand(z);
+  read_stage<MB, BMIN, SOFF>(c, w, sw, z);
   float s1[4];
   scales4(sw[0], s1);
-  // base: sum_k x_k (1.5 - Q_k) + sum_k x_k (z - 1.5), accumulated in place
+  float zc[4];  // s1 (h - z) of the lane's output rows (BMIN >= 3)
+  if constexpr (BMIN >= 3) {
+    constexpr float h = 0.5f * (float)((1 << BMIN) - 1);
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) {
-    const v8i bb = b8(t, cb);
-    v4f m = mfma_fp4_fp8(au, bb, 127, bsc[cb]);
-    m = mfma_fp4_fp8(a0, bb, m, 127, bsc[cb]);
-    m = mfma_fp4_fp8(a1, bb, m, 128, bsc[cb]);
+    for (int r = 0; r < 4; ++r) zc[r] = s1[r] * (h - (float)((z >> (8 * r)) & 0xffu));
+  }
+  // base chain, one expanded plane operand at a time for all column blocks
+  v4f m[NCB];
+  if constexpr (BMIN <= 2) {
+    const v8i au = zero_operand<BMIN>(z);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-s1[r], m[r], acc[cb][r]);
+    for (int cb = 0; cb < NCB; ++cb) m[cb] = mfma_fp4_fp8(au, b8(t, cb), 127, bsc[cb]);
+  } else {
+    const v8i a0 = expand_sigma(w[0], k);
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) m[cb] = mfma_fp4_fp8(a0, b8(t, cb), 127, bsc[cb]);
   }
 #pragma unroll
-  for (int p = 2; p < MB; ++p) {
+  for (int p = BMIN <= 2 ? 0 : 1; p < BMIN; ++p) {
+    const v8i ap = expand_sigma(w[p], k);
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) m[cb] = mfma_fp4_fp8(ap, b8(t, cb), m[cb], 127 + p, bsc[cb]);
+  }
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-s1[r], m[cb][r], acc[cb][r]);
+    if constexpr (BMIN >= 3) {
+      const v4f so = mfma_fp4_fp8(ones_operand(), b8(t, cb), 127, bsc[cb]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(zc[r], so[r], acc[cb][r]);
+    }
+  }
+#pragma unroll
+  for (int p = BMIN; p < MB; ++p) {
     const v8i ap = expand_sigma(w[p], k);
     float sp[4];
-    scales4(sw[p - 1], sp);
+    scales4(sw[p - BMIN + 1], sp);
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
       const int bs = p < bit[cb] ? bsc[cb] : 0;
@@ -548,8 +615,9 @@ __device__ inline void wait_vm() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// One wave's share: groups [g0, g1) at MB planes, through this wave's ring
-// of kDepth stages (kStage bytes apart, starting at `ring`).  Order of issue:
+// One wave's share: groups [g0, g1) at MB planes of a nest starting at BMIN
+// bits, through this wave's ring of kDepth stages (stage_bytes<BMIN>() bytes
+// apart, starting at `ring`).  Order of issue:
 // the prologue sends the DMA of g0 and g0+1, the activations of g0, then the
 // DMA of g0+2; the step that computes group g sends the activations of g+1
 // and the DMA of g+3, then waits.  Before that wait, the memory instructions
@@ -560,29 +628,30 @@ __device__ inline void wait_vm() {
 // activations of g ready.  The DMA of g+3 overwrites the stage of g-1, whose
 // LDS reads completed in the previous step.  The loop is unrolled by kDepth
 // so every stage offset is a constant.
-template <int MB, int NCB>
+template <int MB, int BMIN, int NCB>
 __device__ inline void decode_groups(const WaveCtx<NCB>& c, uint8_t* ring, int g0, int g1,
                                      v4f (&acc)[NCB]) {
   static_assert(kDepth == 4, "the unrolled step below assumes four stages");
   if (g0 >= g1) return;
-  constexpr int ND = StageLayout<MB>::ops, NB = 2 * NCB;
-  const DmaPlan<MB> plan = dma_plan<MB>(c);
+  constexpr int ND = StageLayout<MB, BMIN>::ops, NB = 2 * NCB;
+  constexpr int kStage = stage_bytes<BMIN>();
+  const DmaPlan<MB, BMIN> plan = dma_plan<MB, BMIN>(c);
   BData<NCB> B[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) B[i].lo[cb] = B[i].hi[cb] = v4i{0, 0, 0, 0};
-  dma_group<MB>(plan, c, g0, ring);
-  if (g0 + 1 < g1) dma_group<MB>(plan, c, g0 + 1, ring + kStage);
+  dma_group<MB, BMIN>(plan, c, g0, ring);
+  if (g0 + 1 < g1) dma_group<MB, BMIN>(plan, c, g0 + 1, ring + kStage);
   load_b(B[0], c, g0);
-  if (g0 + 2 < g1) dma_group<MB>(plan, c, g0 + 2, ring + 2 * kStage);
+  if (g0 + 2 < g1) dma_group<MB, BMIN>(plan, c, g0 + 2, ring + 2 * kStage);
 #define D2MOE_STEP(K)                                                        \
   {                                                                          \
     const int gg = g + (K);                                                  \
     if (gg >= g1) break;                                                     \
     if (gg + 1 < g1) load_b(B[((K) + 1) & 1], c, gg + 1);                    \
     if (gg + 3 < g1) {                                                       \
-      dma_group<MB>(plan, c, gg + 3, ring + (((K) + 3) % kDepth) * kStage);  \
+      dma_group<MB, BMIN>(plan, c, gg + 3, ring + (((K) + 3) % kDepth) * kStage); \
       wait_vm<2 * ND + NB>();                                                \
     } else if (gg + 2 < g1) {                                                \
       wait_vm<ND + NB>();                                                    \
@@ -592,7 +661,7 @@ __device__ inline void decode_groups(const WaveCtx<NCB>& c, uint8_t* ring, int g
       wait_vm<0>();                                                          \
     }                                                                        \
     ready_b(B[(K) & 1]);                                                     \
-    compute_group<MB, ((K) % kDepth) * kStage, NCB>(B[(K) & 1], c, acc);     \
+    compute_group<MB, BMIN, ((K) % kDepth) * kStage, NCB>(B[(K) & 1], c, acc); \
   }
   for (int g = g0; g < g1; g += kDepth) {
     D2MOE_STEP(0)
@@ -614,18 +683,21 @@ __device__ inline void decode_groups(const WaveCtx<NCB>& c, uint8_t* ring, int g
 // which is idle by then).  NCB column blocks of 8 tokens share every plane
 // operand (two when experts hold more than 8 positions on average), at 4
 // waves per SIMD for one block and 3 for two.
-template <bool SWIGLU, int NW, int NCB>
+template <bool SWIGLU, int NW, int NCB, int BMIN>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NCB == 1 ? 4 : 3)))
 void decode_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* __restrict__ Xq,
                    const uint32_t* __restrict__ Xs, int npos, int f, float* __restrict__ out,
                    int out_ld, uint32_t* __restrict__ rowmax) {
+  constexpr int kStage = stage_bytes<BMIN>();
   __shared__ __attribute__((aligned(16))) uint8_t ring[NW][kDepth * kStage];
   static_assert(kDepth * kStage >= NCB * 64 * 4 * (int)sizeof(float),
                 "partial sums fit the ring");
   const int ei = blockIdx.y;
   const int e = elist[4 * ei], p0 = elist[4 * ei + 1], p1 = elist[4 * ei + 2];
-  const int mb = elist[4 * ei + 3];
-  if (mb == 0) return;
+  const int mb_req = elist[4 * ei + 3];
+  if (mb_req == 0) return;
+  // planes actually read never exceed the packed nest, whatever the routing
+  const int mb = mb_req < W.b_max ? mb_req : W.b_max;
   const int rb = blockIdx.x;
   const int lane = threadIdx.x & 63;
   // wave-uniform by construction; readfirstlane lets the compiler keep the
@@ -685,19 +757,20 @@ void decode_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* 
     c.lds_pl = base + 4 * lane;
     c.lds_sc = base + 8 * c.q;
     c.lds_z = base + c.j;
+    c.lds_zq = base + 4 * c.q;
   }
 
   v4f acc[NCB];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) acc[cb] = v4f{0.f, 0.f, 0.f, 0.f};
   switch (mb) {
-    case 2: decode_groups<2, NCB>(c, ring[wave], g0, g1, acc); break;
-    case 3: decode_groups<3, NCB>(c, ring[wave], g0, g1, acc); break;
-    case 4: decode_groups<4, NCB>(c, ring[wave], g0, g1, acc); break;
-    case 5: decode_groups<5, NCB>(c, ring[wave], g0, g1, acc); break;
-    case 6: decode_groups<6, NCB>(c, ring[wave], g0, g1, acc); break;
-    case 7: decode_groups<7, NCB>(c, ring[wave], g0, g1, acc); break;
-    case 8: decode_groups<8, NCB>(c, ring[wave], g0, g1, acc); break;
+#define D2MOE_CASE(MB) \
+  case MB:             \
+    if constexpr (MB >= BMIN) decode_groups<MB, BMIN, NCB>(c, ring[wave], g0, g1, acc); \
+    break;
+    D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
+    D2MOE_CASE(7) D2MOE_CASE(8)
+#undef D2MOE_CASE
     default: break;
   }
 
@@ -763,13 +836,31 @@ hipError_t run_xprep(const TIN* in, int in_ld, const int32_t* perm, int kdiv, in
 }  // namespace
 
 bool decode_path_ok(const d2moe_mwq* w13, const d2moe_mwq* w2, int T) {
-  return T <= kDecodeMaxTokens && w13->group == 128 && w2->group == 128 && w13->b_min == 2 &&
-         w2->b_min == 2;
+  return T <= kDecodeMaxTokens && w13->group == 128 && w2->group == 128;
 }
 
 // Waves per workgroup: one per SIMD, so that the per-SIMD register budget,
 // not the workgroup size, sets how many workgroups share a compute unit.
 constexpr int kDecodeWaves = 4;
+
+template <bool SWIGLU, int NCB>
+hipError_t launch_decode_kernel(int b_min, dim3 grid, const MwqView& W, const int32_t* elist,
+                                const uint8_t* Xq, const uint32_t* Xs, int npos, int f,
+                                float* out, int out_ld, uint32_t* rowmax, hipStream_t s) {
+  switch (b_min) {
+#define D2MOE_CASE(B)                                                                      \
+  case B:                                                                                  \
+    decode_kernel<SWIGLU, kDecodeWaves, NCB, B><<<grid, 64 * kDecodeWaves, 0, s>>>(        \
+        W, elist, Xq, Xs, npos, f, out, out_ld, rowmax);                                   \
+    break;
+    D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
+    D2MOE_CASE(7) D2MOE_CASE(8)
+#undef D2MOE_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_ff, int E, int k,
                              const d2moe_mwq* w13, const d2moe_mwq* w2, const d2moe_routing* r,
@@ -793,25 +884,22 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   if (err != hipSuccess) return err;
   const MwqView W13 = view_of(w13), W2 = view_of(w2);
   if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
-  if (ncb == 1)
-    decode_kernel<true, kDecodeWaves, 1><<<dim3(d_ff / 16, ny), 64 * kDecodeWaves, 0, s>>>(
-        W13, b.elist, b.xq13, b.xs13, npos, d_ff, b.h32, d_ff, b.hmax);
-  else
-    decode_kernel<true, kDecodeWaves, 2><<<dim3(d_ff / 16, ny), 64 * kDecodeWaves, 0, s>>>(
-        W13, b.elist, b.xq13, b.xs13, npos, d_ff, b.h32, d_ff, b.hmax);
-  if ((err = hipGetLastError()) != hipSuccess) return err;
+  const dim3 g13(d_ff / 16, ny), g2(d / 16, ny);
+  err = ncb == 1 ? launch_decode_kernel<true, 1>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13,
+                                                 npos, d_ff, b.h32, d_ff, b.hmax, s)
+                 : launch_decode_kernel<true, 2>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13,
+                                                 npos, d_ff, b.h32, d_ff, b.hmax, s);
+  if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
   err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.hmax, d_ff / 16, b.xq2, b.xs2, r,
                          false, E, L, nullptr, 0, item, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
-  if (ncb == 1)
-    decode_kernel<false, kDecodeWaves, 1><<<dim3(d / 16, ny), 64 * kDecodeWaves, 0, s>>>(
-        W2, b.elist, b.xq2, b.xs2, npos, 0, b.y, d, nullptr);
-  else
-    decode_kernel<false, kDecodeWaves, 2><<<dim3(d / 16, ny), 64 * kDecodeWaves, 0, s>>>(
-        W2, b.elist, b.xq2, b.xs2, npos, 0, b.y, d, nullptr);
-  if ((err = hipGetLastError()) != hipSuccess) return err;
+  err = ncb == 1 ? launch_decode_kernel<false, 1>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
+                                                  0, b.y, d, nullptr, s)
+                 : launch_decode_kernel<false, 2>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
+                                                  0, b.y, d, nullptr, s);
+  if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
   return hipSuccess;
 }

@@ -60,7 +60,7 @@ def round_to_bf16(a: np.ndarray) -> np.ndarray:
     return upper.astype(np.uint32).view(np.float32)
 
 
-# ---- the five workloads -----------------------------------------------------
+# ---- workloads ----------------------------------------------------------------
 
 def tiny(seed: int = 0) -> LayerSpec:
     """d_model 256, d_ff 512, 8 SwiGLU experts, top-2, 64 tokens, fp32
@@ -94,6 +94,34 @@ def fine_grained(seed: int = 4) -> LayerSpec:
     return LayerSpec("fine_grained", d=2048, f=1408, E=64, k=6, T=512, group=64,
                      x_dtype="bf16", seed=seed, shared_f=5632, shared_bits=8,
                      bits_mode="hottest_first")
+
+
+def mixtral_decode_v1(T: int = 16, seed: int = 6) -> LayerSpec:
+    """The Mixtral decode layer under the paper's first configuration (Sec. 5):
+    nest b_1 = 2 to b_K = 4, group 128, per-(request, expert) bit-widths
+    {2,3,4} drawn with the expert capacities {.3,.4,.3}."""
+    return LayerSpec("mixtral_decode_v1", d=4096, f=14336, E=8, k=2, T=T, group=128,
+                     x_dtype="bf16", n_requests=T, seed=seed, b_min=2, b_max=4,
+                     bits_choices=(2, 3, 4), bits_probs=(0.3, 0.4, 0.3))
+
+
+def mixtral_decode_v2(T: int = 16, seed: int = 7) -> LayerSpec:
+    """The Mixtral decode layer under the paper's second configuration
+    (Sec. 5): nest b_1 = 5 to b_K = 8, group 128, per-(request, expert)
+    bit-widths {5,6,7,8} with capacity .25 each."""
+    return LayerSpec("mixtral_decode_v2", d=4096, f=14336, E=8, k=2, T=T, group=128,
+                     x_dtype="bf16", n_requests=T, seed=seed, b_min=5, b_max=8,
+                     bits_choices=(5, 6, 7, 8), bits_probs=(0.25, 0.25, 0.25, 0.25))
+
+
+def dense_decode(T: int = 16, seed: int = 8) -> LayerSpec:
+    """A dense LLM's SwiGLU FFN (LLaMA2-13B shape: d_model 5120, d_ff 13824)
+    as the one-expert, top-1 case of the same layer (the paper's dense-model
+    extension, Sec. 5), decoding T requests with per-request bit-widths of the
+    first configuration's nest {2,3,4} ({.3,.4,.3}), group 128."""
+    return LayerSpec("dense_decode", d=5120, f=13824, E=1, k=1, T=T, group=128,
+                     x_dtype="bf16", n_requests=T, seed=seed, b_min=2, b_max=4,
+                     bits_choices=(2, 3, 4), bits_probs=(0.3, 0.4, 0.3))
 
 
 def mixtral_stack(seed: int = 5) -> LayerSpec:

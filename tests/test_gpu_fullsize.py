@@ -213,3 +213,22 @@ def test_fine_grained_full_size_sampled():
     s = wl.fine_grained()
     rows = np.arange(0, s.d, 8) + np.arange(s.d // 8) % 8
     _sampled_full_layer(s, t0, rows)
+
+
+def test_mixtral_v2_decode_full_size_sampled():
+    """Batch-16 decode of the full Mixtral layer under the paper's second
+    nest (b_min 5, b_max 8): routing on every token, the output on tokens
+    covering every (expert, bit) bucket, 256 of the 4096 output columns."""
+    t0 = time.time()
+    s = wl.mixtral_decode_v2(T=16)
+    rows = np.arange(0, s.d, 16) + np.arange(s.d // 16) % 16
+    _sampled_full_layer(s, t0, rows)
+
+
+def test_dense_full_size_sampled():
+    """LLaMA2-13B-shaped dense SwiGLU FFN (one expert, top-1), batch 16 at
+    bits {2,3,4}: every token's output on 320 of the 5120 columns."""
+    t0 = time.time()
+    s = wl.dense_decode(T=16)
+    rows = np.arange(0, s.d, 16) + np.arange(s.d // 16) % 16
+    _sampled_full_layer(s, t0, rows)

@@ -175,6 +175,21 @@ FWD_SPECS = {
     "decode_T64": wl.scaled(wl.mixtral_decode(T=64), d=256, f=256),
     "prefill_small": wl.scaled(wl.mixtral_prefill(), d=256, f=384, T=600),
     "fine_small": wl.scaled(wl.fine_grained(), d=256, f=128, T=200, shared_f=192),
+    # the paper's two nests and its dense-model case, and other nest starts
+    # (decode kernels at b_min 1, 3, 5 and 8; two column blocks at T 24, 40)
+    "decode_v1_T16": wl.scaled(wl.mixtral_decode_v1(T=16), d=512, f=384),
+    "decode_v2_T16": wl.scaled(wl.mixtral_decode_v2(T=16), d=512, f=384),
+    "decode_v2_T40": wl.scaled(wl.mixtral_decode_v2(T=40), d=256, f=256),
+    "decode_b1_T8": wl.scaled(wl.mixtral_decode(T=8), d=256, f=256, b_min=1, b_max=8,
+                              bits_choices=(1, 3, 8), bits_probs=None),
+    "decode_b3_T24": wl.scaled(wl.mixtral_decode(T=24), d=256, f=256, b_min=3, b_max=6,
+                               bits_choices=(3, 4, 6), bits_probs=None),
+    "decode_b8_T4": wl.scaled(wl.mixtral_decode(T=4), d=256, f=256, b_min=8, b_max=8,
+                              bits_choices=(8,), bits_probs=None),
+    "dense_T16": wl.scaled(wl.dense_decode(T=16), d=512, f=768),
+    "dense_T64": wl.scaled(wl.dense_decode(T=64), d=256, f=512),
+    "prefill_v2_small": wl.scaled(wl.mixtral_prefill(), d=256, f=384, T=300, b_min=5, b_max=8,
+                                  bits_choices=(5, 6, 8)),
 }
 
 
