@@ -253,19 +253,22 @@ __device__ inline v8i expand_sigma(uint32_t w, const SigmaConsts& k) {
 //
 // This 8-pass MFMA must not write registers it is still reading, but the
 // compiler treats a 4-register result as free to overlap the operands.  Each
-// call therefore keeps its operands live past the instruction (an empty asm
-// that reads them), so the result is always given registers of its own.
+// call therefore passes its result through an empty asm that also reads the
+// operands: the asm must follow the MFMA (it consumes the result), and the
+// operands are live up to it, so the result is always given registers of
+// its own.  (An asm that only reads the operands is not enough: nothing
+// orders it after the MFMA, and the scheduler may move it above.)
 __device__ inline v4i lo4(const v8i& a) { return v4i{a[0], a[1], a[2], a[3]}; }
 
 __device__ inline v4f mfma_fp4_fp8(const v8i& a, const v8i& b, int sa, int sb) {
-  const v4f d = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
+  v4f d = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
       a, b, v4f{0.f, 0.f, 0.f, 0.f}, 4, 0, 0, sa, 0, sb);
-  asm volatile("" ::"v"(lo4(a)), "v"(b), "v"(sa), "v"(sb));
+  asm volatile("" : "+v"(d) : "v"(lo4(a)), "v"(b), "v"(sa), "v"(sb));
   return d;
 }
 __device__ inline v4f mfma_fp4_fp8(const v8i& a, const v8i& b, v4f c, int sa, int sb) {
-  const v4f d = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 4, 0, 0, sa, 0, sb);
-  asm volatile("" ::"v"(lo4(a)), "v"(b), "v"(c), "v"(sa), "v"(sb));
+  v4f d = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 4, 0, 0, sa, 0, sb);
+  asm volatile("" : "+v"(d) : "v"(lo4(a)), "v"(b), "v"(c), "v"(sa), "v"(sb));
   return d;
 }
 
