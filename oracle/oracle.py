@@ -13,6 +13,10 @@ Every routine follows a passage of the paper (D^2MoE, arXiv 2504.15299):
   * ``gate_logits`` / ``route_from_logits`` -- dual routing (Fig. 1): top-k
                           expert IDs plus a bit-width per activated expert, and
                           the selection counts B_{j,k} of Sec. 3.4.3;
+  * ``bit_router_probs`` / ``bit_router_choice`` / ``route_learned`` -- the
+                          token-adaptive bit-width routers of Sec. 3.2 (one
+                          per expert, a probability over the nest's widths,
+                          the most probable width used at inference);
   * ``expert_ffn`` / ``combine`` / ``moe_layer`` -- a SwiGLU expert FFN at the
                           selected bit-width and the weighted combine.
 """
@@ -194,6 +198,46 @@ def route_from_logits(logits: np.ndarray, k: int, token_req: np.ndarray | None,
         _p(o["slot_of"]), _p(o["maxbit"]))
     _ok(rc, "route_from_logits")
     return o
+
+
+# ---- learned bit-width routers (Sec. 3.2) -----------------------------------
+
+def bit_router_probs(bit_logits: np.ndarray) -> np.ndarray:
+    """Sec. 3.2: each expert's bit-width router assigns the token a probability
+    over the nest's candidate widths b_min..b_max, the softmax of its scores
+    (the p_k of Eq. 1).  bit_logits [..., L] -> probabilities [..., L],
+    binary64."""
+    z = np.asarray(bit_logits, dtype=np.float64)
+    e = np.exp(z - z.max(axis=-1, keepdims=True))
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def bit_router_choice(bit_logits: np.ndarray, b_min: int) -> np.ndarray:
+    """The width each router selects at inference: its most probable
+    candidate, i.e. the largest score (the softmax is increasing), the lowest
+    width when scores are equal.  bit_logits [T][E][L] -> uint8 [T][E]."""
+    z = np.asarray(bit_logits, dtype=np.float64)
+    T, E, L = z.shape
+    out = np.zeros((T, E), np.uint8)
+    for t in range(T):
+        for e in range(E):
+            best = 0
+            for l in range(1, L):
+                if z[t, e, l] > z[t, e, best]:
+                    best = l
+            out[t, e] = b_min + best
+    return out
+
+
+def route_learned(logits: np.ndarray, k: int, bit_logits: np.ndarray, b_min: int = 2,
+                  b_max: int = 8) -> dict:
+    """Dual routing with the learned routers: the top-k experts of
+    ``route_from_logits``, each activated expert at its router's choice for
+    the token.  The choices form a per-(token, expert) width table, i.e. one
+    request per token."""
+    choice = bit_router_choice(bit_logits, b_min)
+    T = choice.shape[0]
+    return route_from_logits(logits, k, np.arange(T, dtype=np.int32), choice, b_min, b_max)
 
 
 # ---- expert FFN, combine, whole layer --------------------------------------

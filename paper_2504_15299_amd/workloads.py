@@ -17,7 +17,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 # purpose keys for the seed tree
-_X, _WG, _W13, _W2, _BITS, _SH13, _SH2 = range(7)
+_X, _WG, _W13, _W2, _BITS, _SH13, _SH2, _ROUTER = range(8)
 
 
 @dataclass
@@ -186,6 +186,18 @@ def shared_w2(spec: LayerSpec, layer: int = 0) -> np.ndarray:
     return (_rng(spec.seed, layer, _SH2).standard_normal((spec.d, spec.shared_f),
                                                           dtype=np.float32)
             * np.float32(spec.w_std))
+
+
+def bit_routers(spec: LayerSpec, layer: int = 0, std: float = 0.05):
+    """Weights of the per-expert bit-width routers, one linear map from the
+    token to the nest's L = b_max - b_min + 1 widths: Wr [E][L][d] and bias
+    br [E][L] (binary32 Gaussians; trained router weights are not
+    available)."""
+    L = spec.b_max - spec.b_min + 1
+    g = _rng(spec.seed, layer, _ROUTER)
+    Wr = g.standard_normal((spec.E, L, spec.d), dtype=np.float32) * np.float32(std)
+    br = g.standard_normal((spec.E, L), dtype=np.float32) * np.float32(std)
+    return Wr, br
 
 
 def token_requests(spec: LayerSpec) -> np.ndarray:
