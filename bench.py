@@ -63,6 +63,8 @@ def main():
     ap.add_argument("--variant-steps", type=int, default=40,
                     help="also time batch-16 decode under the paper's two nests (b 2-4, b 5-8) "
                          "and the LLaMA2-13B-shaped dense FFN (0: skip)")
+    ap.add_argument("--no-learned", dest="learned", action="store_false",
+                    help="skip the decode step with learned bit-width routers")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of one captured HIP graph per layer step instead of "
                          "eager launches")
@@ -453,7 +455,67 @@ def main():
                 "w13_alg_bytes": b13, "w13_GBps": round(gbps, 1),
                 "w13_hbm_frac": round(gbps / HBM_PEAK_GBPS, 4)}
 
+    def run_learned(T, steps, warmup=5):
+        """The batch-T decode step of the rotating layers with the learned
+        bit-width routers of Sec. 3.2 in place of the width table (one linear
+        router per expert over the 7 widths of the nest, seeded Gaussian
+        weights), and the routing calls alone with either source of widths.
+        Reports the step time and the routers' share of it."""
+        L_ = b_max - b_min + 1
+        rng = np.random.default_rng(17 + T)
+        x = torch.from_numpy(rng.standard_normal((T, d), dtype=np.float32)).to(dev).to(torch.bfloat16)
+        req = torch.arange(T, dtype=torch.int32, device=dev)
+        table = torch.from_numpy(rng.choice(np.array([2, 3, 4, 8], np.uint8), size=(T, E),
+                                            p=[0.2, 0.3, 0.3, 0.2])).to(dev)
+        routers = []
+        for l in range(NL):
+            gen.manual_seed(3_000_000 + l)
+            routers.append((torch.randn((E, L_, d), generator=gen, device=dev) * 0.05,
+                            torch.randn((E, L_), generator=gen, device=dev) * 0.05))
+        r = api.Routing.empty(T, E, k, b_min, b_max, device=dev)
+        bl = torch.empty((T, E, L_), dtype=torch.float32, device=dev)
+        out = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+        ws = torch.empty(api.moe_forward_workspace(T, d, f, E, k), dtype=torch.uint8, device=dev)
+
+        def route_l(i):
+            w13, w2, Wg = layers[i % NL]
+            api.route_learned(x, Wg, None, k, routers[i % NL][0], routers[i % NL][1], b_min,
+                              b_max, out=r, bit_logits=bl)
+
+        def route_t(i):
+            api.route(x, layers[i % NL][2], None, k, req, table, b_min, b_max, out=r)
+
+        def step(i):
+            route_l(i)
+            w13, w2, Wg = layers[i % NL]
+            api.moe_forward(x, w13, w2, r, k, out=out, workspace=ws)
+
+        def timed(fn, n):
+            for i in range(warmup):
+                fn(i)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record()
+            for i in range(n):
+                fn(warmup + i)
+            b.record()
+            torch.cuda.synchronize()
+            return a.elapsed_time(b) / n
+
+        ms = timed(step, steps)
+        ms_rl = timed(route_l, steps)
+        ms_rt = timed(route_t, steps)
+        bits = r.topk_bits.cpu().numpy().ravel()
+        return {"workload": f"Mixtral-8x7B-shaped MoE layer decode, batch {T}, bit-widths from "
+                            f"learned per-expert routers over the 2..8 nest (seeded weights), "
+                            f"{NL} rotating layers",
+                "tokens": T, "ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms * 1e-3), 1),
+                "route_ms_learned": round(ms_rl, 4), "route_ms_table": round(ms_rt, 4),
+                "router_share_of_step": round((ms_rl - ms_rt) / ms, 4),
+                "widths_used_last_step": np.bincount(bits, minlength=b_max + 1)[b_min:].tolist()}
+
     main_res = run_batch(args.batch, args.steps, args.warmup, profile=True)
+    learned = run_learned(args.batch, max(args.steps // 2, 10)) if args.learned else None
     sweep = []
     for T in [int(v) for v in args.sweep.split(",") if v.strip()]:
         r = run_batch(T, max(args.steps // 2, 5), args.warmup, profile=True)
@@ -521,6 +583,7 @@ def main():
         "fine_grained": fine,
         "stack": stack_res,
         "variants": variants,
+        "learned_router": learned,
         "cpu_baseline": cpu,
         "pack_seconds": round(pack_s, 2),
     }

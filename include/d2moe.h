@@ -145,6 +145,29 @@ d2moe_status d2moe_route(const void* x, d2moe_dtype x_dtype, int32_t T,
                          int32_t b_max, const d2moe_routing* out,
                          void* stream);
 
+/*
+ * Dual routing with the learned bit-width routers of Sec. 3.2 in place of a
+ * bit-width table: a lightweight router per expert scores the nest's
+ * L = b_max - b_min + 1 candidate widths for each token (a softmax over those
+ * scores gives the width probabilities the routers are trained with, Eq. 1),
+ * and each activated expert runs at its router's most probable width.  The
+ * router is read as one linear map per expert:
+ *     bit_logits[t][e][l] = Wr[e][l] . x[t] + br[e][l],
+ *     bits[t][i] = b_min + argmax_l bit_logits[t][topk_idx[t][i]][l]
+ * (the lowest width wins ties).  Expert selection, weights, counts, scan and
+ * permutation are exactly those of d2moe_route.
+ *   Wr: device [E][L][d] float; br: device [E][L] float or NULL;
+ *   bit_logits: device [T][E][L] float, written for every (token, expert).
+ * Same constraints as d2moe_route (no request ids or table; flags stay 0).
+ * The routers' trained weights are not available; callers supply their own.
+ */
+d2moe_status d2moe_route_learned(const void* x, d2moe_dtype x_dtype, int32_t T,
+                                 int32_t d, const float* Wg, const float* bias,
+                                 int32_t E, int32_t k, const float* Wr,
+                                 const float* br, int32_t b_min, int32_t b_max,
+                                 float* bit_logits, const d2moe_routing* out,
+                                 void* stream);
+
 /* Workspace bytes needed by d2moe_moe_forward for these sizes (host). */
 d2moe_status d2moe_moe_forward_workspace(int32_t T, int32_t d, int32_t d_ff,
                                          int32_t E, int32_t k,

@@ -53,6 +53,8 @@ def lib():
         L.d2moe_debug_unpack.argtypes = [ctypes.POINTER(_Mwq), _I, _I, _P, _P, _P]
         L.d2moe_route.argtypes = [_P, _I, _I, _I, _P, _P, _I, _I, _P, _P, _I, _I, _I,
                                   ctypes.POINTER(_Routing), _P]
+        L.d2moe_route_learned.argtypes = [_P, _I, _I, _I, _P, _P, _I, _I, _P, _P, _I, _I, _P,
+                                          ctypes.POINTER(_Routing), _P]
         L.d2moe_moe_forward_workspace.argtypes = [_I, _I, _I, _I, _I, _I, sz]
         L.d2moe_moe_forward.argtypes = [_P, _I, _I, _I, _I, _I, _I, ctypes.POINTER(_Mwq),
                                         ctypes.POINTER(_Mwq), ctypes.POINTER(_Routing),
@@ -61,6 +63,7 @@ def lib():
         L.d2moe_moe_forward_profiled.argtypes = L.d2moe_moe_forward.argtypes + [_P]
         L.d2moe_residual_rmsnorm.argtypes = [_P, _P, _I, _I, _I, ctypes.c_float, _P, _I, _P]
         for name in ("d2moe_mwq_size", "d2moe_pack_mwq", "d2moe_debug_unpack", "d2moe_route",
+                     "d2moe_route_learned",
                      "d2moe_moe_forward_workspace", "d2moe_moe_forward",
                      "d2moe_moe_forward_profiled", "d2moe_residual_rmsnorm"):
             getattr(L, name).restype = _I
@@ -215,6 +218,29 @@ def route(x: torch.Tensor, Wg: torch.Tensor, bias, k: int, token_req, bit_table:
                                             bit_table.shape[0], b_min, b_max, ctypes.byref(c),
                                             _stream(stream)))
     return out
+
+
+def route_learned(x: torch.Tensor, Wg: torch.Tensor, bias, k: int, Wr: torch.Tensor, br,
+                  b_min=2, b_max=8, out: Routing | None = None,
+                  bit_logits: torch.Tensor | None = None, stream=None):
+    """Dual routing with learned bit-width routers (``d2moe_route_learned``):
+    Wr [E][L][d] float, br [E][L] float or None, L = b_max - b_min + 1.
+    Returns (routing, bit_logits [T][E][L])."""
+    T, d = x.shape
+    E = Wg.shape[0]
+    L_ = b_max - b_min + 1
+    if tuple(Wr.shape) != (E, L_, d):
+        raise ValueError(f"Wr must be [E][L][d] = {(E, L_, d)}, got {tuple(Wr.shape)}")
+    if out is None:
+        out = Routing.empty(T, E, k, b_min, b_max, device=x.device)
+    if bit_logits is None:
+        bit_logits = torch.empty((T, E, L_), dtype=torch.float32, device=x.device)
+    c = out._c()
+    _check("d2moe_route_learned",
+           lib().d2moe_route_learned(_ptr(x), _dtype_code(x), T, d, _ptr(Wg), _ptr(bias), E, k,
+                                     _ptr(Wr), _ptr(br), b_min, b_max, _ptr(bit_logits),
+                                     ctypes.byref(c), _stream(stream)))
+    return out, bit_logits
 
 
 # ---- forward ----------------------------------------------------------------

@@ -81,6 +81,25 @@ d2moe_status d2moe_route(const void* x, d2moe_dtype x_dtype, int32_t T, int32_t 
                                b_max, out, (hipStream_t)stream));
 }
 
+d2moe_status d2moe_route_learned(const void* x, d2moe_dtype x_dtype, int32_t T, int32_t d,
+                                 const float* Wg, const float* bias, int32_t E, int32_t k,
+                                 const float* Wr, const float* br, int32_t b_min, int32_t b_max,
+                                 float* bit_logits, const d2moe_routing* out, void* stream) {
+  if (T < 0 || d < 1 || E < 1 || E > 64 || k < 1 || k > E || !ladder_ok(b_min, b_max))
+    return D2MOE_EINVAL;
+  if (x_dtype != D2MOE_F32 && x_dtype != D2MOE_BF16) return D2MOE_EUNSUPPORTED;
+  if (!out || !out->hist || !out->offsets || !out->expert_maxbit || !out->flags)
+    return D2MOE_EINVAL;
+  if (T > 0 && (!out->topk_idx || !out->topk_w || !out->topk_bits || !out->perm ||
+                !out->slot_of || !out->logits))
+    return D2MOE_EINVAL;
+  if (T > 0 && (!x || !Wg || !Wr || !bit_logits)) return D2MOE_EINVAL;
+  if ((long long)T * k > (1ll << 30) || (long long)T * E * (b_max - b_min + 1) > (1ll << 31))
+    return D2MOE_EINVAL;
+  return from_hip(launch_route_learned(x, x_dtype, T, d, Wg, bias, E, k, Wr, br, b_min, b_max,
+                                       bit_logits, out, (hipStream_t)stream));
+}
+
 d2moe_status d2moe_moe_forward_workspace(int32_t T, int32_t d, int32_t d_ff, int32_t E,
                                          int32_t k, int32_t shared_d_ff, size_t* bytes) {
   if (T < 0 || d < 1 || d_ff < 1 || E < 1 || E > 64 || k < 1 || k > E || shared_d_ff < 0 ||

@@ -69,6 +69,10 @@ hipError_t launch_route(const void* x, d2moe_dtype xd, int T, int d, const float
                         const float* bias, int E, int k, const int32_t* token_req,
                         const uint8_t* bit_table, int R, int b_min, int b_max,
                         const d2moe_routing* out, hipStream_t s);
+hipError_t launch_route_learned(const void* x, d2moe_dtype xd, int T, int d, const float* Wg,
+                                const float* bias, int E, int k, const float* Wr,
+                                const float* br, int b_min, int b_max, float* bit_logits,
+                                const d2moe_routing* out, hipStream_t s);
 
 // Forward workspace layout (256-byte aligned sub-buffers).  The decode
 // buffers exist only when T <= kDecodeMaxTokens.

@@ -119,23 +119,50 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(
 // [0, R) was clamped), the same on every lane.
 struct TopkIn {
   float v;  // this lane's logit
-  int b;    // this lane's table bit-width
+  int b;    // this lane's bit-width for the token
   int flag;
 };
 
+// Where each (token, expert) bit-width comes from: a per-(request, expert)
+// table, or the learned bit-width routers' logits [T][E][L] over the nest's
+// L = b_max - b_min + 1 widths, whose argmax (lowest width on ties) selects
+// the width (Sec. 3.2).
+struct BitSource {
+  const int32_t* token_req;
+  const uint8_t* bit_table;
+  int R;
+  const float* rlogits;
+  int L, b_min;
+};
+
 __device__ inline TopkIn topk_load(const float* __restrict__ logits, int t, int E,
-                                   const int32_t* __restrict__ token_req,
-                                   const uint8_t* __restrict__ bit_table, int R, int lane) {
+                                   const BitSource& bs, int lane) {
   TopkIn in;
-  int r = token_req ? token_req[t] : 0;
   in.flag = 0;
-  if (r < 0 || r >= R) {
-    in.flag = 2;
-    r = r < 0 ? 0 : R - 1;
-  }
   const bool have = lane < E;
   in.v = have ? logits[(size_t)t * E + lane] : 0.0f;
-  in.b = have ? (int)bit_table[(size_t)r * E + lane] : 0;
+  if (bs.rlogits) {
+    int best = 0;
+    if (have) {
+      const float* rl = bs.rlogits + ((size_t)t * E + lane) * bs.L;
+      float bv = rl[0];
+      for (int l = 1; l < bs.L; ++l) {
+        const float v = rl[l];
+        if (v > bv) {
+          bv = v;
+          best = l;
+        }
+      }
+    }
+    in.b = bs.b_min + best;
+    return in;
+  }
+  int r = bs.token_req ? bs.token_req[t] : 0;
+  if (r < 0 || r >= bs.R) {
+    in.flag = 2;
+    r = r < 0 ? 0 : bs.R - 1;
+  }
+  in.b = have ? (int)bs.bit_table[(size_t)r * E + lane] : 0;
   return in;
 }
 
@@ -182,14 +209,13 @@ constexpr int kInlineTopk = 64;
 constexpr int kTopkThreads = 256;
 
 __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
-    const float* __restrict__ logits, int T, int E, int k, const int32_t* __restrict__ token_req,
-    const uint8_t* __restrict__ bit_table, int R, int b_min, int b_max,
+    const float* __restrict__ logits, int T, int E, int k, BitSource bs, int b_min, int b_max,
     int32_t* __restrict__ topk_idx, float* __restrict__ topk_w, uint8_t* __restrict__ topk_bits,
     int32_t* __restrict__ tflags) {
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * (kTopkThreads / 64) + (threadIdx.x >> 6);
   if (t >= T) return;
-  const TopkIn in = topk_load(logits, t, E, token_req, bit_table, R, lane);
+  const TopkIn in = topk_load(logits, t, E, bs, lane);
   const int fl = topk_wave(in, t, E, k, b_min, b_max, lane, topk_idx, topk_w, topk_bits);
   if (lane == 0) tflags[t] = fl;
 }
@@ -206,8 +232,7 @@ constexpr int kMaxKeys = 64 * 8;  // E <= 64, L <= 8
 // earlier slots with the same key comes from wave ballots (equal-key lane
 // masks) plus per-wave counts of earlier waves.
 __global__ __launch_bounds__(kHistThreads) void hist_perm_kernel(
-    const float* __restrict__ logits, int k, const int32_t* __restrict__ token_req,
-    const uint8_t* __restrict__ bit_table, int R, int b_max, int32_t* __restrict__ topk_idx,
+    const float* __restrict__ logits, int k, BitSource bs, int b_max, int32_t* __restrict__ topk_idx,
     float* __restrict__ topk_w, uint8_t* __restrict__ topk_bits, int T, int n, int E, int L,
     int b_min, int32_t* __restrict__ flags, int32_t* __restrict__ hist,
     int32_t* __restrict__ offsets, int32_t* __restrict__ perm, int32_t* __restrict__ slot_of,
@@ -230,7 +255,7 @@ __global__ __launch_bounds__(kHistThreads) void hist_perm_kernel(
 #pragma unroll
     for (int j = 0; j < TPW; ++j) {
       const int t = wave + kHistWaves * j;
-      if (t < T) in[j] = topk_load(logits, t, E, token_req, bit_table, R, lane);
+      if (t < T) in[j] = topk_load(logits, t, E, bs, lane);
     }
 #pragma unroll
     for (int j = 0; j < TPW; ++j) {
@@ -311,10 +336,9 @@ hipError_t run_gate(const XT* x, int T, int d, const float* Wg, const float* bia
 
 }  // namespace
 
-hipError_t launch_route(const void* x, d2moe_dtype xd, int T, int d, const float* Wg,
-                        const float* bias, int E, int k, const int32_t* token_req,
-                        const uint8_t* bit_table, int R, int b_min, int b_max,
-                        const d2moe_routing* out, hipStream_t s) {
+static hipError_t route_common(const void* x, d2moe_dtype xd, int T, int d, const float* Wg,
+                               const float* bias, int E, int k, const BitSource& bs, int b_min,
+                               int b_max, const d2moe_routing* out, hipStream_t s) {
   hipError_t err;
   const int L = b_max - b_min + 1;
   if (T > 0) {
@@ -326,16 +350,39 @@ hipError_t launch_route(const void* x, d2moe_dtype xd, int T, int d, const float
     if (T > kInlineTopk) {
       const int per = kTopkThreads / 64;
       topk_kernel<<<(T + per - 1) / per, kTopkThreads, 0, s>>>(
-          out->logits, T, E, k, token_req, bit_table, R, b_min, b_max, out->topk_idx,
-          out->topk_w, out->topk_bits, out->perm);
+          out->logits, T, E, k, bs, b_min, b_max, out->topk_idx, out->topk_w, out->topk_bits,
+          out->perm);
       if ((err = hipGetLastError()) != hipSuccess) return err;
     }
   }
   hist_perm_kernel<<<1, kHistThreads, 0, s>>>(
-      out->logits, k, token_req, bit_table, R, b_max, out->topk_idx, out->topk_w, out->topk_bits,
-      T, T * k, E, L, b_min, out->flags, out->hist, out->offsets, out->perm, out->slot_of,
-      out->expert_maxbit);
+      out->logits, k, bs, b_max, out->topk_idx, out->topk_w, out->topk_bits, T, T * k, E, L,
+      b_min, out->flags, out->hist, out->offsets, out->perm, out->slot_of, out->expert_maxbit);
   return hipGetLastError();
+}
+
+hipError_t launch_route(const void* x, d2moe_dtype xd, int T, int d, const float* Wg,
+                        const float* bias, int E, int k, const int32_t* token_req,
+                        const uint8_t* bit_table, int R, int b_min, int b_max,
+                        const d2moe_routing* out, hipStream_t s) {
+  const BitSource bs{token_req, bit_table, R, nullptr, b_max - b_min + 1, b_min};
+  return route_common(x, xd, T, d, Wg, bias, E, k, bs, b_min, b_max, out, s);
+}
+
+hipError_t launch_route_learned(const void* x, d2moe_dtype xd, int T, int d, const float* Wg,
+                                const float* bias, int E, int k, const float* Wr,
+                                const float* br, int b_min, int b_max, float* bit_logits,
+                                const d2moe_routing* out, hipStream_t s) {
+  const int L = b_max - b_min + 1;
+  if (T > 0) {
+    // the bit-width routers' logits, the E * L router rows taken as gate rows
+    const hipError_t err =
+        xd == D2MOE_BF16 ? run_gate((const uint16_t*)x, T, d, Wr, br, E * L, bit_logits, s)
+                         : run_gate((const float*)x, T, d, Wr, br, E * L, bit_logits, s);
+    if (err != hipSuccess) return err;
+  }
+  const BitSource bs{nullptr, nullptr, 1, bit_logits, L, b_min};
+  return route_common(x, xd, T, d, Wg, bias, E, k, bs, b_min, b_max, out, s);
 }
 
 }  // namespace d2moe

@@ -85,6 +85,13 @@ def test_validation_before_launch():
     r0 = api._Routing(*([1 << 20] * 9 + [0]))
     assert L.d2moe_route(fake, 1, 4, 64, fake, None, 8, 2, None, fake, 1, 2, 8, ctypes.byref(r0),
                          None) == api.EINVAL
+    # learned route: bad ladder, missing router weights or router logits
+    lr = L.d2moe_route_learned
+    assert lr(fake, 1, 4, 64, fake, None, 8, 2, fake, None, 3, 2, fake, rb, None) == api.EINVAL
+    assert lr(fake, 1, 4, 64, fake, None, 8, 2, None, None, 2, 8, fake, rb, None) == api.EINVAL
+    assert lr(fake, 1, 4, 64, fake, None, 8, 2, fake, None, 2, 8, None, rb, None) == api.EINVAL
+    assert lr(fake, 7, 4, 64, fake, None, 8, 2, fake, None, 2, 8, fake, rb, None) == \
+        api.EUNSUPPORTED
     # forward: shape mismatches and workspace
     w13 = _mwq(n_experts=8, rows=2 * 256, cols=128)
     w2 = _mwq(n_experts=8, rows=128, cols=256)

@@ -263,3 +263,91 @@ def test_forward_empty_batch():
     torch.cuda.synchronize()
     assert out.shape == (0, spec.d)
     assert int(r.hist.sum().item()) == 0 and int(r.offsets[-1].item()) == 0
+
+
+LEARNED_SPECS = {
+    "decode16_small": wl.scaled(wl.mixtral_decode(T=16), d=512, f=256),
+    "v2_T16": wl.scaled(wl.mixtral_decode_v2(T=16), d=512, f=256),
+    "prefill_small": wl.scaled(wl.mixtral_prefill(), d=256, f=256, T=300),
+    "fine_small": wl.scaled(wl.fine_grained(), d=256, f=64, T=200, shared_f=128),
+}
+
+
+@pytest.mark.parametrize("name", list(LEARNED_SPECS))
+def test_route_learned_parity(name):
+    """Learned bit-width routers (Sec. 3.2): gate and router logits within the
+    fp32 bound, expert choices exact on tokens decided beyond it, widths
+    exact on slots whose router is decided beyond it (otherwise a width
+    within twice the bound of the best), counts and permutation consistent
+    with the GPU's own choices, and the layer output on every fully decided
+    token within the forward tolerance."""
+    s = LEARNED_SPECS[name]
+    L = Layer(s)
+    Lw = s.b_max - s.b_min + 1
+    Wr, br = wl.bit_routers(s)
+    L.xt = L.x_dev()
+    bias = None if L.bias is None else torch.from_numpy(L.bias).to(DEV)
+    r, bl = api.route_learned(L.xt, torch.from_numpy(L.Wg).to(DEV), bias, s.k,
+                              torch.from_numpy(Wr).to(DEV), torch.from_numpy(br).to(DEV),
+                              s.b_min, s.b_max)
+    torch.cuda.synchronize()
+    ref_bl = O.gate_logits(L.x, Wr.reshape(s.E * Lw, s.d), br.reshape(-1)).reshape(s.T, s.E, Lw)
+    rbound = logit_error_bound(L.x, Wr.reshape(s.E * Lw, s.d), br.reshape(-1))
+    gbound = logit_error_bound(L.x, L.Wg, L.bias)
+    got_bl = bl.cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(got_bl - ref_bl) <= rbound[:, None, None])
+    logits = r.logits.cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(logits - L.ref_logits) <= gbound[:, None])
+    ref = O.route_learned(L.ref_logits, s.k, ref_bl, s.b_min, s.b_max)
+    amb = ambiguous_tokens(L.ref_logits, s.k, gbound)
+    assert amb.sum() <= max(1, s.T // 50)
+    idx = r.topk_idx.cpu().numpy()
+    bits = r.topk_bits.cpu().numpy().astype(np.int64)
+    assert np.array_equal(idx[~amb], ref["topk_idx"][~amb])
+    srt = -np.sort(-ref_bl, axis=2)
+    margin = srt[:, :, 0] - srt[:, :, 1] if Lw > 1 else np.full((s.T, s.E), np.inf)
+    decided = ~amb
+    for t in np.nonzero(~amb)[0]:
+        for i in range(s.k):
+            e = idx[t, i]
+            if margin[t, e] > 2 * rbound[t]:
+                assert bits[t, i] == ref["topk_bits"][t, i]
+            else:
+                decided[t] = False
+                assert ref_bl[t, e, bits[t, i] - s.b_min] >= srt[t, e, 0] - 2 * rbound[t]
+    check_routing_consistent(r, s.E, s.k, s.b_min, s.b_max)
+    assert int(r.flags.cpu().item()) == 0
+    print(f"{name}: near-tied tokens {int(amb.sum())}, tokens with a near-tied width "
+          f"{int((~amb & ~decided).sum())}, widths used {np.bincount(bits.ravel())}")
+    # the layer on the learned routing
+    L.pack()
+    L.r = r
+    got = L.forward()
+    c13, c2, sh = L.codes()
+    toks = np.nonzero(decided)[0]
+    want = O.moe_layer(L.x, ref, c13, c2, tokens=toks, shared=sh)
+    err = row_max_abs_rel(got[toks], want)
+    assert err.max() <= FWD_TOL, f"worst row {err.max():.3e}"
+
+
+def test_route_learned_fixed_widths_match_table():
+    """Routers with a decisive per-expert bias and no weights pick one width
+    per expert whatever the token: the routing equals d2moe_route with that
+    width table, output for output."""
+    s = wl.scaled(wl.mixtral_decode(T=40), d=256, f=128, n_requests=1)
+    L = Layer(s)
+    Lw = s.b_max - s.b_min + 1
+    widths = np.array([2, 8, 3, 5, 4, 7, 6, 2], np.uint8)
+    Wr = np.zeros((s.E, Lw, s.d), np.float32)
+    br = np.zeros((s.E, Lw), np.float32)
+    br[np.arange(s.E), widths - s.b_min] = 5.0
+    x = L.x_dev()
+    Wg = torch.from_numpy(L.Wg).to(DEV)
+    r1, _ = api.route_learned(x, Wg, None, s.k, torch.from_numpy(Wr).to(DEV),
+                              torch.from_numpy(br).to(DEV), s.b_min, s.b_max)
+    r2 = api.route(x, Wg, None, s.k, None, torch.from_numpy(widths[None, :]).to(DEV),
+                   s.b_min, s.b_max)
+    torch.cuda.synchronize()
+    for key in ("logits", "topk_idx", "topk_w", "topk_bits", "hist", "offsets", "perm",
+                "slot_of", "expert_maxbit", "flags"):
+        assert torch.equal(getattr(r1, key), getattr(r2, key)), key
