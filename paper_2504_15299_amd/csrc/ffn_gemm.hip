@@ -60,14 +60,14 @@ constexpr int kWTile = kTileRows * kStepK * 2;  // dequantized bf16 tile bytes
 constexpr int kChunkThreads = 512;
 __global__ __launch_bounds__(kChunkThreads) void chunk_kernel(
     const int32_t* __restrict__ hist, const int32_t* __restrict__ offsets, int nb, int L, int b_min,
-    int one_cnt, int one_bit, int n_ub, int32_t* __restrict__ chunks) {
+    int one_cnt, int one_bit, int one_cs, int n_ub, int32_t* __restrict__ chunks) {
   __shared__ int cnt[kChunkThreads], nch[kChunkThreads], first[kChunkThreads];
   const int j = threadIdx.x;
-  if (hist == nullptr) {  // one bucket: every position, expert 0
+  if (hist == nullptr) {  // one bucket: every position, expert 0, chunks of one_cs
     for (int c = j; c < n_ub; c += kChunkThreads) {
-      const int m0 = c * kChunk;
+      const int m0 = c * one_cs;
       chunks[4 * c] = m0;
-      chunks[4 * c + 1] = m0 < one_cnt ? min(kChunk, one_cnt - m0) : 0;
+      chunks[4 * c + 1] = m0 < one_cnt ? min(one_cs, one_cnt - m0) : 0;
       chunks[4 * c + 2] = one_bit;
       chunks[4 * c + 3] = 0;
     }
@@ -79,11 +79,13 @@ __global__ __launch_bounds__(kChunkThreads) void chunk_kernel(
   __syncthreads();
   // chunks of the buckets that come before this one in size order
   int before = 0;
+#pragma unroll 16
   for (int i = 0; i < nb; ++i)
     if (cnt[i] > cj || (cnt[i] == cj && i < j)) before += nch[i];
   first[j] = before;
   __syncthreads();
   int total = 0;
+#pragma unroll 16
   for (int i = 0; i < nb; ++i) total += nch[i];
   if (j < nb) {
     const int b0 = offsets[j];
@@ -223,12 +225,15 @@ __device__ __attribute__((always_inline)) inline void dequant_pairs(
 //           0..63) and W3 rows f+n0.. (tile rows 64..127); out = h [pos][f] bf16
 //   else:   W is [N][K], out = y [pos][N] fp32
 // `expert_fixed` >= 0 overrides the chunk's expert (the shared expert).
-template <int G, bool SWIGLU>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void bgemm_kernel(
+template <int G, bool SWIGLU, bool NARROW>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2)))
+void bgemm_kernel(
     const uint16_t* __restrict__ in, int in_ld, const int32_t* __restrict__ perm, int kdiv,
     MwqView W, const int32_t* __restrict__ chunks, int f, int N, void* __restrict__ out,
-    int out_ld) {
-  __shared__ __attribute__((aligned(16))) uint8_t xring[kXRing][8][kXStage];
+    int out_ld, int split, size_t out_split) {
+  // narrow chunks stage only wave 0's activations (56 KB of LDS in all, two
+  // workgroups per compute unit); wide ones each wave's (140 KB, one)
+  __shared__ __attribute__((aligned(16))) uint8_t xring[kXRing][NARROW ? 1 : 8][kXStage];
   __shared__ __attribute__((aligned(16))) uint8_t rraw[kRawRing][kRawStage];
   __shared__ __attribute__((aligned(16))) uint8_t wtile[2][kWTile];
   __shared__ __attribute__((aligned(16))) uint8_t dummy[1][16];
@@ -241,10 +246,27 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n0 = blockIdx.x * (SWIGLU ? kTileRows / 2 : kTileRows);
-  const int K = W.cols, nsteps = K / kStepK, b_min = W.b_min;
+  // reduction part blockIdx.z of gridDim.z (the plain variant only): steps
+  // [s_lo, s_lo + nsteps), partial sums to plane blockIdx.z of `out`
+  const int K = W.cols, b_min = W.b_min;
+  const int s_all = K / kStepK;
+  const int s_lo = SWIGLU ? 0 : (int)((long)blockIdx.z * s_all / gridDim.z);
+  const int nsteps = SWIGLU ? s_all : (int)((long)(blockIdx.z + 1) * s_all / gridDim.z) - s_lo;
+  if (!SWIGLU) out = (float*)out + (size_t)blockIdx.z * out_split;
   const int nlev = bits - b_min + 1;
   const int nout = SWIGLU ? f : N;
   const bool active = kWaveM * wave < m_cnt;  // wave-uniform
+  // Narrow chunk (at most one wave's 64 positions): instead of one wave
+  // running all 32 products of a step while seven wait at the barrier, every
+  // wave takes a share of the tile's rows for those positions (W2: 16 rows
+  // each; W1/W3: one 16-row block of W1 and the same block of W3, for 32 of
+  // the 64 positions), reading the activations that wave 0 stages.  When
+  // `split` is set, narrow and wide chunks run in two launches of the two
+  // instantiations of this kernel (one MFMA path each keeps the register
+  // allocation of either unchanged), each skipping the other's chunks;
+  // otherwise the wide one takes every chunk.
+  constexpr bool narrow = NARROW;
+  if (NARROW ? m_cnt > kWaveM : (split && m_cnt <= kWaveM)) return;
 
   // ---- raw weight DMA: this lane's 16-byte slot u of the stage ----
   // global row of tile row r
@@ -291,7 +313,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const bool rissue = rreal || lane == 0;
   const uint32_t rdst_off = wave < kRawWaves ? 1024u * wave : 0u;
   auto raw_dma = [&](int step) {
-    const int st = step < nsteps ? step : nsteps - 1;  // past the end: reload, unused
+    const int st = s_lo + (step < nsteps ? step : nsteps - 1);  // past the end: reload, unused
     const uint8_t* src = rsrc + (size_t)(st / SPG) * rstride_b + (st % SPG) * rstride_c;
     uint8_t* dst = wave < kRawWaves ? &rraw[step % kRawRing][rdst_off] : dummy[0];
     if (rissue)
@@ -309,14 +331,19 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     const int q = (lane & 3) ^ ((rl >> 2) & 3);
     xsrc[i] = in + (size_t)src * in_ld + 8 * q;
   }
+  // every wave issues four per step (lane 0 at least) so that all waves
+  // count the same memory instructions; in a narrow chunk waves 1..7 hold no
+  // positions and their lane-0 loads go to the dummy area
   auto x_dma = [&](int step) {
-    const int st = step < nsteps ? step : nsteps - 1;
-    uint8_t* dst = xring[step % kXRing][wave];
+    const int st = s_lo + (step < nsteps ? step : nsteps - 1);
+    uint8_t* dst = NARROW ? (wave == 0 ? xring[step % kXRing][0] : dummy[0])
+                          : xring[step % kXRing][wave];
+    const int stride = NARROW && wave != 0 ? 0 : 1024;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       if (active || lane == 0)
         __builtin_amdgcn_global_load_lds(D2MOE_GPTR(xsrc[i] + kStepK * st),
-                                         D2MOE_LPTR(dst + 1024 * i), 16, 0, 0);
+                                         D2MOE_LPTR(dst + stride * i), 16, 0, 0);
   };
 
   // ---- dequantization: tile row dr, columns 4 dq .. 4 dq + 3 and +16 ----
@@ -372,7 +399,41 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     const uint32_t wd = lds_addr(wtile[dstep & 1]);
     st64(wd + swz(dr, dq >> 1) + 8 * (dq & 1), o[0], o[1]);
     st64(wd + swz(dr, 2 + (dq >> 1)) + 8 * (dq & 1), o[2], o[3]);
-    if (mma) {
+    if constexpr (NARROW) {
+     if (mma) {
+      const uint32_t xb = lds_addr(xring[mstep % kXRing][0]);
+      const uint32_t wb = lds_addr(wtile[mstep & 1]);
+      if constexpr (SWIGLU) {
+        const int mh = wave >> 2, rbw = wave & 3;
+        ld128(R.A[0], xb + swz(32 * mh + fr, fq));
+        ld128(R.A[1], xb + swz(32 * mh + 16 + fr, fq));
+        ld128(R.B[0], wb + swz(16 * rbw + fr, fq));
+        ld128(R.B[1], wb + swz(16 * (4 + rbw) + fr, fq));
+        wait_lgkm();
+        R.rebind();
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(bf16x8, R.A[i]), __builtin_bit_cast(bf16x8, R.B[0]), acc[i][0], 0,
+              0, 0);
+          acc[i][4] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(bf16x8, R.A[i]), __builtin_bit_cast(bf16x8, R.B[1]), acc[i][4], 0,
+              0, 0);
+        }
+      } else {
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) ld128(R.A[mt], xb + swz(16 * mt + fr, fq));
+        ld128(R.B[0], wb + swz(16 * wave + fr, fq));
+        wait_lgkm();
+        R.rebind();
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+          acc[mt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(bf16x8, R.A[mt]), __builtin_bit_cast(bf16x8, R.B[0]), acc[mt][0],
+              0, 0, 0);
+      }
+     }
+    } else if (mma) {
       const uint32_t xb = lds_addr(xring[mstep % kXRing][wave]);
       const uint32_t wb = lds_addr(wtile[mstep & 1]);
 #pragma unroll
@@ -423,11 +484,36 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     bar();
     raw_dma(s + 4);
     x_dma(s + 2);
-    step(s + 1, s, active);
+    step(s + 1, s, active || narrow);
   }
   wait_vm<0>();  // no DMA may still be writing this workgroup's LDS at exit
 
   // ---- epilogue ----
+  if constexpr (NARROW) {
+    if constexpr (SWIGLU) {
+      const int mh = wave >> 2, n = n0 + 16 * (wave & 3) + (lane & 15);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = 32 * mh + 16 * i + 4 * (lane >> 4) + r;
+          if (m >= m_cnt || n >= f) continue;
+          ((uint16_t*)out)[(size_t)(m_first + m) * out_ld + n] =
+              f2bf(silu(acc[i][0][r]) * acc[i][4][r]);
+        }
+    } else {
+      const int n = n0 + 16 * wave + (lane & 15);
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = 16 * mt + 4 * (lane >> 4) + r;
+          if (m >= m_cnt || n >= N) continue;
+          ((float*)out)[(size_t)(m_first + m) * out_ld + n] = acc[mt][0][r];
+        }
+    }
+    return;
+  }
   if (!active) return;
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt) {
@@ -462,10 +548,11 @@ __global__ void to_bf16_kernel(const float* __restrict__ in, size_t n, uint16_t*
   if (i < n) out[i] = f2bf(in[i]);
 }
 
-// out[t][c] = sum_i w[t][i] * y[slot_of[t*k+i]][c] (+ ys[t][c]), i ascending.
+// out[t][c] = sum_i w[t][i] * y[slot_of[t*k+i]][c] (+ the shared expert's
+// output, the sum of its ys_parts partial planes), i ascending.
 template <typename TOUT>
 __global__ void combine_kernel(const float* __restrict__ y, const float* __restrict__ ys,
-                               const float* __restrict__ topk_w,
+                               int ys_parts, size_t ys_split, const float* __restrict__ topk_w,
                                const int32_t* __restrict__ slot_of, int k, int d,
                                TOUT* __restrict__ out) {
   const int t = blockIdx.y;
@@ -476,7 +563,12 @@ __global__ void combine_kernel(const float* __restrict__ y, const float* __restr
     const int pos = slot_of[t * k + i];
     acc += topk_w[t * k + i] * y[(size_t)pos * d + c];
   }
-  if (ys) acc += ys[(size_t)t * d + c];
+  if (ys) {
+    // the shared expert's reduction parts, summed in order
+    float sh = 0.0f;
+    for (int z = 0; z < ys_parts; ++z) sh += ys[(size_t)z * ys_split + (size_t)t * d + c];
+    acc += sh;
+  }
   if constexpr (sizeof(TOUT) == 2)
     out[(size_t)t * d + c] = f2bf(acc);
   else
@@ -489,24 +581,56 @@ size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 // contributes one chunk plus one per kChunk positions.
 int chunk_bound(int n, int nb) { return (nb < n ? nb : n) + (n + kChunk - 1) / kChunk; }
 
+// The shared expert is one bucket of T positions, so its launches are small:
+// its positions are cut into chunks of the largest multiple of 64 that still
+// gives the W1/W3 GEMM at least kFillWgs workgroups, and its W2 reduction is
+// split into parts until W2 has as many (each part at least 16 steps); the
+// parts' partial sums are added by the combine.  A function of the sizes
+// only, so the workspace layout and the launches agree.
+constexpr int kFillWgs = 256;
+void shared_plan(int T, int d, int shared_d_ff, int* cs, int* ksplit) {
+  const long tiles13 = (shared_d_ff + kTileRows / 2 - 1) / (kTileRows / 2);
+  int c = kChunk;
+  while (c > kWaveM && tiles13 * ((T + c - 1) / c) < kFillWgs) c -= kWaveM;
+  *cs = c;
+  const long wg2 = (long)((d + kTileRows - 1) / kTileRows) * ((T + c - 1) / c);
+  const int steps2 = shared_d_ff / kStepK;
+  int sp = (int)((kFillWgs + wg2 - 1) / wg2);
+  const int most = steps2 / 16 > 1 ? steps2 / 16 : 1;
+  *ksplit = sp < 1 ? 1 : (sp > most ? most : sp);
+}
+
+// `split`: run chunks of at most 64 positions in the narrow kernel (worth
+// it when most chunks are narrow: a second launch runs after the first, and
+// its workgroups are as long as the reduction dimension).
 template <bool SWIGLU>
 hipError_t run_gemm(const uint16_t* in, int in_ld, const int32_t* perm, int kdiv, const MwqView& W,
-                    const int32_t* chunks, int n_ub, int f, void* out, int out_ld,
-                    hipStream_t s) {
+                    const int32_t* chunks, int n_ub, int f, void* out, int out_ld, bool split,
+                    hipStream_t s, int ksplit = 1, size_t out_split = 0) {
   const int N = SWIGLU ? W.rows / 2 : W.rows;
   const int per = SWIGLU ? kTileRows / 2 : kTileRows;
   // weight-row tiles vary fastest: consecutive workgroups, which the
   // dispatcher deals round-robin to the 8 XCDs, share one chunk, so every
   // XCD's L2 holds the activations of the one or two chunks in flight
   // rather than of all of them
-  dim3 grid((N + per - 1) / per, n_ub);
+  dim3 grid((N + per - 1) / per, n_ub, SWIGLU ? 1 : ksplit);
   if (n_ub <= 0) return hipSuccess;
-  if (W.group == 128)
-    bgemm_kernel<128, SWIGLU><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f, N,
-                                                        out, out_ld);
-  else
-    bgemm_kernel<64, SWIGLU><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f, N,
-                                                       out, out_ld);
+  // chunks of more than 64 positions (all of them without split), then the
+  // chunks of at most 64
+  const int sp = split ? 1 : 0;
+  if (W.group == 128) {
+    bgemm_kernel<128, SWIGLU, false><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, chunks,
+                                                               f, N, out, out_ld, sp, out_split);
+    if (split)
+      bgemm_kernel<128, SWIGLU, true><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, chunks,
+                                                                f, N, out, out_ld, sp, out_split);
+  } else {
+    bgemm_kernel<64, SWIGLU, false><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, chunks,
+                                                              f, N, out, out_ld, sp, out_split);
+    if (split)
+      bgemm_kernel<64, SWIGLU, true><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, chunks,
+                                                               f, N, out, out_ld, sp, out_split);
+  }
   return hipGetLastError();
 }
 
@@ -518,12 +642,16 @@ FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shar
   // chunk tables of the routed experts (at most 8 bit-widths per expert) and
   // of the shared expert
   L.chunk_n = chunk_bound(T * k, E * 8);
-  L.schunk_n = shared_d_ff > 0 ? chunk_bound(T, 1) : 0;
+  L.shared_chunk = kChunk;
+  L.shared_ksplit = 1;
+  if (shared_d_ff > 0) shared_plan(T, d, shared_d_ff, &L.shared_chunk, &L.shared_ksplit);
+  L.schunk_n = shared_d_ff > 0 ? (T + L.shared_chunk - 1) / L.shared_chunk : 0;
   L.sched_off = off;  off += align256(sizeof(int32_t) * 4 * (size_t)(L.chunk_n + L.schunk_n));
   L.h_off = off;      off += align256(sizeof(uint16_t) * (size_t)T * k * d_ff);
   L.hs_off = off;     off += align256(sizeof(uint16_t) * (size_t)T * shared_d_ff);
   L.y_off = off;      off += align256(sizeof(float) * (size_t)T * k * d);
-  L.ys_off = off;     off += align256(sizeof(float) * (size_t)T * (shared_d_ff > 0 ? d : 0));
+  L.ys_off = off;
+  off += align256(sizeof(float) * (size_t)L.shared_ksplit * T * (shared_d_ff > 0 ? d : 0));
   L.xb_off = off;     off += align256(sizeof(uint16_t) * (size_t)T * d);
   const size_t nd = T <= kDecodeMaxTokens ? (size_t)T * k : 0;  // decode positions
   // decode work list: at most one run per active expert plus one per 8 positions
@@ -586,39 +714,46 @@ hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff,
     if (err != hipSuccess) return err;
   } else {
     const int n_ub = chunk_bound(T * k, nb);
-    chunk_kernel<<<1, kChunkThreads, 0, s>>>(r->hist, r->offsets, nb, Lv, w13->b_min, 0, 0, n_ub,
-                                            chunks);
+    chunk_kernel<<<1, kChunkThreads, 0, s>>>(r->hist, r->offsets, nb, Lv, w13->b_min, 0, 0,
+                                            kChunk, n_ub, chunks);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     const MwqView W13 = view_of(w13), W2 = view_of(w2);
     if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
-    err = run_gemm<true>(xb, d, r->perm, k, W13, chunks, n_ub, d_ff, h, d_ff, s);
+    // narrow chunks get their own launch when experts average at most 64
+    // positions
+    const bool split = (long)T * k <= 64L * E;
+    err = run_gemm<true>(xb, d, r->perm, k, W13, chunks, n_ub, d_ff, h, d_ff, split, s);
     if (err != hipSuccess) return err;
     if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
     if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
-    err = run_gemm<false>(h, d_ff, nullptr, 1, W2, chunks, n_ub, d_ff, y, d, s);
+    err = run_gemm<false>(h, d_ff, nullptr, 1, W2, chunks, n_ub, d_ff, y, d, split, s);
     if (err != hipSuccess) return err;
     if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
   }
 
   if (has_shared) {
-    const int ns_ub = chunk_bound(T, 1);
+    const int ns_ub = L.schunk_n, cs = L.shared_chunk, ks = L.shared_ksplit;
     chunk_kernel<<<1, kChunkThreads, 0, s>>>(nullptr, nullptr, 0, 1, sw13->b_min, T, shared_bits,
-                                            ns_ub, schunks);
+                                            cs, ns_ub, schunks);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     const MwqView S13 = view_of(sw13), S2 = view_of(sw2);
-    err = run_gemm<true>(xb, d, nullptr, 1, S13, schunks, ns_ub, shared_d_ff, hs, shared_d_ff, s);
+    err = run_gemm<true>(xb, d, nullptr, 1, S13, schunks, ns_ub, shared_d_ff, hs, shared_d_ff,
+                         cs <= kWaveM, s);
     if (err != hipSuccess) return err;
-    err = run_gemm<false>(hs, shared_d_ff, nullptr, 1, S2, schunks, ns_ub, shared_d_ff, ys, d, s);
+    err = run_gemm<false>(hs, shared_d_ff, nullptr, 1, S2, schunks, ns_ub, shared_d_ff, ys, d,
+                          cs <= kWaveM, s, ks, (size_t)T * d);
     if (err != hipSuccess) return err;
   }
 
   dim3 cg((d + 255) / 256, T);
   if (xd == D2MOE_BF16)
-    combine_kernel<uint16_t><<<cg, 256, 0, s>>>(y, has_shared ? ys : nullptr, r->topk_w,
-                                                r->slot_of, k, d, (uint16_t*)out);
+    combine_kernel<uint16_t><<<cg, 256, 0, s>>>(y, has_shared ? ys : nullptr, L.shared_ksplit,
+                                                (size_t)T * d, r->topk_w, r->slot_of, k, d,
+                                                (uint16_t*)out);
   else
-    combine_kernel<float><<<cg, 256, 0, s>>>(y, has_shared ? ys : nullptr, r->topk_w, r->slot_of,
-                                             k, d, (float*)out);
+    combine_kernel<float><<<cg, 256, 0, s>>>(y, has_shared ? ys : nullptr, L.shared_ksplit,
+                                             (size_t)T * d, r->topk_w, r->slot_of, k, d,
+                                             (float*)out);
   return hipGetLastError();
 }
 

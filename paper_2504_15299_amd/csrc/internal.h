@@ -82,6 +82,8 @@ struct FwdWorkspace {
   size_t elist_off, xq13_off, xs13_off, h32_off, xq2_off, xs2_off, hmax_off;
   size_t total;
   int chunk_n, schunk_n;  // grouped-GEMM chunk-table entries (routed, shared)
+  int shared_chunk;       // positions per chunk of the shared expert
+  int shared_ksplit;      // parts of the shared W2 reduction (partial sums summed by combine)
 };
 
 struct DecodeBuffers {

@@ -190,6 +190,9 @@ FWD_SPECS = {
     "dense_T64": wl.scaled(wl.dense_decode(T=64), d=256, f=512),
     "prefill_v2_small": wl.scaled(wl.mixtral_prefill(), d=256, f=384, T=300, b_min=5, b_max=8,
                                   bits_choices=(5, 6, 8)),
+    # shared expert cut into 64-position chunks with its W2 reduction split in
+    # two parts summed by the combine
+    "fine_shared_split": wl.scaled(wl.fine_grained(), d=256, f=64, T=200, shared_f=1024),
 }
 
 
