@@ -38,14 +38,17 @@ constexpr int kWaveM = 64;                  // positions per wave
 constexpr int kChunk = 8 * kWaveM;          // positions per chunk
 constexpr int kTileRows = 128;              // weight rows per workgroup
 constexpr int kStepK = 32;                  // reduction columns per step
-constexpr int kRawRing = 4;                 // raw stages: DMA 3 steps ahead of dequantization
+// raw stages: the DMA runs kRawRing - 1 steps ahead of dequantization (4
+// stages in the wide kernel; the narrow one has LDS to spare and takes 8)
+template <bool NARROW>
+constexpr int raw_ring() { return NARROW ? 8 : 4; }
 constexpr int kXRing = 3;                   // activation stages: DMA 2 steps ahead of use
 constexpr int kXStage = kWaveM * kStepK * 2;  // bytes per wave and stage
 // Raw stage layout (bytes): plane p at 512 p (one word per tile row), scales
 // of level l at 4096 + 256 l (one binary16 per tile row, up to 8 levels),
 // zero points at 6144 (one byte per tile row).  16-byte DMA slots 0..391
 // carry them; waves 0..6 move slots 64 w .. 64 w + 63.
-constexpr int kRawScaleOff = 4096, kRawZeroOff = 6144, kRawStage = 7168;
+constexpr int kRawScaleOff = 4096, kRawZeroOff = 6144, kRawStage = 6272;
 constexpr int kRawSlots = 392, kRawWaves = 7;
 constexpr int kWTile = kTileRows * kStepK * 2;  // dequantized bf16 tile bytes
 
@@ -56,12 +59,13 @@ constexpr int kWTile = kTileRows * kStepK * 2;  // dequantized bf16 tile bytes
 // chunks[4 c] = first position, positions (0: no work), bit-width, expert.
 // Buckets are taken in order of size (largest first, ties in bucket order)
 // so that the longest workgroups start first.  One workgroup of kChunkThreads
-// threads, one bucket per thread (nb <= kChunkThreads).
+// threads, one bucket per thread (nb <= kChunkThreads, bucket index < 1024).
 constexpr int kChunkThreads = 512;
 __global__ __launch_bounds__(kChunkThreads) void chunk_kernel(
     const int32_t* __restrict__ hist, const int32_t* __restrict__ offsets, int nb, int L, int b_min,
     int one_cnt, int one_bit, int one_cs, int n_ub, int32_t* __restrict__ chunks) {
-  __shared__ int cnt[kChunkThreads], nch[kChunkThreads], first[kChunkThreads];
+  __shared__ unsigned long long key[kChunkThreads];
+  __shared__ int scan[kChunkThreads];
   const int j = threadIdx.x;
   if (hist == nullptr) {  // one bucket: every position, expert 0, chunks of one_cs
     for (int c = j; c < n_ub; c += kChunkThreads) {
@@ -73,29 +77,49 @@ __global__ __launch_bounds__(kChunkThreads) void chunk_kernel(
     }
     return;
   }
+  // sort buckets by (size descending, index ascending): bitonic sort of one
+  // 64-bit key per thread, size in the high bits and 1023 - index in the low
+  // ten (empty slots have key 0 and sort last)
   const int cj = j < nb ? hist[j] : 0;
-  cnt[j] = cj;
-  nch[j] = (cj + kChunk - 1) / kChunk;
+  key[j] = j < nb ? ((unsigned long long)cj << 10) | (unsigned)(1023 - j) : 0ull;
   __syncthreads();
-  // chunks of the buckets that come before this one in size order
-  int before = 0;
-#pragma unroll 16
-  for (int i = 0; i < nb; ++i)
-    if (cnt[i] > cj || (cnt[i] == cj && i < j)) before += nch[i];
-  first[j] = before;
+  for (int kk = 2; kk <= kChunkThreads; kk <<= 1) {
+    for (int jj = kk >> 1; jj > 0; jj >>= 1) {
+      const int ix = j ^ jj;
+      if (ix > j) {
+        const unsigned long long a = key[j], b = key[ix];
+        const bool desc = (j & kk) == 0;  // this pair's segment runs descending
+        if (desc ? a < b : a > b) {
+          key[j] = b;
+          key[ix] = a;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // chunks of the bucket at sorted position j, and their exclusive prefix
+  const unsigned long long kj = key[j];
+  const int cnt_j = (int)(kj >> 10), bkt = 1023 - (int)(kj & 1023ull);
+  const int nch_j = (cnt_j + kChunk - 1) / kChunk;
+  scan[j] = nch_j;
   __syncthreads();
-  int total = 0;
-#pragma unroll 16
-  for (int i = 0; i < nb; ++i) total += nch[i];
-  if (j < nb) {
-    const int b0 = offsets[j];
-    for (int q = 0; q < nch[j]; ++q) {
-      const int c = first[j] + q;
+  for (int off = 1; off < kChunkThreads; off <<= 1) {
+    const int v = j >= off ? scan[j - off] : 0;
+    __syncthreads();
+    scan[j] += v;
+    __syncthreads();
+  }
+  const int first = scan[j] - nch_j;
+  const int total = scan[kChunkThreads - 1];
+  if (nch_j > 0) {
+    const int b0 = offsets[bkt];
+    for (int q = 0; q < nch_j; ++q) {
+      const int c = first + q;
       if (c >= n_ub) break;
       chunks[4 * c] = b0 + q * kChunk;
-      chunks[4 * c + 1] = min(kChunk, cj - q * kChunk);
-      chunks[4 * c + 2] = b_min + j % L;
-      chunks[4 * c + 3] = j / L;
+      chunks[4 * c + 1] = min(kChunk, cnt_j - q * kChunk);
+      chunks[4 * c + 2] = b_min + bkt % L;
+      chunks[4 * c + 3] = bkt / L;
     }
   }
   for (int c = total + j; c < n_ub; c += kChunkThreads) chunks[4 * c + 1] = 0;
@@ -234,6 +258,7 @@ void bgemm_kernel(
   // narrow chunks stage only wave 0's activations (56 KB of LDS in all, two
   // workgroups per compute unit); wide ones each wave's (140 KB, one)
   __shared__ __attribute__((aligned(16))) uint8_t xring[kXRing][NARROW ? 1 : 8][kXStage];
+  constexpr int kRawRing = raw_ring<NARROW>();
   __shared__ __attribute__((aligned(16))) uint8_t rraw[kRawRing][kRawStage];
   __shared__ __attribute__((aligned(16))) uint8_t wtile[2][kWTile];
   __shared__ __attribute__((aligned(16))) uint8_t dummy[1][16];
@@ -457,23 +482,24 @@ void bgemm_kernel(
     wait_lgkm();
   };
 
-  // ---- prologue: raw 0..3 and activations 0..1 in flight, tile 0 ready ----
-  // issue order: raw 0, raw 1, [raw 2, x 0], [raw 3, x 1]; the wait leaves the
-  // last 11 instructions outstanding, i.e. raw 0 has landed
-  raw_dma(0);
-  raw_dma(1);
-  raw_dma(2);
+  // ---- prologue: raw 0..kRawRing-1 and activations 0..1 in flight, tile 0
+  // ready.  Issue order: raw 0 .. raw kRawRing-2, x 0, raw kRawRing-1, x 1;
+  // the wait leaves the instructions after raw 0 outstanding (one per raw
+  // stage, four per activation stage), i.e. raw 0 has landed.
+#pragma unroll
+  for (int i = 0; i + 1 < kRawRing; ++i) raw_dma(i);
   x_dma(0);
-  raw_dma(3);
+  raw_dma(kRawRing - 1);
   x_dma(1);
-  wait_vm<11>();
+  wait_vm<kRawRing + 7>();
   bar();
   step(0, 0, false);
 
-  // ---- main loop: step s issues raw s+4 and activations s+2, dequantizes
-  // s+1 and multiplies s.  At the top of step s the instructions issued after
-  // the activations of s are the 5 of step s-1 (raw s+3, activations s+1), and
-  // raw s+1 was issued before the activations of s, so vmcnt(5) makes both
+  // ---- main loop: step s issues raw s+kRawRing and activations s+2,
+  // dequantizes s+1 and multiplies s.  At the top of step s the instructions
+  // issued after the activations of s are the 5 of step s-1 (raw
+  // s+kRawRing-1, activations s+1), and raw s+1 was issued before the
+  // activations of s (kRawRing > 3), so vmcnt(5) makes both
   // this wave's raw s+1 and its activations of s ready; the barrier then
   // makes every wave's raw s+1 and tile s visible, and retires all reads of
   // the stages and the tile buffer that this step overwrites.  In the last
@@ -482,7 +508,7 @@ void bgemm_kernel(
   for (int s = 0; s < nsteps; ++s) {
     wait_vm<5>();
     bar();
-    raw_dma(s + 4);
+    raw_dma(s + kRawRing);
     x_dma(s + 2);
     step(s + 1, s, active || narrow);
   }
@@ -582,16 +608,20 @@ size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 int chunk_bound(int n, int nb) { return (nb < n ? nb : n) + (n + kChunk - 1) / kChunk; }
 
 // The shared expert is one bucket of T positions, so its launches are small:
-// its positions are cut into chunks of the largest multiple of 64 that still
-// gives the W1/W3 GEMM at least kFillWgs workgroups, and its W2 reduction is
-// split into parts until W2 has as many (each part at least 16 steps); the
-// parts' partial sums are added by the combine.  A function of the sizes
-// only, so the workspace layout and the launches agree.
+// its positions are cut into as many equal chunks (multiples of 64, at most
+// kChunk) as keep the W1/W3 GEMM within one round of kFillWgs workgroups,
+// and its W2 reduction is split into parts until W2 has about as many (each
+// part at least 16 steps); the parts' partial sums are added by the
+// combine.  A function of the sizes only, so the workspace layout and the
+// launches agree.
 constexpr int kFillWgs = 256;
 void shared_plan(int T, int d, int shared_d_ff, int* cs, int* ksplit) {
   const long tiles13 = (shared_d_ff + kTileRows / 2 - 1) / (kTileRows / 2);
-  int c = kChunk;
-  while (c > kWaveM && tiles13 * ((T + c - 1) / c) < kFillWgs) c -= kWaveM;
+  long nch = kFillWgs / tiles13;
+  const long most_ch = (T + kWaveM - 1) / kWaveM;
+  nch = nch < 1 ? 1 : (nch > most_ch ? most_ch : nch);
+  int c = (int)(((T + nch - 1) / nch + kWaveM - 1) / kWaveM * kWaveM);
+  c = c > kChunk ? kChunk : (c < kWaveM ? kWaveM : c);
   *cs = c;
   const long wg2 = (long)((d + kTileRows - 1) / kTileRows) * ((T + c - 1) / c);
   const int steps2 = shared_d_ff / kStepK;
