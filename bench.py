@@ -616,41 +616,42 @@ def profiled_traffic():
     return int(kv["traffic_w13_bytes"]), int(kv["traffic_w2_bytes"])
 
 
-def cpu_baseline(d, f, E, k, g):
-    """The CPU oracle (single thread, as it stands) on one decode token of the
-    same layer shape: gate logits, dual routing, the two selected experts'
-    SwiGLU FFNs from their MWQ codes, combine.  Quantizing the two experts is
-    setup and is not timed."""
+def cpu_baseline(d, f, E, k, g, n_tokens=4):
+    """The CPU oracle (single thread, as it stands) on a bounded sample of the
+    decode workload: n_tokens decode tokens of the same layer shape, one
+    request each with bits per expert from {2,3,4,8}; gate logits, dual
+    routing, each token's selected experts' SwiGLU FFNs from their MWQ codes,
+    combine.  Quantizing the experts is setup and is not timed."""
     import numpy as np
 
     from oracle import oracle as O
 
     rng = np.random.default_rng(11)
-    x = rng.standard_normal((1, d), dtype=np.float32)
+    x = rng.standard_normal((n_tokens, d), dtype=np.float32)
     Wg = (rng.standard_normal((E, d), dtype=np.float32) * 0.02)
-    table = np.array([[2, 3, 4, 8, 2, 3, 4, 8]], np.uint8)
-    logits = O.gate_logits(x, Wg)
-    route = O.route_from_logits(logits, k, None, table)
+    table = rng.choice(np.array([2, 3, 4, 8], np.uint8), size=(n_tokens, E),
+                       p=[0.2, 0.3, 0.3, 0.2]).astype(np.uint8)
+    req = np.arange(n_tokens, dtype=np.int32)
+    route = O.route_from_logits(O.gate_logits(x, Wg), k, req, table)
     codes13, codes2 = {}, {}
-    for e in route["topk_idx"][0]:
-        e = int(e)
+    for e in sorted({int(e) for e in route["topk_idx"].ravel()}):
         codes13[e] = O.mwq_quantize((rng.standard_normal((2 * f, d), dtype=np.float32) * 0.02), g)
         codes2[e] = O.mwq_quantize((rng.standard_normal((d, f), dtype=np.float32) * 0.02), g)
     t0 = time.perf_counter()
-    logits = O.gate_logits(x, Wg)
-    route = O.route_from_logits(logits, k, None, table)
-    ys = []
-    for i in range(k):
-        e = int(route["topk_idx"][0, i])
-        ys.append(O.expert_ffn(codes13[e], codes2[e], int(route["topk_bits"][0, i]),
-                               x.astype(np.float64))[0])
-    O.combine(route["topk_w"], np.stack(ys)[None])
+    route = O.route_from_logits(O.gate_logits(x, Wg), k, req, table)
+    for t in range(n_tokens):
+        ys = []
+        for i in range(k):
+            e = int(route["topk_idx"][t, i])
+            ys.append(O.expert_ffn(codes13[e], codes2[e], int(route["topk_bits"][t, i]),
+                                   x[t:t + 1].astype(np.float64))[0])
+        O.combine(route["topk_w"][t:t + 1], np.stack(ys)[None])
     secs = time.perf_counter() - t0
-    return {"value": round(1.0 / secs, 5), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+    return {"value": round(n_tokens / secs, 5), "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "seconds": round(secs, 3),
-            "sample": "1 decode token of the same layer shape (gate, routing, its 2 experts' "
-                      "SwiGLU FFNs from MWQ codes at bits from {2,3,4,8}, combine); expert "
-                      "quantization untimed"}
+            "sample": f"{n_tokens} decode tokens of the same layer shape, one request each "
+                      f"(gate, routing, each token's 2 experts' SwiGLU FFNs from MWQ codes at "
+                      f"bits from {{2,3,4,8}}, combine); expert quantization untimed"}
 
 
 if __name__ == "__main__":
