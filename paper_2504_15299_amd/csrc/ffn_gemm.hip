@@ -42,7 +42,10 @@ constexpr int kStepK = 32;                  // reduction columns per step
 // stages in the wide kernel; the narrow one has LDS to spare and takes 8)
 template <bool NARROW>
 constexpr int raw_ring() { return NARROW ? 8 : 4; }
-constexpr int kXRing = 3;                   // activation stages: DMA 2 steps ahead of use
+// activation lookahead in steps: one in the wide kernel (its 2-stage ring
+// leaves LDS for the tiles; the activations mostly come from L2), two in the
+// narrow one
+template <bool NARROW> constexpr int x_lead() { return NARROW ? 2 : 1; }
 constexpr int kXStage = kWaveM * kStepK * 2;  // bytes per wave and stage
 // Raw stage layout (bytes): plane p at 512 p (one word per tile row), scales
 // of level l at 4096 + 256 l (one binary16 per tile row, up to 8 levels),
@@ -257,6 +260,7 @@ void bgemm_kernel(
     int out_ld, int split, size_t out_split) {
   // narrow chunks stage only wave 0's activations (56 KB of LDS in all, two
   // workgroups per compute unit); wide ones each wave's (140 KB, one)
+  constexpr int XL = x_lead<NARROW>(), kXRing = XL + 1;
   __shared__ __attribute__((aligned(16))) uint8_t xring[kXRing][NARROW ? 1 : 8][kXStage];
   constexpr int kRawRing = raw_ring<NARROW>();
   __shared__ __attribute__((aligned(16))) uint8_t rraw[kRawRing][kRawStage];
@@ -482,34 +486,40 @@ void bgemm_kernel(
     wait_lgkm();
   };
 
-  // ---- prologue: raw 0..kRawRing-1 and activations 0..1 in flight, tile 0
-  // ready.  Issue order: raw 0 .. raw kRawRing-2, x 0, raw kRawRing-1, x 1;
-  // the wait leaves the instructions after raw 0 outstanding (one per raw
-  // stage, four per activation stage), i.e. raw 0 has landed.
+  // ---- prologue: raw 0..kRawRing-1 and activations 0..XL-1 in flight, tile
+  // 0 ready.  Issue order: raw 0 .. raw kRawRing-2, x 0, raw kRawRing-1
+  // (, x 1); the wait leaves the instructions after raw 0 outstanding (one
+  // per raw stage, four per activation stage), i.e. raw 0 has landed.
 #pragma unroll
   for (int i = 0; i + 1 < kRawRing; ++i) raw_dma(i);
   x_dma(0);
   raw_dma(kRawRing - 1);
-  x_dma(1);
-  wait_vm<kRawRing + 7>();
+  if constexpr (XL == 2) x_dma(1);
+  wait_vm<kRawRing + 3 + (XL == 2 ? 4 : 0)>();
   bar();
   step(0, 0, false);
 
-  // ---- main loop: step s issues raw s+kRawRing and activations s+2,
-  // dequantizes s+1 and multiplies s.  At the top of step s the instructions
-  // issued after the activations of s are the 5 of step s-1 (raw
-  // s+kRawRing-1, activations s+1), and raw s+1 was issued before the
-  // activations of s (kRawRing > 3), so vmcnt(5) makes both
+  // ---- main loop: step s issues raw s+kRawRing and activations s+XL,
+  // dequantizes s+1 and multiplies s.  With XL = 2 (order raw, x) the
+  // instructions issued after the activations of s at the top of step s are
+  // the 5 of step s-1 (raw s+kRawRing-1, activations s+1); with XL = 1
+  // (order x, raw) the one raw s+kRawRing-1.  Raw s+1 was issued before the
+  // activations of s (kRawRing > 3), so that wait makes both
   // this wave's raw s+1 and its activations of s ready; the barrier then
   // makes every wave's raw s+1 and tile s visible, and retires all reads of
   // the stages and the tile buffer that this step overwrites.  In the last
   // step the dequantization works on a reloaded stage and its tile is never
   // read.
   for (int s = 0; s < nsteps; ++s) {
-    wait_vm<5>();
+    wait_vm<XL == 2 ? 5 : 1>();
     bar();
-    raw_dma(s + kRawRing);
-    x_dma(s + 2);
+    if constexpr (XL == 2) {
+      raw_dma(s + kRawRing);
+      x_dma(s + 2);
+    } else {
+      x_dma(s + 1);
+      raw_dma(s + kRawRing);
+    }
     step(s + 1, s, active || narrow);
   }
   wait_vm<0>();  // no DMA may still be writing this workgroup's LDS at exit
