@@ -11,6 +11,12 @@ that overlap its own source operands: multi-pass MFMAs read their sources
 while they write, and the compiler does not always keep a 4-register result
 apart from them (the decode kernels pin their operands to prevent it).
 
+It also fails if the registers of an untracked (inline-asm) activation load
+are read or written by anything else before the load's covering wait: their
+data arrives late, so such a use would see, or be overwritten by, stale
+data (a decode build whose loop copied a pointer through such registers
+faulted on the GPU).
+
 The build fails if any kernel needs per-lane scratch memory: the decode
 kernels place their own vmcnt waits around the LDS DMA ring, which assume
 that no other vector-memory traffic (such as register spills) is
@@ -96,6 +102,109 @@ def mfma_overlaps(asm: str) -> list[str]:
     return bad
 
 
+def _vregs(tok: str) -> set[int]:
+    m = re.match(r"v\[(\d+):(\d+)\]", tok)
+    if m:
+        return set(range(int(m.group(1)), int(m.group(2)) + 1))
+    m = re.match(r"v(\d+)$", tok)
+    return {int(m.group(1))} if m else set()
+
+
+def _basic_blocks(lines: list[str]) -> list[dict]:
+    """Basic blocks of one function's assembly (split at labels and after
+    branches) with their successor indices."""
+    blocks, cur = [], {"name": "entry", "ins": []}
+    for line in lines:
+        s = line.strip()
+        m = re.match(r"^(\.LBB\S+):", s)
+        if m:
+            blocks.append(cur)
+            cur = {"name": m.group(1), "ins": []}
+            continue
+        if not s or s.startswith((";", ".")):
+            continue
+        cur["ins"].append(s)
+        if s.split()[0].startswith(("s_cbranch", "s_branch")):
+            blocks.append(cur)
+            cur = {"name": None, "ins": []}
+    blocks.append(cur)
+    index = {b["name"]: i for i, b in enumerate(blocks) if b["name"]}
+    for i, b in enumerate(blocks):
+        succ, falls = [], True
+        for x in b["ins"]:
+            op = x.split()[0]
+            if op == "s_branch":
+                succ.append(index[x.split()[1]])
+                falls = False
+            elif op.startswith("s_cbranch"):
+                succ.append(index[x.split()[1]])
+            elif op in ("s_endpgm", "s_setpc_b64"):
+                falls = False
+        if falls and i + 1 < len(blocks):
+            succ.append(i + 1)
+        b["succ"] = succ
+    return blocks
+
+
+def untracked_load_hazards(asm: str) -> list[tuple[str, str, str]]:
+    """The decode kernels issue their activation loads as inline assembly
+    (global_load_dwordx4 under a narrowed EXEC) that the compiler does not
+    track: the data lands in the destination registers some time later, when
+    the explicit vmcnt wait covers it.  On every path from such a load, no
+    other instruction may read or write those registers before an MFMA reads
+    them as its B operand (the intended first use, after the covering wait)
+    or an s_waitcnt vmcnt(0): the compiler would be using the registers for
+    another value that the late data can overwrite.  Returns (function,
+    load, offending instruction) triples."""
+    funcs, name = {}, None
+    for line in asm.splitlines():
+        m = re.match(r"^(_Z\S+):", line)
+        if m:
+            name = m.group(1)
+            funcs[name] = []
+        elif name:
+            funcs[name].append(line)
+    bad = []
+    for fname, lines in funcs.items():
+        blocks = _basic_blocks(lines)
+        for bi, b in enumerate(blocks):
+            for ii, x in enumerate(b["ins"]):
+                if not x.startswith("global_load_dwordx4"):
+                    continue
+                if not any("s_and_saveexec" in y for y in b["ins"][max(0, ii - 2):ii]):
+                    continue
+                dst = _vregs(x.split()[1].rstrip(","))
+                stack, seen = [(bi, ii + 1)], set()
+                while stack:
+                    cb, ci = stack.pop()
+                    if (cb, ci) in seen:
+                        continue
+                    seen.add((cb, ci))
+                    stop = False
+                    for y in blocks[cb]["ins"][ci:]:
+                        op = y.split()[0]
+                        if op == "s_waitcnt" and "vmcnt(0)" in y:
+                            stop = True
+                            break
+                        if op.startswith("v_mfma"):
+                            ops = [o.strip() for o in y.split(None, 1)[1].split(",")]
+                            if _vregs(ops[2].split()[0]) & dst:
+                                stop = True
+                                break
+                        if op == "global_load_dwordx4":
+                            continue
+                        hit = set()
+                        for t in re.findall(r"v\[\d+:\d+\]|v\d+\b", y):
+                            hit |= _vregs(t)
+                        if hit & dst:
+                            bad.append((fname, x, y))
+                            stop = True
+                            break
+                    if not stop:
+                        stack.extend((sb, 0) for sb in blocks[cb]["succ"])
+    return bad
+
+
 def _check_mfma(src: str) -> None:
     cmd = [_hipcc(), *COMMON, *EXTRA.get(src, []), "--cuda-device-only", "-S", "-o", "-",
            os.path.join(CSRC, src)]
@@ -105,6 +214,10 @@ def _check_mfma(src: str) -> None:
     bad = mfma_overlaps(r.stdout)
     if bad:
         raise RuntimeError(f"{src}: {len(bad)} MFMAs write over their own operands, e.g. {bad[0]}")
+    hz = untracked_load_hazards(r.stdout)
+    if hz:
+        raise RuntimeError(f"{src}: {len(hz)} untracked activation loads whose registers are used "
+                           f"before their covering wait, e.g. {hz[0]}")
 
 
 def scratch_users(remarks: str) -> dict[str, int]:

@@ -673,6 +673,7 @@ __device__ inline void decode_groups(const WaveCtx<NCB>& c, uint8_t* ring, int g
     D2MOE_STEP(3)
   }
 #undef D2MOE_STEP
+  wait_vm<0>();  // as in decode_pairs: explicit on every exit edge of the loop
 }
 
 
@@ -824,6 +825,244 @@ void decode_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* 
   }
 }
 
+// ---- W1/W3 kernel: one wave per 16-row block, W1 and W3 in alternate stages
+//
+// Each wave owns one 16-row block of the output (rows of h) and streams, over
+// the whole reduction dimension, the W1 block and the matching W3 block of
+// every group in turn: ring stage s holds group s / 2 of W1 (s even) or W3
+// (s odd).  One activation load serves both stages of a group, the stream of
+// a wave is four times longer than a quarter of one matrix, and each lane
+// ends with a and c of the same outputs, so the waves of a workgroup never
+// exchange data.
+//
+// Order of issue: the prologue sends the DMA of stage 0, the activations of
+// group 0, then the DMA of stages 1 and 2; the step that computes stage s
+// sends the activations of group s/2 + 1 (even s) and the DMA of stage s + 3,
+// then waits.  In issue order the newest instructions needed by stage s are
+// the activations of its group (even s) or its own DMA (odd s); in both cases
+// exactly the DMA of stages s+1..s+3 and the activations of group s/2 + 1
+// (those that exist) were issued after them, and vector-memory instructions
+// of a wave complete in order, so waiting until only those remain
+// outstanding makes the stage and its activations ready.  The DMA of stage
+// s + 3 overwrites the stage of s - 1, whose LDS reads completed in the
+// previous step.  The loop is unrolled by kDepth stages (two groups) so that
+// every ring offset and activation buffer index is a constant.
+// DMA of one stage.  Instructions that carry only plane words address them
+// as the wave-uniform base of group g's planes plus a 32-bit lane offset
+// (16 bytes per lane, 1 KB per instruction), which the hardware takes as a
+// scalar base and a vector offset; the offset is made opaque inside the loop
+// so that the compiler does not hoist a 64-bit per-lane pointer per
+// instruction.  The last, mixed instruction (scales and zero points, and plane
+// words when the nest is not a multiple of four planes) keeps a per-lane
+// source pointer, stride and W3 offset (MixedDma).  `w3` selects the W3 block.
+struct W3Offsets {
+  int pl, sc, zp;
+};
+struct MixedDma {
+  const uint8_t* a0;  // this lane's source for group 0 of the W1 block
+  int step;           // bytes per group
+  int off3;           // W3 block minus W1 block
+};
+
+template <int MB, int BMIN, typename Ctx>
+__device__ inline MixedDma mixed_dma(const Ctx& c, const W3Offsets& o3) {
+  using SL = StageLayout<MB, BMIN>;
+  constexpr int i = SL::ops - 1;
+  const int slot = 64 * i + c.lane;
+  MixedDma m;
+  if (slot < 16 * MB) {
+    m.a0 = c.pl + 16 * slot; m.step = c.pl_step; m.off3 = o3.pl;
+  } else if (slot < 16 * MB + 2 * SL::levels) {
+    m.a0 = c.sc + 16 * (slot - 16 * MB); m.step = c.sc_step; m.off3 = o3.sc;
+  } else {
+    m.a0 = c.zp; m.step = 16; m.off3 = o3.zp;
+  }
+  return m;
+}
+
+template <int MB, int BMIN, bool W3, typename Ctx>
+__device__ inline void dma_stage(const Ctx& c, const MixedDma& m, int pl3, int g, uint8_t* st) {
+  using SL = StageLayout<MB, BMIN>;
+  const uint8_t* pl = c.pl + (size_t)g * c.pl_step + (W3 ? pl3 : 0);
+#pragma unroll
+  for (int i = 0; i < SL::ops; ++i) {
+    if (64 * (i + 1) <= 16 * MB) {  // constant once the loop is unrolled
+      __builtin_amdgcn_global_load_lds(D2MOE_GPTR(pl + 1024 * i + 16 * c.lane),
+                                       D2MOE_LPTR(st + 1024 * i), 16, 0, kCpolNT);
+    } else if (64 * i + c.lane < SL::slots) {
+      const uint8_t* src = m.a0 + (size_t)g * m.step + (W3 ? m.off3 : 0);
+      __builtin_amdgcn_global_load_lds(D2MOE_GPTR(src), D2MOE_LPTR(st + 1024 * i), 16, 0, 0);
+    }
+  }
+}
+
+// The W1 and W3 sums are independent chains, so without an ordering point
+// the compiler defers a stage's scale FMAs past the next stage's LDS reads and
+// keeps all of its MFMA results live (register spills).  A volatile asm that
+// takes the sums after each stage ends that stage's FMAs before the next
+// stage's (volatile) LDS reads.
+template <int NCB>
+__device__ inline void settle(v4f (&acc)[NCB]) {
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) asm volatile("" : "+v"(acc[cb]));
+}
+
+template <int MB, int BMIN, int NCB>
+__device__ inline void decode_pairs(const WaveCtx<NCB>& c, const W3Offsets& o3, uint8_t* ring,
+                                    int g0, int g1, v4f (&acc)[2][NCB]) {
+  static_assert(kDepth == 4, "the unrolled step below assumes four stages");
+  using SL = StageLayout<MB, BMIN>;
+  constexpr int ND = SL::ops, NB = 2 * NCB;
+  constexpr int kStage = stage_bytes<BMIN>();
+  const MixedDma mx = mixed_dma<MB, BMIN>(c, o3);
+  const int N = 2 * (g1 - g0);  // stages
+  BData<NCB> B[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) B[i].lo[cb] = B[i].hi[cb] = v4i{0, 0, 0, 0};
+  if (N <= 0) return;
+  dma_stage<MB, BMIN, false>(c, mx, o3.pl, g0, ring);
+  load_b(B[0], c, g0);
+  if (1 < N) dma_stage<MB, BMIN, true>(c, mx, o3.pl, g0, ring + kStage);
+  if (2 < N) dma_stage<MB, BMIN, false>(c, mx, o3.pl, g0 + 1, ring + 2 * kStage);
+#define D2MOE_PSTEP(K)                                                                   \
+  {                                                                                      \
+    const int ss = s + (K);                                                              \
+    if (ss >= N) break;                                                                  \
+    if (((K) & 1) == 0 && ss + 2 < N) load_b(B[(((K) >> 1) + 1) & 1], c, g0 + (ss >> 1) + 1); \
+    if (ss + 3 < N) {                                                                    \
+      dma_stage<MB, BMIN, ((K) + 3) & 1>(c, mx, o3.pl, g0 + ((ss + 3) >> 1),            \
+                                         ring + (((K) + 3) % kDepth) * kStage);          \
+      wait_vm<3 * ND + NB>();                                                            \
+    } else if (ss + 2 < N) {                                                             \
+      wait_vm<2 * ND + NB>();                                                            \
+    } else if (ss + 1 < N) {                                                             \
+      wait_vm<ND>();                                                                     \
+    } else {                                                                             \
+      wait_vm<0>();                                                                      \
+    }                                                                                    \
+    if (((K) & 1) == 0) ready_b(B[(K) >> 1]);                                            \
+    compute_group<MB, BMIN, ((K) % kDepth) * kStage, NCB>(B[(K) >> 1], c, acc[(K) & 1]); \
+    settle(acc[(K) & 1]);                                                                \
+  }
+  for (int s = 0; s < N; s += kDepth) {
+    D2MOE_PSTEP(0)
+    D2MOE_PSTEP(1)
+    D2MOE_PSTEP(2)
+    D2MOE_PSTEP(3)
+  }
+#undef D2MOE_PSTEP
+  // every real exit has already waited for all (its last stage waits with
+  // vmcnt 0); the wait here puts one on every exit edge of the loop as well
+  wait_vm<0>();
+}
+
+// elist, Xq, Xs, npos as for decode_kernel; f = d_ff (W3 rows start at row f
+// of the stacked W13).  Workgroup x covers row blocks NW x .. NW x + NW - 1,
+// one per wave; there is no barrier, so a wave past the last row block leaves.
+template <int NW, int NCB, int BMIN>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NCB == 1 ? 4 : 3)))
+void decode13_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* __restrict__ Xq,
+                     const uint32_t* __restrict__ Xs, int npos, int f, float* __restrict__ out,
+                     int out_ld, uint32_t* __restrict__ rowmax) {
+  constexpr int kStage = stage_bytes<BMIN>();
+  __shared__ __attribute__((aligned(16))) uint8_t ring[NW][kDepth * kStage];
+  const int ei = blockIdx.y;
+  const int e = elist[4 * ei], p0 = elist[4 * ei + 1], p1 = elist[4 * ei + 2];
+  const int mb_req = elist[4 * ei + 3];
+  if (mb_req == 0) return;
+  const int mb = mb_req < W.b_max ? mb_req : W.b_max;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nrb = f / 16;
+  const int rb = blockIdx.x * NW + wave;
+  if (rb >= nrb) return;
+  const int NG = W.cols / G;
+  const int ncol = p1 - p0;
+
+  WaveCtx<NCB> c;
+  c.lane = lane;
+  c.q = lane >> 4;
+  c.j = lane & 15;
+  const int piece = lane & 1;
+  const int t = c.j >> 1;
+  c.info_shift = 8 + 8 * piece;
+  bool valid[NCB];
+  int pos[NCB];
+  {
+    uint32_t iw[NCB * kDecodeCols];
+#pragma unroll
+    for (int i = 0; i < NCB * kDecodeCols; ++i) iw[i] = Xs[p0 + i];
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      const int tc = kDecodeCols * cb + t;
+      valid[cb] = tc < ncol;
+      pos[cb] = p0 + tc;
+      const int src = valid[cb] ? pos[cb] : npos;
+      const size_t base = ((size_t)src * NG) * 2 + piece;
+      c.xq[cb] = Xq + base * 128 + c.q * 32;
+      c.lmask[cb] = __ballot(valid[cb]) | 1ull;
+      uint32_t info = 0u;
+#pragma unroll
+      for (int i = 0; i < kDecodeCols; ++i) info = t == i ? iw[kDecodeCols * cb + i] : info;
+      c.info[cb] = valid[cb] ? info : 0u;
+    }
+  }
+
+  const size_t blk1 = W.block(e, rb, 0), blk3 = W.block(e, rb + nrb, 0);
+  c.pl = (const uint8_t*)(W.planes + W.plane_word(blk1, 0, 0));
+  c.sc = (const uint8_t*)(W.scales + W.scale_idx(blk1, 0, 0));
+  c.zp = W.zeros + W.zero_idx(blk1, 0);
+  c.pl_step = W.b_max * 64 * 4;
+  c.sc_step = W.levels() * 16 * 2;
+  const int dblk = (int)(blk3 - blk1);  // the launcher checks that the offsets fit
+  const W3Offsets o3{dblk * c.pl_step, dblk * c.sc_step, dblk * 16};
+  c.k = sigma_consts();
+  {
+    const uint32_t base = lds_addr(ring[wave]);
+    c.lds_pl = base + 4 * lane;
+    c.lds_sc = base + 8 * c.q;
+    c.lds_z = base + c.j;
+    c.lds_zq = base + 4 * c.q;
+  }
+
+  v4f acc[2][NCB];
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) acc[h][cb] = v4f{0.f, 0.f, 0.f, 0.f};
+  switch (mb) {
+#define D2MOE_CASE(MB) \
+  case MB:             \
+    if constexpr (MB >= BMIN) decode_pairs<MB, BMIN, NCB>(c, o3, ring[wave], 0, NG, acc); \
+    break;
+    D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
+    D2MOE_CASE(7) D2MOE_CASE(8)
+#undef D2MOE_CASE
+    default: break;
+  }
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    float o[4];
+    float m = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float a = acc[0][cb][r] + __shfl_xor(acc[0][cb][r], 1, 64);  // hi + lo pieces
+      const float u = acc[1][cb][r] + __shfl_xor(acc[1][cb][r], 1, 64);
+      o[r] = silu(a) * u;
+      m = fmaxf(m, fabsf(o[r]));
+    }
+    if (valid[cb] && piece == 0)
+      *(float4*)(out + (size_t)pos[cb] * out_ld + rb * 16 + 4 * c.q) = float4{o[0], o[1], o[2], o[3]};
+    if (rowmax) {
+      m = fmaxf(m, __shfl_xor(m, 16, 64));
+      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      if (valid[cb] && piece == 0 && c.q == 0) rowmax[(size_t)pos[cb] * nrb + rb] = __float_as_uint(m);
+    }
+  }
+}
+
 template <typename TIN>
 hipError_t run_xprep(const TIN* in, int in_ld, const int32_t* perm, int kdiv, int npos, int K,
                      const uint32_t* rowmax, int rowmax_parts, uint8_t* Xq, uint32_t* Xs,
@@ -865,6 +1104,28 @@ hipError_t launch_decode_kernel(int b_min, dim3 grid, const MwqView& W, const in
   return hipGetLastError();
 }
 
+// W1/W3 with one wave per row block (decode13_kernel), kDecodeWaves row blocks
+// per workgroup.
+template <int NCB>
+hipError_t launch_decode13_kernel(int b_min, int ny, const MwqView& W, const int32_t* elist,
+                                  const uint8_t* Xq, const uint32_t* Xs, int npos, int f,
+                                  float* out, int out_ld, uint32_t* rowmax, hipStream_t s) {
+  const dim3 grid((f / 16 + kDecodeWaves - 1) / kDecodeWaves, ny);
+  switch (b_min) {
+#define D2MOE_CASE(B)                                                                      \
+  case B:                                                                                  \
+    decode13_kernel<kDecodeWaves, NCB, B><<<grid, 64 * kDecodeWaves, 0, s>>>(              \
+        W, elist, Xq, Xs, npos, f, out, out_ld, rowmax);                                   \
+    break;
+    D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
+    D2MOE_CASE(7) D2MOE_CASE(8)
+#undef D2MOE_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_ff, int E, int k,
                              const d2moe_mwq* w13, const d2moe_mwq* w2, const d2moe_routing* r,
                              const DecodeBuffers& b, hipStream_t s, const hipEvent_t* events) {
@@ -888,10 +1149,23 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   const MwqView W13 = view_of(w13), W2 = view_of(w2);
   if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
   const dim3 g13(d_ff / 16, ny), g2(d / 16, ny);
-  err = ncb == 1 ? launch_decode_kernel<true, 1>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13,
-                                                 npos, d_ff, b.h32, d_ff, b.hmax, s)
-                 : launch_decode_kernel<true, 2>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13,
-                                                 npos, d_ff, b.h32, d_ff, b.hmax, s);
+  // Two column blocks (more than 4 positions per expert on average): one wave
+  // per row block streams both W1 and W3 over the whole reduction, so one
+  // activation load serves both and the streams are long (decode13_kernel).
+  // Fewer positions: four waves per row block split the reduction
+  // (decode_kernel), which leaves more, shorter streams for the grid and was
+  // as fast or faster at batches of 1 to 16.  decode13_kernel addresses the
+  // W3 block as a 32-bit byte offset from the W1 block of the same rows.
+  const bool fits = (size_t)(d_ff / 16) * (d / G) * (size_t)w13->b_max * 256 < ((size_t)1 << 31);
+  if (ncb == 2 && fits)
+    err = launch_decode13_kernel<2>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos, d_ff,
+                                    b.h32, d_ff, b.hmax, s);
+  else if (ncb == 2)
+    err = launch_decode_kernel<true, 2>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13, npos,
+                                        d_ff, b.h32, d_ff, b.hmax, s);
+  else
+    err = launch_decode_kernel<true, 1>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13, npos,
+                                        d_ff, b.h32, d_ff, b.hmax, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
   err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.hmax, d_ff / 16, b.xq2, b.xs2, r,

@@ -1,0 +1,51 @@
+"""CPU tests of the assembly checks that build.py applies to every device
+object: the untracked-activation-load hazard scan and the MFMA operand
+overlap scan, on small hand-written assembly listings."""
+from paper_2504_15299_amd import build
+
+HEAD = "_Zkernel:\n"
+
+SAFE = HEAD + """
+\ts_and_saveexec_b64 s[4:5], s[6:7]
+\tglobal_load_dwordx4 v[0:3], v[16:17], off
+\ts_mov_b64 exec, s[4:5]
+\ts_cbranch_vccnz .LBB0_2
+\tv_mov_b32_e32 v20, v21
+.LBB0_2:
+\ts_waitcnt vmcnt(3)
+\tv_mfma_scale_f32_16x16x128_f8f6f4 v[24:27], v[32:35], v[0:7], 0, v8, v9 op_sel_hi:[0,0,0] cbsz:4
+\tv_mov_b32_e32 v0, 0
+\ts_endpgm
+"""
+
+# the same listing with a copy through the load's registers on one branch
+# only, before the covering wait: the data can land after the copy
+HAZARD = SAFE.replace("\tv_mov_b32_e32 v20, v21\n", "\tv_readfirstlane_b32 s44, v1\n")
+
+# a use after vmcnt(0) on every path is fine
+AFTER_DRAIN = HEAD + """
+\ts_and_saveexec_b64 s[4:5], s[6:7]
+\tglobal_load_dwordx4 v[0:3], v[16:17], off
+\ts_mov_b64 exec, s[4:5]
+\ts_waitcnt vmcnt(0)
+\tv_mov_b32_e32 v5, v0
+\ts_endpgm
+"""
+
+
+def test_untracked_load_check_accepts_safe_listing():
+    assert build.untracked_load_hazards(SAFE) == []
+    assert build.untracked_load_hazards(AFTER_DRAIN) == []
+
+
+def test_untracked_load_check_finds_use_on_a_branch():
+    bad = build.untracked_load_hazards(HAZARD)
+    assert len(bad) == 1
+    assert "readfirstlane" in bad[0][2]
+
+
+def test_mfma_overlap_check():
+    ok = "\tv_mfma_f32_16x16x32_bf16 v[0:3], v[4:7], v[8:11], v[0:3]\n"
+    bad = "\tv_mfma_f32_16x16x32_bf16 v[4:7], v[4:7], v[8:11], 0\n"
+    assert build.mfma_overlaps(ok) == []
+    assert len(build.mfma_overlaps(bad)) == 1
