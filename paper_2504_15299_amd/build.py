@@ -17,6 +17,11 @@ data arrives late, so such a use would see, or be overwritten by, stale
 data (a decode build whose loop copied a pointer through such registers
 faulted on the GPU).
 
+And it fails if an inline-asm block that writes SCC is followed by a read of
+SCC with no write in between: the compiler does not always treat the asm as
+a definition of SCC, and a stale carry in a 64-bit scalar address add made
+a decode build read from an illegal address.
+
 The build fails if any kernel needs per-lane scratch memory: the decode
 kernels place their own vmcnt waits around the LDS DMA ring, which assume
 that no other vector-memory traffic (such as register spills) is
@@ -110,9 +115,11 @@ def _vregs(tok: str) -> set[int]:
     return {int(m.group(1))} if m else set()
 
 
-def _basic_blocks(lines: list[str]) -> list[dict]:
+def _basic_blocks(lines: list[str], asm_markers: bool = False) -> list[dict]:
     """Basic blocks of one function's assembly (split at labels and after
-    branches) with their successor indices."""
+    branches) with their successor indices.  With `asm_markers`, the
+    compiler's inline-asm delimiters are kept as the pseudo-instructions
+    ASMSTART / ASMEND."""
     blocks, cur = [], {"name": "entry", "ins": []}
     for line in lines:
         s = line.strip()
@@ -120,6 +127,9 @@ def _basic_blocks(lines: list[str]) -> list[dict]:
         if m:
             blocks.append(cur)
             cur = {"name": m.group(1), "ins": []}
+            continue
+        if asm_markers and s.startswith((";;#ASMSTART", ";;#ASMEND")):
+            cur["ins"].append("ASMSTART" if "START" in s else "ASMEND")
             continue
         if not s or s.startswith((";", ".")):
             continue
@@ -133,6 +143,8 @@ def _basic_blocks(lines: list[str]) -> list[dict]:
         succ, falls = [], True
         for x in b["ins"]:
             op = x.split()[0]
+            if op in ("ASMSTART", "ASMEND"):
+                continue
             if op == "s_branch":
                 succ.append(index[x.split()[1]])
                 falls = False
@@ -156,16 +168,8 @@ def untracked_load_hazards(asm: str) -> list[tuple[str, str, str]]:
     or an s_waitcnt vmcnt(0): the compiler would be using the registers for
     another value that the late data can overwrite.  Returns (function,
     load, offending instruction) triples."""
-    funcs, name = {}, None
-    for line in asm.splitlines():
-        m = re.match(r"^(_Z\S+):", line)
-        if m:
-            name = m.group(1)
-            funcs[name] = []
-        elif name:
-            funcs[name].append(line)
     bad = []
-    for fname, lines in funcs.items():
+    for fname, lines in _funcs(asm).items():
         blocks = _basic_blocks(lines)
         for bi, b in enumerate(blocks):
             for ii, x in enumerate(b["ins"]):
@@ -205,6 +209,71 @@ def untracked_load_hazards(asm: str) -> list[tuple[str, str, str]]:
     return bad
 
 
+_SCC_READERS = ("s_addc_u32", "s_subb_u32", "s_cselect_", "s_cbranch_scc", "s_cmov_", "s_cmovk_")
+_SCC_WRITERS = ("s_add_", "s_sub_", "s_addc_", "s_subb_", "s_min_", "s_max_", "s_and_", "s_or_",
+                "s_xor_", "s_andn2_", "s_orn2_", "s_nand_", "s_nor_", "s_xnor_", "s_lshl", "s_lshr",
+                "s_ashr", "s_bfe_", "s_cmp_", "s_cmpk_", "s_bitcmp", "s_abs_", "s_not_", "s_absdiff")
+
+
+def _funcs(asm: str) -> dict[str, list[str]]:
+    funcs, name = {}, None
+    for line in asm.splitlines():
+        m = re.match(r"^(_Z\S+):", line)
+        if m:
+            name = m.group(1)
+            funcs[name] = []
+        elif name:
+            funcs[name].append(line)
+    return funcs
+
+
+def scc_clobber_hazards(asm: str) -> list[tuple[str, str]]:
+    """Inline-asm blocks that write SCC (s_and_saveexec, scalar arithmetic)
+    after which, on some path, SCC is read before anything writes it again:
+    the compiler kept a value in SCC across the asm (for instance the carry
+    of a 64-bit scalar add), and the asm replaced it.  Returns (function,
+    reading instruction) pairs."""
+    bad = []
+    for fname, lines in _funcs(asm).items():
+        blocks = _basic_blocks(lines, asm_markers=True)
+        for bi, b in enumerate(blocks):
+            inside, writes = False, False
+            for ii, x in enumerate(b["ins"]):
+                if x == "ASMSTART":
+                    inside, writes = True, False
+                    continue
+                if x == "ASMEND":
+                    inside = False
+                    if not writes:
+                        continue
+                    stack, seen = [(bi, ii + 1)], set()
+                    while stack:
+                        cb, ci = stack.pop()
+                        if (cb, ci) in seen:
+                            continue
+                        seen.add((cb, ci))
+                        stop = False
+                        for y in blocks[cb]["ins"][ci:]:
+                            if y in ("ASMSTART", "ASMEND"):
+                                continue
+                            op = y.split()[0]
+                            if op.startswith(_SCC_READERS):
+                                bad.append((fname, y))
+                                stop = True
+                                break
+                            if op.startswith(_SCC_WRITERS) or "_saveexec_" in op:
+                                stop = True
+                                break
+                        if not stop:
+                            stack.extend((sb, 0) for sb in blocks[cb]["succ"])
+                    continue
+                if inside:
+                    op = x.split()[0]
+                    if op.startswith(_SCC_WRITERS) or "_saveexec_" in op:
+                        writes = True
+    return bad
+
+
 def _check_mfma(src: str) -> None:
     cmd = [_hipcc(), *COMMON, *EXTRA.get(src, []), "--cuda-device-only", "-S", "-o", "-",
            os.path.join(CSRC, src)]
@@ -214,6 +283,10 @@ def _check_mfma(src: str) -> None:
     bad = mfma_overlaps(r.stdout)
     if bad:
         raise RuntimeError(f"{src}: {len(bad)} MFMAs write over their own operands, e.g. {bad[0]}")
+    sc = scc_clobber_hazards(r.stdout)
+    if sc:
+        raise RuntimeError(f"{src}: {len(sc)} reads of SCC that an inline-asm block overwrote, "
+                           f"e.g. {sc[0]}")
     hz = untracked_load_hazards(r.stdout)
     if hz:
         raise RuntimeError(f"{src}: {len(hz)} untracked activation loads whose registers are used "

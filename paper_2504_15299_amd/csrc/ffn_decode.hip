@@ -401,7 +401,9 @@ struct BData {
 // which the wait counts rely on.
 // Only the lanes in `m` load (EXEC is narrowed and restored inside the asm);
 // the other lanes keep `v`.  `m` always contains lane 0, so the instruction
-// is always issued and counted by vmcnt.
+// is always issued and counted by vmcnt.  s_and_saveexec writes SCC, which
+// the compiler may otherwise keep live across the asm (for instance the carry
+// between the two halves of a 64-bit scalar address add), hence the clobber.
 __device__ inline void gload16(v4i& v, const uint8_t* p, uint64_t m) {
   uint64_t saved;
   asm volatile(
@@ -410,7 +412,7 @@ __device__ inline void gload16(v4i& v, const uint8_t* p, uint64_t m) {
       "s_mov_b64 exec, %1"
       : "+v"(v), "=&s"(saved)
       : "v"(p), "s"(m)
-      : "memory");
+      : "memory", "scc");
 }
 
 // Two memory instructions per column block, issued by the lanes that hold a

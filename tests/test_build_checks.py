@@ -49,3 +49,38 @@ def test_mfma_overlap_check():
     bad = "\tv_mfma_f32_16x16x32_bf16 v[4:7], v[4:7], v[8:11], 0\n"
     assert build.mfma_overlaps(ok) == []
     assert len(build.mfma_overlaps(bad)) == 1
+
+
+# a 64-bit scalar address add split around an inline-asm block that writes
+# SCC: the carry the second half reads is the asm's, not the first half's
+SCC_LIVE = HEAD + """
+\ts_add_u32 s30, s30, s62
+\t;;#ASMSTART
+\ts_and_saveexec_b64 s[38:39], s[4:5]
+\tglobal_load_dwordx4 v[0:3], v[10:11], off
+\ts_mov_b64 exec, s[38:39]
+\t;;#ASMEND
+\ts_addc_u32 s31, s31, s36
+\ts_endpgm
+"""
+
+# the same asm with the add completed before it
+SCC_DEAD = HEAD + """
+\ts_add_u32 s30, s30, s62
+\ts_addc_u32 s31, s31, s36
+\t;;#ASMSTART
+\ts_and_saveexec_b64 s[38:39], s[4:5]
+\tglobal_load_dwordx4 v[0:3], v[10:11], off
+\ts_mov_b64 exec, s[38:39]
+\t;;#ASMEND
+\ts_cmp_eq_u32 s2, 0
+\ts_cbranch_scc1 .LBB0_1
+.LBB0_1:
+\ts_endpgm
+"""
+
+
+def test_scc_check_finds_carry_across_asm():
+    bad = build.scc_clobber_hazards(SCC_LIVE)
+    assert len(bad) == 1 and bad[0][1].startswith("s_addc_u32")
+    assert build.scc_clobber_hazards(SCC_DEAD) == []
