@@ -20,12 +20,15 @@
 // is ever materialised as a number.  Tokens whose bit-width is below a plane get
 // a zero coefficient for it; they share the loads.
 //
-// Work split: a workgroup owns one 16-row block (for SwiGLU, half its waves
-// take the W1 block and half the matching W3 block) of one active expert; the
-// waves of each half split the groups of the reduction dimension and reduce
-// through LDS.  Requirement: group 128 (any nest start b_min).  An expert's
-// positions are cut into work items of at most 8 or 16, each of which
-// streams the expert's planes; the forward takes this path up to 64 tokens.
+// Work split: W1/W3 (decode13_kernel) gives each 16-row block of one active
+// expert to one or two waves, each of which streams the W1 block and the
+// matching W3 block of its share of the reduction dimension in alternate
+// ring stages (so that a and c of the same outputs meet in its lanes); W2
+// (decode_kernel) gives each 16-row block to a 4-wave workgroup whose waves
+// split the reduction.  Split waves reduce through LDS.  Requirement: group
+// 128 (any nest start b_min).  An expert's positions are cut into work items
+// of at most 8 or 16, each of which streams the expert's planes; the forward
+// takes this path up to 64 tokens.
 #include "internal.h"
 
 namespace d2moe {
@@ -961,26 +964,35 @@ __device__ inline void decode_pairs(const WaveCtx<NCB>& c, const W3Offsets& o3, 
 }
 
 // elist, Xq, Xs, npos as for decode_kernel; f = d_ff (W3 rows start at row f
-// of the stacked W13).  Workgroup x covers row blocks NW x .. NW x + NW - 1,
-// one per wave; there is no barrier, so a wave past the last row block leaves.
-template <int NW, int NCB, int BMIN>
+// of the stacked W13).  KS waves share one row block, each streaming both
+// matrices over 1/KS of the groups; workgroup x covers row blocks
+// (NW / KS) x .. + NW / KS - 1.  With KS > 1 the waves' partial sums meet in
+// their (then idle) rings and the first wave of each row block finishes.
+template <int NW, int KS, int NCB, int BMIN>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NCB == 1 ? 4 : 3)))
 void decode13_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* __restrict__ Xq,
                      const uint32_t* __restrict__ Xs, int npos, int f, float* __restrict__ out,
                      int out_ld, uint32_t* __restrict__ rowmax) {
   constexpr int kStage = stage_bytes<BMIN>();
+  static_assert(NW % KS == 0, "whole row blocks per workgroup");
+  static_assert(kDepth * kStage >= 2 * NCB * 64 * 4 * (int)sizeof(float), "partial sums fit the ring");
   __shared__ __attribute__((aligned(16))) uint8_t ring[NW][kDepth * kStage];
   const int ei = blockIdx.y;
   const int e = elist[4 * ei], p0 = elist[4 * ei + 1], p1 = elist[4 * ei + 2];
   const int mb_req = elist[4 * ei + 3];
-  if (mb_req == 0) return;
+  if (mb_req == 0) return;  // workgroup-uniform
   const int mb = mb_req < W.b_max ? mb_req : W.b_max;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nrb = f / 16;
-  const int rb = blockIdx.x * NW + wave;
-  if (rb >= nrb) return;
+  const int rb = blockIdx.x * (NW / KS) + wave / KS;
+  const int kp = wave % KS;
+  // a row block past the end (f / 16 not a multiple of NW / KS) does no work
+  // but still meets the workgroup barrier below
+  const bool active = rb < nrb;
+  if (KS == 1 && !active) return;
   const int NG = W.cols / G;
+  const int g0 = kp * NG / KS, g1 = (kp + 1) * NG / KS;
   const int ncol = p1 - p0;
 
   WaveCtx<NCB> c;
@@ -1034,16 +1046,43 @@ void decode13_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t
   for (int h = 0; h < 2; ++h)
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) acc[h][cb] = v4f{0.f, 0.f, 0.f, 0.f};
-  switch (mb) {
+  if (active) {
+    switch (mb) {
 #define D2MOE_CASE(MB) \
   case MB:             \
-    if constexpr (MB >= BMIN) decode_pairs<MB, BMIN, NCB>(c, o3, ring[wave], 0, NG, acc); \
+    if constexpr (MB >= BMIN) decode_pairs<MB, BMIN, NCB>(c, o3, ring[wave], g0, g1, acc); \
     break;
-    D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
-    D2MOE_CASE(7) D2MOE_CASE(8)
+      D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
+      D2MOE_CASE(7) D2MOE_CASE(8)
 #undef D2MOE_CASE
-    default: break;
+      default: break;
+    }
   }
+  if constexpr (KS > 1) {
+    // every DMA of this wave has completed (its last step waits for all), so
+    // its ring can hold its partial sums
+    float4* red = (float4*)ring[wave];
+    if (kp != 0) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+          red[64 * (NCB * h + cb) + lane] = float4{acc[h][cb][0], acc[h][cb][1], acc[h][cb][2], acc[h][cb][3]};
+    }
+    __syncthreads();
+    if (kp != 0 || !active) return;
+    for (int w = 1; w < KS; ++w) {
+      const float4* part = (const float4*)ring[wave + w];
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+          const float4 v = part[64 * (NCB * h + cb) + lane];
+          acc[h][cb][0] += v.x; acc[h][cb][1] += v.y; acc[h][cb][2] += v.z; acc[h][cb][3] += v.w;
+        }
+    }
+  }
+
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) {
     float o[4];
@@ -1108,15 +1147,16 @@ hipError_t launch_decode_kernel(int b_min, dim3 grid, const MwqView& W, const in
 
 // W1/W3 with one wave per row block (decode13_kernel), kDecodeWaves row blocks
 // per workgroup.
-template <int NCB>
+template <int KS, int NCB>
 hipError_t launch_decode13_kernel(int b_min, int ny, const MwqView& W, const int32_t* elist,
                                   const uint8_t* Xq, const uint32_t* Xs, int npos, int f,
                                   float* out, int out_ld, uint32_t* rowmax, hipStream_t s) {
-  const dim3 grid((f / 16 + kDecodeWaves - 1) / kDecodeWaves, ny);
+  constexpr int rpw = kDecodeWaves / KS;  // row blocks per workgroup
+  const dim3 grid((f / 16 + rpw - 1) / rpw, ny);
   switch (b_min) {
 #define D2MOE_CASE(B)                                                                      \
   case B:                                                                                  \
-    decode13_kernel<kDecodeWaves, NCB, B><<<grid, 64 * kDecodeWaves, 0, s>>>(              \
+    decode13_kernel<kDecodeWaves, KS, NCB, B><<<grid, 64 * kDecodeWaves, 0, s>>>(          \
         W, elist, Xq, Xs, npos, f, out, out_ld, rowmax);                                   \
     break;
     D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
@@ -1151,23 +1191,25 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   const MwqView W13 = view_of(w13), W2 = view_of(w2);
   if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
   const dim3 g13(d_ff / 16, ny), g2(d / 16, ny);
-  // Two column blocks (more than 4 positions per expert on average): one wave
-  // per row block streams both W1 and W3 over the whole reduction, so one
-  // activation load serves both and the streams are long (decode13_kernel).
-  // Fewer positions: four waves per row block split the reduction
-  // (decode_kernel), which leaves more, shorter streams for the grid and was
-  // as fast or faster at batches of 1 to 16.  decode13_kernel addresses the
-  // W3 block as a 32-bit byte offset from the W1 block of the same rows.
+  // W1/W3: each wave streams both matrices' blocks of its rows (one
+  // activation load serves both).  One column block: two waves per row block,
+  // each over half of the reduction (the fastest split at batches of 1 to
+  // 16); two column blocks: one wave per row block (the split variants do not
+  // fit 3 waves per SIMD without spilling).  decode13_kernel addresses the W3
+  // block as a 32-bit byte offset from the W1 block of the same rows; larger
+  // layers fall back to decode_kernel, whose waves take W1 or W3 blocks.
   const bool fits = (size_t)(d_ff / 16) * (d / G) * (size_t)w13->b_max * 256 < ((size_t)1 << 31);
-  if (ncb == 2 && fits)
-    err = launch_decode13_kernel<2>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos, d_ff,
-                                    b.h32, d_ff, b.hmax, s);
-  else if (ncb == 2)
-    err = launch_decode_kernel<true, 2>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13, npos,
-                                        d_ff, b.h32, d_ff, b.hmax, s);
+  if (!fits)
+    err = ncb == 1 ? launch_decode_kernel<true, 1>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13,
+                                                   npos, d_ff, b.h32, d_ff, b.hmax, s)
+                   : launch_decode_kernel<true, 2>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13,
+                                                   npos, d_ff, b.h32, d_ff, b.hmax, s);
+  else if (ncb == 1)
+    err = launch_decode13_kernel<2, 1>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos, d_ff,
+                                       b.h32, d_ff, b.hmax, s);
   else
-    err = launch_decode_kernel<true, 1>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13, npos,
-                                        d_ff, b.h32, d_ff, b.hmax, s);
+    err = launch_decode13_kernel<1, 2>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos, d_ff,
+                                       b.h32, d_ff, b.hmax, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
   err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.hmax, d_ff / 16, b.xq2, b.xs2, r,

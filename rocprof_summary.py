@@ -19,7 +19,7 @@ from collections import defaultdict
 
 
 def _short(name: str) -> str:
-    for key in ("decode_kernel<true", "decode_kernel<false", "xprep_kernel", "bgemm_kernel", "gemm_kernel",
+    for key in ("decode13_kernel", "decode_kernel<true", "decode_kernel<false", "xprep_kernel", "bgemm_kernel", "gemm_kernel",
                 "combine_kernel", "gate_kernel", "topk_kernel", "hist_perm_kernel",
                 "schedule_kernel", "pack_kernel", "chunk_kernel", "route_kernel", "to_bf16_kernel"):
         if key in name:
@@ -67,7 +67,7 @@ def decode_traffic(fetch_db, write_db):
         factor, avg = _per_kernel(db, cname)
         for name, kib in avg.items():
             total[name] += kib / factor * 1024
-    w13 = [v for k, v in total.items() if k.startswith("decode_kernel<true")]
+    w13 = [v for k, v in total.items() if k.startswith(("decode13_kernel", "decode_kernel<true"))]
     w2 = [v for k, v in total.items() if k.startswith("decode_kernel<false")]
     print("traffic per launch (FETCH + WRITE, calibrated), used by bench.py as roofline.traffic:")
     print(f"kernel_source_sha256_16: {kernel_source_hash()}")
