@@ -963,12 +963,16 @@ __device__ inline void decode_pairs(const WaveCtx<NCB>& c, const W3Offsets& o3, 
   wait_vm<0>();
 }
 
-// elist, Xq, Xs, npos as for decode_kernel; f = d_ff (W3 rows start at row f
-// of the stacked W13).  KS waves share one row block, each streaming both
-// matrices over 1/KS of the groups; workgroup x covers row blocks
-// (NW / KS) x .. + NW / KS - 1.  With KS > 1 the waves' partial sums meet in
-// their (then idle) rings and the first wave of each row block finishes.
-template <int NW, int KS, int NCB, int BMIN>
+// elist, Xq, Xs, npos as for decode_kernel.  Each wave streams two 16-row
+// blocks in alternate ring stages over 1/KS of the groups (KS waves share
+// them):
+//   SWIGLU: f = d_ff; the W1 block rb and the W3 block rb + f/16 of the stacked
+//   W13 (rows f.. are W3), combined as silu(a) * c into h rows rb*16..;
+//   otherwise (W2): f = the matrix's rows; the adjacent blocks 2p and 2p + 1,
+//   written to output rows 32p.. (f / 16 must be even).
+// Workgroup x covers NW / KS such units.  With KS > 1 the waves' partial sums
+// meet in their (then idle) rings and the first wave of each unit finishes.
+template <int NW, int KS, int NCB, int BMIN, bool SWIGLU>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NCB == 1 ? 4 : 3)))
 void decode13_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* __restrict__ Xq,
                      const uint32_t* __restrict__ Xs, int npos, int f, float* __restrict__ out,
@@ -985,7 +989,8 @@ void decode13_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nrb = f / 16;
-  const int rb = blockIdx.x * (NW / KS) + wave / KS;
+  const int unit = blockIdx.x * (NW / KS) + wave / KS;
+  const int rb = SWIGLU ? unit : 2 * unit;  // first row block of the pair
   const int kp = wave % KS;
   // a row block past the end (f / 16 not a multiple of NW / KS) does no work
   // but still meets the workgroup barrier below
@@ -1024,7 +1029,7 @@ void decode13_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t
     }
   }
 
-  const size_t blk1 = W.block(e, rb, 0), blk3 = W.block(e, rb + nrb, 0);
+  const size_t blk1 = W.block(e, rb, 0), blk3 = W.block(e, SWIGLU ? rb + nrb : rb + 1, 0);
   c.pl = (const uint8_t*)(W.planes + W.plane_word(blk1, 0, 0));
   c.sc = (const uint8_t*)(W.scales + W.scale_idx(blk1, 0, 0));
   c.zp = W.zeros + W.zero_idx(blk1, 0);
@@ -1083,6 +1088,20 @@ void decode13_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t
     }
   }
 
+  if constexpr (!SWIGLU) {
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        float o[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[r] = acc[h][cb][r] + __shfl_xor(acc[h][cb][r], 1, 64);
+        if (valid[cb] && piece == 0)
+          *(float4*)(out + (size_t)pos[cb] * out_ld + (rb + h) * 16 + 4 * c.q) =
+              float4{o[0], o[1], o[2], o[3]};
+      }
+    return;
+  }
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) {
     float o[4];
@@ -1147,16 +1166,17 @@ hipError_t launch_decode_kernel(int b_min, dim3 grid, const MwqView& W, const in
 
 // W1/W3 with one wave per row block (decode13_kernel), kDecodeWaves row blocks
 // per workgroup.
-template <int KS, int NCB>
+template <int KS, int NCB, bool SWIGLU = true>
 hipError_t launch_decode13_kernel(int b_min, int ny, const MwqView& W, const int32_t* elist,
                                   const uint8_t* Xq, const uint32_t* Xs, int npos, int f,
                                   float* out, int out_ld, uint32_t* rowmax, hipStream_t s) {
-  constexpr int rpw = kDecodeWaves / KS;  // row blocks per workgroup
-  const dim3 grid((f / 16 + rpw - 1) / rpw, ny);
+  constexpr int upw = kDecodeWaves / KS;        // units (row blocks or pairs) per workgroup
+  const int units = SWIGLU ? f / 16 : f / 32;
+  const dim3 grid((units + upw - 1) / upw, ny);
   switch (b_min) {
 #define D2MOE_CASE(B)                                                                      \
   case B:                                                                                  \
-    decode13_kernel<kDecodeWaves, KS, NCB, B><<<grid, 64 * kDecodeWaves, 0, s>>>(          \
+    decode13_kernel<kDecodeWaves, KS, NCB, B, SWIGLU><<<grid, 64 * kDecodeWaves, 0, s>>>(  \
         W, elist, Xq, Xs, npos, f, out, out_ld, rowmax);                                   \
     break;
     D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
@@ -1216,10 +1236,25 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
                          false, E, L, nullptr, 0, item, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
-  err = ncb == 1 ? launch_decode_kernel<false, 1>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
-                                                  0, b.y, d, nullptr, s)
-                 : launch_decode_kernel<false, 2>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
-                                                  0, b.y, d, nullptr, s);
+  // W2 at one column block: when the grid still fills the GPU's wave slots
+  // (256 CUs x 16 waves) about 1.25 times over, each wave streams a pair of
+  // adjacent row blocks over a quarter of the reduction (decode13_kernel, one
+  // activation load for both blocks); with fewer work items (batches below
+  // 8 at the Mixtral shape) the 4-wave-per-row-block kernel keeps more
+  // streams in flight and is faster.  The second block's offset is one row
+  // block of groups.
+  constexpr int kW2Split = 4;
+  const bool pairs2 = ncb == 1 && (d / 16) % 2 == 0 &&
+                      (long)(d / 32) * ny * kW2Split >= 5120 &&
+                      (size_t)(d_ff / G) * (size_t)w2->b_max * 256 < ((size_t)1 << 31);
+  if (pairs2)
+    err = launch_decode13_kernel<kW2Split, 1, false>(w2->b_min, ny, W2, b.elist, b.xq2, b.xs2,
+                                                     npos, d, b.y, d, nullptr, s);
+  else
+    err = ncb == 1 ? launch_decode_kernel<false, 1>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
+                                                    0, b.y, d, nullptr, s)
+                   : launch_decode_kernel<false, 2>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
+                                                    0, b.y, d, nullptr, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
   return hipSuccess;

@@ -67,8 +67,14 @@ def decode_traffic(fetch_db, write_db):
         factor, avg = _per_kernel(db, cname)
         for name, kib in avg.items():
             total[name] += kib / factor * 1024
-    w13 = [v for k, v in total.items() if k.startswith(("decode13_kernel", "decode_kernel<true"))]
-    w2 = [v for k, v in total.items() if k.startswith("decode_kernel<false")]
+    def w13_kernel(k):  # W1/W3 + SwiGLU: decode13_kernel<..., true> or decode_kernel<true, ...>
+        return k.startswith("decode_kernel<true") or (k.startswith("decode13_kernel") and "true>" in k)
+
+    def w2_kernel(k):
+        return k.startswith("decode_kernel<false") or (k.startswith("decode13_kernel") and "false>" in k)
+
+    w13 = [v for k, v in total.items() if w13_kernel(k)]
+    w2 = [v for k, v in total.items() if w2_kernel(k)]
     print("traffic per launch (FETCH + WRITE, calibrated), used by bench.py as roofline.traffic:")
     print(f"kernel_source_sha256_16: {kernel_source_hash()}")
     print(f"traffic_w13_bytes: {int(round(sum(w13) / len(w13)))}")
