@@ -21,11 +21,13 @@
 // a zero coefficient for it; they share the loads.
 //
 // Work split: W1/W3 (decode13_kernel) gives each 16-row block of one active
-// expert to one or two waves, each of which streams the W1 block and the
-// matching W3 block of its share of the reduction dimension in alternate
-// ring stages (so that a and c of the same outputs meet in its lanes); W2
-// (decode_kernel) gives each 16-row block to a 4-wave workgroup whose waves
-// split the reduction.  Split waves reduce through LDS.  Requirement: group
+// expert to two waves, each of which streams the W1 block and the matching
+// W3 block of half the reduction dimension in alternate ring stages (so that
+// a and c of the same outputs meet in its lanes); W2 gives each pair of
+// adjacent 16-row blocks to four waves that stream both blocks of a quarter
+// of the reduction (decode13_kernel) or, for small grids, each 16-row block
+// to a 4-wave workgroup whose waves split the reduction (decode_kernel).
+// Split waves reduce through LDS.  Requirement: group
 // 128 (any nest start b_min).  An expert's positions are cut into work items
 // of at most 8 or 16, each of which streams the expert's planes; the forward
 // takes this path up to 64 tokens.
@@ -1020,7 +1022,7 @@ void decode13_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t
       pos[cb] = p0 + tc;
       const int src = valid[cb] ? pos[cb] : npos;
       const size_t base = ((size_t)src * NG) * 2 + piece;
-      c.xq[cb] = Xq + base * 128 + c.q * 32;
+      c.xq[cb] = Xq + base * 128 + c.q * 32 + (size_t)g0 * 256;
       c.lmask[cb] = __ballot(valid[cb]) | 1ull;
       uint32_t info = 0u;
 #pragma unroll
@@ -1029,7 +1031,9 @@ void decode13_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t
     }
   }
 
-  const size_t blk1 = W.block(e, rb, 0), blk3 = W.block(e, SWIGLU ? rb + nrb : rb + 1, 0);
+  // the bases point at group g0, so that the stream below always starts at
+  // group 0 (the same loop as an unsplit wave, with no per-wave offsets live)
+  const size_t blk1 = W.block(e, rb, g0), blk3 = W.block(e, SWIGLU ? rb + nrb : rb + 1, g0);
   c.pl = (const uint8_t*)(W.planes + W.plane_word(blk1, 0, 0));
   c.sc = (const uint8_t*)(W.scales + W.scale_idx(blk1, 0, 0));
   c.zp = W.zeros + W.zero_idx(blk1, 0);
@@ -1055,7 +1059,7 @@ void decode13_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t
     switch (mb) {
 #define D2MOE_CASE(MB) \
   case MB:             \
-    if constexpr (MB >= BMIN) decode_pairs<MB, BMIN, NCB>(c, o3, ring[wave], g0, g1, acc); \
+    if constexpr (MB >= BMIN) decode_pairs<MB, BMIN, NCB>(c, o3, ring[wave], 0, g1 - g0, acc); \
     break;
       D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
       D2MOE_CASE(7) D2MOE_CASE(8)
@@ -1212,12 +1216,11 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
   const dim3 g13(d_ff / 16, ny), g2(d / 16, ny);
   // W1/W3: each wave streams both matrices' blocks of its rows (one
-  // activation load serves both).  One column block: two waves per row block,
-  // each over half of the reduction (the fastest split at batches of 1 to
-  // 16); two column blocks: one wave per row block (the split variants do not
-  // fit 3 waves per SIMD without spilling).  decode13_kernel addresses the W3
-  // block as a 32-bit byte offset from the W1 block of the same rows; larger
-  // layers fall back to decode_kernel, whose waves take W1 or W3 blocks.
+  // activation load serves both), two waves per row block, each over half of
+  // the reduction (the fastest split at every batch measured, 1 to 64).
+  // decode13_kernel addresses the W3 block as a 32-bit byte offset from the
+  // W1 block of the same rows; larger layers fall back to decode_kernel,
+  // whose waves take W1 or W3 blocks.
   const bool fits = (size_t)(d_ff / 16) * (d / G) * (size_t)w13->b_max * 256 < ((size_t)1 << 31);
   if (!fits)
     err = ncb == 1 ? launch_decode_kernel<true, 1>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13,
@@ -1228,7 +1231,7 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
     err = launch_decode13_kernel<2, 1>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos, d_ff,
                                        b.h32, d_ff, b.hmax, s);
   else
-    err = launch_decode13_kernel<1, 2>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos, d_ff,
+    err = launch_decode13_kernel<2, 2>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos, d_ff,
                                        b.h32, d_ff, b.hmax, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
@@ -1236,7 +1239,7 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
                          false, E, L, nullptr, 0, item, s);
   if (err != hipSuccess) return err;
   if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
-  // W2 at one column block: when the grid still fills the GPU's wave slots
+  // W2: when the grid still fills the GPU's wave slots
   // (256 CUs x 16 waves) about 1.25 times over, each wave streams a pair of
   // adjacent row blocks over a quarter of the reduction (decode13_kernel, one
   // activation load for both blocks); with fewer work items (batches below
@@ -1244,11 +1247,14 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   // streams in flight and is faster.  The second block's offset is one row
   // block of groups.
   constexpr int kW2Split = 4;
-  const bool pairs2 = ncb == 1 && (d / 16) % 2 == 0 &&
+  const bool pairs2 = (d / 16) % 2 == 0 &&
                       (long)(d / 32) * ny * kW2Split >= 5120 &&
                       (size_t)(d_ff / G) * (size_t)w2->b_max * 256 < ((size_t)1 << 31);
-  if (pairs2)
+  if (pairs2 && ncb == 1)
     err = launch_decode13_kernel<kW2Split, 1, false>(w2->b_min, ny, W2, b.elist, b.xq2, b.xs2,
+                                                     npos, d, b.y, d, nullptr, s);
+  else if (pairs2)
+    err = launch_decode13_kernel<kW2Split, 2, false>(w2->b_min, ny, W2, b.elist, b.xq2, b.xs2,
                                                      npos, d, b.y, d, nullptr, s);
   else
     err = ncb == 1 ? launch_decode_kernel<false, 1>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
