@@ -193,6 +193,11 @@ FWD_SPECS = {
     # shared expert cut into 64-position chunks with its W2 reduction split in
     # two parts summed by the combine
     "fine_shared_split": wl.scaled(wl.fine_grained(), d=256, f=64, T=200, shared_f=1024),
+    # enough decode work items (64 experts) for the W2 kernel that streams
+    # pairs of adjacent row blocks, at one column block (k 4: 256 positions)
+    # and at two (k 10: 640 positions)
+    "decode_64e_k4_T64": wl.scaled(wl.mixtral_decode(T=64), d=512, f=128, E=64, k=4),
+    "decode_64e_k10_T64": wl.scaled(wl.mixtral_decode(T=64), d=512, f=128, E=64, k=10),
 }
 
 
