@@ -204,10 +204,14 @@ d2moe_status d2moe_moe_forward(const void* x, d2moe_dtype x_dtype, int32_t T,
 
 /*
  * Same as d2moe_moe_forward, and additionally records events[0] / events[1]
- * (hipEvent_t) on `stream` immediately before / after the W1-W3 expert
- * kernel and events[2] / events[3] around the W2 expert kernel, so a caller
- * can time the expert kernels on the stream they run on.  events must hold
- * four created events.  Nothing is recorded when T == 0.
+ * (hipEvent_t) at the start / end of the W1-W3 expert kernel and events[2] /
+ * events[3] at the start / end of the W2 expert kernel, on `stream`, so a
+ * caller can time the expert kernels on the stream they run on.  Up to 64
+ * tokens the events are the expert kernels' own start and end time stamps
+ * (recorded as part of their launch, so timing adds no idle time to the
+ * stream); above, they are recorded on the stream immediately before / after
+ * the kernels.  events must hold four created events.  Nothing is recorded
+ * when T == 0.
  */
 d2moe_status d2moe_moe_forward_profiled(const void* x, d2moe_dtype x_dtype, int32_t T,
                                         int32_t d, int32_t d_ff, int32_t E, int32_t k,

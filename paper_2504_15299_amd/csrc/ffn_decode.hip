@@ -33,6 +33,8 @@
 // takes this path up to 64 tokens.
 #include "internal.h"
 
+#include <hip/hip_ext.h>
+
 namespace d2moe {
 
 namespace {
@@ -1149,15 +1151,30 @@ bool decode_path_ok(const d2moe_mwq* w13, const d2moe_mwq* w2, int T) {
 // not the workgroup size, sets how many workgroups share a compute unit.
 constexpr int kDecodeWaves = 4;
 
+// The expert kernels take optional start / stop events.  Given events, the
+// kernel is launched through hipExtLaunchKernel, which records them as the
+// kernel's own start and end time stamps; events recorded as separate stream
+// markers around the launch would also count the kernel's wait for the
+// previous one (about 5 us).
+template <typename K, typename... A>
+inline void launch_timed(K kernel, dim3 grid, dim3 block, hipStream_t s, hipEvent_t ev0,
+                         hipEvent_t ev1, A... args) {
+  if (ev0 || ev1)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, ev0, ev1, 0, args...);
+  else
+    kernel<<<grid, block, 0, s>>>(args...);
+}
+
 template <bool SWIGLU, int NCB>
 hipError_t launch_decode_kernel(int b_min, dim3 grid, const MwqView& W, const int32_t* elist,
                                 const uint8_t* Xq, const uint32_t* Xs, int npos, int f,
-                                float* out, int out_ld, uint32_t* rowmax, hipStream_t s) {
+                                float* out, int out_ld, uint32_t* rowmax, hipStream_t s,
+                                hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr) {
   switch (b_min) {
 #define D2MOE_CASE(B)                                                                      \
   case B:                                                                                  \
-    decode_kernel<SWIGLU, kDecodeWaves, NCB, B><<<grid, 64 * kDecodeWaves, 0, s>>>(        \
-        W, elist, Xq, Xs, npos, f, out, out_ld, rowmax);                                   \
+    launch_timed(decode_kernel<SWIGLU, kDecodeWaves, NCB, B>, grid, dim3(64 * kDecodeWaves), \
+                 s, ev0, ev1, W, elist, Xq, Xs, npos, f, out, out_ld, rowmax);            \
     break;
     D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
     D2MOE_CASE(7) D2MOE_CASE(8)
@@ -1173,15 +1190,17 @@ hipError_t launch_decode_kernel(int b_min, dim3 grid, const MwqView& W, const in
 template <int KS, int NCB, bool SWIGLU = true>
 hipError_t launch_decode13_kernel(int b_min, int ny, const MwqView& W, const int32_t* elist,
                                   const uint8_t* Xq, const uint32_t* Xs, int npos, int f,
-                                  float* out, int out_ld, uint32_t* rowmax, hipStream_t s) {
+                                  float* out, int out_ld, uint32_t* rowmax, hipStream_t s,
+                                  hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr) {
   constexpr int upw = kDecodeWaves / KS;        // units (row blocks or pairs) per workgroup
   const int units = SWIGLU ? f / 16 : f / 32;
   const dim3 grid((units + upw - 1) / upw, ny);
   switch (b_min) {
 #define D2MOE_CASE(B)                                                                      \
   case B:                                                                                  \
-    decode13_kernel<kDecodeWaves, KS, NCB, B, SWIGLU><<<grid, 64 * kDecodeWaves, 0, s>>>(  \
-        W, elist, Xq, Xs, npos, f, out, out_ld, rowmax);                                   \
+    launch_timed(decode13_kernel<kDecodeWaves, KS, NCB, B, SWIGLU>, grid,                \
+                 dim3(64 * kDecodeWaves), s, ev0, ev1, W, elist, Xq, Xs, npos, f, out,    \
+                 out_ld, rowmax);                                                          \
     break;
     D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
     D2MOE_CASE(7) D2MOE_CASE(8)
@@ -1213,7 +1232,9 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
                            r, true, E, L, b.elist, ny, item, s);
   if (err != hipSuccess) return err;
   const MwqView W13 = view_of(w13), W2 = view_of(w2);
-  if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
+  // the expert kernels record the caller's events themselves (launch_timed)
+  const hipEvent_t e0 = events ? events[0] : nullptr, e1 = events ? events[1] : nullptr;
+  const hipEvent_t e2 = events ? events[2] : nullptr, e3 = events ? events[3] : nullptr;
   const dim3 g13(d_ff / 16, ny), g2(d / 16, ny);
   // W1/W3: each wave streams both matrices' blocks of its rows (one
   // activation load serves both), two waves per row block, each over half of
@@ -1224,21 +1245,19 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   const bool fits = (size_t)(d_ff / 16) * (d / G) * (size_t)w13->b_max * 256 < ((size_t)1 << 31);
   if (!fits)
     err = ncb == 1 ? launch_decode_kernel<true, 1>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13,
-                                                   npos, d_ff, b.h32, d_ff, b.hmax, s)
+                                                   npos, d_ff, b.h32, d_ff, b.hmax, s, e0, e1)
                    : launch_decode_kernel<true, 2>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13,
-                                                   npos, d_ff, b.h32, d_ff, b.hmax, s);
+                                                   npos, d_ff, b.h32, d_ff, b.hmax, s, e0, e1);
   else if (ncb == 1)
     err = launch_decode13_kernel<2, 1>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos, d_ff,
-                                       b.h32, d_ff, b.hmax, s);
+                                       b.h32, d_ff, b.hmax, s, e0, e1);
   else
     err = launch_decode13_kernel<2, 2>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos, d_ff,
-                                       b.h32, d_ff, b.hmax, s);
+                                       b.h32, d_ff, b.hmax, s, e0, e1);
   if (err != hipSuccess) return err;
-  if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
   err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.hmax, d_ff / 16, b.xq2, b.xs2, r,
                          false, E, L, nullptr, 0, item, s);
   if (err != hipSuccess) return err;
-  if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
   // W2: when the grid still fills the GPU's wave slots
   // (256 CUs x 16 waves) about 1.25 times over, each wave streams a pair of
   // adjacent row blocks over a quarter of the reduction (decode13_kernel, one
@@ -1252,17 +1271,16 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
                       (size_t)(d_ff / G) * (size_t)w2->b_max * 256 < ((size_t)1 << 31);
   if (pairs2 && ncb == 1)
     err = launch_decode13_kernel<kW2Split, 1, false>(w2->b_min, ny, W2, b.elist, b.xq2, b.xs2,
-                                                     npos, d, b.y, d, nullptr, s);
+                                                     npos, d, b.y, d, nullptr, s, e2, e3);
   else if (pairs2)
     err = launch_decode13_kernel<kW2Split, 2, false>(w2->b_min, ny, W2, b.elist, b.xq2, b.xs2,
-                                                     npos, d, b.y, d, nullptr, s);
+                                                     npos, d, b.y, d, nullptr, s, e2, e3);
   else
     err = ncb == 1 ? launch_decode_kernel<false, 1>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
-                                                    0, b.y, d, nullptr, s)
+                                                    0, b.y, d, nullptr, s, e2, e3)
                    : launch_decode_kernel<false, 2>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
-                                                    0, b.y, d, nullptr, s);
+                                                    0, b.y, d, nullptr, s, e2, e3);
   if (err != hipSuccess) return err;
-  if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
   return hipSuccess;
 }
 
