@@ -594,11 +594,18 @@ PROFILE = os.path.join(ROOT, "profiles", "decode_step_mixtral_T16_hbm_bytes.txt"
 
 
 def kernel_source_hash() -> str:
+    """Hash of the decode kernels' code (ffn_decode.hip and internal.h with
+    comments and blank space removed, so that editing a comment does not
+    mark the committed byte counters as stale)."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for name in ("ffn_decode.hip", "internal.h"):
-        with open(os.path.join(ROOT, "paper_2504_15299_amd", "csrc", name), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2504_15299_amd", "csrc", name)) as fh:
+            code = fh.read()
+        code = re.sub(r"/\*.*?\*/", " ", code, flags=re.S)
+        code = re.sub(r"//[^\n]*", " ", code)
+        h.update(" ".join(code.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -834,15 +834,14 @@ void decode_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* 
   }
 }
 
-// ---- W1/W3 kernel: one wave per 16-row block, W1 and W3 in alternate stages
+// ---- paired-block kernels: each wave streams two weight blocks in turn
 //
-// Each wave owns one 16-row block of the output (rows of h) and streams, over
-// the whole reduction dimension, the W1 block and the matching W3 block of
-// every group in turn: ring stage s holds group s / 2 of W1 (s even) or W3
-// (s odd).  One activation load serves both stages of a group, the stream of
-// a wave is four times longer than a quarter of one matrix, and each lane
-// ends with a and c of the same outputs, so the waves of a workgroup never
-// exchange data.
+// A wave streams two 16-row blocks over its share of the reduction
+// dimension, one group of each in turn: ring stage s holds group s / 2 of the
+// first block (s even) or of the second (s odd).  One activation load serves
+// both stages of a group.  For W1/W3 the two blocks are the W1 block and the
+// matching W3 block, so each lane ends with a and c of the same outputs; for
+// W2 they are two adjacent row blocks.
 //
 // Order of issue: the prologue sends the DMA of stage 0, the activations of
 // group 0, then the DMA of stages 1 and 2; the step that computes stage s
@@ -857,13 +856,11 @@ void decode_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* 
 // previous step.  The loop is unrolled by kDepth stages (two groups) so that
 // every ring offset and activation buffer index is a constant.
 // DMA of one stage.  Instructions that carry only plane words address them
-// as the wave-uniform base of group g's planes plus a 32-bit lane offset
-// (16 bytes per lane, 1 KB per instruction), which the hardware takes as a
-// scalar base and a vector offset; the offset is made opaque inside the loop
-// so that the compiler does not hoist a 64-bit per-lane pointer per
-// instruction.  The last, mixed instruction (scales and zero points, and plane
-// words when the nest is not a multiple of four planes) keeps a per-lane
-// source pointer, stride and W3 offset (MixedDma).  `w3` selects the W3 block.
+// from the wave-uniform base of group g's planes (16 bytes per lane, 1 KB per
+// instruction), so they hold no per-lane pointer.  The last, mixed
+// instruction (scales and zero points, and plane words when the nest is not
+// a multiple of four planes) keeps a per-lane source pointer, stride and
+// second-block offset (MixedDma).  `W3` selects the second block.
 struct W3Offsets {
   int pl, sc, zp;
 };
