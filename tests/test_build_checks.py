@@ -84,3 +84,19 @@ def test_scc_check_finds_carry_across_asm():
     bad = build.scc_clobber_hazards(SCC_LIVE)
     assert len(bad) == 1 and bad[0][1].startswith("s_addc_u32")
     assert build.scc_clobber_hazards(SCC_DEAD) == []
+
+
+def test_kernel_source_hash_ignores_comments(tmp_path, monkeypatch):
+    """The hash that gates the committed HBM byte counters changes with the
+    decode kernels' code, not with their comments or blank space."""
+    import bench
+    src = tmp_path / "paper_2504_15299_amd" / "csrc"
+    src.mkdir(parents=True)
+    (src / "internal.h").write_text("int f(int x) { return x; }\n")
+    (src / "ffn_decode.hip").write_text("// a kernel\nint g(int y) {\n  return y + 1;  // add one\n}\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    h0 = bench.kernel_source_hash()
+    (src / "ffn_decode.hip").write_text("/* the kernel */\nint g(int y)   {\n\n  return y + 1;\n}\n")
+    assert bench.kernel_source_hash() == h0
+    (src / "ffn_decode.hip").write_text("int g(int y) { return y + 2; }\n")
+    assert bench.kernel_source_hash() != h0
