@@ -1214,10 +1214,13 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   hipError_t err;
   const int L = w13->b_max - w13->b_min + 1;
   const int npos = T * k;
-  // two column blocks per work item once experts hold more than 4 positions
+  // two column blocks per work item once experts hold more than 7 positions
   // on average (an expert's planes are then streamed once for up to 16 of
-  // its positions instead of once per 8)
-  const int ncb = npos > 4 * E ? 2 : 1;
+  // its positions instead of once per 8).  Below that, streaming the few
+  // experts with more than 8 positions twice costs less than doubling the
+  // MFMAs and scale FMAs per plane for every expert (measured from 20 to 32
+  // tokens at the Mixtral shape).
+  const int ncb = npos > 7 * E ? 2 : 1;
   const int item = ncb * kDecodeCols;
   // work items: each active expert's positions in runs of `item`
   const int ny = (E < npos ? E : npos) + (npos + item - 1) / item;
