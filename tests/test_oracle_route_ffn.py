@@ -162,3 +162,58 @@ def test_shared_expert_adds_with_weight_one():
                           shared=(sh[0], sh[1], 8))
     ysh = O.expert_ffn(sh[0], sh[1], 8, x.astype(np.float64))
     np.testing.assert_allclose(with_sh - base, ysh, rtol=1e-10, atol=1e-15)
+
+
+def _numpy_layer(x, r, c13, c2):
+    """Fig. 1 written out with numpy on the dequantized weights: every token's
+    output is the sum over its k slots of the slot's routing weight times the
+    SwiGLU output of the slot's expert at the slot's bit-width."""
+    T, k = r["topk_idx"].shape
+    f = c2[0].cols
+    out = np.zeros((T, x.shape[1]))
+    for t in range(T):
+        xt = x[t].astype(np.float64)
+        for i in range(k):
+            e, b = int(r["topk_idx"][t, i]), int(r["topk_bits"][t, i])
+            W13, W2 = O.mwq_dequant(c13[e], b), O.mwq_dequant(c2[e], b)
+            a, c = W13[:f] @ xt, W13[f:] @ xt
+            out[t] += r["topk_w"][t, i] * (W2 @ (a / (1 + np.exp(-a)) * c))
+    return out
+
+
+def _check_weighted_combine(k, E, seed):
+    d, f, T = 64, 64, 9
+    codes = [_codes(f, d, 64, seed + e) for e in range(E)]
+    c13, c2 = [c[0] for c in codes], [c[1] for c in codes]
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((T, d)).astype(np.float32)
+    # well separated logits: distinct experts, clearly unequal slot weights
+    logits = rng.permuted(np.tile(np.arange(E, dtype=np.float64) * 0.7, (T, 1)), axis=1)
+    table = rng.choice(np.array([2, 3, 5, 8], np.uint8), size=(T, E))
+    r = O.route_from_logits(logits, k, np.arange(T, dtype=np.int32), table)
+    w = r["topk_w"]
+    assert np.all(np.diff(w, axis=1) < -1e-3), "slot weights must differ"
+    np.testing.assert_allclose(O.moe_layer(x, r, c13, c2), _numpy_layer(x, r, c13, c2),
+                               rtol=1e-11, atol=1e-14)
+
+
+@pytest.mark.parametrize("k,E", [(2, 8), (6, 64)])
+def test_combine_pairs_each_weight_with_its_slot(k, E):
+    """Pin of the weighted combine at k >= 2 (Fig. 1): the layer equals an
+    independent numpy sum of w[t,i] * SwiGLU_{e(t,i), b(t,i)}(x_t) with
+    distinct experts, widths and weights per slot."""
+    _check_weighted_combine(k, E, 300 + k)
+
+
+@pytest.mark.parametrize("k,E", [(2, 8), (6, 64)])
+def test_combine_pin_catches_slot_swap(k, E, monkeypatch):
+    """A combine that pairs w[t,i] with the output of slot k-1-i (planted in
+    the oracle's combine) fails the pin above."""
+    real = O.combine
+
+    def swapped(topk_w, y_slot):
+        return real(np.ascontiguousarray(np.asarray(topk_w)[:, ::-1]), y_slot)
+
+    monkeypatch.setattr(O, "combine", swapped)
+    with pytest.raises(AssertionError):
+        _check_weighted_combine(k, E, 300 + k)
