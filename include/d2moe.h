@@ -9,8 +9,10 @@
  *
  * Conventions for every entry point
  *  - Pointers named as device buffers are caller-owned device memory (HIP);
- *    the library never allocates, frees or keeps them, and keeps no global
- *    state, so calls on different streams are independent.
+ *    the library never allocates, frees or keeps them, so calls on different
+ *    streams are independent.  The one piece of global state is the fixed
+ *    scratch array of d2moe_moe_forward_noalloc (one per GPU, process
+ *    lifetime).
  *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *    All argument checks run on the host before any launch; on failure a
  *    negative status is returned and nothing is launched.  Work after a
@@ -37,8 +39,13 @@ enum {
   D2MOE_EINVAL = -1,        /* bad argument (shape, null pointer, range) */
   D2MOE_EUNSUPPORTED = -2,  /* valid but not implemented (e.g. dtype) */
   D2MOE_EHIP = -3,          /* a HIP launch or runtime call failed */
-  D2MOE_EWORKSPACE = -4     /* workspace missing or smaller than required */
+  D2MOE_EWORKSPACE = -4,    /* workspace missing or smaller than required */
+  D2MOE_ESCRATCH = -5       /* sizes need more than the fixed no-allocation
+                               scratch of d2moe_moe_forward_noalloc */
 };
+
+/* Bytes of the fixed per-GPU scratch array of d2moe_moe_forward_noalloc. */
+#define D2MOE_NOALLOC_SCRATCH_BYTES (32u << 20)
 
 typedef enum { D2MOE_F32 = 0, D2MOE_BF16 = 1 } d2moe_dtype;
 
@@ -222,6 +229,30 @@ d2moe_status d2moe_moe_forward_profiled(const void* x, d2moe_dtype x_dtype, int3
                                         int32_t shared_d_ff, void* out, void* workspace,
                                         size_t ws_bytes, void* stream,
                                         void* const* events);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * MoE layer forward as d2moe_moe_forward, with the workspace taken from a
+ * fixed array of D2MOE_NOALLOC_SCRATCH_BYTES that the library holds on every
+ * GPU it runs on (a static device array, kept until the process ends; its
+ * address is looked up once per device at the first call on it).  The call
+ * allocates nothing; the caller still owns x, the weights, the routing and
+ * out.  Sizes whose workspace (d2moe_moe_forward_workspace) exceeds the
+ * array return D2MOE_ESCRATCH before anything is launched: 32 MiB covers,
+ * for example, decode of up to 64 tokens of the Mixtral-8x7B layer shape.
+ * Every call on one GPU uses that GPU's one array, whatever the stream:
+ * calls that overlap in time on the same GPU race on it and must be ordered
+ * by the caller (one stream, or events).  The kernels need no initialised
+ * workspace, so the array's contents left by a previous call do not matter.
+ */
+d2moe_status d2moe_moe_forward_noalloc(const void* x, d2moe_dtype x_dtype, int32_t T,
+                                       int32_t d, int32_t d_ff, int32_t E, int32_t k,
+                                       const d2moe_mwq* w13, const d2moe_mwq* w2,
+                                       const d2moe_routing* r,
+                                       const d2moe_mwq* shared_w13,
+                                       const d2moe_mwq* shared_w2, int32_t shared_bits,
+                                       int32_t shared_d_ff, void* out, void* stream);
 
 /*
  * Residual update and normalisation between the MoE layers of a decoder

@@ -18,7 +18,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("D2MOE_LIB") or os.path.join(_HERE, "libd2moe.so")
 
 D2MOE_F32, D2MOE_BF16 = 0, 1
-OK, EINVAL, EUNSUPPORTED, EHIP, EWORKSPACE = 0, -1, -2, -3, -4
+OK, EINVAL, EUNSUPPORTED, EHIP, EWORKSPACE, ESCRATCH = 0, -1, -2, -3, -4, -5
+NOALLOC_SCRATCH_BYTES = 32 << 20   # D2MOE_NOALLOC_SCRATCH_BYTES
 
 _P = ctypes.c_void_p
 _I = ctypes.c_int32
@@ -61,11 +62,16 @@ def lib():
                                         ctypes.POINTER(_Mwq), ctypes.POINTER(_Mwq), _I, _I, _P,
                                         _P, ctypes.c_size_t, _P]
         L.d2moe_moe_forward_profiled.argtypes = L.d2moe_moe_forward.argtypes + [_P]
+        L.d2moe_moe_forward_noalloc.argtypes = [_P, _I, _I, _I, _I, _I, _I,
+                                                ctypes.POINTER(_Mwq), ctypes.POINTER(_Mwq),
+                                                ctypes.POINTER(_Routing), ctypes.POINTER(_Mwq),
+                                                ctypes.POINTER(_Mwq), _I, _I, _P, _P]
         L.d2moe_residual_rmsnorm.argtypes = [_P, _P, _I, _I, _I, ctypes.c_float, _P, _I, _P]
         for name in ("d2moe_mwq_size", "d2moe_pack_mwq", "d2moe_debug_unpack", "d2moe_route",
                      "d2moe_route_learned",
                      "d2moe_moe_forward_workspace", "d2moe_moe_forward",
-                     "d2moe_moe_forward_profiled", "d2moe_residual_rmsnorm"):
+                     "d2moe_moe_forward_profiled", "d2moe_moe_forward_noalloc",
+                     "d2moe_residual_rmsnorm"):
             getattr(L, name).restype = _I
         _lib = L
     return _lib
@@ -285,6 +291,30 @@ def moe_forward(x: torch.Tensor, w13: MWQ, w2: MWQ, r: Routing, k: int, shared=N
     return out
 
 
+def moe_forward_noalloc(x: torch.Tensor, w13: MWQ, w2: MWQ, r: Routing, k: int, shared=None,
+                        out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """``d2moe_moe_forward_noalloc``: the forward with the library's fixed
+    per-GPU scratch array as workspace (nothing is allocated by the call;
+    ``out`` is allocated here only when not given)."""
+    T, d = x.shape
+    sw13 = sw2 = None
+    sbits = sff = 0
+    if shared is not None:
+        sw13, sw2, sbits = shared
+        sff = sw2.cols
+    if out is None:
+        out = torch.empty_like(x)
+    c13, c2, cr = w13._c(), w2._c(), r._c()
+    cs13 = ctypes.byref(sw13._c()) if sw13 is not None else None
+    cs2 = ctypes.byref(sw2._c()) if sw2 is not None else None
+    _check("d2moe_moe_forward_noalloc",
+           lib().d2moe_moe_forward_noalloc(_ptr(x), _dtype_code(x), T, d, w2.cols,
+                                           w13.n_experts, k, ctypes.byref(c13),
+                                           ctypes.byref(c2), ctypes.byref(cr), cs13, cs2, sbits,
+                                           sff, _ptr(out), _stream(stream)))
+    return out
+
+
 def residual_rmsnorm(x: torch.Tensor, y: torch.Tensor | None, eps: float = 1e-5,
                      h: torch.Tensor | None = None, h_dtype=torch.bfloat16,
                      stream=None) -> torch.Tensor:
@@ -302,3 +332,4 @@ def residual_rmsnorm(x: torch.Tensor, y: torch.Tensor | None, eps: float = 1e-5,
                                         _dtype_code(y) if y is not None else D2MOE_F32, T, d,
                                         float(eps), _ptr(h), _dtype_code(h), _stream(stream)))
     return h
+

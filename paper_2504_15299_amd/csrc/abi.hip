@@ -1,8 +1,19 @@
 // C ABI of libd2moe: argument validation on the host, then asynchronous
-// launches on the caller's stream.  No allocation, no global state.
+// launches on the caller's stream.  No allocation.  The only global state is
+// the per-device address of the fixed scratch array that the allocation-free
+// forward uses (d2moe_moe_forward_noalloc).
+#include <mutex>
+
 #include "internal.h"
 
 using namespace d2moe;
+
+// Fixed forward workspace for callers that cannot allocate (HIP graph
+// capture, serving loops that forbid hipMalloc).  Each GPU the library runs
+// on holds its own copy until the process ends.  Host code never uses the
+// array's name as an address: its device address is looked up once per
+// device with hipGetSymbolAddress (noalloc_scratch below).
+static __device__ __align__(256) uint8_t scratch[D2MOE_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -21,6 +32,26 @@ bool mwq_ok(const d2moe_mwq* m) {
 
 d2moe_status from_hip(hipError_t e) { return e == hipSuccess ? D2MOE_OK : D2MOE_EHIP; }
 
+// Device address of `scratch` on the current device, looked up at the first
+// call on that device (with that device current) and kept for the process.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+d2moe_status noalloc_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return D2MOE_EHIP;
+  if (dev >= kMaxDevices) return D2MOE_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return D2MOE_EHIP;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return D2MOE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -32,6 +63,7 @@ const char* d2moe_status_string(d2moe_status s) {
     case D2MOE_EUNSUPPORTED: return "unsupported";
     case D2MOE_EHIP: return "HIP error";
     case D2MOE_EWORKSPACE: return "workspace too small";
+    case D2MOE_ESCRATCH: return "sizes need more than the fixed no-allocation scratch";
     default: return "unknown status";
   }
 }
@@ -157,6 +189,27 @@ d2moe_status d2moe_moe_forward(const void* x, d2moe_dtype x_dtype, int32_t T, in
                                void* workspace, size_t ws_bytes, void* stream) {
   return forward_impl(x, x_dtype, T, d, d_ff, E, k, w13, w2, r, shared_w13, shared_w2,
                       shared_bits, shared_d_ff, out, workspace, ws_bytes, stream, nullptr);
+}
+
+d2moe_status d2moe_moe_forward_noalloc(const void* x, d2moe_dtype x_dtype, int32_t T,
+                                       int32_t d, int32_t d_ff, int32_t E, int32_t k,
+                                       const d2moe_mwq* w13, const d2moe_mwq* w2,
+                                       const d2moe_routing* r, const d2moe_mwq* shared_w13,
+                                       const d2moe_mwq* shared_w2, int32_t shared_bits,
+                                       int32_t shared_d_ff, void* out, void* stream) {
+  // the workspace size check comes first so that an oversized call is
+  // reported as such, with nothing launched
+  if (T < 0 || d < 1 || d_ff < 1 || E < 1 || E > 64 || k < 1 || k > E || shared_d_ff < 0)
+    return D2MOE_EINVAL;
+  const bool has_shared = shared_w13 || shared_w2;
+  const size_t need = fwd_workspace_layout(T, d, d_ff, E, k, has_shared ? shared_d_ff : 0).total;
+  if (need > (size_t)D2MOE_NOALLOC_SCRATCH_BYTES) return D2MOE_ESCRATCH;
+  void* ws = nullptr;
+  const d2moe_status st = noalloc_scratch(&ws);
+  if (st != D2MOE_OK) return st;
+  return forward_impl(x, x_dtype, T, d, d_ff, E, k, w13, w2, r, shared_w13, shared_w2,
+                      shared_bits, shared_d_ff, out, ws, (size_t)D2MOE_NOALLOC_SCRATCH_BYTES,
+                      stream, nullptr);
 }
 
 d2moe_status d2moe_moe_forward_profiled(const void* x, d2moe_dtype x_dtype, int32_t T,

@@ -117,3 +117,21 @@ def test_workspace_size_grows_with_tokens():
     b = api.moe_forward_workspace(16, 4096, 14336, 8, 2)
     c = api.moe_forward_workspace(16, 4096, 14336, 8, 2, 5632)
     assert 0 < a < b < c
+
+
+def test_noalloc_forward_refuses_oversized_sizes_on_the_host():
+    """Sizes whose workspace exceeds the fixed scratch array are refused before
+    the library looks up or touches the array (no GPU needed)."""
+    L = api.lib()
+    fake = ctypes.c_void_p(1 << 20)
+    r = api._Routing(*([1 << 20] * 10))
+    w13 = _mwq(n_experts=8, rows=2 * 14336, cols=4096)
+    w2 = _mwq(n_experts=8, rows=4096, cols=14336)
+    assert api.moe_forward_workspace(4096, 4096, 14336, 8, 2) > api.NOALLOC_SCRATCH_BYTES
+    assert L.d2moe_moe_forward_noalloc(fake, 1, 4096, 4096, 14336, 8, 2, ctypes.byref(w13),
+                                       ctypes.byref(w2), ctypes.byref(r), None, None, 0, 0, fake,
+                                       None) == api.ESCRATCH
+    assert L.d2moe_moe_forward_noalloc(fake, 1, 4, 128, 256, 8, 9, ctypes.byref(w13),
+                                       ctypes.byref(w2), ctypes.byref(r), None, None, 0, 0, fake,
+                                       None) == api.EINVAL
+    assert api.status_string(api.ESCRATCH).startswith("sizes need more")
