@@ -64,13 +64,17 @@ def _compile(src: str) -> str:
     obj = os.path.join(OBJ_DIR, src.replace(".hip", ".o"))
     cmd = [_hipcc(), *COMMON, *EXTRA.get(src, []), "-Rpass-analysis=kernel-resource-usage",
            "-c", os.path.join(CSRC, src), "-o", obj]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
-    spills = scratch_users(r.stderr)
-    if spills:
-        raise RuntimeError(f"{src}: kernels use scratch memory (register spills): {spills}")
-    _check_mfma(src)
+    # the device-assembly checks compile the source a second time; run that
+    # compilation alongside the object build
+    with cf.ThreadPoolExecutor(1) as ex:
+        checks = ex.submit(_check_mfma, src)
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
+        spills = scratch_users(r.stderr)
+        if spills:
+            raise RuntimeError(f"{src}: kernels use scratch memory (register spills): {spills}")
+        checks.result()
     return obj
 
 
