@@ -34,6 +34,33 @@ HBM_PEAK_GBPS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
+# The GPU leaves its idle clocks only after some milliseconds of sustained
+# load: at the Mixtral decode step the first 16 steps averaged 0.64 ms, steps
+# 16-31 0.31 ms, 32-47 0.28 ms, and every later block of 16 0.261-0.268 ms.
+# Every timed workload is therefore preceded by its warm-up steps and then by
+# more untimed steps until the GPU has been kept busy for WARM_MS.
+WARM_MS = 100.0
+
+
+def warm(step, warmup, min_ms=WARM_MS):
+    """Untimed warm-up: `warmup` calls of step(i), then further calls in
+    batches of 16 until at least min_ms of wall time has passed with the GPU
+    busy.  Returns the number of calls made (the next step index)."""
+    import torch
+    n = 0
+    for _ in range(warmup):
+        step(n)
+        n += 1
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while (time.perf_counter() - t0) * 1e3 < min_ms:
+        for _ in range(16):
+            step(n)
+            n += 1
+        torch.cuda.synchronize()
+    return n
+
+
 def mwq_bytes(rows, cols, group, b_min, bits):
     """Packed bytes of a b-bit read of one [rows][cols] matrix: b planes,
     the scales of levels <= b and the zeros."""
@@ -50,7 +77,14 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--batch", type=int, default=16)
     ap.add_argument("--layers", type=int, default=8)
-    ap.add_argument("--sweep", default="", help="extra batch sizes reported alongside, e.g. 1,4")
+    ap.add_argument("--sweep", default="1,4",
+                    help="extra batch sizes of the same decode layer reported alongside")
+    ap.add_argument("--tiny-steps", type=int, default=100,
+                    help="also time the tiny layer (d_model 256, d_ff 512, 8 experts top-2, "
+                         "64 fp32 tokens; 0: skip)")
+    ap.add_argument("--ceiling-gib", type=float, default=4.0,
+                    help="size of the plain streaming read that measures this GPU's HBM read "
+                         "ceiling in the same run (0: skip)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--prefill-steps", type=int, default=5,
                     help="also time the 2048-token prefill of the same layers (0: skip)")
@@ -68,6 +102,8 @@ def main():
     ap.add_argument("--graph", action="store_true",
                     help="time replays of one captured HIP graph per layer step instead of "
                          "eager launches")
+    ap.add_argument("--dump-steps", action="store_true",
+                    help="print the per-step times of the main workload to stderr")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 256 MiB device copy three times (reference for "
                          "hardware byte counters)")
@@ -132,22 +168,26 @@ def main():
             api.route(x, Wg, None, k, req, tables[l], b_min, b_max, out=routs[l])
             api.moe_forward(x, w13, w2, routs[l], k, out=out, workspace=ws, events=events)
 
-        for i in range(warmup):
-            step(i)
+        w0 = warm(step, warmup)
         # eager pass: per-kernel durations from HIP events on the launch stream
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
         for row in evs:            # torch creates the HIP event at its first record
             for ev in row:
                 ev.record()
         torch.cuda.synchronize()
-        t_start = torch.cuda.Event(enable_timing=True)
-        t_stop = torch.cuda.Event(enable_timing=True)
+        # one stream marker at every step boundary: per-step durations
+        bounds = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        for ev in bounds:
+            ev.record()
+        torch.cuda.synchronize()
+        t_start, t_stop = bounds[0], bounds[-1]
         t_start.record()
         for i in range(steps):
-            step(warmup + i, evs[i] if profile else None)
-        t_stop.record()
+            step(w0 + i, evs[i] if profile else None)
+            bounds[i + 1].record()
         torch.cuda.synchronize()
         ms_eager = t_start.elapsed_time(t_stop) / steps
+        per_step = np.array([bounds[i].elapsed_time(bounds[i + 1]) for i in range(steps)])
         ms = ms_eager
         if use_graphs:
             # one captured step (route + forward) per rotating layer, replayed
@@ -165,12 +205,10 @@ def main():
                 with torch.cuda.graph(g_):
                     step(l)
                 graphs.append(g_)
-            for i in range(warmup):
-                graphs[i % NL].replay()
-            torch.cuda.synchronize()
+            wg = warm(lambda i: graphs[i % NL].replay(), warmup)
             t_start.record()
             for i in range(steps):
-                graphs[(warmup + i) % NL].replay()
+                graphs[(wg + i) % NL].replay()
             t_stop.record()
             torch.cuda.synchronize()
             ms = t_start.elapsed_time(t_stop) / steps
@@ -180,13 +218,19 @@ def main():
             mb = routs[l].expert_maxbit.cpu().numpy()
             alg13.append(sum(mwq_bytes(2 * f, d, g, b_min, int(b)) for b in mb))
             alg2.append(sum(mwq_bytes(d, f, g, b_min, int(b)) for b in mb))
-        per_step13 = [alg13[(warmup + i) % NL] for i in range(steps)]
-        per_step2 = [alg2[(warmup + i) % NL] for i in range(steps)]
-        res = dict(T=T, ms_per_step=ms, ms_per_step_eager=ms_eager, tokens_per_s=T / (ms * 1e-3),
+        per_step13 = [alg13[(w0 + i) % NL] for i in range(steps)]
+        per_step2 = [alg2[(w0 + i) % NL] for i in range(steps)]
+        res = dict(T=T, warmup_steps_run=w0, ms_per_step=ms, ms_per_step_eager=ms_eager,
+                   tokens_per_s=T / (ms * 1e-3),
                    layer_bytes=float(np.mean([a + b for a, b in zip(per_step13, per_step2)])))
         res["layer_GBps"] = res["layer_bytes"] / (ms * 1e-3) / 1e9
+        res["step_ms_p10_p50_p90"] = [round(float(v), 5) for v in
+                                      np.percentile(per_step, [10, 50, 90])]
+        res["per_step_ms"] = [round(float(v), 4) for v in per_step]
         if profile:
             d13 = np.array([e[0].elapsed_time(e[1]) for e in evs])
+            res["w13_ms_p10_p50_p90"] = [round(float(v), 5) for v in np.percentile(d13, [10, 50, 90])]
+            res["per_step_w13_ms"] = [round(float(v), 4) for v in d13]
             d2 = np.array([e[2].elapsed_time(e[3]) for e in evs])
             res["w13_ms"] = float(d13.mean())
             res["w2_ms"] = float(d2.mean())
@@ -220,8 +264,7 @@ def main():
             api.route(x, Wg, bias, k, req, tables[l], b_min, b_max, out=routs[l])
             api.moe_forward(x, w13, w2, routs[l], k, out=out, workspace=ws, events=events)
 
-        for i in range(warmup):
-            step(i)
+        w0 = warm(step, warmup)
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
         for row in evs:
             for ev in row:
@@ -231,7 +274,7 @@ def main():
         t_stop = torch.cuda.Event(enable_timing=True)
         t_start.record()
         for i in range(steps):
-            step(warmup + i, evs[i])
+            step(w0 + i, evs[i])
         t_stop.record()
         torch.cuda.synchronize()
         ms = t_start.elapsed_time(t_stop) / steps
@@ -239,7 +282,7 @@ def main():
         d2 = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
         flop13 = 2.0 * 2 * d * f * T * k
         flop2 = 2.0 * d * f * T * k
-        hist = routs[(warmup + steps - 1) % NL].hist.cpu().numpy().sum(axis=1)
+        hist = routs[(w0 + steps - 1) % NL].hist.cpu().numpy().sum(axis=1)
         return {"tokens": T, "ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms * 1e-3), 1),
                 "w13_ms": round(d13, 4), "w2_ms": round(d2, 4),
                 "w13_TFLOPs": round(flop13 / (d13 * 1e-3) / 1e12, 1),
@@ -294,14 +337,12 @@ def main():
             api.route(x, Wg, None, kF, None, table, b_min, b_max, out=r)
             api.moe_forward(x, w13, w2, r, kF, shared=(s13, s2, 8), out=out, workspace=ws)
 
-        for i in range(warmup):
-            step(i)
-        torch.cuda.synchronize()
+        w0 = warm(step, warmup)
         t_start = torch.cuda.Event(enable_timing=True)
         t_stop = torch.cuda.Event(enable_timing=True)
         t_start.record()
         for i in range(steps):
-            step(warmup + i)
+            step(w0 + i)
         t_stop.record()
         torch.cuda.synchronize()
         ms = t_start.elapsed_time(t_stop) / steps
@@ -311,7 +352,7 @@ def main():
             byts.append(sum(mwq_bytes(2 * fF, dF, gF, b_min, int(b)) + mwq_bytes(dF, fF, gF, b_min, int(b))
                             for b in mb)
                         + mwq_bytes(2 * fS, dF, gF, b_min, 8) + mwq_bytes(dF, fS, gF, b_min, 8))
-        nbytes = float(np.mean([byts[(warmup + i) % copies] for i in range(steps)]))
+        nbytes = float(np.mean([byts[(w0 + i) % copies] for i in range(steps)]))
         flop = 2.0 * 3 * dF * fF * T * kF + 2.0 * 3 * dF * fS * T
         gbps = nbytes / (ms * 1e-3) / 1e9
         tflops = flop / (ms * 1e-3) / 1e12
@@ -364,7 +405,7 @@ def main():
                 api.residual_rmsnorm(x, y, eps, h=h)
 
         api.residual_rmsnorm(x, None, eps, h=h)
-        decode_step()                      # warm-up step, then restart from x0
+        warm(lambda i: decode_step(), 1)   # warm-up steps, then restart from x0
         x.copy_(x0)
         api.residual_rmsnorm(x, None, eps, h=h)
         torch.cuda.synchronize()
@@ -428,8 +469,7 @@ def main():
             api.route(x, Wg, None, kV, req, tables[i % copies], bmin, bmax, out=r)
             api.moe_forward(x, w13, w2, r, kV, out=out, workspace=ws, events=events)
 
-        for i in range(warmup):
-            step(i)
+        w0 = warm(step, warmup)
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
         for row in evs:
             for ev in row:
@@ -439,13 +479,13 @@ def main():
         t_stop = torch.cuda.Event(enable_timing=True)
         t_start.record()
         for i in range(steps):
-            step(warmup + i, evs[i])
+            step(w0 + i, evs[i])
         t_stop.record()
         torch.cuda.synchronize()
         ms = t_start.elapsed_time(t_stop) / steps
         alg13 = [sum(mwq_bytes(2 * fV, dV, g, bmin, int(b))
                      for b in sets[c][3].expert_maxbit.cpu().numpy()) for c in range(copies)]
-        b13 = float(np.mean([alg13[(warmup + i) % copies] for i in range(steps)]))
+        b13 = float(np.mean([alg13[(w0 + i) % copies] for i in range(steps)]))
         d13 = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
         gbps = b13 / (d13 * 1e-3) / 1e9
         del sets
@@ -491,13 +531,11 @@ def main():
             api.moe_forward(x, w13, w2, r, k, out=out, workspace=ws)
 
         def timed(fn, n):
-            for i in range(warmup):
-                fn(i)
+            w0 = warm(fn, warmup)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            torch.cuda.synchronize()
             a.record()
             for i in range(n):
-                fn(warmup + i)
+                fn(w0 + i)
             b.record()
             torch.cuda.synchronize()
             return a.elapsed_time(b) / n
@@ -514,13 +552,89 @@ def main():
                 "router_share_of_step": round((ms_rl - ms_rt) / ms, 4),
                 "widths_used_last_step": np.bincount(bits, minlength=b_max + 1)[b_min:].tolist()}
 
+    def run_tiny(steps, warmup=10):
+        """The tiny layer: d_model 256, d_ff 512, 8 SwiGLU experts top-2,
+        64 tokens of fp32 activations N(0,1), weights N(0, 0.02) packed with
+        group 64 nested to 8 bits, one request with bits per expert uniform
+        from {2,4,8} (seed 0).  All of its weights fit in the caches, so it
+        carries no roofline claim: route + forward time only."""
+        dT, fT, ET, kT, gT, T = 256, 512, 8, 2, 64, 64
+        rng = np.random.default_rng(0)
+        x = torch.from_numpy(rng.standard_normal((T, dT), dtype=np.float32)).to(dev)
+        w13 = api.MWQ.empty(ET, 2 * fT, dT, gT, b_min, b_max, device=dev)
+        w2 = api.MWQ.empty(ET, dT, fT, gT, b_min, b_max, device=dev)
+        gen.manual_seed(0)
+        api.pack_mwq(torch.randn((ET, 2 * fT, dT), generator=gen, device=dev) * 0.02, w13)
+        api.pack_mwq(torch.randn((ET, dT, fT), generator=gen, device=dev) * 0.02, w2)
+        Wg = torch.randn((ET, dT), generator=gen, device=dev) * 0.02
+        table = torch.from_numpy(rng.choice(np.array([2, 4, 8], np.uint8), size=(1, ET))).to(dev)
+        r = api.Routing.empty(T, ET, kT, b_min, b_max, device=dev)
+        out = torch.empty((T, dT), dtype=torch.float32, device=dev)
+        ws = torch.empty(api.moe_forward_workspace(T, dT, fT, ET, kT), dtype=torch.uint8,
+                         device=dev)
+
+        def step(i):
+            api.route(x, Wg, None, kT, None, table, b_min, b_max, out=r)
+            api.moe_forward(x, w13, w2, r, kT, out=out, workspace=ws)
+
+        w0 = warm(step, warmup)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for i in range(steps):
+            step(w0 + i)
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / steps
+        return {"workload": "tiny MoE layer (d_model 256, d_ff 512, 8 SwiGLU experts top-2, 64 "
+                            "tokens of fp32 activations, group 64, 8-bit nest, bits per expert "
+                            "from {2,4,8}); computed on bf16/fp8-piece operands with fp32 "
+                            "accumulation; cache-resident, no roofline claim",
+                "tokens": T, "ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms * 1e-3), 1)}
+
+    def run_ceiling(gib, reps=10):
+        """This GPU's HBM read ceiling: a plain kernel that streams `gib` GiB
+        once with 16-byte nontemporal loads (d2moe_stream_read), timed with
+        HIP events; best and median of `reps` reads."""
+        n = int(gib * (1 << 30)) // 16 * 16
+        buf = torch.empty(n // 4, dtype=torch.int32, device=dev)
+        buf.fill_(1)
+        best = None
+        for blocks in (1024, 2048, 4096, 8192, 32768):
+            sink = torch.empty(blocks, dtype=torch.int32, device=dev)
+            warm(lambda i: api.stream_read(buf, sink), 1, min_ms=20.0)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+            ev[0].record()
+            for i in range(reps):
+                api.stream_read(buf, sink)
+                ev[i + 1].record()
+            torch.cuda.synchronize()
+            rates = np.array([n / (ev[i].elapsed_time(ev[i + 1]) * 1e-3) / 1e9
+                              for i in range(reps)])
+            if best is None or np.median(rates) > np.median(best[1]):
+                best = (blocks, rates)
+        del buf
+        torch.cuda.empty_cache()
+        blocks, rates = best
+        return {"kernel": f"plain streaming read of {gib:g} GiB, 16-byte nontemporal loads, "
+                          f"{blocks} workgroups of 256 threads (best of 1024-32768)",
+                "best_GBps": round(float(rates.max()), 1),
+                "median_GBps": round(float(np.median(rates)), 1),
+                "median_frac_of_peak": round(float(np.median(rates)) / HBM_PEAK_GBPS, 4)}
+
     main_res = run_batch(args.batch, args.steps, args.warmup, profile=True)
+    if args.dump_steps:
+        print("per-step ms:", main_res["per_step_ms"], file=sys.stderr)
+        print("per-step W1/W3 ms:", main_res["per_step_w13_ms"], file=sys.stderr)
+    for key in ("per_step_ms", "per_step_w13_ms"):
+        main_res.pop(key, None)
     learned = run_learned(args.batch, max(args.steps // 2, 10)) if args.learned else None
     sweep = []
     for T in [int(v) for v in args.sweep.split(",") if v.strip()]:
         r = run_batch(T, max(args.steps // 2, 5), args.warmup, profile=True)
         sweep.append({kk: (round(v, 4) if isinstance(v, float) else v) for kk, v in r.items()})
 
+    ceiling = run_ceiling(args.ceiling_gib) if args.ceiling_gib > 0 else None
+    tiny = run_tiny(args.tiny_steps) if args.tiny_steps > 0 else None
     prefill = run_prefill(args.prefill_steps, 2) if args.prefill_steps > 0 else None
     fine = run_fine(args.fine_steps, 2) if args.fine_steps > 0 else None
     stack_res = run_stack(args.stack_steps) if args.stack_steps > 0 else None
@@ -567,6 +681,8 @@ def main():
                                f"{{.2,.3,.3,.2}}, {NL} rotating layers",
                    "batch": args.batch, "d_model": d, "d_ff": f, "experts": E, "top_k": k,
                    "group": g},
+        "warmup_steps_run": main_res["warmup_steps_run"],
+        "step_ms_p10_p50_p90": main_res["step_ms_p10_p50_p90"],
         "hbm_GBps": round(main_res["layer_GBps"], 1),
         "hbm_frac": round(main_res["layer_GBps"] / HBM_PEAK_GBPS, 4),
         "roofline": {"bound": "hbm", "kernel": "W1/W3 expert kernel",
@@ -575,10 +691,13 @@ def main():
                      "traffic": traffic[0],
                      "traffic_unit": "bytes/launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                      "alg_bytes_per_launch": main_res["w13_bytes"],
-                     "avg_ms": round(main_res["w13_ms"], 5)},
+                     "avg_ms": round(main_res["w13_ms"], 5),
+                     "ms_p10_p50_p90": main_res["w13_ms_p10_p50_p90"],
+                     "stream_read_ceiling": ceiling},
         "w2_kernel": {"achieved": round(main_res["w2_GBps"], 1), "avg_ms": round(main_res["w2_ms"], 5),
                       "traffic": traffic[1]},
         "sweep": sweep,
+        "tiny": tiny,
         "prefill": prefill,
         "fine_grained": fine,
         "stack": stack_res,
@@ -623,12 +742,25 @@ def profiled_traffic():
     return int(kv["traffic_w13_bytes"]), int(kv["traffic_w2_bytes"])
 
 
+def host_cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(d, f, E, k, g, n_tokens=4):
     """The CPU oracle (single thread, as it stands) on a bounded sample of the
     decode workload: n_tokens decode tokens of the same layer shape, one
-    request each with bits per expert from {2,3,4,8}; gate logits, dual
-    routing, each token's selected experts' SwiGLU FFNs from their MWQ codes,
-    combine.  Quantizing the experts is setup and is not timed."""
+    request each with bits per expert from {2,3,4,8}; gate logits and dual
+    routing (timed as `route`), each token's selected experts' SwiGLU FFNs
+    from their MWQ codes and the combine (timed as `forward`).  Quantizing
+    the experts is setup and is not timed.  The process is pinned to one
+    host CPU for the timed part (and unpinned afterwards)."""
     import numpy as np
 
     from oracle import oracle as O
@@ -644,18 +776,31 @@ def cpu_baseline(d, f, E, k, g, n_tokens=4):
     for e in sorted({int(e) for e in route["topk_idx"].ravel()}):
         codes13[e] = O.mwq_quantize((rng.standard_normal((2 * f, d), dtype=np.float32) * 0.02), g)
         codes2[e] = O.mwq_quantize((rng.standard_normal((d, f), dtype=np.float32) * 0.02), g)
-    t0 = time.perf_counter()
-    route = O.route_from_logits(O.gate_logits(x, Wg), k, req, table)
-    for t in range(n_tokens):
-        ys = []
-        for i in range(k):
-            e = int(route["topk_idx"][t, i])
-            ys.append(O.expert_ffn(codes13[e], codes2[e], int(route["topk_bits"][t, i]),
-                                   x[t:t + 1].astype(np.float64))[0])
-        O.combine(route["topk_w"][t:t + 1], np.stack(ys)[None])
-    secs = time.perf_counter() - t0
+    allowed = sorted(os.sched_getaffinity(0))
+    cpu = allowed[0]
+    os.sched_setaffinity(0, {cpu})
+    try:
+        t0 = time.perf_counter()
+        route = O.route_from_logits(O.gate_logits(x, Wg), k, req, table)
+        t1 = time.perf_counter()
+        for t in range(n_tokens):
+            ys = []
+            for i in range(k):
+                e = int(route["topk_idx"][t, i])
+                ys.append(O.expert_ffn(codes13[e], codes2[e], int(route["topk_bits"][t, i]),
+                                       x[t:t + 1].astype(np.float64))[0])
+            O.combine(route["topk_w"][t:t + 1], np.stack(ys)[None])
+        t2 = time.perf_counter()
+    finally:
+        os.sched_setaffinity(0, set(allowed))
+    secs = t2 - t0
+    ncpu = os.cpu_count()
     return {"value": round(n_tokens / secs, 5), "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "seconds": round(secs, 3),
+            "seconds": round(secs, 3), "route_seconds": round(t1 - t0, 4),
+            "forward_seconds": round(t2 - t1, 3),
+            "host": f"oracle on 1 of {ncpu} host cores (pinned to CPU {cpu}; "
+                    f"{len(allowed)} in this process's affinity), {host_cpu_model()}",
+            "host_cores": ncpu, "cpu_model": host_cpu_model(),
             "sample": f"{n_tokens} decode tokens of the same layer shape, one request each "
                       f"(gate, routing, each token's 2 experts' SwiGLU FFNs from MWQ codes at "
                       f"bits from {{2,3,4,8}}, combine); expert quantization untimed"}

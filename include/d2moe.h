@@ -271,6 +271,17 @@ d2moe_status d2moe_residual_rmsnorm(float* x, const void* y, d2moe_dtype y_dtype
                                     int32_t T, int32_t d, float eps, void* h,
                                     d2moe_dtype h_dtype, void* stream);
 
+/*
+ * Measurement helper (not part of the layer): reads `bytes` of device memory
+ * at `buf` once with 16-byte nontemporal loads in a grid-stride loop over
+ * `blocks` workgroups of 256 threads and writes one XOR word per workgroup to
+ * sink (device [blocks] uint32), so that the achieved HBM read rate of the
+ * expert kernels can be set beside the rate a plain streaming read reaches
+ * on the same GPU.  bytes % 16 == 0, buf 16-byte aligned, blocks >= 1.
+ */
+d2moe_status d2moe_stream_read(const void* buf, size_t bytes, uint32_t* sink, int32_t blocks,
+                               void* stream);
+
 #ifdef __cplusplus
 }
 #endif

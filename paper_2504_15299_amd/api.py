@@ -66,12 +66,13 @@ def lib():
                                                 ctypes.POINTER(_Mwq), ctypes.POINTER(_Mwq),
                                                 ctypes.POINTER(_Routing), ctypes.POINTER(_Mwq),
                                                 ctypes.POINTER(_Mwq), _I, _I, _P, _P]
+        L.d2moe_stream_read.argtypes = [_P, ctypes.c_size_t, _P, _I, _P]
         L.d2moe_residual_rmsnorm.argtypes = [_P, _P, _I, _I, _I, ctypes.c_float, _P, _I, _P]
         for name in ("d2moe_mwq_size", "d2moe_pack_mwq", "d2moe_debug_unpack", "d2moe_route",
                      "d2moe_route_learned",
                      "d2moe_moe_forward_workspace", "d2moe_moe_forward",
                      "d2moe_moe_forward_profiled", "d2moe_moe_forward_noalloc",
-                     "d2moe_residual_rmsnorm"):
+                     "d2moe_residual_rmsnorm", "d2moe_stream_read"):
             getattr(L, name).restype = _I
         _lib = L
     return _lib
@@ -333,3 +334,11 @@ def residual_rmsnorm(x: torch.Tensor, y: torch.Tensor | None, eps: float = 1e-5,
                                         float(eps), _ptr(h), _dtype_code(h), _stream(stream)))
     return h
 
+
+def stream_read(buf: torch.Tensor, sink: torch.Tensor, stream=None) -> None:
+    """``d2moe_stream_read``: read all of ``buf`` once (plain HBM read
+    kernel, a measurement helper); ``sink`` is a device int32 tensor with one
+    word per workgroup."""
+    _check("d2moe_stream_read",
+           lib().d2moe_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink),
+                                   sink.numel(), _stream(stream)))

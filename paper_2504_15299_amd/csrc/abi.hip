@@ -236,4 +236,11 @@ d2moe_status d2moe_residual_rmsnorm(float* x, const void* y, d2moe_dtype y_dtype
                                           (hipStream_t)stream));
 }
 
+d2moe_status d2moe_stream_read(const void* buf, size_t bytes, uint32_t* sink, int32_t blocks,
+                               void* stream) {
+  if (!buf || !sink || blocks < 1 || bytes % 16 != 0 || ((uintptr_t)buf & 15u) != 0)
+    return D2MOE_EINVAL;
+  return from_hip(launch_stream_read(buf, bytes, sink, blocks, (hipStream_t)stream));
+}
+
 }  // extern "C"

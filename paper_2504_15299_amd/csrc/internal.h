@@ -102,6 +102,8 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
 FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shared_d_ff);
 
 int norm_max_cols();
+hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, int blocks,
+                              hipStream_t s);
 hipError_t launch_residual_rmsnorm(float* x, const void* y, d2moe_dtype yd, int T, int d,
                                    float eps, void* h, d2moe_dtype hd, hipStream_t s);
 
