@@ -162,16 +162,26 @@ def _basic_blocks(lines: list[str], asm_markers: bool = False) -> list[dict]:
     return blocks
 
 
+_VMEM_PREFIXES = ("global_", "buffer_", "flat_", "scratch_")
+
+
 def untracked_load_hazards(asm: str) -> list[tuple[str, str, str]]:
     """The decode kernels issue their activation loads as inline assembly
     (global_load_dwordx4 under a narrowed EXEC) that the compiler does not
     track: the data lands in the destination registers some time later, when
-    the explicit vmcnt wait covers it.  On every path from such a load, no
-    other instruction may read or write those registers before an MFMA reads
-    them as its B operand (the intended first use, after the covering wait)
-    or an s_waitcnt vmcnt(0): the compiler would be using the registers for
-    another value that the late data can overwrite.  Returns (function,
-    load, offending instruction) triples."""
+    an explicit vmcnt wait covers it.  Vector-memory instructions of a wave
+    complete in order, so a wait `s_waitcnt vmcnt(N)` covers the load once at
+    most N vector-memory instructions were issued after it on the path taken.
+    On every path from such a load, no instruction may read or write its
+    destination registers before the MFMA that consumes them as its B operand
+    (the intended first use) or a covering wait: not another load, tracked or
+    not, that reads them (as its address), nor anything else the compiler put
+    there.  A later load may write them: its data lands after this one's.  (That each consuming MFMA sits behind a covering
+    wait is not proven here: the walk is not path-sensitive, and the branch
+    flags the compiler keeps in scalar registers make infeasible paths that
+    skip the waits.  The wait counts are derived next to the loops that place
+    them and exercised by the parity tests.)  Returns (function, load,
+    offending instruction) triples."""
     bad = []
     for fname, lines in _funcs(asm).items():
         blocks = _basic_blocks(lines)
@@ -182,35 +192,50 @@ def untracked_load_hazards(asm: str) -> list[tuple[str, str, str]]:
                 if not any("s_and_saveexec" in y for y in b["ins"][max(0, ii - 2):ii]):
                     continue
                 dst = _vregs(x.split()[1].rstrip(","))
-                stack, seen = [(bi, ii + 1)], set()
+                stack, seen = [(bi, ii + 1, 0)], set()
                 while stack:
-                    cb, ci = stack.pop()
-                    if (cb, ci) in seen:
+                    cb, ci, after = stack.pop()
+                    if (cb, ci, after) in seen:
                         continue
-                    seen.add((cb, ci))
+                    seen.add((cb, ci, after))
                     stop = False
                     for y in blocks[cb]["ins"][ci:]:
                         op = y.split()[0]
-                        if op == "s_waitcnt" and "vmcnt(0)" in y:
-                            stop = True
-                            break
+                        if op == "s_waitcnt":
+                            m = re.search(r"vmcnt\((\d+)\)", y)
+                            if m and int(m.group(1)) <= after:
+                                stop = True      # the load has landed
+                                break
+                            continue
                         if op.startswith("v_mfma"):
                             ops = [o.strip() for o in y.split(None, 1)[1].split(",")]
                             if _vregs(ops[2].split()[0]) & dst:
-                                stop = True
+                                stop = True      # the consuming MFMA
                                 break
-                        if op == "global_load_dwordx4":
-                            continue
+                        # a later load may write the same registers (its data
+                        # lands after this load's: loads complete in order),
+                        # but none may read them, e.g. as its address
+                        operands = y.split(None, 1)[1] if " " in y else ""
+                        if _is_vector_load(op):
+                            operands = operands.split(",", 1)[1] if "," in operands else ""
                         hit = set()
-                        for t in re.findall(r"v\[\d+:\d+\]|v\d+\b", y):
+                        for t in re.findall(r"v\[\d+:\d+\]|v\d+\b", operands):
                             hit |= _vregs(t)
                         if hit & dst:
                             bad.append((fname, x, y))
                             stop = True
                             break
+                        if op.startswith(_VMEM_PREFIXES):
+                            after = min(after + 1, 64)
                     if not stop:
-                        stack.extend((sb, 0) for sb in blocks[cb]["succ"])
+                        stack.extend((sb, 0, after) for sb in blocks[cb]["succ"])
     return bad
+
+
+def _is_vector_load(op: str) -> bool:
+    """A vector-memory load that writes VGPRs (its first operand)."""
+    return op.startswith(("global_load", "buffer_load", "flat_load", "scratch_load")) and \
+        "_lds" not in op
 
 
 _SCC_READERS = ("s_addc_u32", "s_subb_u32", "s_cselect_", "s_cbranch_scc", "s_cmov_", "s_cmovk_")

@@ -690,17 +690,16 @@ __device__ inline void decode_groups(const WaveCtx<NCB>& c, uint8_t* ring, int g
 // positions), largest bit-width of the expert (0: no work).  Xs: position
 // info words (bit-width, activation scale codes) from the activation prep,
 // padded so that NCB * kDecodeCols words can be read from any position.
-// SwiGLU variant: waves [0, NW/2) stream the W1 row-block, waves [NW/2, NW)
-// the matching W3 row-block, each half splitting the groups; the epilogue
-// combines them through LDS (each wave's partial sums go to its own ring,
-// which is idle by then).  NCB column blocks of 8 tokens share every plane
-// operand (two when experts hold more than 8 positions on average), at 4
-// waves per SIMD for one block and 3 for two.
-template <bool SWIGLU, int NW, int NCB, int BMIN>
+// One W2 row block per workgroup: its NW waves split the groups and combine
+// their partial sums through LDS (each wave's partial sums go to its own
+// ring, which is idle by then).  NCB column blocks of 8 tokens share every
+// plane operand (two when experts hold more than 7 positions on average), at
+// 4 waves per SIMD for one block and 3 for two.
+template <int NW, int NCB, int BMIN>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NCB == 1 ? 4 : 3)))
 void decode_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* __restrict__ Xq,
-                   const uint32_t* __restrict__ Xs, int npos, int f, float* __restrict__ out,
-                   int out_ld, uint32_t* __restrict__ rowmax) {
+                   const uint32_t* __restrict__ Xs, int npos, float* __restrict__ out,
+                   int out_ld) {
   constexpr int kStage = stage_bytes<BMIN>();
   __shared__ __attribute__((aligned(16))) uint8_t ring[NW][kDepth * kStage];
   static_assert(kDepth * kStage >= NCB * 64 * 4 * (int)sizeof(float),
@@ -717,9 +716,8 @@ void decode_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* 
   // group loop in scalar control flow
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int NG = W.cols / G;
-  constexpr int KS = SWIGLU ? NW / 2 : NW;  // waves splitting the groups
-  const int rr = SWIGLU ? wave / KS : 0;
-  const int wk = wave % KS;
+  constexpr int KS = NW;  // waves splitting the groups
+  const int wk = wave;
   const int g0 = wk * NG / KS, g1 = (wk + 1) * NG / KS;
   const int ncol = p1 - p0;
 
@@ -757,8 +755,7 @@ void decode_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* 
     }
   }
 
-  const int rowblock = rr == 0 ? rb : rb + f / 16;
-  const size_t blk0 = W.block(e, rowblock, 0);
+  const size_t blk0 = W.block(e, rb, 0);
   c.pl = (const uint8_t*)(W.planes + W.plane_word(blk0, 0, 0));
   c.sc = (const uint8_t*)(W.scales + W.scale_idx(blk0, 0, 0));
   c.zp = W.zeros + W.zero_idx(blk0, 0);
@@ -795,42 +792,19 @@ void decode_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* 
     red[64 * cb + lane] = float4{acc[cb][0], acc[cb][1], acc[cb][2], acc[cb][3]};
   __syncthreads();
   if (wave != 0) return;
-  constexpr int NRR = SWIGLU ? 2 : 1;
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) {
-    float v[NRR][4];
-#pragma unroll
-    for (int h = 0; h < NRR; ++h) {
-      float4 sum = float4{0.f, 0.f, 0.f, 0.f};
-      for (int w = 0; w < KS; ++w) {
-        const float4 part = ((const float4*)ring[h * KS + w])[64 * cb + lane];
-        sum.x += part.x; sum.y += part.y; sum.z += part.z; sum.w += part.w;
-      }
-      v[h][0] = sum.x + __shfl_xor(sum.x, 1, 64);  // hi + lo pieces
-      v[h][1] = sum.y + __shfl_xor(sum.y, 1, 64);
-      v[h][2] = sum.z + __shfl_xor(sum.z, 1, 64);
-      v[h][3] = sum.w + __shfl_xor(sum.w, 1, 64);
+    float4 sum = float4{0.f, 0.f, 0.f, 0.f};
+    for (int w = 0; w < KS; ++w) {
+      const float4 part = ((const float4*)ring[w])[64 * cb + lane];
+      sum.x += part.x; sum.y += part.y; sum.z += part.z; sum.w += part.w;
     }
-    float o[4];
-    float m = 0.0f;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      o[r] = SWIGLU ? silu(v[0][r]) * v[NRR - 1][r] : v[0][r];
-      m = fmaxf(m, fabsf(o[r]));
-    }
+    const float o0 = sum.x + __shfl_xor(sum.x, 1, 64);  // hi + lo pieces
+    const float o1 = sum.y + __shfl_xor(sum.y, 1, 64);
+    const float o2 = sum.z + __shfl_xor(sum.z, 1, 64);
+    const float o3 = sum.w + __shfl_xor(sum.w, 1, 64);
     if (valid[cb] && piece == 0)
-      *(float4*)(out + (size_t)pos[cb] * out_ld + rb * 16 + 4 * c.q) =
-          float4{o[0], o[1], o[2], o[3]};
-    if (rowmax) {
-      // largest |output| of each position over this row-block, for the scale
-      // of its fp8 pieces: max over this lane's rows, then over the four lanes
-      // (q) of the token; one word per (position, row-block), so the
-      // workgroups of a position never contend for one address
-      m = fmaxf(m, __shfl_xor(m, 16, 64));
-      m = fmaxf(m, __shfl_xor(m, 32, 64));
-      if (valid[cb] && piece == 0 && c.q == 0)
-        rowmax[(size_t)pos[cb] * gridDim.x + rb] = __float_as_uint(m);
-    }
+      *(float4*)(out + (size_t)pos[cb] * out_ld + rb * 16 + 4 * c.q) = float4{o0, o1, o2, o3};
   }
 }
 
@@ -1140,8 +1114,15 @@ hipError_t run_xprep(const TIN* in, int in_ld, const int32_t* perm, int kdiv, in
 
 }  // namespace
 
+// decode13_kernel addresses the second block of a wave (the W3 block of the
+// same rows, or the next W2 row block) as a 32-bit byte offset from the
+// first.  Layers whose offsets do not fit (W1 half of one expert's planes
+// of 2 GB or more, far beyond the paper's models) take the grouped-GEMM path.
 bool decode_path_ok(const d2moe_mwq* w13, const d2moe_mwq* w2, int T) {
-  return T <= kDecodeMaxTokens && w13->group == 128 && w2->group == 128;
+  if (T > kDecodeMaxTokens || w13->group != 128 || w2->group != 128) return false;
+  const size_t w3_off = (size_t)(w13->rows / 2 / 16) * (w13->cols / G) * (size_t)w13->b_max * 256;
+  const size_t w2_off = (size_t)(w2->cols / G) * (size_t)w2->b_max * 256;
+  return w3_off < ((size_t)1 << 31) && w2_off < ((size_t)1 << 31);
 }
 
 // Waves per workgroup: one per SIMD, so that the per-SIMD register budget,
@@ -1162,16 +1143,16 @@ inline void launch_timed(K kernel, dim3 grid, dim3 block, hipStream_t s, hipEven
     kernel<<<grid, block, 0, s>>>(args...);
 }
 
-template <bool SWIGLU, int NCB>
+template <int NCB>
 hipError_t launch_decode_kernel(int b_min, dim3 grid, const MwqView& W, const int32_t* elist,
-                                const uint8_t* Xq, const uint32_t* Xs, int npos, int f,
-                                float* out, int out_ld, uint32_t* rowmax, hipStream_t s,
-                                hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr) {
+                                const uint8_t* Xq, const uint32_t* Xs, int npos, float* out,
+                                int out_ld, hipStream_t s, hipEvent_t ev0 = nullptr,
+                                hipEvent_t ev1 = nullptr) {
   switch (b_min) {
 #define D2MOE_CASE(B)                                                                      \
   case B:                                                                                  \
-    launch_timed(decode_kernel<SWIGLU, kDecodeWaves, NCB, B>, grid, dim3(64 * kDecodeWaves), \
-                 s, ev0, ev1, W, elist, Xq, Xs, npos, f, out, out_ld, rowmax);            \
+    launch_timed(decode_kernel<kDecodeWaves, NCB, B>, grid, dim3(64 * kDecodeWaves), s,    \
+                 ev0, ev1, W, elist, Xq, Xs, npos, out, out_ld);                          \
     break;
     D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
     D2MOE_CASE(7) D2MOE_CASE(8)
@@ -1235,20 +1216,12 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   // the expert kernels record the caller's events themselves (launch_timed)
   const hipEvent_t e0 = events ? events[0] : nullptr, e1 = events ? events[1] : nullptr;
   const hipEvent_t e2 = events ? events[2] : nullptr, e3 = events ? events[3] : nullptr;
-  const dim3 g13(d_ff / 16, ny), g2(d / 16, ny);
+  const dim3 g2(d / 16, ny);
   // W1/W3: each wave streams both matrices' blocks of its rows (one
   // activation load serves both), two waves per row block, each over half of
   // the reduction (the fastest split at every batch measured, 1 to 64).
-  // decode13_kernel addresses the W3 block as a 32-bit byte offset from the
-  // W1 block of the same rows; larger layers fall back to decode_kernel,
-  // whose waves take W1 or W3 blocks.
-  const bool fits = (size_t)(d_ff / 16) * (d / G) * (size_t)w13->b_max * 256 < ((size_t)1 << 31);
-  if (!fits)
-    err = ncb == 1 ? launch_decode_kernel<true, 1>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13,
-                                                   npos, d_ff, b.h32, d_ff, b.hmax, s, e0, e1)
-                   : launch_decode_kernel<true, 2>(w13->b_min, g13, W13, b.elist, b.xq13, b.xs13,
-                                                   npos, d_ff, b.h32, d_ff, b.hmax, s, e0, e1);
-  else if (ncb == 1)
+  // decode_path_ok has checked that the W3 block's 32-bit offset fits.
+  if (ncb == 1)
     err = launch_decode13_kernel<2, 1>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos, d_ff,
                                        b.h32, d_ff, b.hmax, s, e0, e1);
   else
@@ -1266,9 +1239,7 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   // streams in flight and is faster.  The second block's offset is one row
   // block of groups.
   constexpr int kW2Split = 4;
-  const bool pairs2 = (d / 16) % 2 == 0 &&
-                      (long)(d / 32) * ny * kW2Split >= 5120 &&
-                      (size_t)(d_ff / G) * (size_t)w2->b_max * 256 < ((size_t)1 << 31);
+  const bool pairs2 = (d / 16) % 2 == 0 && (long)(d / 32) * ny * kW2Split >= 5120;
   if (pairs2 && ncb == 1)
     err = launch_decode13_kernel<kW2Split, 1, false>(w2->b_min, ny, W2, b.elist, b.xq2, b.xs2,
                                                      npos, d, b.y, d, nullptr, s, e2, e3);
@@ -1276,10 +1247,10 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
     err = launch_decode13_kernel<kW2Split, 2, false>(w2->b_min, ny, W2, b.elist, b.xq2, b.xs2,
                                                      npos, d, b.y, d, nullptr, s, e2, e3);
   else
-    err = ncb == 1 ? launch_decode_kernel<false, 1>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
-                                                    0, b.y, d, nullptr, s, e2, e3)
-                   : launch_decode_kernel<false, 2>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
-                                                    0, b.y, d, nullptr, s, e2, e3);
+    err = ncb == 1 ? launch_decode_kernel<1>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos, b.y,
+                                             d, s, e2, e3)
+                   : launch_decode_kernel<2>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos, b.y,
+                                             d, s, e2, e3);
   if (err != hipSuccess) return err;
   return hipSuccess;
 }

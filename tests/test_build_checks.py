@@ -9,10 +9,13 @@ SAFE = HEAD + """
 \ts_and_saveexec_b64 s[4:5], s[6:7]
 \tglobal_load_dwordx4 v[0:3], v[16:17], off
 \ts_mov_b64 exec, s[4:5]
+\tglobal_load_lds_dwordx4 v[40:41], off
+\tglobal_load_lds_dwordx4 v[42:43], off
 \ts_cbranch_vccnz .LBB0_2
 \tv_mov_b32_e32 v20, v21
+\tglobal_load_lds_dwordx4 v[44:45], off
 .LBB0_2:
-\ts_waitcnt vmcnt(3)
+\ts_waitcnt vmcnt(2)
 \tv_mfma_scale_f32_16x16x128_f8f6f4 v[24:27], v[32:35], v[0:7], 0, v8, v9 op_sel_hi:[0,0,0] cbsz:4
 \tv_mov_b32_e32 v0, 0
 \ts_endpgm
@@ -21,6 +24,13 @@ SAFE = HEAD + """
 # the same listing with a copy through the load's registers on one branch
 # only, before the covering wait: the data can land after the copy
 HAZARD = SAFE.replace("\tv_mov_b32_e32 v20, v21\n", "\tv_readfirstlane_b32 s44, v1\n")
+
+# a compiler-tracked load whose address overlaps the pending one
+TRACKED_OVERLAP = SAFE.replace("\tv_mov_b32_e32 v20, v21\n",
+                               "\tglobal_load_dwordx4 v[20:23], v[2:3], off\n")
+# a later load into the same registers is fine: loads complete in order
+TRACKED_WAW = SAFE.replace("\tv_mov_b32_e32 v20, v21\n",
+                           "\tglobal_load_dwordx4 v[0:3], v[20:21], off\n")
 
 # a use after vmcnt(0) on every path is fine
 AFTER_DRAIN = HEAD + """
@@ -36,12 +46,23 @@ AFTER_DRAIN = HEAD + """
 def test_untracked_load_check_accepts_safe_listing():
     assert build.untracked_load_hazards(SAFE) == []
     assert build.untracked_load_hazards(AFTER_DRAIN) == []
+    # a copy after a covering wait (two DMA instructions issued after the
+    # load on either path, vmcnt(2)) is fine
+    covered = SAFE.replace("\tv_mov_b32_e32 v0, 0\n", "\tv_mov_b32_e32 v50, v1\n")
+    assert build.untracked_load_hazards(covered) == []
 
 
 def test_untracked_load_check_finds_use_on_a_branch():
     bad = build.untracked_load_hazards(HAZARD)
     assert len(bad) == 1
     assert "readfirstlane" in bad[0][2]
+
+
+def test_untracked_load_check_sees_overlapping_tracked_loads():
+    bad = build.untracked_load_hazards(TRACKED_OVERLAP)
+    assert len(bad) == 1
+    assert "v[2:3]" in bad[0][2]
+    assert build.untracked_load_hazards(TRACKED_WAW) == []
 
 
 def test_mfma_overlap_check():

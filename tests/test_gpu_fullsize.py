@@ -18,7 +18,8 @@ import numpy as np
 import pytest
 import torch
 
-from layer_cases import DEV, FWD_TOL, Layer, ambiguous_tokens, logit_error_bound, row_max_abs_rel
+from layer_cases import (DEV, FWD_TOL, Layer, ambiguous_tokens, logit_error_bound,
+                         row_max_abs_rel)
 from oracle import oracle as O
 from paper_2504_15299_amd import api
 from paper_2504_15299_amd import workloads as wl
@@ -192,6 +193,19 @@ def _sampled_full_layer(spec, t0, rows, per_group=None):
     print(f"{spec.name} full size: {len(toks)} tokens, worst row {err.max():.3e}, "
           f"median {np.median(err):.3e}", flush=True)
     assert err.max() <= FWD_TOL
+
+
+@pytest.mark.parametrize("T", [1, 4, 32])
+def test_mixtral_decode_other_batches_full_size_sampled(T):
+    """Decode batches of 1 and 4 tokens (their W2 grids are too small for the
+    row-block-pair kernel: one 4-wave workgroup per W2 row block) and of 32
+    (more than 7 positions per expert: two 8-token column blocks per work
+    item) at the full Mixtral layer: routing on every token, the output on
+    tokens covering every (expert, bit) bucket, 256 of the 4096 columns."""
+    t0 = time.time()
+    s = wl.mixtral_decode(T=T)
+    rows = np.arange(0, s.d, 16) + np.arange(s.d // 16) % 16
+    _sampled_full_layer(s, t0, rows)
 
 
 def test_mixtral_prefill_full_size_sampled():

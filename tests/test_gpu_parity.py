@@ -133,6 +133,38 @@ def test_route_parity(name):
     assert np.all(np.abs(tw[ok] - ref["topk_w"][ok]) <= 2 * bound[ok, None] + 1e-6)
 
 
+@pytest.mark.parametrize("T,d,E,k,R", [(16, 4096, 8, 2, 16), (512, 2048, 64, 6, 1),
+                                       (300, 640, 64, 6, 3)])
+def test_route_exact_arithmetic_every_token(T, d, E, k, R):
+    """Routing bit-exact on every token, exact ties included: integer
+    activations in [-8, 8] and gate weights that are multiples of 1/256 below
+    1/4 in magnitude make every product and every partial sum a multiple of
+    1/256 below 2^13, exact in binary32, so the GPU's fp32 logits equal the
+    oracle's whatever the summation order, and the two sides decide top-k,
+    bit-widths, counts, scan and permutation on identical values (many
+    logits tie exactly; ties go to the lower expert index on both sides)."""
+    rng = np.random.default_rng(T + E)
+    x = rng.integers(-8, 9, (T, d)).astype(np.float32)
+    Wg = (rng.integers(-64, 65, (E, d)) / 256.0).astype(np.float32)
+    Wg[E // 2] = Wg[0]                               # identical rows: exact ties
+    table = rng.choice(np.array([2, 3, 4, 8], np.uint8), size=(R, E))
+    req = rng.integers(0, R, T).astype(np.int32)
+    ref_logits = O.gate_logits(x, Wg)
+    assert np.array_equal(ref_logits, ref_logits.astype(np.float32).astype(np.float64))
+    ref = O.route_from_logits(ref_logits, k, req, table)
+    r = api.route(torch.from_numpy(x).to(DEV).to(torch.bfloat16), torch.from_numpy(Wg).to(DEV),
+                  None, k, torch.from_numpy(req).to(DEV), torch.from_numpy(table).to(DEV))
+    torch.cuda.synchronize()
+    assert np.array_equal(r.logits.cpu().numpy().astype(np.float64), ref_logits)
+    assert np.array_equal(r.topk_idx.cpu().numpy(), ref["topk_idx"])
+    assert np.array_equal(r.topk_bits.cpu().numpy(), ref["topk_bits"])
+    for name in ("hist", "offsets", "perm", "slot_of"):
+        assert np.array_equal(getattr(r, name).cpu().numpy().ravel(),
+                              np.asarray(ref[name]).ravel()), name
+    assert np.array_equal(r.expert_maxbit.cpu().numpy(), ref["maxbit"])
+    assert np.abs(r.topk_w.cpu().numpy() - ref["topk_w"]).max() <= 1e-6
+
+
 def test_route_ties_go_to_lower_index():
     """Duplicated gate rows give exactly equal logits on both sides: the lower
     expert index must win."""
@@ -176,14 +208,18 @@ FWD_SPECS = {
     "prefill_small": wl.scaled(wl.mixtral_prefill(), d=256, f=384, T=600),
     "fine_small": wl.scaled(wl.fine_grained(), d=256, f=128, T=200, shared_f=192),
     # the paper's two nests and its dense-model case, and other nest starts
-    # (decode kernels at b_min 1, 3, 5 and 8; two column blocks at T 24, 40)
+    # (decode kernels at b_min 1, 3, 5 and 8; two 8-token column blocks per
+    # work item once positions exceed 7 per expert: T 40 at top-2 of 8, and
+    # the b_min 1 and 3 cases at T 32)
     "decode_v1_T16": wl.scaled(wl.mixtral_decode_v1(T=16), d=512, f=384),
     "decode_v2_T16": wl.scaled(wl.mixtral_decode_v2(T=16), d=512, f=384),
     "decode_v2_T40": wl.scaled(wl.mixtral_decode_v2(T=40), d=256, f=256),
     "decode_b1_T8": wl.scaled(wl.mixtral_decode(T=8), d=256, f=256, b_min=1, b_max=8,
                               bits_choices=(1, 3, 8), bits_probs=None),
-    "decode_b3_T24": wl.scaled(wl.mixtral_decode(T=24), d=256, f=256, b_min=3, b_max=6,
+    "decode_b3_T32": wl.scaled(wl.mixtral_decode(T=32), d=256, f=256, b_min=3, b_max=6,
                                bits_choices=(3, 4, 6), bits_probs=None),
+    "decode_b1_T32": wl.scaled(wl.mixtral_decode(T=32), d=256, f=256, b_min=1, b_max=5,
+                               bits_choices=(1, 2, 5), bits_probs=None),
     "decode_b8_T4": wl.scaled(wl.mixtral_decode(T=4), d=256, f=256, b_min=8, b_max=8,
                               bits_choices=(8,), bits_probs=None),
     "dense_T16": wl.scaled(wl.dense_decode(T=16), d=512, f=768),
