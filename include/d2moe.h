@@ -75,7 +75,13 @@ typedef struct {
   uint8_t* zeros;
 } d2moe_mwq;
 
-/* Byte sizes of the three packed buffers.  Pure host function. */
+/*
+ * Byte sizes of the three packed buffers (Sec. 3.3.1: one nested tensor per
+ * matrix holds the base codes, one sign plane per further bit and the
+ * per-group scales and zero points of Eq. 2 and Eq. 4-5, so every bit-width
+ * of the ladder is stored once).  Pure host function; returns D2MOE_EINVAL
+ * for shapes or ladders the layout does not allow.
+ */
 d2moe_status d2moe_mwq_size(int32_t n_experts, int32_t rows, int32_t cols,
                             int32_t group, int32_t b_min, int32_t b_max,
                             size_t* planes_bytes, size_t* scales_bytes,
@@ -96,8 +102,10 @@ d2moe_status d2moe_pack_mwq(const void* W, d2moe_dtype w_dtype,
                             const d2moe_mwq* out, void* stream);
 
 /*
- * Test hook: unpack expert `expert` of `w` at bit-width `bits` with the
- * device decoding routine the forward kernels use.
+ * Test hook: unpack expert `expert` of `w` at bit-width `bits` into the
+ * integer codes of Eq. 2 (base code Q_b1) and Eq. 4 (residual signs of the
+ * bit-widths b_min+1 .. bits), with the device decoding routine the forward
+ * kernels use.
  *   q1    device [rows][cols] uint8, base codes;
  *   signs device [bits-b_min][rows][cols] int8 (+1/-1), may be NULL when
  *         bits == b_min.
@@ -175,7 +183,13 @@ d2moe_status d2moe_route_learned(const void* x, d2moe_dtype x_dtype, int32_t T,
                                  float* bit_logits, const d2moe_routing* out,
                                  void* stream);
 
-/* Workspace bytes needed by d2moe_moe_forward for these sizes (host). */
+/*
+ * Workspace bytes needed by d2moe_moe_forward for these sizes (host): the
+ * (expert, bit-width) work lists built from the counts B_{j,k} of Sec. 3.4.3,
+ * the intermediate SwiGLU activations and expert outputs of the routed
+ * (token, expert) pairs of Fig. 1, and the decode path's activation pieces.
+ * shared_d_ff = 0 when there is no shared expert.
+ */
 d2moe_status d2moe_moe_forward_workspace(int32_t T, int32_t d, int32_t d_ff,
                                          int32_t E, int32_t k,
                                          int32_t shared_d_ff, size_t* bytes);
