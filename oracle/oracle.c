@@ -169,6 +169,145 @@ int oracle_mwq_quantize(const float* W, int rows, int cols, int group,
   return 0;
 }
 
+/* ---- calibration-aware MWQ (Sec. 3.3.1, Eq. 3 and Eq. 5 with calibration
+ * activations; Algorithm 1's block compensation) ------------------------
+ *
+ * Algorithm 1 quantizes W block by block (gamma columns at a time) and, as
+ * GPTQ does, moves each block's quantization error onto the columns not yet
+ * quantized, weighted by the inverse Hessian of the calibration inputs; the
+ * text keeps only this block-level compensation and drops GPTQ's
+ * column-by-column corrections inside a block.  With U the upper Cholesky
+ * factor of H^-1, H = 2 X X^T + lambda I (so H^-1 = U^T U), the error D_B of
+ * block B is carried to the later columns F as
+ *     E = D_B U_BB^-1,      T_F <- T_F - E U_BF,
+ * which is the least-squares optimal change of T_F for the error D_B
+ * ((H^-1)_BB^-1 (H^-1)_BF = U_BB^-1 U_BF).
+ * Each bit-width level is one such pass over the blocks, restarting from the
+ * uncompensated quantity of that level, with every lower level fixed:
+ *   level 0 (Eq. 2): T = W, the block's base codes come from the current T_B
+ *     (same per-group rule as oracle_mwq_quantize), D_B = T_B - W^_b1,B;
+ *   level l >= 1 (Eq. 4-5): T = R, the residual W - W^ of the levels below
+ *     (kept as a chain, updated after each level exactly as in
+ *     oracle_mwq_quantize), the block's signs and scales come from the
+ *     current T_B, D_B = T_B - s sigma.
+ * With U diagonal (X = I) no compensation happens and the codes equal
+ * oracle_mwq_quantize's bit for bit.  The integer decisions are taken on
+ * binary32 values, as on the GPU; the compensation is written with fmaf in
+ * ascending index order so that it has one defined rounding sequence. */
+static void base_group(const float* w, int group, int qmax, uint8_t* q,
+                       uint8_t* z_out, uint16_t* s_out, float* what) {
+  float mn = 0.0f, mx = 0.0f;
+  for (int k = 0; k < group; ++k) {
+    if (w[k] < mn) mn = w[k];
+    if (w[k] > mx) mx = w[k];
+  }
+  const float range = mx - mn;
+  uint16_t s_h = oracle_f32_to_f16(range / (float)qmax);
+  float s1 = oracle_f16_to_f32(s_h);
+  if (!(s1 > 0.0f) || isinf(s1)) {
+    s_h = 0x3c00u;
+    s1 = 1.0f;
+  }
+  float zf = rintf(-mn / s1);
+  if (zf < 0.0f) zf = 0.0f;
+  if (zf > (float)qmax) zf = (float)qmax;
+  const int z = (int)zf;
+  *z_out = (uint8_t)z;
+  *s_out = s_h;
+  for (int k = 0; k < group; ++k) {
+    float qf = rintf(w[k] / s1 + (float)z);
+    if (qf < 0.0f) qf = 0.0f;
+    if (qf > (float)qmax) qf = (float)qmax;
+    q[k] = (uint8_t)(int)qf;
+    what[k] = (float)((int)qf - z) * s1;
+  }
+}
+
+int oracle_mwq_quantize_calibrated(const float* W, int rows, int cols, int group,
+                                   int b_min, int b_max, const float* U, int gamma,
+                                   uint8_t* q1, uint8_t* zeros, uint16_t* scales,
+                                   uint8_t* signs, float* targets) {
+  if (!W || !U || !q1 || !zeros || !scales || rows <= 0 || cols <= 0 ||
+      group <= 0 || cols % group != 0 || gamma <= 0 || gamma % group != 0 ||
+      cols % gamma != 0 || !check_ladder(b_min, b_max))
+    return -1;
+  if (b_max > b_min && !signs) return -1;
+  const int ng = cols / group;
+  const int levels = b_max - b_min + 1;
+  const int qmax = (1 << b_min) - 1;
+  float* T = (float*)malloc(sizeof(float) * (size_t)cols);
+  float* R = (float*)malloc(sizeof(float) * (size_t)cols);
+  float* what = (float*)malloc(sizeof(float) * (size_t)cols);
+  float* D = (float*)malloc(sizeof(float) * (size_t)gamma);
+  float* E = (float*)malloc(sizeof(float) * (size_t)gamma);
+  if (!T || !R || !what || !D || !E) {
+    free(T); free(R); free(what); free(D); free(E);
+    return -1;
+  }
+  for (int n = 0; n < rows; ++n) {
+    const float* w = W + (size_t)n * cols;
+    for (int lev = 0; lev < levels; ++lev) {
+      for (int c = 0; c < cols; ++c) T[c] = lev == 0 ? w[c] : R[c];
+      for (int b0 = 0; b0 < cols; b0 += gamma) {
+        if (targets)
+          for (int c = b0; c < b0 + gamma; ++c)
+            targets[((size_t)lev * rows + n) * cols + c] = T[c];
+        /* quantize the block from its current values */
+        for (int G = b0 / group; G < (b0 + gamma) / group; ++G) {
+          const size_t gi = (size_t)n * ng + G;
+          const int c0 = G * group;
+          if (lev == 0) {
+            base_group(T + c0, group, qmax, q1 + (size_t)n * cols + c0, zeros + gi,
+                       scales + gi, what + c0);
+            for (int k = 0; k < group; ++k) D[c0 - b0 + k] = T[c0 + k] - what[c0 + k];
+          } else {
+            float acc = 0.0f;
+            for (int k = 0; k < group; ++k) acc = acc + fabsf(T[c0 + k]);
+            const uint16_t sb_h = oracle_f32_to_f16(acc / (float)group);
+            const float sb = oracle_f16_to_f32(sb_h);
+            scales[(size_t)lev * rows * ng + gi] = sb_h;
+            uint8_t* sg = signs + (size_t)(lev - 1) * rows * cols + (size_t)n * cols + c0;
+            for (int k = 0; k < group; ++k) {
+              const int pos = T[c0 + k] >= 0.0f; /* -0.0 >= 0: sign +1 */
+              sg[k] = (uint8_t)pos;
+              D[c0 - b0 + k] = pos ? (T[c0 + k] - sb) : (T[c0 + k] + sb);
+            }
+          }
+        }
+        /* E = D U_BB^-1 (forward substitution, ascending order) */
+        for (int j = 0; j < gamma; ++j) {
+          float e = D[j];
+          for (int i = 0; i < j; ++i)
+            e = fmaf(-E[i], U[(size_t)(b0 + i) * cols + (b0 + j)], e);
+          E[j] = e / U[(size_t)(b0 + j) * cols + (b0 + j)];
+        }
+        /* T_F -= E U_BF */
+        for (int f = b0 + gamma; f < cols; ++f) {
+          float acc = T[f];
+          for (int j = 0; j < gamma; ++j)
+            acc = fmaf(-E[j], U[(size_t)(b0 + j) * cols + f], acc);
+          T[f] = acc;
+        }
+      }
+      /* the residual chain of the original row after this level's codes */
+      for (int G = 0; G < ng; ++G) {
+        const size_t gi = (size_t)n * ng + G;
+        const int c0 = G * group;
+        if (lev == 0) {
+          for (int k = 0; k < group; ++k) R[c0 + k] = w[c0 + k] - what[c0 + k];
+        } else {
+          const float sb = oracle_f16_to_f32(scales[(size_t)lev * rows * ng + gi]);
+          const uint8_t* sg = signs + (size_t)(lev - 1) * rows * cols + (size_t)n * cols + c0;
+          for (int k = 0; k < group; ++k)
+            R[c0 + k] = sg[k] ? (R[c0 + k] - sb) : (R[c0 + k] + sb);
+        }
+      }
+    }
+  }
+  free(T); free(R); free(what); free(D); free(E);
+  return 0;
+}
+
 /* W^_b = (Q_b1 - z) s_b1 + sum_{levels 1..b-b1} s_l * sigma_l  (exact). */
 int oracle_mwq_dequant(int rows, int cols, int group, int b_min, int b_max,
                        int b, const uint8_t* q1, const uint8_t* zeros,

@@ -48,6 +48,20 @@ int oracle_mwq_quantize(const float* W, int rows, int cols, int group,
                         int b_min, int b_max, uint8_t* q1, uint8_t* zeros,
                         uint16_t* scales, uint8_t* signs, double* resid_sq);
 
+/* Calibration-aware MWQ of one matrix (Sec. 3.3.1, Eq. 3 and Eq. 5 with
+ * calibration activations X; Algorithm 1's block-level error compensation).
+ * U: [cols][cols] binary32, the upper Cholesky factor of (2 X X^T + lambda I)^-1
+ * (upper triangle read); gamma: columns per compensation block, a multiple
+ * of group dividing cols.  Outputs as oracle_mwq_quantize (no resid_sq);
+ * targets (optional) [levels][rows][cols]: the value each column had when
+ * its block was quantized at that level (weights at level 0, residuals of
+ * the lower levels above).  With U diagonal the codes equal
+ * oracle_mwq_quantize's.  Returns 0, or -1 on invalid arguments. */
+int oracle_mwq_quantize_calibrated(const float* W, int rows, int cols, int group,
+                                   int b_min, int b_max, const float* U, int gamma,
+                                   uint8_t* q1, uint8_t* zeros, uint16_t* scales,
+                                   uint8_t* signs, float* targets);
+
 /* Dequantized weights at bit-width b (Eq. 2 and the nested sum under Eq. 5),
  * exact in binary64. */
 int oracle_mwq_dequant(int rows, int cols, int group, int b_min, int b_max,

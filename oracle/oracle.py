@@ -8,6 +8,11 @@ and driven through ctypes, and this module only marshals numpy arrays.
 Every routine follows a passage of the paper (D^2MoE, arXiv 2504.15299):
   * ``mwq_quantize``   -- Sec. 3.3.1, Eq. 2-5, Algorithm 1 read with X = I;
   * ``mwq_dequant``    -- the nested dequantized weight defined under Eq. 5;
+  * ``mwq_hessian`` / ``mwq_inv_chol_upper`` / ``mwq_quantize_calibrated``
+                       -- calibration-aware MWQ: the regularised Hessian of
+                          Algorithm 1, the upper Cholesky factor of its
+                          inverse, and MWQ with Algorithm 1's block-level
+                          error compensation (Eq. 3 and Eq. 5 with X);
   * ``mwq_pack``       -- the canonical bit-plane layout (planes 0..b-1 are a
                           b-bit read; Sec. 3.4 nested reuse of low bit-widths);
   * ``gate_logits`` / ``route_from_logits`` -- dual routing (Fig. 1): top-k
@@ -62,6 +67,7 @@ def _L():
         lib.oracle_round_bf16.restype = ctypes.c_float
         lib.oracle_mwq_quantize.argtypes = [P, I, I, I, I, I, P, P, P, P, P]
         lib.oracle_mwq_dequant.argtypes = [I, I, I, I, I, I, P, P, P, P, P]
+        lib.oracle_mwq_quantize_calibrated.argtypes = [P, I, I, I, I, I, P, I, P, P, P, P, P]
         lib.oracle_mwq_pack.argtypes = [I, I, I, I, I, P, P, P, P, P, P, P]
         lib.oracle_gate_logits.argtypes = [P, I, I, P, P, I, P]
         lib.oracle_route_from_logits.argtypes = [P, I, I, I, P, P, I, I, I, P, P, P, P, P, P, P, P]
@@ -69,6 +75,7 @@ def _L():
         lib.oracle_combine.argtypes = [I, I, I, P, P, P]
         lib.oracle_rmsnorm.argtypes = [I, I, ctypes.c_double, P, P]
         for name in ("oracle_mwq_quantize", "oracle_mwq_dequant", "oracle_mwq_pack",
+                     "oracle_mwq_quantize_calibrated",
                      "oracle_gate_logits", "oracle_route_from_logits", "oracle_expert_ffn",
                      "oracle_combine", "oracle_rmsnorm"):
             getattr(lib, name).restype = ctypes.c_int
@@ -138,6 +145,46 @@ def mwq_quantize(W: np.ndarray, group: int, b_min: int = 2, b_max: int = 8) -> M
                                  _p(scales), _p(signs), _p(resid)), "mwq_quantize")
     return MWQCodes(rows, cols, group, b_min, b_max, q1, zeros, scales,
                     signs[: b_max - b_min], resid)
+
+
+# ---- calibration-aware MWQ (Sec. 3.3.1, Algorithm 1) ---------------------
+
+def mwq_hessian(X: np.ndarray, lam: float) -> np.ndarray:
+    """H = 2 X X^T + lambda I of Algorithm 1, binary64.  X is given as
+    [tokens][features] (the paper's X^T), so H = 2 X^T X + lambda I here."""
+    X = np.asarray(X, dtype=np.float64)
+    return 2.0 * (X.T @ X) + lam * np.eye(X.shape[1])
+
+
+def mwq_inv_chol_upper(H: np.ndarray) -> np.ndarray:
+    """The H^c of Algorithm 1: the upper-triangular Cholesky factor U of
+    H^-1 (H^-1 = U^T U), binary64, from numpy's inverse and Cholesky."""
+    L = np.linalg.cholesky(np.linalg.inv(np.asarray(H, dtype=np.float64)))
+    return np.ascontiguousarray(L.T)
+
+
+def mwq_quantize_calibrated(W: np.ndarray, U: np.ndarray, group: int, gamma: int = 128,
+                            b_min: int = 2, b_max: int = 8, with_targets: bool = False):
+    """MWQ with Algorithm 1's block compensation (oracle.c documents the
+    steps).  U: [cols][cols] upper factor, used in binary32.  Returns the
+    codes, and with ``with_targets`` also the per-level values each column
+    had when its block was quantized ([levels][rows][cols] float32)."""
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    U32 = np.ascontiguousarray(U, dtype=np.float32)
+    rows, cols = W.shape
+    ng = cols // group
+    L = b_max - b_min + 1
+    q1 = np.zeros((rows, cols), np.uint8)
+    zeros = np.zeros((rows, ng), np.uint8)
+    scales = np.zeros((L, rows, ng), np.uint16)
+    signs = np.zeros((max(b_max - b_min, 1), rows, cols), np.uint8)
+    targets = np.zeros((L, rows, cols), np.float32) if with_targets else None
+    _ok(_L().oracle_mwq_quantize_calibrated(_p(W), rows, cols, group, b_min, b_max, _p(U32),
+                                            gamma, _p(q1), _p(zeros), _p(scales), _p(signs),
+                                            _p(targets)), "mwq_quantize_calibrated")
+    c = MWQCodes(rows, cols, group, b_min, b_max, q1, zeros, scales, signs[: b_max - b_min],
+                 None)
+    return (c, targets) if with_targets else c
 
 
 def mwq_dequant(c: MWQCodes, b: int) -> np.ndarray:
