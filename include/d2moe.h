@@ -102,6 +102,49 @@ d2moe_status d2moe_pack_mwq(const void* W, d2moe_dtype w_dtype,
                             const d2moe_mwq* out, void* stream);
 
 /*
+ * Calibration-aware MWQ, step 1 (Algorithm 1, first line): the factor H^c
+ * of the regularised Hessian of the calibration activations,
+ *     H = 2 X X^T + lambda I,   U upper triangular with H^-1 = U^T U,
+ * computed in binary64 (Cholesky factorization of the order-reversed H and
+ * a triangular inverse) and stored rounded to binary32.
+ *   X:  device [tokens][h] float, calibration activations of the matrix's
+ *       input (one row per token; X of the paper is its transpose);
+ *   U:  device [h][h] float, written in full (zeros below the diagonal);
+ *   info: device int32, 0 on success, else the 1-based column at which H
+ *       was found not positive definite (the output is then meaningless);
+ *   workspace: device, at least d2moe_mwq_calib_factor_workspace bytes,
+ *       256-byte aligned.
+ * h % 64 == 0, tokens >= 0, lambda >= 0 (lambda > 0 keeps H definite).
+ */
+d2moe_status d2moe_mwq_calib_factor_workspace(int32_t h, size_t* bytes);
+d2moe_status d2moe_mwq_calib_factor(const float* X, int32_t tokens, int32_t h, double lambda,
+                                    float* U, int32_t* info, void* workspace, size_t ws_bytes,
+                                    void* stream);
+
+/*
+ * Calibration-aware MWQ, step 2 (Sec. 3.3.1, Eq. 3 and Eq. 5 with
+ * calibration activations; Algorithm 1's block-level compensation): quantize
+ * and pack like d2moe_pack_mwq, but column block by column block (`gamma`
+ * columns, 64 or 128, a multiple of the group), moving each block's error
+ * onto the later columns of its row before they are quantized:
+ *     E = D U_BB^-1,   T_F <- T_F - E U_BF,
+ * with D the block's quantization error, U the factor of step 1 (device
+ * [cols][cols] float, upper triangle read) shared by all experts of `out`.
+ * Every bit-width level is one such pass, restarting from the residual of
+ * the levels below, which stay fixed, so lower bit-widths remain prefixes.
+ * The codes follow one defined binary32 operation sequence (fmaf chains in
+ * ascending index order) and equal the CPU definition bit for bit; with a
+ * diagonal U they equal d2moe_pack_mwq's.  W: device [E][rows][cols] float;
+ * workspace: at least d2moe_pack_mwq_calibrated_workspace bytes, 256-byte
+ * aligned.
+ */
+d2moe_status d2moe_pack_mwq_calibrated_workspace(int32_t rows, int32_t cols, int32_t gamma,
+                                                 size_t* bytes);
+d2moe_status d2moe_pack_mwq_calibrated(const void* W, d2moe_dtype w_dtype, const float* U,
+                                       int32_t gamma, const d2moe_mwq* out, void* workspace,
+                                       size_t ws_bytes, void* stream);
+
+/*
  * Test hook: unpack expert `expert` of `w` at bit-width `bits` into the
  * integer codes of Eq. 2 (base code Q_b1) and Eq. 4 (residual signs of the
  * bit-widths b_min+1 .. bits), with the device decoding routine the forward

@@ -52,6 +52,12 @@ def lib():
         L.d2moe_mwq_size.argtypes = [_I, _I, _I, _I, _I, _I, sz, sz, sz]
         L.d2moe_pack_mwq.argtypes = [_P, _I, ctypes.POINTER(_Mwq), _P]
         L.d2moe_debug_unpack.argtypes = [ctypes.POINTER(_Mwq), _I, _I, _P, _P, _P]
+        L.d2moe_mwq_calib_factor_workspace.argtypes = [_I, sz]
+        L.d2moe_mwq_calib_factor.argtypes = [_P, _I, _I, ctypes.c_double, _P, _P, _P,
+                                             ctypes.c_size_t, _P]
+        L.d2moe_pack_mwq_calibrated_workspace.argtypes = [_I, _I, _I, sz]
+        L.d2moe_pack_mwq_calibrated.argtypes = [_P, _I, _P, _I, ctypes.POINTER(_Mwq), _P,
+                                                ctypes.c_size_t, _P]
         L.d2moe_route.argtypes = [_P, _I, _I, _I, _P, _P, _I, _I, _P, _P, _I, _I, _I,
                                   ctypes.POINTER(_Routing), _P]
         L.d2moe_route_learned.argtypes = [_P, _I, _I, _I, _P, _P, _I, _I, _P, _P, _I, _I, _P,
@@ -69,6 +75,8 @@ def lib():
         L.d2moe_stream_read.argtypes = [_P, ctypes.c_size_t, _P, _I, _P]
         L.d2moe_residual_rmsnorm.argtypes = [_P, _P, _I, _I, _I, ctypes.c_float, _P, _I, _P]
         for name in ("d2moe_mwq_size", "d2moe_pack_mwq", "d2moe_debug_unpack", "d2moe_route",
+                     "d2moe_mwq_calib_factor_workspace", "d2moe_mwq_calib_factor",
+                     "d2moe_pack_mwq_calibrated_workspace", "d2moe_pack_mwq_calibrated",
                      "d2moe_route_learned",
                      "d2moe_moe_forward_workspace", "d2moe_moe_forward",
                      "d2moe_moe_forward_profiled", "d2moe_moe_forward_noalloc",
@@ -163,6 +171,38 @@ def pack_mwq(W: torch.Tensor, out: MWQ, stream=None) -> MWQ:
     c = out._c()
     _check("d2moe_pack_mwq", lib().d2moe_pack_mwq(_ptr(W), _dtype_code(W), ctypes.byref(c),
                                                   _stream(stream)))
+    return out
+
+
+def mwq_calib_factor(X: torch.Tensor, lam: float, stream=None):
+    """``d2moe_mwq_calib_factor``: X [tokens][h] float (device) ->
+    (U [h][h] float, info int32 tensor of one element)."""
+    T, h = X.shape
+    n = ctypes.c_size_t()
+    _check("d2moe_mwq_calib_factor_workspace",
+           lib().d2moe_mwq_calib_factor_workspace(h, ctypes.byref(n)))
+    ws = torch.empty(n.value, dtype=torch.uint8, device=X.device)
+    U = torch.empty((h, h), dtype=torch.float32, device=X.device)
+    info = torch.empty(1, dtype=torch.int32, device=X.device)
+    _check("d2moe_mwq_calib_factor",
+           lib().d2moe_mwq_calib_factor(_ptr(X), T, h, float(lam), _ptr(U), _ptr(info), _ptr(ws),
+                                        n.value, _stream(stream)))
+    return U, info
+
+
+def pack_mwq_calibrated(W: torch.Tensor, U: torch.Tensor, gamma: int, out: MWQ,
+                        stream=None) -> MWQ:
+    """``d2moe_pack_mwq_calibrated``: W [n_experts][rows][cols] float and the
+    factor U [cols][cols] float, both on the device."""
+    assert W.is_cuda and W.is_contiguous() and U.is_contiguous()
+    n = ctypes.c_size_t()
+    _check("d2moe_pack_mwq_calibrated_workspace",
+           lib().d2moe_pack_mwq_calibrated_workspace(out.rows, out.cols, gamma, ctypes.byref(n)))
+    ws = torch.empty(n.value, dtype=torch.uint8, device=W.device)
+    c = out._c()
+    _check("d2moe_pack_mwq_calibrated",
+           lib().d2moe_pack_mwq_calibrated(_ptr(W), _dtype_code(W), _ptr(U), gamma,
+                                           ctypes.byref(c), _ptr(ws), n.value, _stream(stream)))
     return out
 
 

@@ -45,7 +45,7 @@ ARCH = "gfx950"
 COMMON = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}", "-I", INCLUDE,
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wno-unused-command-line-argument"]
-EXTRA = {"pack.hip": ["-ffp-contract=off"]}
+EXTRA = {"pack.hip": ["-ffp-contract=off"], "calib.hip": ["-ffp-contract=off"]}
 
 
 def _hipcc() -> str:

@@ -87,6 +87,47 @@ d2moe_status d2moe_pack_mwq(const void* W, d2moe_dtype w_dtype, const d2moe_mwq*
   return from_hip(launch_pack((const float*)W, out, (hipStream_t)stream));
 }
 
+d2moe_status d2moe_mwq_calib_factor_workspace(int32_t h, size_t* bytes) {
+  if (h < 64 || h % 64 != 0 || !bytes) return D2MOE_EINVAL;
+  *bytes = calib_factor_workspace(h);
+  return D2MOE_OK;
+}
+
+d2moe_status d2moe_mwq_calib_factor(const float* X, int32_t tokens, int32_t h, double lambda,
+                                    float* U, int32_t* info, void* workspace, size_t ws_bytes,
+                                    void* stream) {
+  if (h < 64 || h % 64 != 0 || tokens < 0 || !(lambda >= 0.0) || !U || !info ||
+      (tokens > 0 && !X))
+    return D2MOE_EINVAL;
+  if ((long long)tokens * h > (1ll << 40)) return D2MOE_EINVAL;
+  if (!workspace || ws_bytes < calib_factor_workspace(h) || ((uintptr_t)workspace & 255u) != 0)
+    return D2MOE_EWORKSPACE;
+  return from_hip(launch_calib_factor(X, tokens, h, lambda, U, workspace, info,
+                                      (hipStream_t)stream));
+}
+
+d2moe_status d2moe_pack_mwq_calibrated_workspace(int32_t rows, int32_t cols, int32_t gamma,
+                                                 size_t* bytes) {
+  if (rows < 1 || cols < 1 || (gamma != 64 && gamma != 128) || cols % gamma != 0 || !bytes)
+    return D2MOE_EINVAL;
+  *bytes = calib_pack_workspace(rows, cols, gamma);
+  return D2MOE_OK;
+}
+
+d2moe_status d2moe_pack_mwq_calibrated(const void* W, d2moe_dtype w_dtype, const float* U,
+                                       int32_t gamma, const d2moe_mwq* out, void* workspace,
+                                       size_t ws_bytes, void* stream) {
+  if (!W || !U || !mwq_ok(out)) return D2MOE_EINVAL;
+  if (w_dtype != D2MOE_F32) return D2MOE_EUNSUPPORTED;
+  if ((gamma != 64 && gamma != 128) || gamma % out->group != 0 || out->cols % gamma != 0)
+    return D2MOE_EINVAL;
+  if (!workspace || ws_bytes < calib_pack_workspace(out->rows, out->cols, gamma) ||
+      ((uintptr_t)workspace & 255u) != 0)
+    return D2MOE_EWORKSPACE;
+  return from_hip(launch_pack_calibrated((const float*)W, U, gamma, out, workspace,
+                                         (hipStream_t)stream));
+}
+
 d2moe_status d2moe_debug_unpack(const d2moe_mwq* w, int32_t expert, int32_t bits, uint8_t* q1,
                                 int8_t* signs, void* stream) {
   if (!mwq_ok(w) || expert < 0 || expert >= w->n_experts || bits < w->b_min ||

@@ -102,6 +102,12 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
 FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shared_d_ff);
 
 int norm_max_cols();
+size_t calib_factor_workspace(int n);
+hipError_t launch_calib_factor(const float* X, int tokens, int n, double lambda, float* U,
+                               void* ws, int32_t* info, hipStream_t s);
+size_t calib_pack_workspace(int rows, int cols, int gamma);
+hipError_t launch_pack_calibrated(const float* W, const float* U, int gamma,
+                                  const d2moe_mwq* out, void* ws, hipStream_t s);
 hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, int blocks,
                               hipStream_t s);
 hipError_t launch_residual_rmsnorm(float* x, const void* y, d2moe_dtype yd, int T, int d,
