@@ -82,6 +82,9 @@ def main():
     ap.add_argument("--tiny-steps", type=int, default=100,
                     help="also time the tiny layer (d_model 256, d_ff 512, 8 experts top-2, "
                          "64 fp32 tokens; 0: skip)")
+    ap.add_argument("--no-calib", dest="calib", action="store_false",
+                    help="skip timing the calibration-aware MWQ setup (factor and calibrated "
+                         "pack of one Mixtral W1/W3 and W2 expert)")
     ap.add_argument("--ceiling-gib", type=float, default=4.0,
                     help="size of the plain streaming read that measures this GPU's HBM read "
                          "ceiling in the same run (0: skip)")
@@ -621,6 +624,56 @@ def main():
                 "median_GBps": round(float(np.median(rates)), 1),
                 "median_frac_of_peak": round(float(np.median(rates)) / HBM_PEAK_GBPS, 4)}
 
+    def run_calib(tokens=2048, corr=0.8, gamma=128):
+        """Calibration-aware MWQ setup at the Mixtral shapes: the binary64 factor
+        of the regularised Hessian of `tokens` synthetic calibration tokens
+        (AR(1) feature correlation `corr`, lambda 1 % of the mean Hessian
+        diagonal) for the W1/W3 input (4096 features) and the W2 input (14336),
+        and the calibrated pack of one expert of each (blocks of 128 columns,
+        nest 2..8).  Setup work, untimed in the layer step; reported with the
+        binary32 rate of the compensation arithmetic (2 flops per fmaf of
+        E U_BF, summed over levels and blocks) against the chip's fp32 vector
+        peak."""
+        res = {}
+        for name, h, N in (("w13", d, 2 * f), ("w2", f, d)):
+            rng = np.random.default_rng(31 + h)
+            Z = rng.standard_normal((tokens, h), dtype=np.float32)
+            X = np.empty_like(Z)
+            X[:, 0] = Z[:, 0]
+            c2 = np.float32(np.sqrt(1 - corr * corr))
+            for c in range(1, h):
+                X[:, c] = np.float32(corr) * X[:, c - 1] + c2 * Z[:, c]
+            lam = 0.01 * float(np.mean(2.0 * np.sum(X.astype(np.float64) ** 2, axis=0)))
+            Xd = torch.from_numpy(X).to(dev)
+            gen.manual_seed(77_000 + h)
+            W = torch.randn((1, N, h), generator=gen, device=dev) * 0.02
+            m = api.MWQ.empty(1, N, h, g, b_min, b_max, device=dev)
+            api.mwq_calib_factor(Xd[:128], lam)          # first launches, untimed
+            torch.cuda.synchronize()
+            a, b, c_ = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            a.record()
+            U, info = api.mwq_calib_factor(Xd, lam)
+            b.record()
+            api.pack_mwq_calibrated(W, U, gamma, m)
+            c_.record()
+            torch.cuda.synchronize()
+            ms_f, ms_p = a.elapsed_time(b), b.elapsed_time(c_)
+            levels = b_max - b_min + 1
+            flop = 2.0 * N * levels * sum(gamma * (h - b0 - gamma) for b0 in range(0, h, gamma))
+            res[name] = {"rows": N, "cols": h, "factor_ms": round(ms_f, 2),
+                         "factor_ok": int(info.item()) == 0,
+                         "calibrated_pack_ms": round(ms_p, 2),
+                         "compensation_TFLOPs": round(flop / (ms_p * 1e-3) / 1e12, 2),
+                         "fp32_vector_peak_TFLOPs": 157.3,
+                         "frac": round(flop / (ms_p * 1e-3) / 1e12 / 157.3, 4)}
+            del W, U, Xd, m
+            torch.cuda.empty_cache()
+        res["workload"] = (f"calibration-aware MWQ setup, one Mixtral-8x7B-shaped expert's W1/W3 "
+                           f"(28672 x 4096) and W2 (4096 x 14336), {tokens} synthetic calibration "
+                           f"tokens (AR(1) correlation {corr}), blocks of {gamma} columns, group "
+                           f"128, nest 2..8")
+        return res
+
     main_res = run_batch(args.batch, args.steps, args.warmup, profile=True)
     if args.dump_steps:
         print("per-step ms:", main_res["per_step_ms"], file=sys.stderr)
@@ -634,6 +687,7 @@ def main():
         sweep.append({kk: (round(v, 4) if isinstance(v, float) else v) for kk, v in r.items()})
 
     ceiling = run_ceiling(args.ceiling_gib) if args.ceiling_gib > 0 else None
+    calib = run_calib() if args.calib else None
     tiny = run_tiny(args.tiny_steps) if args.tiny_steps > 0 else None
     prefill = run_prefill(args.prefill_steps, 2) if args.prefill_steps > 0 else None
     fine = run_fine(args.fine_steps, 2) if args.fine_steps > 0 else None
@@ -703,6 +757,7 @@ def main():
         "stack": stack_res,
         "variants": variants,
         "learned_router": learned,
+        "calibrated_mwq": calib,
         "cpu_baseline": cpu,
         "pack_seconds": round(pack_s, 2),
     }
