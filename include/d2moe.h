@@ -329,6 +329,88 @@ d2moe_status d2moe_residual_rmsnorm(float* x, const void* y, d2moe_dtype y_dtype
                                     d2moe_dtype h_dtype, void* stream);
 
 /*
+ * Bit-width-aware I/O-compute planning (Sec. 3.4), for weights streamed into
+ * device memory rather than held there.
+ *
+ * One (expert, bit-width) unit of a layer: its computation is the `count`
+ * requests routed to `expert` at `bits`; its load brings the expert's nested
+ * planes (and their scales) from the width already on the device,
+ * `load_from` (0: nothing), up to `load_to` (nothing when equal).
+ */
+typedef struct {
+  int32_t expert, bits, load_from, load_to, count;
+} d2moe_unit;
+
+/*
+ * Hottest-Expert-Bit-First order (Sec. 3.4.3): a queue per expert of its
+ * requested bit-widths, ascending (so lower widths load first and are
+ * reused, constraint 6b); repeatedly the queue head with the largest count
+ * B_{j,k} (ties: the lower expert index) joins the I/O queue.  Host
+ * function.  hist: host [E][L] selection counts (L = b_max - b_min + 1, as
+ * d2moe_route writes them); resident: host [E] widths already on the device
+ * or NULL (none); units: host array of at least E*L entries; *n_units
+ * receives the count.
+ */
+d2moe_status d2moe_hebf_order(const int32_t* hist, int32_t E, int32_t b_min, int32_t b_max,
+                              const uint8_t* resident, d2moe_unit* units, int32_t* n_units);
+
+/* One step of a memory-budget plan: action 0 = free, 1 = load, of `level`
+ * (0: base planes, scale and zero points; l >= 1: residual plane l and its
+ * scales) of `expert` in `layer`. */
+typedef struct {
+  int32_t action, layer, expert, level;
+} d2moe_budget_action;
+
+/*
+ * Memory-budget scheduler (Algorithm 2, Sec. 3.4.1) over one pass of
+ * n_layers layers: for each layer, when the levels it still needs
+ * (want[layer][expert] levels, 0 = unused) do not fit the budget left, the
+ * levels of earlier layers are released, the previous layer first and its
+ * highest levels first, the base level last, until they fit; then the
+ * layer's missing levels are loaded.  Host function.
+ *   level_bytes: host [K] bytes of one expert's level l;
+ *   resident: host [n_layers][E] levels present, updated in place;
+ *   actions: host array of max_actions entries; *n_actions the count
+ *     (D2MOE_EINVAL, with *n_actions the count needed, if it is too small).
+ * A layer that alone exceeds the budget is still loaded (the plan then
+ * overdraws the budget; callers size the budget to at least one layer).
+ */
+d2moe_status d2moe_budget_plan(const uint8_t* want, int32_t n_layers, int32_t E,
+                               const int64_t* level_bytes, int32_t K, int64_t budget,
+                               uint8_t* resident, d2moe_budget_action* actions,
+                               int32_t max_actions, int32_t* n_actions);
+
+/*
+ * The MoE layer forward with the expert weights streamed into device memory
+ * (Sec. 3.4's bit-width-aware I/O-compute pipeline, for models whose
+ * experts are not all resident): the units are executed in the given order
+ * (e.g. from d2moe_hebf_order); each unit's nested delta is copied from the
+ * host copy of the weights into the device copy on `io_stream`, and the
+ * unit's bucket (its requests at its bit-width) is computed on `stream` as
+ * soon as that copy has landed, so that the copy of a later unit overlaps
+ * the computation of an earlier one (events[i] orders unit i).
+ *   host_w13 / host_w2: the weights in host memory (pinned: allocated with
+ *       hipHostMalloc), canonical layout, same shapes as w13 / w2;
+ *   w13 / w2: the device copy (canonical layout) the kernels read;
+ *   resident: host [E], the width each expert's planes already have in the
+ *       device copy (0: none); updated to the widths after the call;
+ *   hist_host: host [E][L], the routing's counts (copied from r->hist);
+ *   units: must load each expert's planes in increasing width starting from
+ *       `resident` and cover every nonempty bucket exactly once
+ *       (D2MOE_EINVAL otherwise); events: n_units created hipEvent_t.
+ * Other arguments as d2moe_moe_forward (no shared expert).  The per-token
+ * arithmetic is that of d2moe_moe_forward's grouped-GEMM path (more than 64
+ * tokens), whatever the batch.  Both streams are the caller's; the call
+ * returns after enqueueing.
+ */
+d2moe_status d2moe_moe_forward_streamed(
+    const void* x, d2moe_dtype x_dtype, int32_t T, int32_t d, int32_t d_ff, int32_t E, int32_t k,
+    const d2moe_mwq* host_w13, const d2moe_mwq* host_w2, const d2moe_mwq* w13,
+    const d2moe_mwq* w2, uint8_t* resident, const d2moe_routing* r, const int32_t* hist_host,
+    const d2moe_unit* units, int32_t n_units, void* out, void* workspace, size_t ws_bytes,
+    void* stream, void* io_stream, void* const* events);
+
+/*
  * Measurement helper (not part of the layer): reads `bytes` of device memory
  * at `buf` once with 16-byte nontemporal loads in a grid-stride loop over
  * `blocks` workgroups of 256 threads and writes one XOR word per workgroup to

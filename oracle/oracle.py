@@ -23,7 +23,10 @@ Every routine follows a passage of the paper (D^2MoE, arXiv 2504.15299):
                           per expert, a probability over the nest's widths,
                           the most probable width used at inference);
   * ``expert_ffn`` / ``combine`` / ``moe_layer`` -- a SwiGLU expert FFN at the
-                          selected bit-width and the weighted combine.
+                          selected bit-width and the weighted combine;
+  * ``hebf_order`` / ``budget_plan`` -- the Hottest-Expert-Bit-First I/O order
+                          of Sec. 3.4.3 and the memory-budget scheduler of
+                          Algorithm 2 (Sec. 3.4.1), host-side planning.
 """
 from __future__ import annotations
 
@@ -377,3 +380,91 @@ def moe_stack(x0: np.ndarray, layers: list, k: int, token_req, bit_table, eps: f
         y = moe_layer(h, route, c13, c2)
         x = x + round_bf16(y.astype(np.float32)).reshape(y.shape).astype(np.float64)
     return x, logits_per_layer
+
+
+# ---- bit-width-aware I/O-compute planning (Sec. 3.4) -----------------------
+
+def hebf_order(B: np.ndarray, b_min: int, resident=None):
+    """Hottest-Expert-Bit-First (Sec. 3.4.3).  B[j][k]: how many requests
+    selected bit-width b_min + k of expert j (the B_{j,k} of the planning
+    problem).  resident[j]: the bit-width whose planes are already on the
+    device (0: none).
+      1. a queue per expert of its requested bit-widths, ascending;
+      2. repeatedly take, among the heads of all queues, the one with the
+         highest count B_{j,k} (ties: lower expert index) and append it to
+         the I/O queue;
+      3. (execution) load the units in that order, computing each once its
+         load is done.
+    A unit is (expert, bit-width, loaded from, loaded to, count): its
+    computation is the requests at that bit-width, and its load brings the
+    expert's planes from the width already present up to the unit's, the
+    nested delta that this width adds to the lower ones (nothing when the
+    width is already present)."""
+    B = np.asarray(B)
+    E, L = B.shape
+    res = [0] * E if resident is None else [int(v) for v in resident]
+    queues = [[b_min + k for k in range(L) if B[j][k] > 0] for j in range(E)]
+    have = list(res)
+    out = []
+    while any(queues):
+        best = None
+        for j in range(E):
+            if not queues[j]:
+                continue
+            c = int(B[j][queues[j][0] - b_min])
+            if best is None or c > best[1]:
+                best = (j, c)
+        j = best[0]
+        b = queues[j].pop(0)
+        frm = have[j]
+        out.append((j, b, frm, max(frm, b), int(B[j][b - b_min])))
+        have[j] = max(frm, b)
+    return out
+
+
+def budget_plan(want, unit_bytes, budget, resident=None):
+    """Memory-budget scheduler of Algorithm 2 (Sec. 3.4.1) over one pass of
+    the layers.  want[j][e]: how many levels layer j's expert e needs (0:
+    unused; a bit-width b is b - b_min + 1 levels);
+    unit_bytes[l]: bytes one expert's level l occupies (level 0: the base
+    planes with their scale and zero points, level l >= 1: one residual
+    plane with its scales); budget: bytes available for expert weights;
+    resident[j][e]: the level count already on the device (0: none).
+    For each layer j: if loading what it needs (the levels above the
+    resident ones) exceeds the free budget, free levels of the layers before
+    it, the previous layer first (j-1, then j-2, ...), highest levels first
+    (one level of every expert of that layer at a time, experts ascending),
+    the base level last, until the load fits; then load.  The layer itself
+    is never freed.  Returns (actions, resident): actions is a list of
+    ("free" | "load", layer, expert, level) in order, resident the final
+    level counts."""
+    want = np.asarray(want)
+    nl, E = want.shape
+    K = len(unit_bytes)
+    res = np.zeros((nl, E), np.int64) if resident is None else np.array(resident, np.int64)
+    used = int(sum(sum(unit_bytes[l] for l in range(res[j][e])) for j in range(nl)
+                   for e in range(E)))
+    free = budget - used
+    actions = []
+    for j in range(nl):
+        need = 0
+        for e in range(E):
+            for l in range(res[j][e], want[j][e]):
+                need += unit_bytes[l]
+        for jj in range(j - 1, -1, -1):
+            if need <= free:
+                break
+            for l in range(K - 1, -1, -1):
+                if need <= free:
+                    break
+                for e in range(E):
+                    if res[jj][e] == l + 1:
+                        actions.append(("free", jj, e, l))
+                        res[jj][e] = l
+                        free += unit_bytes[l]
+        for e in range(E):
+            for l in range(res[j][e], want[j][e]):
+                actions.append(("load", j, e, l))
+                free -= unit_bytes[l]
+            res[j][e] = max(res[j][e], want[j][e])
+    return actions, res

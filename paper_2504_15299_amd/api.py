@@ -30,6 +30,14 @@ class _Mwq(ctypes.Structure):
                 ("b_max", _I), ("planes", _P), ("scales", _P), ("zeros", _P)]
 
 
+class _Unit(ctypes.Structure):
+    _fields_ = [("expert", _I), ("bits", _I), ("load_from", _I), ("load_to", _I), ("count", _I)]
+
+
+class _BudgetAction(ctypes.Structure):
+    _fields_ = [("action", _I), ("layer", _I), ("expert", _I), ("level", _I)]
+
+
 class _Routing(ctypes.Structure):
     _fields_ = [("logits", _P), ("topk_idx", _P), ("topk_w", _P), ("topk_bits", _P),
                 ("hist", _P), ("offsets", _P), ("perm", _P), ("slot_of", _P),
@@ -73,6 +81,12 @@ def lib():
                                                 ctypes.POINTER(_Routing), ctypes.POINTER(_Mwq),
                                                 ctypes.POINTER(_Mwq), _I, _I, _P, _P]
         L.d2moe_stream_read.argtypes = [_P, ctypes.c_size_t, _P, _I, _P]
+        L.d2moe_hebf_order.argtypes = [_P, _I, _I, _I, _P, _P, _P]
+        L.d2moe_budget_plan.argtypes = [_P, _I, _I, _P, _I, ctypes.c_int64, _P, _P, _I, _P]
+        L.d2moe_moe_forward_streamed.argtypes = [
+            _P, _I, _I, _I, _I, _I, _I, ctypes.POINTER(_Mwq), ctypes.POINTER(_Mwq),
+            ctypes.POINTER(_Mwq), ctypes.POINTER(_Mwq), _P, ctypes.POINTER(_Routing), _P, _P, _I,
+            _P, _P, ctypes.c_size_t, _P, _P, _P]
         L.d2moe_residual_rmsnorm.argtypes = [_P, _P, _I, _I, _I, ctypes.c_float, _P, _I, _P]
         for name in ("d2moe_mwq_size", "d2moe_pack_mwq", "d2moe_debug_unpack", "d2moe_route",
                      "d2moe_mwq_calib_factor_workspace", "d2moe_mwq_calib_factor",
@@ -80,7 +94,8 @@ def lib():
                      "d2moe_route_learned",
                      "d2moe_moe_forward_workspace", "d2moe_moe_forward",
                      "d2moe_moe_forward_profiled", "d2moe_moe_forward_noalloc",
-                     "d2moe_residual_rmsnorm", "d2moe_stream_read"):
+                     "d2moe_residual_rmsnorm", "d2moe_stream_read", "d2moe_hebf_order",
+                     "d2moe_budget_plan", "d2moe_moe_forward_streamed"):
             getattr(L, name).restype = _I
         _lib = L
     return _lib
@@ -382,3 +397,76 @@ def stream_read(buf: torch.Tensor, sink: torch.Tensor, stream=None) -> None:
     _check("d2moe_stream_read",
            lib().d2moe_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink),
                                    sink.numel(), _stream(stream)))
+
+
+# ---- streamed weights: HEBF order, memory budget, streamed forward -------------
+
+def hebf_order(hist, b_min=2, b_max=8, resident=None):
+    """``d2moe_hebf_order`` on host arrays: hist [E][L] int -> list of units
+    (expert, bits, load_from, load_to, count) in I/O order."""
+    import numpy as np
+    h = np.ascontiguousarray(hist, dtype=np.int32)
+    E = h.shape[0]
+    res = None if resident is None else np.ascontiguousarray(resident, dtype=np.uint8)
+    units = (_Unit * max(1, h.size))()
+    n = ctypes.c_int32()
+    _check("d2moe_hebf_order",
+           lib().d2moe_hebf_order(h.ctypes.data_as(_P), E, b_min, b_max,
+                                  None if res is None else res.ctypes.data_as(_P), units,
+                                  ctypes.byref(n)))
+    return [(u.expert, u.bits, u.load_from, u.load_to, u.count) for u in units[:n.value]]
+
+
+def budget_plan(want, level_bytes, budget, resident):
+    """``d2moe_budget_plan`` on host arrays: want [n_layers][E] level counts,
+    level_bytes [K], resident [n_layers][E] uint8 (updated in place).
+    Returns the actions as (action, layer, expert, level) tuples."""
+    import numpy as np
+    w = np.ascontiguousarray(want, dtype=np.uint8)
+    lb = np.ascontiguousarray(level_bytes, dtype=np.int64)
+    assert resident.dtype == np.uint8 and resident.flags["C_CONTIGUOUS"]
+    nl, E = w.shape
+    n = ctypes.c_int32()
+    cap = 64
+    while True:
+        acts = (_BudgetAction * cap)()
+        rc = lib().d2moe_budget_plan(w.ctypes.data_as(_P), nl, E, lb.ctypes.data_as(_P), lb.size,
+                                     int(budget), resident.ctypes.data_as(_P), acts, cap,
+                                     ctypes.byref(n))
+        if rc == EINVAL and n.value > cap:
+            cap = n.value
+            continue
+        _check("d2moe_budget_plan", rc)
+        return [(a.action, a.layer, a.expert, a.level) for a in acts[:n.value]]
+
+
+def moe_forward_streamed(x, host_w13: MWQ, host_w2: MWQ, w13: MWQ, w2: MWQ, resident, r: Routing,
+                         k: int, hist_host, units, events, io_stream, out=None, workspace=None,
+                         stream=None):
+    """``d2moe_moe_forward_streamed``: host_w13 / host_w2 hold pinned host
+    tensors, w13 / w2 the device copy; resident is a host uint8 numpy array
+    [E] (updated in place); units as returned by hebf_order; events: one
+    torch.cuda.Event per unit; io_stream: a torch.cuda.Stream."""
+    import numpy as np
+    T, d = x.shape
+    E, d_ff = w13.n_experts, w2.cols
+    if out is None:
+        out = torch.empty_like(x)
+    need = moe_forward_workspace(T, d, d_ff, E, k)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    h = np.ascontiguousarray(hist_host, dtype=np.int32)
+    assert resident.dtype == np.uint8 and resident.flags["C_CONTIGUOUS"]
+    arr_u = (_Unit * max(1, len(units)))(*[_Unit(*u) for u in units])
+    for ev in events:
+        if ev.cuda_event == 0:
+            ev.record(io_stream)          # torch creates the HIP event at its first record
+    arr_e = (ctypes.c_void_p * max(1, len(units)))(*[ev.cuda_event for ev in events])
+    c_h13, c_h2, c13, c2, cr = host_w13._c(), host_w2._c(), w13._c(), w2._c(), r._c()
+    _check("d2moe_moe_forward_streamed",
+           lib().d2moe_moe_forward_streamed(
+               _ptr(x), _dtype_code(x), T, d, d_ff, E, k, ctypes.byref(c_h13), ctypes.byref(c_h2),
+               ctypes.byref(c13), ctypes.byref(c2), resident.ctypes.data_as(_P), ctypes.byref(cr),
+               h.ctypes.data_as(_P), arr_u, len(units), _ptr(out), _ptr(workspace),
+               workspace.numel(), _stream(stream), ctypes.c_void_p(io_stream.cuda_stream), arr_e))
+    return out

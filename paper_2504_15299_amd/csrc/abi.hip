@@ -2,7 +2,9 @@
 // launches on the caller's stream.  No allocation.  The only global state is
 // the per-device address of the fixed scratch array that the allocation-free
 // forward uses (d2moe_moe_forward_noalloc).
+#include <algorithm>
 #include <mutex>
+#include <vector>
 
 #include "internal.h"
 
@@ -282,6 +284,99 @@ d2moe_status d2moe_stream_read(const void* buf, size_t bytes, uint32_t* sink, in
   if (!buf || !sink || blocks < 1 || bytes % 16 != 0 || ((uintptr_t)buf & 15u) != 0)
     return D2MOE_EINVAL;
   return from_hip(launch_stream_read(buf, bytes, sink, blocks, (hipStream_t)stream));
+}
+
+d2moe_status d2moe_moe_forward_streamed(
+    const void* x, d2moe_dtype x_dtype, int32_t T, int32_t d, int32_t d_ff, int32_t E, int32_t k,
+    const d2moe_mwq* host_w13, const d2moe_mwq* host_w2, const d2moe_mwq* w13,
+    const d2moe_mwq* w2, uint8_t* resident, const d2moe_routing* r, const int32_t* hist_host,
+    const d2moe_unit* units, int32_t n_units, void* out, void* workspace, size_t ws_bytes,
+    void* stream, void* io_stream, void* const* events) {
+  if (T < 0 || d < 1 || d_ff < 1 || E < 1 || E > 64 || k < 1 || k > E) return D2MOE_EINVAL;
+  if (x_dtype != D2MOE_F32 && x_dtype != D2MOE_BF16) return D2MOE_EUNSUPPORTED;
+  if (!mwq_ok(w13) || !mwq_ok(w2) || !mwq_ok(host_w13) || !mwq_ok(host_w2) || !r || !resident ||
+      !hist_host || n_units < 0 || (n_units > 0 && (!units || !events)))
+    return D2MOE_EINVAL;
+  if (w13->n_experts != E || w13->rows != 2 * d_ff || w13->cols != d) return D2MOE_EINVAL;
+  if (w2->n_experts != E || w2->rows != d || w2->cols != d_ff) return D2MOE_EINVAL;
+  if (w13->b_min != w2->b_min || w13->b_max != w2->b_max) return D2MOE_EINVAL;
+  for (const d2moe_mwq* hm : {host_w13, host_w2}) {
+    const d2moe_mwq* dm = hm == host_w13 ? w13 : w2;
+    if (hm->n_experts != dm->n_experts || hm->rows != dm->rows || hm->cols != dm->cols ||
+        hm->group != dm->group || hm->b_min != dm->b_min || hm->b_max != dm->b_max)
+      return D2MOE_EINVAL;
+  }
+  if (d_ff % 32 != 0 || d % 64 != 0) return D2MOE_EUNSUPPORTED;
+  if (T > 0 && (!x || !out || !r->topk_w || !r->perm || !r->slot_of)) return D2MOE_EINVAL;
+  const int b_min = w13->b_min, b_max = w13->b_max, L = b_max - b_min + 1;
+  // the units must load each expert's planes in the order they are needed and
+  // compute every nonempty bucket exactly once
+  uint8_t have[64];
+  int seen[64 * 8] = {0};
+  long total = 0;
+  for (int e = 0; e < E; ++e) {
+    if (resident[e] != 0 && (resident[e] < b_min || resident[e] > b_max)) return D2MOE_EINVAL;
+    have[e] = resident[e];
+  }
+  for (int i = 0; i < n_units; ++i) {
+    const d2moe_unit& u = units[i];
+    if (u.expert < 0 || u.expert >= E || u.bits < b_min || u.bits > b_max) return D2MOE_EINVAL;
+    const int want_to = have[u.expert] > u.bits ? have[u.expert] : u.bits;
+    if (u.load_from != have[u.expert] || u.load_to != want_to) return D2MOE_EINVAL;
+    const int bk = u.expert * L + (u.bits - b_min);
+    if (u.count < 1 || u.count != hist_host[bk] || seen[bk]) return D2MOE_EINVAL;
+    seen[bk] = 1;
+    have[u.expert] = (uint8_t)want_to;
+    total += u.count;
+  }
+  for (int i = 0; i < E * L; ++i)
+    if (hist_host[i] < 0 || (hist_host[i] > 0 && !seen[i])) return D2MOE_EINVAL;
+  if (total != (long)T * k) return D2MOE_EINVAL;
+  const size_t need = fwd_workspace_layout(T, d, d_ff, E, k, 0).total;
+  if (T > 0 && (!workspace || ws_bytes < need || ((uintptr_t)workspace & 255u) != 0))
+    return D2MOE_EWORKSPACE;
+  for (int i = 0; i < n_units; ++i)
+    if (!events[i]) return D2MOE_EINVAL;
+  return from_hip(launch_forward_streamed(x, x_dtype, T, d, d_ff, E, k, host_w13, host_w2, w13,
+                                          w2, resident, r, hist_host, units, n_units, out,
+                                          workspace, (hipStream_t)stream, (hipStream_t)io_stream,
+                                          (hipEvent_t const*)events));
+}
+
+d2moe_status d2moe_hebf_order(const int32_t* hist, int32_t E, int32_t b_min, int32_t b_max,
+                              const uint8_t* resident, d2moe_unit* units, int32_t* n_units) {
+  if (!hist || E < 1 || E > 64 || !ladder_ok(b_min, b_max) || !units || !n_units)
+    return D2MOE_EINVAL;
+  if (resident)
+    for (int j = 0; j < E; ++j)
+      if (resident[j] != 0 && (resident[j] < b_min || resident[j] > b_max)) return D2MOE_EINVAL;
+  *n_units = hebf_order(hist, E, b_min, b_max, resident, units);
+  return D2MOE_OK;
+}
+
+d2moe_status d2moe_budget_plan(const uint8_t* want, int32_t n_layers, int32_t E,
+                               const int64_t* level_bytes, int32_t K, int64_t budget,
+                               uint8_t* resident, d2moe_budget_action* actions,
+                               int32_t max_actions, int32_t* n_actions) {
+  if (!want || n_layers < 1 || E < 1 || !level_bytes || K < 1 || K > 8 || !resident ||
+      !n_actions || max_actions < 0 || (max_actions > 0 && !actions))
+    return D2MOE_EINVAL;
+  for (long i = 0; i < (long)n_layers * E; ++i)
+    if (want[i] > K || resident[i] > K) return D2MOE_EINVAL;
+  for (int l = 0; l < K; ++l)
+    if (level_bytes[l] < 0) return D2MOE_EINVAL;
+  // plan on a copy, so that a too-small action array leaves the caller's
+  // residency untouched
+  std::vector<uint8_t> res(resident, resident + (size_t)n_layers * E);
+  const int n = budget_plan(want, n_layers, E, level_bytes, K, budget, res.data(), actions,
+                            max_actions);
+  if (n < 0) {
+    *n_actions = -n - 1;
+    return D2MOE_EINVAL;
+  }
+  std::copy(res.begin(), res.end(), resident);
+  *n_actions = n;
+  return D2MOE_OK;
 }
 
 }  // extern "C"

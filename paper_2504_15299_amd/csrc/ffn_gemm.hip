@@ -611,6 +611,51 @@ __global__ void combine_kernel(const float* __restrict__ y, const float* __restr
     out[(size_t)t * d + c] = acc;
 }
 
+// Chunk table of one (expert, bit-width) bucket: positions m_first .. +cnt
+// in chunks of at most kChunk (the streamed forward computes one bucket per
+// launch pair).
+__global__ void unit_chunks_kernel(int m_first, int cnt, int bits, int expert, int n_ub,
+                                   int32_t* __restrict__ chunks) {
+  for (int c = threadIdx.x; c < n_ub; c += blockDim.x) {
+    const int m0 = c * kChunk;
+    chunks[4 * c] = m_first + m0;
+    chunks[4 * c + 1] = m0 < cnt ? min(kChunk, cnt - m0) : 0;
+    chunks[4 * c + 2] = bits;
+    chunks[4 * c + 3] = expert;
+  }
+}
+
+// Copy the nested delta of expert e from host to device memory: planes
+// [from, to) (the bit-widths' planes; from = 0: nothing present), the scale
+// levels they add, and the zero points with the first load.  Both buffers are
+// in the canonical tiled layout, so every copy is one strided rectangle (one
+// row per (row block, group) block).
+hipError_t copy_delta(const d2moe_mwq* hm, const d2moe_mwq* dm, int e, int from, int to,
+                      hipStream_t io) {
+  if (to <= from) return hipSuccess;
+  const int BR = 2048 / dm->group, KB = dm->cols / dm->group;
+  const size_t nblk = (size_t)(dm->rows / BR) * KB;
+  const int levels = dm->b_max - dm->b_min + 1;
+  const int p0 = from, p1 = to;
+  const size_t ppitch = (size_t)dm->b_max * 256;
+  const size_t poff = (size_t)e * nblk * ppitch + (size_t)p0 * 256;
+  hipError_t err = hipMemcpy2DAsync((char*)dm->planes + poff, ppitch, (const char*)hm->planes + poff,
+                                    ppitch, (size_t)(p1 - p0) * 256, nblk,
+                                    hipMemcpyHostToDevice, io);
+  if (err != hipSuccess) return err;
+  const int l0 = from == 0 ? 0 : from - dm->b_min + 1, l1 = to - dm->b_min + 1;
+  const size_t spitch = (size_t)levels * BR * 2;
+  const size_t soff = (size_t)e * nblk * spitch + (size_t)l0 * BR * 2;
+  err = hipMemcpy2DAsync((char*)dm->scales + soff, spitch, (const char*)hm->scales + soff, spitch,
+                         (size_t)(l1 - l0) * BR * 2, nblk, hipMemcpyHostToDevice, io);
+  if (err != hipSuccess) return err;
+  if (from == 0) {
+    const size_t zoff = (size_t)e * nblk * BR;
+    err = hipMemcpyAsync(dm->zeros + zoff, hm->zeros + zoff, nblk * BR, hipMemcpyHostToDevice, io);
+  }
+  return err;
+}
+
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 // Chunk-table bound for n positions in nb buckets: every nonempty bucket
@@ -708,6 +753,69 @@ FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shar
   L.hmax_off = off;   off += align256(nd * ((size_t)(d_ff + 15) / 16) * sizeof(uint32_t));
   L.total = off;
   return L;
+}
+
+// The layer with its expert weights streamed in (Sec. 3.4): units in the
+// given order; each unit's nested delta is copied on `io`, and the unit's
+// bucket is computed on `s` once that copy has landed (an event per unit), so
+// the copy of the next unit overlaps the computation of this one.  The
+// per-position arithmetic is that of the grouped GEMM path of
+// launch_forward (same chunking of a bucket, same narrow/wide split).
+hipError_t launch_forward_streamed(const void* x, d2moe_dtype xd, int T, int d, int d_ff, int E,
+                                   int k, const d2moe_mwq* hw13, const d2moe_mwq* hw2,
+                                   const d2moe_mwq* w13, const d2moe_mwq* w2, uint8_t* resident,
+                                   const d2moe_routing* r, const int32_t* hist_host,
+                                   const d2moe_unit* units, int n_units, void* out, void* ws,
+                                   hipStream_t s, hipStream_t io, const hipEvent_t* events) {
+  const FwdWorkspace L = fwd_workspace_layout(T, d, d_ff, E, k, 0);
+  char* base = (char*)ws;
+  const int Lv = w13->b_max - w13->b_min + 1, b_min = w13->b_min;
+  int32_t* chunks = (int32_t*)(base + L.sched_off);
+  uint16_t* h = (uint16_t*)(base + L.h_off);
+  float* y = (float*)(base + L.y_off);
+  hipError_t err;
+  const uint16_t* xb = (const uint16_t*)x;
+  if (T > 0 && xd == D2MOE_F32) {
+    uint16_t* xw = (uint16_t*)(base + L.xb_off);
+    const size_t n = (size_t)T * d;
+    to_bf16_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>((const float*)x, n, xw);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    xb = xw;
+  }
+  // bucket offsets from the host counts (exclusive scan, expert major)
+  int off[64 * 8 + 1];
+  off[0] = 0;
+  for (int i = 0; i < E * Lv; ++i) off[i + 1] = off[i] + hist_host[i];
+  const MwqView W13 = view_of(w13), W2 = view_of(w2);
+  const bool split = (long)T * k <= 64L * E;
+  for (int i = 0; i < n_units; ++i) {
+    const d2moe_unit& u = units[i];
+    if ((err = copy_delta(hw13, w13, u.expert, u.load_from, u.load_to, io)) != hipSuccess)
+      return err;
+    if ((err = copy_delta(hw2, w2, u.expert, u.load_from, u.load_to, io)) != hipSuccess)
+      return err;
+    if ((err = hipEventRecord(events[i], io)) != hipSuccess) return err;
+    if ((err = hipStreamWaitEvent(s, events[i], 0)) != hipSuccess) return err;
+    if (resident[u.expert] < u.load_to) resident[u.expert] = (uint8_t)u.load_to;
+    if (u.count <= 0) continue;
+    const int m_first = off[u.expert * Lv + (u.bits - b_min)];
+    const int n_ub = (u.count + kChunk - 1) / kChunk;
+    unit_chunks_kernel<<<1, 64, 0, s>>>(m_first, u.count, u.bits, u.expert, n_ub, chunks);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    err = run_gemm<true>(xb, d, r->perm, k, W13, chunks, n_ub, d_ff, h, d_ff, split, s);
+    if (err != hipSuccess) return err;
+    err = run_gemm<false>(h, d_ff, nullptr, 1, W2, chunks, n_ub, d_ff, y, d, split, s);
+    if (err != hipSuccess) return err;
+  }
+  if (T == 0) return hipSuccess;
+  dim3 cg((d + 255) / 256, T);
+  if (xd == D2MOE_BF16)
+    combine_kernel<uint16_t><<<cg, 256, 0, s>>>(y, nullptr, 1, 0, r->topk_w, r->slot_of, k, d,
+                                                (uint16_t*)out);
+  else
+    combine_kernel<float><<<cg, 256, 0, s>>>(y, nullptr, 1, 0, r->topk_w, r->slot_of, k, d,
+                                             (float*)out);
+  return hipGetLastError();
 }
 
 hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff, int E, int k,

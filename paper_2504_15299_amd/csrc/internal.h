@@ -101,7 +101,17 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
                              const DecodeBuffers& b, hipStream_t s, const hipEvent_t* events);
 FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shared_d_ff);
 
+hipError_t launch_forward_streamed(const void* x, d2moe_dtype xd, int T, int d, int d_ff, int E,
+                                   int k, const d2moe_mwq* hw13, const d2moe_mwq* hw2,
+                                   const d2moe_mwq* w13, const d2moe_mwq* w2, uint8_t* resident,
+                                   const d2moe_routing* r, const int32_t* hist_host,
+                                   const d2moe_unit* units, int n_units, void* out, void* ws,
+                                   hipStream_t s, hipStream_t io, const hipEvent_t* events);
 int norm_max_cols();
+int hebf_order(const int32_t* hist, int E, int b_min, int b_max, const uint8_t* resident,
+               d2moe_unit* units);
+int budget_plan(const uint8_t* want, int n_layers, int E, const int64_t* level_bytes, int K,
+                int64_t budget, uint8_t* res, d2moe_budget_action* actions, int max_actions);
 size_t calib_factor_workspace(int n);
 hipError_t launch_calib_factor(const float* X, int tokens, int n, double lambda, float* U,
                                void* ws, int32_t* info, hipStream_t s);

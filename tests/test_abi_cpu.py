@@ -135,3 +135,65 @@ def test_noalloc_forward_refuses_oversized_sizes_on_the_host():
                                        ctypes.byref(w2), ctypes.byref(r), None, None, 0, 0, fake,
                                        None) == api.EINVAL
     assert api.status_string(api.ESCRATCH).startswith("sizes need more")
+
+
+def test_planners_match_oracle():
+    """d2moe_hebf_order and d2moe_budget_plan (host C++) against the oracle's
+    plain implementations of Sec. 3.4.3 and Algorithm 2, on random counts
+    with ties, partly resident experts and budgets from tight to loose."""
+    import numpy as np
+
+    from oracle import oracle as O
+    rng = np.random.default_rng(0)
+    for _ in range(300):
+        E, L = int(rng.integers(1, 65)), int(rng.integers(1, 8))
+        b_min = int(rng.integers(1, 9 - L + 1)) if L < 8 else 1
+        B = rng.integers(0, 4, (E, L))
+        B[rng.random((E, L)) < 0.5] = 0
+        res = np.array([0 if rng.random() < 0.5 else int(rng.integers(b_min, b_min + L))
+                        for _ in range(E)], np.uint8)
+        assert api.hebf_order(B, b_min, b_min + L - 1, res) == O.hebf_order(B, b_min, res)
+        nl, K = int(rng.integers(1, 6)), int(rng.integers(1, 9))
+        want = rng.integers(0, K + 1, (nl, min(E, 8))).astype(np.uint8)
+        lb = rng.integers(1, 100, K)
+        resi = rng.integers(0, K + 1, want.shape).astype(np.uint8)
+        budget = int(rng.integers(0, 4000))
+        acts, fin = O.budget_plan(want, lb, budget, resi)
+        got_res = resi.copy()
+        got = api.budget_plan(want, lb, budget, got_res)
+        assert got == [(0 if a[0] == "free" else 1,) + tuple(a[1:]) for a in acts]
+        assert np.array_equal(got_res, fin)
+
+
+def test_streamed_forward_validates_units_on_the_host():
+    """Unit sequences that would compute a bucket before its planes are
+    loaded, skip or repeat a bucket, or disagree with the counts are refused
+    before anything is launched (the pointers are fake)."""
+    import numpy as np
+    L = api.lib()
+    fake = ctypes.c_void_p(1 << 20)
+    E, k, T, d, f = 4, 2, 3, 128, 256
+    w13 = _mwq(n_experts=E, rows=2 * f, cols=d)
+    w2 = _mwq(n_experts=E, rows=d, cols=f)
+    r = api._Routing(*([1 << 20] * 10))
+    hist = np.zeros((E, 7), np.int32)
+    hist[0, 0], hist[1, 2], hist[3, 6] = 2, 3, 1           # (0,2) x2, (1,4) x3, (3,8) x1
+    good = api.hebf_order(hist, 2, 8)
+    assert good == [(1, 4, 0, 4, 3), (0, 2, 0, 2, 2), (3, 8, 0, 8, 1)]
+
+    def call(units, resident=None):
+        res = np.zeros(E, np.uint8) if resident is None else np.array(resident, np.uint8)
+        arr = (api._Unit * len(units))(*[api._Unit(*u) for u in units])
+        ev = (ctypes.c_void_p * len(units))(*([fake] * len(units)))
+        return L.d2moe_moe_forward_streamed(
+            fake, 1, T, d, f, E, k, ctypes.byref(w13), ctypes.byref(w2), ctypes.byref(w13),
+            ctypes.byref(w2), res.ctypes.data_as(ctypes.c_void_p), ctypes.byref(r),
+            hist.ctypes.data_as(ctypes.c_void_p), arr, len(units), fake, None, 0, None, None, ev)
+
+    assert call(good) == api.EWORKSPACE                    # valid units; no workspace given
+    assert call(good[:2]) == api.EINVAL                    # bucket (3, 8) never computed
+    assert call(good + [good[0]]) == api.EINVAL            # bucket computed twice
+    assert call([(1, 4, 0, 3, 3)] + good[1:]) == api.EINVAL    # loads too few planes
+    assert call([(1, 4, 2, 4, 3)] + good[1:]) == api.EINVAL    # assumes planes not present
+    assert call([(1, 4, 0, 4, 2)] + good[1:]) == api.EINVAL    # count disagrees with hist
+    assert call([(1, 4, 5, 5, 3)] + good[1:], [0, 5, 0, 0]) == api.EWORKSPACE  # resident
