@@ -85,6 +85,9 @@ def main():
     ap.add_argument("--no-calib", dest="calib", action="store_false",
                     help="skip timing the calibration-aware MWQ setup (factor and calibrated "
                          "pack of one Mixtral W1/W3 and W2 expert)")
+    ap.add_argument("--stream-steps", type=int, default=3,
+                    help="also time the Mixtral decode layer with its experts streamed from "
+                         "pinned host memory, HEBF against ascending unit order (0: skip)")
     ap.add_argument("--ceiling-gib", type=float, default=4.0,
                     help="size of the plain streaming read that measures this GPU's HBM read "
                          "ceiling in the same run (0: skip)")
@@ -674,6 +677,91 @@ def main():
                            f"128, nest 2..8")
         return res
 
+    def run_streamed(steps, T=16):
+        """One Mixtral-8x7B-shaped layer (8-bit nest, group 128) whose packed
+        experts live in pinned host memory and are streamed into a device copy
+        for each step (the device copy starts empty every step, as when the
+        layer does not stay resident), batch T, bits from {2,3,4,8}: the
+        units of the step in HEBF order and in ascending expert order
+        (Sec. 3.4.3, Fig. 9), each unit's nested delta copied on an I/O
+        stream and its bucket computed when it lands.  Reported with the
+        bytes copied and the rate of a plain pinned host-to-device copy of
+        the same size measured in the same run."""
+        w13, w2, Wg = layers[0]
+
+        def pin(t):
+            h_ = torch.empty(t.shape, dtype=t.dtype, pin_memory=True)
+            h_.copy_(t)
+            return h_
+
+        def host_copy(m):
+            return api.MWQ(m.n_experts, m.rows, m.cols, m.group, m.b_min, m.b_max,
+                           pin(m.planes), pin(m.scales), pin(m.zeros))
+
+        h13, h2 = host_copy(w13), host_copy(w2)
+        d13 = api.MWQ.empty(E, 2 * f, d, g, b_min, b_max, device=dev)
+        d2 = api.MWQ.empty(E, d, f, g, b_min, b_max, device=dev)
+        rng = np.random.default_rng(41)
+        x = torch.from_numpy(rng.standard_normal((T, d), dtype=np.float32)).to(dev).to(torch.bfloat16)
+        req = torch.arange(T, dtype=torch.int32, device=dev)
+        table = torch.from_numpy(rng.choice(np.array([2, 3, 4, 8], np.uint8), size=(T, E),
+                                            p=[0.2, 0.3, 0.3, 0.2])).to(dev)
+        r = api.route(x, Wg, None, k, req, table, b_min, b_max)
+        hist = r.hist.cpu().numpy()
+        io = torch.cuda.Stream()
+        out = torch.empty((T, d), dtype=torch.bfloat16, device=dev)
+        ws = torch.empty(api.moe_forward_workspace(T, d, f, E, k), dtype=torch.uint8, device=dev)
+
+        def ascending():
+            units, Lv = [], b_max - b_min + 1
+            for j in range(E):
+                have = 0
+                for kk in range(Lv):
+                    if hist[j, kk] > 0:
+                        b = b_min + kk
+                        units.append((j, b, have, max(have, b), int(hist[j, kk])))
+                        have = max(have, b)
+            return units
+
+        orders = {"hebf": api.hebf_order(hist, b_min, b_max), "ascending": ascending()}
+        evs = [torch.cuda.Event() for _ in range(E * (b_max - b_min + 1))]
+        res = {}
+        for name, units in orders.items():
+            times = []
+            for i in range(steps + 1):
+                resident = np.zeros(E, np.uint8)
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                api.moe_forward_streamed(x, h13, h2, d13, d2, resident, r, k, hist, units,
+                                         evs[:len(units)], io, out=out, workspace=ws)
+                torch.cuda.synchronize()
+                if i > 0:
+                    times.append((time.perf_counter() - t0) * 1e3)
+            res[name] = round(float(np.median(times)), 3)
+        nbytes = sum(mwq_bytes(2 * f, d, g, b_min, int(b)) + mwq_bytes(d, f, g, b_min, int(b))
+                     for b in r.expert_maxbit.cpu().numpy())
+        src = torch.empty(nbytes // 4, dtype=torch.int32, pin_memory=True)
+        dst = torch.empty(nbytes // 4, dtype=torch.int32, device=dev)
+        dst.copy_(src, non_blocking=True)
+        torch.cuda.synchronize()
+        ct = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            dst.copy_(src, non_blocking=True)
+            torch.cuda.synchronize()
+            ct.append((time.perf_counter() - t0) * 1e3)
+        copy_ms = float(np.median(ct))
+        del h13, h2, d13, d2, src, dst
+        torch.cuda.empty_cache()
+        return {"workload": f"Mixtral-8x7B-shaped MoE layer decode, batch {T}, bits from "
+                            f"{{2,3,4,8}}, experts streamed from pinned host memory into an empty "
+                            f"device copy each step (nested delta planes per unit)",
+                "tokens": T, "units": len(orders["hebf"]), "bytes_streamed": int(nbytes),
+                "ms_per_step_hebf": res["hebf"], "ms_per_step_ascending": res["ascending"],
+                "plain_h2d_copy_ms": round(copy_ms, 3),
+                "h2d_GBps_plain": round(nbytes / (copy_ms * 1e-3) / 1e9, 1),
+                "h2d_GBps_streamed_hebf": round(nbytes / (res["hebf"] * 1e-3) / 1e9, 1)}
+
     main_res = run_batch(args.batch, args.steps, args.warmup, profile=True)
     if args.dump_steps:
         print("per-step ms:", main_res["per_step_ms"], file=sys.stderr)
@@ -688,6 +776,7 @@ def main():
 
     ceiling = run_ceiling(args.ceiling_gib) if args.ceiling_gib > 0 else None
     calib = run_calib() if args.calib else None
+    streamed = run_streamed(args.stream_steps) if args.stream_steps > 0 else None
     tiny = run_tiny(args.tiny_steps) if args.tiny_steps > 0 else None
     prefill = run_prefill(args.prefill_steps, 2) if args.prefill_steps > 0 else None
     fine = run_fine(args.fine_steps, 2) if args.fine_steps > 0 else None
@@ -758,6 +847,7 @@ def main():
         "variants": variants,
         "learned_router": learned,
         "calibrated_mwq": calib,
+        "streamed": streamed,
         "cpu_baseline": cpu,
         "pack_seconds": round(pack_s, 2),
     }
