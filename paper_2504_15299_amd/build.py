@@ -17,6 +17,9 @@ data arrives late, so such a use would see, or be overwritten by, stale
 data (a decode build whose loop copied a pointer through such registers
 faulted on the GPU).
 
+The same holds for LDS reads issued as inline assembly: their registers may
+not be touched before the lgkmcnt wait that covers them.
+
 And it fails if an inline-asm block that writes SCC is followed by a read of
 SCC with no write in between: the compiler does not always treat the asm as
 a definition of SCC, and a stale carry in a 64-bit scalar address add made
@@ -238,6 +241,59 @@ def _is_vector_load(op: str) -> bool:
         "_lds" not in op
 
 
+def asm_lds_read_hazards(asm: str) -> list[tuple[str, str, str]]:
+    """LDS reads issued as inline assembly (the decode and GEMM kernels read
+    their DMA rings that way, so that the compiler does not drain the DMA
+    queue before them) are, to the compiler, complete when the asm statement
+    ends; their data lands only at the following `s_waitcnt lgkmcnt(0)`.  On
+    every path from such a read to that wait, no instruction may touch its
+    destination registers (another batched LDS read may use other
+    registers; its address must not be one of them).  Returns (function,
+    read, offending instruction) triples."""
+    bad = []
+    for fname, lines in _funcs(asm).items():
+        blocks = _basic_blocks(lines, asm_markers=True)
+        for bi, b in enumerate(blocks):
+            inside = False
+            for ii, x in enumerate(b["ins"]):
+                if x == "ASMSTART":
+                    inside = True
+                    continue
+                if x == "ASMEND":
+                    inside = False
+                    continue
+                if not (inside and x.startswith("ds_read")):
+                    continue
+                dst = _vregs(x.split()[1].rstrip(","))
+                stack, seen = [(bi, ii + 1)], set()
+                while stack:
+                    cb, ci = stack.pop()
+                    if (cb, ci) in seen:
+                        continue
+                    seen.add((cb, ci))
+                    stop = False
+                    for y in blocks[cb]["ins"][ci:]:
+                        if y in ("ASMSTART", "ASMEND"):
+                            continue
+                        op = y.split()[0]
+                        if op == "s_waitcnt" and "lgkmcnt(0)" in y:
+                            stop = True
+                            break
+                        operands = y.split(None, 1)[1] if " " in y else ""
+                        if op.startswith("ds_read"):
+                            operands = operands.split(",", 1)[1] if "," in operands else ""
+                        hit = set()
+                        for t in re.findall(r"v\[\d+:\d+\]|v\d+\b", operands):
+                            hit |= _vregs(t)
+                        if hit & dst:
+                            bad.append((fname, x, y))
+                            stop = True
+                            break
+                    if not stop:
+                        stack.extend((sb, 0) for sb in blocks[cb]["succ"])
+    return bad
+
+
 _SCC_READERS = ("s_addc_u32", "s_subb_u32", "s_cselect_", "s_cbranch_scc", "s_cmov_", "s_cmovk_")
 _SCC_WRITERS = ("s_add_", "s_sub_", "s_addc_", "s_subb_", "s_min_", "s_max_", "s_and_", "s_or_",
                 "s_xor_", "s_andn2_", "s_orn2_", "s_nand_", "s_nor_", "s_xnor_", "s_lshl", "s_lshr",
@@ -316,6 +372,10 @@ def _check_mfma(src: str) -> None:
     if sc:
         raise RuntimeError(f"{src}: {len(sc)} reads of SCC that an inline-asm block overwrote, "
                            f"e.g. {sc[0]}")
+    lz = asm_lds_read_hazards(r.stdout)
+    if lz:
+        raise RuntimeError(f"{src}: {len(lz)} inline-asm LDS reads whose registers are used before "
+                           f"their lgkmcnt wait, e.g. {lz[0]}")
     hz = untracked_load_hazards(r.stdout)
     if hz:
         raise RuntimeError(f"{src}: {len(hz)} untracked activation loads whose registers are used "

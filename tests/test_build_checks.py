@@ -121,3 +121,29 @@ def test_kernel_source_hash_ignores_comments(tmp_path, monkeypatch):
     assert bench.kernel_source_hash() == h0
     (src / "ffn_decode.hip").write_text("int g(int y) { return y + 2; }\n")
     assert bench.kernel_source_hash() != h0
+
+
+LDS_OK = HEAD + """
+\t;;#ASMSTART
+\tds_read_b32 v10, v40 offset:256
+\t;;#ASMEND
+\t;;#ASMSTART
+\tds_read_b64 v[12:13], v41 offset:512
+\t;;#ASMEND
+\tv_mov_b32_e32 v20, v21
+\t;;#ASMSTART
+\ts_waitcnt lgkmcnt(0)
+\t;;#ASMEND
+\tv_add_u32_e32 v22, v10, v12
+\ts_endpgm
+"""
+# the compiler reuses the pending read's register for another value
+LDS_BAD = LDS_OK.replace("\tv_mov_b32_e32 v20, v21\n", "\tv_mov_b32_e32 v10, v21\n")
+# a later batched read addresses through the pending register
+LDS_BAD_ADDR = LDS_OK.replace("ds_read_b64 v[12:13], v41", "ds_read_b64 v[12:13], v10")
+
+
+def test_asm_lds_read_check():
+    assert build.asm_lds_read_hazards(LDS_OK) == []
+    assert len(build.asm_lds_read_hazards(LDS_BAD)) == 1
+    assert len(build.asm_lds_read_hazards(LDS_BAD_ADDR)) == 1
