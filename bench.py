@@ -10,9 +10,10 @@ layer call: route (gate, top-k, bit lookup, histogram/permutation) plus the
 expert forward (W1/W3 + SwiGLU, W2, combine).
 
 Prints one JSON line.  `value` = tokens per second of the whole step with
-inputs resident in HBM, timed over eager launches (--graph times replays of
-one captured HIP graph per layer step instead; the eager step time is always
-reported as ms_per_step_eager);
+inputs resident in HBM, timed over replays of one captured HIP graph per
+layer step (route + forward, as a serving loop would launch it; --eager times
+eager launches instead; the eager step time is always reported as
+ms_per_step_eager);
 `roofline` = algorithmic bytes of the dominant kernel (W1/W3 expert kernel:
 packed planes, scales and zeros of every active expert up to its largest
 requested bit-width) per launch over its average duration, timed with HIP
@@ -105,9 +106,9 @@ def main():
                          "and the LLaMA2-13B-shaped dense FFN (0: skip)")
     ap.add_argument("--no-learned", dest="learned", action="store_false",
                     help="skip the decode step with learned bit-width routers")
-    ap.add_argument("--graph", action="store_true",
-                    help="time replays of one captured HIP graph per layer step instead of "
-                         "eager launches")
+    ap.add_argument("--eager", dest="graph", action="store_false",
+                    help="time eager launches instead of replays of one captured HIP graph per "
+                         "layer step (the eager step time is reported either way)")
     ap.add_argument("--dump-steps", action="store_true",
                     help="print the per-step times of the main workload to stderr")
     ap.add_argument("--copy-calibration", action="store_true",
