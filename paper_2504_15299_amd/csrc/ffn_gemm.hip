@@ -388,10 +388,42 @@ void bgemm_kernel(
 #pragma unroll
     for (int b = 0; b < 8; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // One step: dequantize tile `dstep` from its raw stage into the other tile
-  // buffer, then (if `mma`) the products of `mstep`, the weight operands read
-  // in two halves of 64 rows.
+  // One step: the products of `mstep` (if `mma`) from the tile buffer and
+  // activation stage written in earlier steps, and the dequantization of tile
+  // `dstep` from its raw stage into the other tile buffer.  The raw words and
+  // the MFMA operands are read together, and the products are issued before
+  // the dequantization, so that the matrix pipe works on them while this
+  // wave's VALU dequantizes.  The wide variant reads the second half of its
+  // weight operands (tile rows 64..127) after the tile store.
   StepRegs R;
+  auto mfma_narrow = [&]() {
+    if constexpr (SWIGLU) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            __builtin_bit_cast(bf16x8, R.A[i]), __builtin_bit_cast(bf16x8, R.B[0]), acc[i][0], 0,
+            0, 0);
+        acc[i][4] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            __builtin_bit_cast(bf16x8, R.A[i]), __builtin_bit_cast(bf16x8, R.B[1]), acc[i][4], 0,
+            0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+        acc[mt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            __builtin_bit_cast(bf16x8, R.A[mt]), __builtin_bit_cast(bf16x8, R.B[0]), acc[mt][0],
+            0, 0, 0);
+    }
+  };
+  auto mfma_wide = [&](int half) {
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+        acc[mt][4 * half + nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            __builtin_bit_cast(bf16x8, R.A[mt]), __builtin_bit_cast(bf16x8, R.B[nt]),
+            acc[mt][4 * half + nt], 0, 0, 0);
+  };
   auto step = [&](int dstep, int mstep, bool mma) {
     const uint32_t rb = lds_addr(rraw[dstep % kRawRing]);
 #pragma unroll
@@ -402,8 +434,36 @@ void bgemm_kernel(
     for (int p = 0; p < 8; ++p)  // level p - b_min + 1 holds the scale of plane p
       if (p >= b_min && p < bits) ldu16(R.sp[p], rb + kRawScaleOff + 256 * (p - b_min + 1) + 2 * dr);
     ldu8(R.z, rb + kRawZeroOff + dr);
+    const uint32_t wb = lds_addr(wtile[mstep & 1]);
+    if constexpr (NARROW) {
+      if (mma) {
+        const uint32_t xb = lds_addr(xring[mstep % kXRing][0]);
+        if constexpr (SWIGLU) {
+          const int mh = wave >> 2, rbw = wave & 3;
+          ld128(R.A[0], xb + swz(32 * mh + fr, fq));
+          ld128(R.A[1], xb + swz(32 * mh + 16 + fr, fq));
+          ld128(R.B[0], wb + swz(16 * rbw + fr, fq));
+          ld128(R.B[1], wb + swz(16 * (4 + rbw) + fr, fq));
+        } else {
+#pragma unroll
+          for (int mt = 0; mt < 4; ++mt) ld128(R.A[mt], xb + swz(16 * mt + fr, fq));
+          ld128(R.B[0], wb + swz(16 * wave + fr, fq));
+        }
+      }
+    } else if (mma) {
+      const uint32_t xb = lds_addr(xring[mstep % kXRing][wave]);
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) ld128(R.A[mt], xb + swz(16 * mt + fr, fq));
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) ld128(R.B[nt], wb + swz(16 * nt + fr, fq));
+    }
     wait_lgkm();
     R.rebind();
+    if constexpr (NARROW) {
+      if (mma) mfma_narrow();
+    } else if (mma) {
+      mfma_wide(0);
+    }
     uint32_t o[4];
     o[0] = o[1] = o[2] = o[3] = 0u;
     if (b_min == 2) {
@@ -428,59 +488,13 @@ void bgemm_kernel(
     const uint32_t wd = lds_addr(wtile[dstep & 1]);
     st64(wd + swz(dr, dq >> 1) + 8 * (dq & 1), o[0], o[1]);
     st64(wd + swz(dr, 2 + (dq >> 1)) + 8 * (dq & 1), o[2], o[3]);
-    if constexpr (NARROW) {
-     if (mma) {
-      const uint32_t xb = lds_addr(xring[mstep % kXRing][0]);
-      const uint32_t wb = lds_addr(wtile[mstep & 1]);
-      if constexpr (SWIGLU) {
-        const int mh = wave >> 2, rbw = wave & 3;
-        ld128(R.A[0], xb + swz(32 * mh + fr, fq));
-        ld128(R.A[1], xb + swz(32 * mh + 16 + fr, fq));
-        ld128(R.B[0], wb + swz(16 * rbw + fr, fq));
-        ld128(R.B[1], wb + swz(16 * (4 + rbw) + fr, fq));
+    if constexpr (!NARROW) {
+      if (mma) {
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) ld128(R.B[nt], wb + swz(16 * (4 + nt) + fr, fq));
         wait_lgkm();
         R.rebind();
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, R.A[i]), __builtin_bit_cast(bf16x8, R.B[0]), acc[i][0], 0,
-              0, 0);
-          acc[i][4] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, R.A[i]), __builtin_bit_cast(bf16x8, R.B[1]), acc[i][4], 0,
-              0, 0);
-        }
-      } else {
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) ld128(R.A[mt], xb + swz(16 * mt + fr, fq));
-        ld128(R.B[0], wb + swz(16 * wave + fr, fq));
-        wait_lgkm();
-        R.rebind();
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt)
-          acc[mt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, R.A[mt]), __builtin_bit_cast(bf16x8, R.B[0]), acc[mt][0],
-              0, 0, 0);
-      }
-     }
-    } else if (mma) {
-      const uint32_t xb = lds_addr(xring[mstep % kXRing][wave]);
-      const uint32_t wb = lds_addr(wtile[mstep & 1]);
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        if (half == 0)
-#pragma unroll
-          for (int mt = 0; mt < 4; ++mt) ld128(R.A[mt], xb + swz(16 * mt + fr, fq));
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) ld128(R.B[nt], wb + swz(16 * (4 * half + nt) + fr, fq));
-        wait_lgkm();
-        R.rebind();
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-          for (int nt = 0; nt < 4; ++nt)
-            acc[mt][4 * half + nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8, R.A[mt]), __builtin_bit_cast(bf16x8, R.B[nt]),
-                acc[mt][4 * half + nt], 0, 0, 0);
+        mfma_wide(1);
       }
     }
     wait_lgkm();
