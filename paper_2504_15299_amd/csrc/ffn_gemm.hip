@@ -23,6 +23,8 @@
 //   * one barrier per step orders the shared buffers.
 // The W1/W3 variant puts 64 rows of W1 and the same 64 rows of W3 in one tile,
 // so a lane holds a and c of the same output and applies SwiGLU in registers.
+#include <type_traits>
+
 #include "internal.h"
 
 namespace d2moe {
@@ -184,18 +186,24 @@ struct StepRegs {
   uint32_t w[8];   // plane words
   uint32_t sp[8];  // binary16 scale of plane p (p >= b_min); register index = plane
   uint32_t s1, z;  // base scale and zero point
-  u32x4 A[4], B[4];  // B: the weight operands of 64 of the tile's 128 rows
+  u32x4 A[4], B[4], B2[4];  // B, B2: weight operands of tile rows 0..63, 64..127
+  // Re-binds, after the covering wait, the registers the inline-asm LDS reads
+  // of a step wrote: MB plane words, the scales of planes SPLO..MB-1, and
+  // the operands of NA A, NB B and NB2 B2 reads.
+  template <int MB, int SPLO, int NA, int NB, int NB2>
   __device__ __attribute__((always_inline)) inline void rebind() {
 #pragma unroll
-    for (int p = 0; p < 8; ++p) asm volatile("" : "+v"(w[p]));
+    for (int p = 0; p < MB; ++p) asm volatile("" : "+v"(w[p]));
 #pragma unroll
-    for (int p = 0; p < 8; ++p) asm volatile("" : "+v"(sp[p]));
+    for (int p = SPLO; p < MB; ++p) asm volatile("" : "+v"(sp[p]));
     asm volatile("" : "+v"(s1));
     asm volatile("" : "+v"(z));
 #pragma unroll
-    for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(A[i]));
+    for (int i = 0; i < NA; ++i) asm volatile("" : "+v"(A[i]));
 #pragma unroll
-    for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(B[i]));
+    for (int i = 0; i < NB; ++i) asm volatile("" : "+v"(B[i]));
+#pragma unroll
+    for (int i = 0; i < NB2; ++i) asm volatile("" : "+v"(B2[i]));
   }
 };
 
@@ -388,122 +396,10 @@ void bgemm_kernel(
 #pragma unroll
     for (int b = 0; b < 8; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // One step: the products of `mstep` (if `mma`) from the tile buffer and
-  // activation stage written in earlier steps, and the dequantization of tile
-  // `dstep` from its raw stage into the other tile buffer.  The raw words and
-  // the MFMA operands are read together, and the products are issued before
-  // the dequantization, so that the matrix pipe works on them while this
-  // wave's VALU dequantizes.  The wide variant reads the second half of its
-  // weight operands (tile rows 64..127) after the tile store.
-  StepRegs R;
-  auto mfma_narrow = [&]() {
-    if constexpr (SWIGLU) {
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            __builtin_bit_cast(bf16x8, R.A[i]), __builtin_bit_cast(bf16x8, R.B[0]), acc[i][0], 0,
-            0, 0);
-        acc[i][4] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            __builtin_bit_cast(bf16x8, R.A[i]), __builtin_bit_cast(bf16x8, R.B[1]), acc[i][4], 0,
-            0, 0);
-      }
-    } else {
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-        acc[mt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            __builtin_bit_cast(bf16x8, R.A[mt]), __builtin_bit_cast(bf16x8, R.B[0]), acc[mt][0],
-            0, 0, 0);
-    }
-  };
-  auto mfma_wide = [&](int half) {
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
-        acc[mt][4 * half + nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            __builtin_bit_cast(bf16x8, R.A[mt]), __builtin_bit_cast(bf16x8, R.B[nt]),
-            acc[mt][4 * half + nt], 0, 0, 0);
-  };
-  auto step = [&](int dstep, int mstep, bool mma) {
-    const uint32_t rb = lds_addr(rraw[dstep % kRawRing]);
-#pragma unroll
-    for (int p = 0; p < 8; ++p)
-      if (p < bits) ld32(R.w[p], rb + 512 * p + 4 * dr);
-    ldu16(R.s1, rb + kRawScaleOff + 2 * dr);
-#pragma unroll
-    for (int p = 0; p < 8; ++p)  // level p - b_min + 1 holds the scale of plane p
-      if (p >= b_min && p < bits) ldu16(R.sp[p], rb + kRawScaleOff + 256 * (p - b_min + 1) + 2 * dr);
-    ldu8(R.z, rb + kRawZeroOff + dr);
-    const uint32_t wb = lds_addr(wtile[mstep & 1]);
-    if constexpr (NARROW) {
-      if (mma) {
-        const uint32_t xb = lds_addr(xring[mstep % kXRing][0]);
-        if constexpr (SWIGLU) {
-          const int mh = wave >> 2, rbw = wave & 3;
-          ld128(R.A[0], xb + swz(32 * mh + fr, fq));
-          ld128(R.A[1], xb + swz(32 * mh + 16 + fr, fq));
-          ld128(R.B[0], wb + swz(16 * rbw + fr, fq));
-          ld128(R.B[1], wb + swz(16 * (4 + rbw) + fr, fq));
-        } else {
-#pragma unroll
-          for (int mt = 0; mt < 4; ++mt) ld128(R.A[mt], xb + swz(16 * mt + fr, fq));
-          ld128(R.B[0], wb + swz(16 * wave + fr, fq));
-        }
-      }
-    } else if (mma) {
-      const uint32_t xb = lds_addr(xring[mstep % kXRing][wave]);
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) ld128(R.A[mt], xb + swz(16 * mt + fr, fq));
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt) ld128(R.B[nt], wb + swz(16 * nt + fr, fq));
-    }
-    wait_lgkm();
-    R.rebind();
-    if constexpr (NARROW) {
-      if (mma) mfma_narrow();
-    } else if (mma) {
-      mfma_wide(0);
-    }
-    uint32_t o[4];
-    o[0] = o[1] = o[2] = o[3] = 0u;
-    if (b_min == 2) {
-      switch (bits) {
-#define D2MOE_CASE(MB) \
-  case MB: dequant_pairs<MB, 2>(R, b_min, sh_m, dq, d_ok, o); break;
-        D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6) D2MOE_CASE(7)
-        D2MOE_CASE(8)
-#undef D2MOE_CASE
-        default: break;
-      }
-    } else {
-      switch (bits) {
-#define D2MOE_CASE(MB) \
-  case MB: dequant_pairs<MB, 0>(R, b_min, sh_m, dq, d_ok, o); break;
-        D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
-        D2MOE_CASE(7) D2MOE_CASE(8)
-#undef D2MOE_CASE
-        default: break;
-      }
-    }
-    const uint32_t wd = lds_addr(wtile[dstep & 1]);
-    st64(wd + swz(dr, dq >> 1) + 8 * (dq & 1), o[0], o[1]);
-    st64(wd + swz(dr, 2 + (dq >> 1)) + 8 * (dq & 1), o[2], o[3]);
-    if constexpr (!NARROW) {
-      if (mma) {
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) ld128(R.B[nt], wb + swz(16 * (4 + nt) + fr, fq));
-        wait_lgkm();
-        R.rebind();
-        mfma_wide(1);
-      }
-    }
-    wait_lgkm();
-  };
-
-  // ---- prologue: raw 0..kRawRing-1 and activations 0..XL-1 in flight, tile
-  // 0 ready.  Issue order: raw 0 .. raw kRawRing-2, x 0, raw kRawRing-1
-  // (, x 1); the wait leaves the instructions after raw 0 outstanding (one
-  // per raw stage, four per activation stage), i.e. raw 0 has landed.
+  // ---- prologue: raw 0..kRawRing-1 and activations 0..XL-1 in flight.
+  // Issue order: raw 0 .. raw kRawRing-2, x 0, raw kRawRing-1 (, x 1); the
+  // wait leaves the instructions after raw 0 outstanding (one per raw stage,
+  // four per activation stage), i.e. raw 0 has landed.
 #pragma unroll
   for (int i = 0; i + 1 < kRawRing; ++i) raw_dma(i);
   x_dma(0);
@@ -511,30 +407,160 @@ void bgemm_kernel(
   if constexpr (XL == 2) x_dma(1);
   wait_vm<kRawRing + 3 + (XL == 2 ? 4 : 0)>();
   bar();
-  step(0, 0, false);
 
-  // ---- main loop: step s issues raw s+kRawRing and activations s+XL,
-  // dequantizes s+1 and multiplies s.  With XL = 2 (order raw, x) the
-  // instructions issued after the activations of s at the top of step s are
-  // the 5 of step s-1 (raw s+kRawRing-1, activations s+1); with XL = 1
-  // (order x, raw) the one raw s+kRawRing-1.  Raw s+1 was issued before the
-  // activations of s (kRawRing > 3), so that wait makes both
-  // this wave's raw s+1 and its activations of s ready; the barrier then
-  // makes every wave's raw s+1 and tile s visible, and retires all reads of
-  // the stages and the tile buffer that this step overwrites.  In the last
-  // step the dequantization works on a reloaded stage and its tile is never
-  // read.
-  for (int s = 0; s < nsteps; ++s) {
-    wait_vm<XL == 2 ? 5 : 1>();
-    bar();
-    if constexpr (XL == 2) {
-      raw_dma(s + kRawRing);
-      x_dma(s + 2);
-    } else {
-      x_dma(s + 1);
-      raw_dma(s + kRawRing);
+  // The step loop is compiled for the chunk's bit-width MB (and for b_min 2,
+  // the common nest start, or any b_min) and separately for waves that
+  // multiply and waves that only dequantize: every LDS read of a step, its
+  // products and its dequantization then form one branch-free block, in which
+  // the products are interleaved with the dequantization's vector
+  // instructions so that the matrix pipe and the vector ALU overlap.
+  auto run = [&](auto mb_c, auto bmin_c) {
+    constexpr int MB = decltype(mb_c)::value, BMIN = decltype(bmin_c)::value;
+    StepRegs R;
+    // One step: the products of `mstep` (if MMA) from the tile buffer and
+    // activation stage written in earlier steps, and the dequantization of
+    // tile `dstep` from its raw stage into the other tile buffer.
+    auto step = [&](int dstep, int mstep, auto mma_c) {
+      constexpr bool MMA = decltype(mma_c)::value;
+      const uint32_t rb = lds_addr(rraw[dstep % kRawRing]);
+#pragma unroll
+      for (int p = 0; p < MB; ++p) ld32(R.w[p], rb + 512 * p + 4 * dr);
+      ldu16(R.s1, rb + kRawScaleOff + 2 * dr);
+#pragma unroll
+      for (int p = 1; p < MB; ++p) {  // level p - b_min + 1 holds the scale of plane p
+        if constexpr (BMIN > 0) {
+          if (p >= BMIN) ldu16(R.sp[p], rb + kRawScaleOff + 256 * (p - BMIN + 1) + 2 * dr);
+        } else {  // below b_min the base scale is read and not used
+          const int lvl = p >= b_min ? p - b_min + 1 : 0;
+          ldu16(R.sp[p], rb + kRawScaleOff + 256 * lvl + 2 * dr);
+        }
+      }
+      ldu8(R.z, rb + kRawZeroOff + dr);
+      const uint32_t wb = lds_addr(wtile[mstep & 1]);
+      if constexpr (MMA) {
+        if constexpr (NARROW) {
+          const uint32_t xb = lds_addr(xring[mstep % kXRing][0]);
+          if constexpr (SWIGLU) {
+            const int mh = wave >> 2, rbw = wave & 3;
+            ld128(R.A[0], xb + swz(32 * mh + fr, fq));
+            ld128(R.A[1], xb + swz(32 * mh + 16 + fr, fq));
+            ld128(R.B[0], wb + swz(16 * rbw + fr, fq));
+            ld128(R.B[1], wb + swz(16 * (4 + rbw) + fr, fq));
+          } else {
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) ld128(R.A[mt], xb + swz(16 * mt + fr, fq));
+            ld128(R.B[0], wb + swz(16 * wave + fr, fq));
+          }
+        } else {
+          const uint32_t xb = lds_addr(xring[mstep % kXRing][wave]);
+#pragma unroll
+          for (int mt = 0; mt < 4; ++mt) ld128(R.A[mt], xb + swz(16 * mt + fr, fq));
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt) ld128(R.B[nt], wb + swz(16 * nt + fr, fq));
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt) ld128(R.B2[nt], wb + swz(16 * (4 + nt) + fr, fq));
+        }
+      }
+      wait_lgkm();
+      constexpr int NA = !MMA ? 0 : NARROW && SWIGLU ? 2 : 4;
+      constexpr int NB = !MMA ? 0 : !NARROW ? 4 : SWIGLU ? 2 : 1;
+      R.template rebind<MB, (BMIN > 0 ? BMIN : 1), NA, NB, (MMA && !NARROW ? 4 : 0)>();
+      constexpr int n_mfma = !MMA ? 0 : NARROW ? 4 : 32;
+      if constexpr (MMA) {
+        if constexpr (NARROW) {
+          if constexpr (SWIGLU) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+              acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(bf16x8, R.A[i]), __builtin_bit_cast(bf16x8, R.B[0]), acc[i][0],
+                  0, 0, 0);
+              acc[i][4] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(bf16x8, R.A[i]), __builtin_bit_cast(bf16x8, R.B[1]), acc[i][4],
+                  0, 0, 0);
+            }
+          } else {
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt)
+              acc[mt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(bf16x8, R.A[mt]), __builtin_bit_cast(bf16x8, R.B[0]),
+                  acc[mt][0], 0, 0, 0);
+          }
+        } else {
+#pragma unroll
+          for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < 8; ++nt)
+              acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(bf16x8, R.A[mt]),
+                  __builtin_bit_cast(bf16x8, nt < 4 ? R.B[nt] : R.B2[nt - 4]), acc[mt][nt], 0, 0, 0);
+        }
+      }
+      uint32_t o[4];
+      dequant_pairs<MB, BMIN>(R, b_min, sh_m, dq, d_ok, o);
+      const uint32_t wd = lds_addr(wtile[dstep & 1]);
+      st64(wd + swz(dr, dq >> 1) + 8 * (dq & 1), o[0], o[1]);
+      st64(wd + swz(dr, 2 + (dq >> 1)) + 8 * (dq & 1), o[2], o[3]);
+      if constexpr (n_mfma > 0) {
+        // one product, then its share of the dequantization's vector
+        // instructions (about 12 per plane and 40 more per step)
+        constexpr int nv = (12 * MB + 40 + n_mfma - 1) / n_mfma;
+#pragma unroll
+        for (int i = 0; i < n_mfma; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, nv, 0);
+        }
+      }
+      wait_lgkm();
+    };
+
+    // Tile 0 first; then step s issues raw s+kRawRing and activations s+XL,
+    // dequantizes s+1 and multiplies s.  With XL = 2 (order raw, x) the
+    // instructions issued after the activations of s at the top of step s are
+    // the 5 of step s-1 (raw s+kRawRing-1, activations s+1); with XL = 1
+    // (order x, raw) the one raw s+kRawRing-1.  Raw s+1 was issued before the
+    // activations of s (kRawRing > 3), so that wait makes both this wave's
+    // raw s+1 and its activations of s ready; the barrier then makes every
+    // wave's raw s+1 and tile s visible, and retires all reads of the stages
+    // and the tile buffer that this step overwrites.  In the last step the
+    // dequantization works on a reloaded stage and its tile is never read.
+    step(0, 0, std::false_type{});
+    auto loop = [&](auto mma_c) {
+      for (int s = 0; s < nsteps; ++s) {
+        wait_vm<XL == 2 ? 5 : 1>();
+        bar();
+        if constexpr (XL == 2) {
+          raw_dma(s + kRawRing);
+          x_dma(s + 2);
+        } else {
+          x_dma(s + 1);
+          raw_dma(s + kRawRing);
+        }
+        step(s + 1, s, mma_c);
+      }
+    };
+    if (active || narrow)
+      loop(std::true_type{});
+    else
+      loop(std::false_type{});
+  };
+  using std::integral_constant;
+  if (b_min == 2) {
+    switch (bits) {
+#define D2MOE_CASE(MB) \
+  case MB: run(integral_constant<int, MB>{}, integral_constant<int, 2>{}); break;
+      D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6) D2MOE_CASE(7) D2MOE_CASE(8)
+#undef D2MOE_CASE
+      default: break;
     }
-    step(s + 1, s, active || narrow);
+  } else {
+    switch (bits) {
+#define D2MOE_CASE(MB) \
+  case MB: run(integral_constant<int, MB>{}, integral_constant<int, 0>{}); break;
+      D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
+      D2MOE_CASE(7) D2MOE_CASE(8)
+#undef D2MOE_CASE
+      default: break;
+    }
   }
   wait_vm<0>();  // no DMA may still be writing this workgroup's LDS at exit
 
