@@ -138,9 +138,6 @@ typedef __bf16 b2 __attribute__((ext_vector_type(2)));
 
 __device__ inline h2 as_h2(uint32_t v) { return __builtin_bit_cast(h2, v); }
 __device__ inline uint32_t as_u(h2 v) { return __builtin_bit_cast(uint32_t, v); }
-__device__ inline uint32_t h2_to_bf2(h2 v) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(__builtin_convertvector(v, f2), b2));
-}
 __device__ inline uint32_t h2_splat(float v) {
   const _Float16 h = (_Float16)v;
   return as_u(h2{h, h});
@@ -154,17 +151,26 @@ __device__ inline uint32_t h2_splat(float v) {
 __device__ inline uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
+// OFF is the instruction's unsigned 16-bit byte offset added to the address.
+template <int OFF = 0>
 __device__ inline void ld128(u32x4& v, uint32_t a) {
-  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(a), "n"(OFF) : "memory");
 }
+template <int OFF = 0>
 __device__ inline void ld32(uint32_t& v, uint32_t a) {
-  asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(a) : "memory");
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+  asm volatile("ds_read_b32 %0, %1 offset:%2" : "=v"(v) : "v"(a), "n"(OFF) : "memory");
 }
+template <int OFF = 0>
 __device__ inline void ldu16(uint32_t& v, uint32_t a) {
-  asm volatile("ds_read_u16 %0, %1" : "=v"(v) : "v"(a) : "memory");
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+  asm volatile("ds_read_u16 %0, %1 offset:%2" : "=v"(v) : "v"(a), "n"(OFF) : "memory");
 }
+template <int OFF = 0>
 __device__ inline void ldu8(uint32_t& v, uint32_t a) {
-  asm volatile("ds_read_u8 %0, %1" : "=v"(v) : "v"(a) : "memory");
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+  asm volatile("ds_read_u8 %0, %1 offset:%2" : "=v"(v) : "v"(a), "n"(OFF) : "memory");
 }
 __device__ inline void st64(uint32_t a, uint32_t lo, uint32_t hi) {
   asm volatile("ds_write_b64 %0, %1" ::"v"(a), "v"(u32x2{lo, hi}) : "memory");
@@ -179,6 +185,16 @@ __device__ inline void bar() { __builtin_amdgcn_s_barrier(); }
 // 16-byte chunk q of tile row r sits at chunk q ^ ((r >> 2) & 3), so that the
 // 16 rows one MFMA operand read touches fall in distinct banks.
 __device__ inline uint32_t swz(int r, int q) { return (uint32_t)(r * 64 + ((q ^ ((r >> 2) & 3)) << 4)); }
+
+// f(integral_constant<int, i>) for i = 0 .. N-1, so that the index can be a
+// template argument (an instruction offset) inside f.
+template <int N, int I = 0, typename F>
+__device__ __attribute__((always_inline)) inline void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, I + 1>(f);
+  }
+}
 
 // Registers of one step: raw words, scales and zero point of the tile row a
 // thread dequantizes, and the MFMA operands of its wave.
@@ -212,23 +228,27 @@ struct StepRegs {
 // tile (o[0..1] columns 4 dq .. 4 dq + 3, o[2..3] columns 16 + 4 dq ..).
 // It works on pairs in packed fp16: shifting a plane word left by 15 - j puts
 // bit j at bit 15 and bit j + 16 at bit 31, the sign positions of the two
-// halves, and v_bfi turns the pair into (+-c_p, +-c_p).  With every plane read
-// as a sign,
+// halves, and one and-or turns the pair into (+-c_p, +-c_p).  With every plane
+// read as a sign,
 //   W^_b = s1 (Q - z) + sum_{p>=b_min} s_p sigma_p
 //        = C + sum_{p<b} c_p (2 bit_p - 1),  c_p = s1 2^(p-1) for p < b_min,
 //          c_p = s_p for p >= b_min,  C = s1 ((2^b_min - 1) / 2 - z),
-// accumulated in fp16 from C, then rounded to bf16 for the MFMA.
+// accumulated in fp16 from C, then rounded to bf16 for the MFMA.  Every scale
+// is >= 0, so the sign bits of c_p are clear and the and-or only has to set
+// them from the plane bits.  Rows past the matrix edge are dequantized from
+// whatever their stage holds: they only reach output columns that are not
+// stored.
 // BMIN > 0 fixes b_min at compile time (the common ladder starts at 2 bits);
 // BMIN == 0 takes it from `b_min_rt`.
 template <int MB, int BMIN>
 __device__ __attribute__((always_inline)) inline void dequant_pairs(
-    const StepRegs& R, int b_min_rt, uint32_t sh_m, int dq, bool d_ok, uint32_t (&o)[4]) {
+    const StepRegs& R, int b_min_rt, uint32_t sh_m, int dq, uint32_t (&o)[4]) {
   const int b_min = BMIN > 0 ? BMIN : b_min_rt;
   const float s1 = h2f((uint16_t)R.s1);
   const uint32_t C = h2_splat(s1 * ((float)((1 << b_min) - 1) * 0.5f - (float)R.z));
-  // base scale as a binary16 pair; every scale is >= 0, so the pair of a
-  // residual plane is its scale bits duplicated, and that of a base plane
-  // p < b_min is s1 2^(p-1), a power-of-two multiple in binary16
+  // base scale as a binary16 pair; the pair of a residual plane is its scale
+  // bits duplicated, and that of a base plane p < b_min is s1 2^(p-1), a
+  // power-of-two multiple in binary16
   const h2 s1p = as_h2(R.s1 | (R.s1 << 16));
   h2 a[4];
 #pragma unroll
@@ -240,17 +260,21 @@ __device__ __attribute__((always_inline)) inline void dequant_pairs(
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const uint32_t t = R.w[p] << (15 - (4 * dq + j));
-      const uint32_t v = (sh_m & t) | (~sh_m & cp);  // bit set -> -c_p
+      const uint32_t v = (sh_m & t) | cp;  // bit set -> -c_p
       a[j] = a[j] - as_h2(v);
     }
   }
-  const uint32_t a0 = h2_to_bf2(a[0]), a1 = h2_to_bf2(a[1]);
-  const uint32_t a2 = h2_to_bf2(a[2]), a3 = h2_to_bf2(a[3]);
-  o[0] = (a0 & 0xffffu) | (a1 << 16);          // columns 4 dq, 4 dq + 1
-  o[1] = (a2 & 0xffffu) | (a3 << 16);          // 4 dq + 2, 4 dq + 3
-  o[2] = (a0 >> 16) | (a1 & 0xffff0000u);      // 16 + 4 dq, ...
-  o[3] = (a2 >> 16) | (a3 & 0xffff0000u);
-  if (!d_ok) o[0] = o[1] = o[2] = o[3] = 0u;
+  // (column j, column j + 16) fp16 pairs to bf16 pairs of adjacent columns
+  f2 f[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) f[j] = __builtin_convertvector(a[j], f2);
+  auto pk = [](float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{lo, hi}, b2));
+  };
+  o[0] = pk(f[0].x, f[1].x);  // columns 4 dq, 4 dq + 1
+  o[1] = pk(f[2].x, f[3].x);  // 4 dq + 2, 4 dq + 3
+  o[2] = pk(f[0].y, f[1].y);  // 16 + 4 dq, ...
+  o[3] = pk(f[2].y, f[3].y);
 }
 
 // One workgroup: chunk blockIdx.y of the chunk table against weight-row tile
@@ -387,7 +411,6 @@ void bgemm_kernel(
   const int dr = tid >> 2, dq = tid & 3;
   uint32_t sh_m;  // opaque copy of the sign mask: keeps v_bfi on registers
   asm volatile("" : "=v"(sh_m) : "0"(0x80008000u));
-  const bool d_ok = row_ok(dr);
   const int fr = lane & 15, fq = lane >> 4;
 
   f32x4 acc[4][8];
@@ -422,43 +445,52 @@ void bgemm_kernel(
     // tile `dstep` from its raw stage into the other tile buffer.
     auto step = [&](int dstep, int mstep, auto mma_c) {
       constexpr bool MMA = decltype(mma_c)::value;
+      // one address register per access width: the stage base plus this
+      // thread's row, with the plane, level and operand block as offsets
       const uint32_t rb = lds_addr(rraw[dstep % kRawRing]);
-#pragma unroll
-      for (int p = 0; p < MB; ++p) ld32(R.w[p], rb + 512 * p + 4 * dr);
-      ldu16(R.s1, rb + kRawScaleOff + 2 * dr);
-#pragma unroll
-      for (int p = 1; p < MB; ++p) {  // level p - b_min + 1 holds the scale of plane p
+      const uint32_t rb4 = rb + 4 * dr, rb2 = rb + 2 * dr, rb1 = rb + dr;
+      static_for<MB>([&](auto pc) {
+        constexpr int P = decltype(pc)::value;
+        ld32<512 * P>(R.w[P], rb4);
+      });
+      ldu16<kRawScaleOff>(R.s1, rb2);
+      static_for<MB>([&](auto pc) {  // level p - b_min + 1 holds the scale of plane p
+        constexpr int P = decltype(pc)::value;
         if constexpr (BMIN > 0) {
-          if (p >= BMIN) ldu16(R.sp[p], rb + kRawScaleOff + 256 * (p - BMIN + 1) + 2 * dr);
-        } else {  // below b_min the base scale is read and not used
-          const int lvl = p >= b_min ? p - b_min + 1 : 0;
-          ldu16(R.sp[p], rb + kRawScaleOff + 256 * lvl + 2 * dr);
+          if constexpr (P >= BMIN) ldu16<kRawScaleOff + 256 * (P - BMIN + 1)>(R.sp[P], rb2);
+        } else if constexpr (P >= 1) {  // below b_min the base scale is read and not used
+          const int lvl = P >= b_min ? P - b_min + 1 : 0;
+          ldu16(R.sp[P], rb2 + kRawScaleOff + 256 * lvl);
         }
-      }
-      ldu8(R.z, rb + kRawZeroOff + dr);
-      const uint32_t wb = lds_addr(wtile[mstep & 1]);
+      });
+      ldu8<kRawZeroOff>(R.z, rb1);
+      // a 16-row operand block m starts 1024 m bytes after block 0 (the
+      // swizzle depends on the row within the block only)
+      const uint32_t wb = lds_addr(wtile[mstep & 1]) + swz(fr, fq);
       if constexpr (MMA) {
         if constexpr (NARROW) {
-          const uint32_t xb = lds_addr(xring[mstep % kXRing][0]);
+          const uint32_t xb = lds_addr(xring[mstep % kXRing][0]) + swz(fr, fq);
           if constexpr (SWIGLU) {
             const int mh = wave >> 2, rbw = wave & 3;
-            ld128(R.A[0], xb + swz(32 * mh + fr, fq));
-            ld128(R.A[1], xb + swz(32 * mh + 16 + fr, fq));
-            ld128(R.B[0], wb + swz(16 * rbw + fr, fq));
-            ld128(R.B[1], wb + swz(16 * (4 + rbw) + fr, fq));
+            ld128<0>(R.A[0], xb + 2048 * mh);
+            ld128<1024>(R.A[1], xb + 2048 * mh);
+            ld128<0>(R.B[0], wb + 1024 * rbw);
+            ld128<4096>(R.B[1], wb + 1024 * rbw);
           } else {
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) ld128(R.A[mt], xb + swz(16 * mt + fr, fq));
-            ld128(R.B[0], wb + swz(16 * wave + fr, fq));
+            static_for<4>([&](auto mc) {
+              constexpr int M = decltype(mc)::value;
+              ld128<1024 * M>(R.A[M], xb);
+            });
+            ld128<0>(R.B[0], wb + 1024 * wave);
           }
         } else {
-          const uint32_t xb = lds_addr(xring[mstep % kXRing][wave]);
-#pragma unroll
-          for (int mt = 0; mt < 4; ++mt) ld128(R.A[mt], xb + swz(16 * mt + fr, fq));
-#pragma unroll
-          for (int nt = 0; nt < 4; ++nt) ld128(R.B[nt], wb + swz(16 * nt + fr, fq));
-#pragma unroll
-          for (int nt = 0; nt < 4; ++nt) ld128(R.B2[nt], wb + swz(16 * (4 + nt) + fr, fq));
+          const uint32_t xb = lds_addr(xring[mstep % kXRing][wave]) + swz(fr, fq);
+          static_for<4>([&](auto mc) {
+            constexpr int M = decltype(mc)::value;
+            ld128<1024 * M>(R.A[M], xb);
+            ld128<1024 * M>(R.B[M], wb);
+            ld128<1024 * (4 + M)>(R.B2[M], wb);
+          });
         }
       }
       wait_lgkm();
@@ -496,7 +528,7 @@ void bgemm_kernel(
         }
       }
       uint32_t o[4];
-      dequant_pairs<MB, BMIN>(R, b_min, sh_m, dq, d_ok, o);
+      dequant_pairs<MB, BMIN>(R, b_min, sh_m, dq, o);
       const uint32_t wd = lds_addr(wtile[dstep & 1]);
       st64(wd + swz(dr, dq >> 1) + 8 * (dq & 1), o[0], o[1]);
       st64(wd + swz(dr, 2 + (dq >> 1)) + 8 * (dq & 1), o[2], o[3]);
