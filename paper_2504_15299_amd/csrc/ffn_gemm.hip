@@ -6,20 +6,22 @@
 // Positions are the (token, slot) pairs sorted by (expert, bit-width), so an
 // (expert, bit-width) bucket is a contiguous run of positions that all read
 // the same b-bit prefix of the expert's planes.  Buckets are cut into chunks
-// of at most kChunk positions; one 512-thread workgroup computes one chunk
-// against 128 weight rows.  Each of its 8 waves owns 64 positions, and all 8
-// share one dequantized weight tile, so a weight is dequantized once per
-// chunk however many positions the chunk holds.
+// of at most kChunk = 256 positions; one 4-wave workgroup computes one chunk
+// against 128 weight rows, and two such workgroups share a compute unit.
+// Each wave owns 64 positions, and all share one dequantized weight tile, so
+// a weight is dequantized once per chunk however many positions it holds.
+// Chunks of at most 64 positions can run in an 8-wave variant in which every
+// wave takes 16 of the tile's rows for the same positions.
 //
 // Per reduction step of 32 columns (one plane word per row):
 //   * the LDS DMA engine brings the raw planes, scales and zero points of a
-//     later step into a 4-stage ring shared by the workgroup (each wave moves
-//     one 1 KB slice), and each wave's gathered activation rows of a later
-//     step into its own 3-stage ring;
-//   * the workgroup dequantizes the next step's 128 x 32 tile into bf16 (one
-//     quarter plane word per thread) while each wave runs the current step's
-//     v_mfma_f32_16x16x32_bf16 products (64 positions x 128 rows, fp32
-//     accumulation) from the other tile buffer;
+//     later step into a ring shared by the workgroup, and each wave's
+//     gathered activation rows of a later step into its own ring;
+//   * the workgroup dequantizes the next step's 128 x 32 tile into bf16 while
+//     each wave runs the current step's v_mfma_f32_16x16x32_bf16 products
+//     (its positions x 128 rows, fp32 accumulation) from the other tile
+//     buffer, the products interleaved with the dequantization's vector
+//     instructions;
 //   * one barrier per step orders the shared buffers.
 // The W1/W3 variant puts 64 rows of W1 and the same 64 rows of W3 in one tile,
 // so a lane holds a and c of the same output and applies SwiGLU in registers.
@@ -35,9 +37,11 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kThreads = 512;               // 8 waves
 constexpr int kWaveM = 64;                  // positions per wave
-constexpr int kChunk = 8 * kWaveM;          // positions per chunk
+// waves per workgroup: 4 in the wide kernel (one per SIMD, two workgroups
+// per compute unit), 8 in the narrow one
+template <bool NARROW> constexpr int n_waves() { return NARROW ? 8 : 4; }
+constexpr int kChunk = n_waves<false>() * kWaveM;  // positions per chunk
 constexpr int kTileRows = 128;              // weight rows per workgroup
 constexpr int kStepK = 32;                  // reduction columns per step
 // raw stages: the DMA runs kRawRing - 1 steps ahead of dequantization (4
@@ -52,9 +56,11 @@ constexpr int kXStage = kWaveM * kStepK * 2;  // bytes per wave and stage
 // Raw stage layout (bytes): plane p at 512 p (one word per tile row), scales
 // of level l at 4096 + 256 l (one binary16 per tile row, up to 8 levels),
 // zero points at 6144 (one byte per tile row).  16-byte DMA slots 0..391
-// carry them; waves 0..6 move slots 64 w .. 64 w + 63.
+// carry them; DMA instruction i of wave w moves slots 256 i + 64 w .. + 63
+// (one instruction per wave in the 8-wave kernel, two in the 4-wave one).
 constexpr int kRawScaleOff = 4096, kRawZeroOff = 6144, kRawStage = 6272;
-constexpr int kRawSlots = 392, kRawWaves = 7;
+constexpr int kRawSlots = 392;
+template <bool NARROW> constexpr int raw_dmas() { return NARROW ? 1 : 2; }
 constexpr int kWTile = kTileRows * kStepK * 2;  // dequantized bf16 tile bytes
 
 #define D2MOE_GPTR(p) ((__attribute__((address_space(1))) void*)(p))
@@ -175,6 +181,9 @@ __device__ inline void ldu8(uint32_t& v, uint32_t a) {
 __device__ inline void st64(uint32_t a, uint32_t lo, uint32_t hi) {
   asm volatile("ds_write_b64 %0, %1" ::"v"(a), "v"(u32x2{lo, hi}) : "memory");
 }
+__device__ inline void st128(uint32_t a, uint32_t x, uint32_t y, uint32_t z, uint32_t w) {
+  asm volatile("ds_write_b128 %0, %1" ::"v"(a), "v"(u32x4{x, y, z, w}) : "memory");
+}
 __device__ inline void wait_lgkm() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 template <int N>
 __device__ inline void wait_vm() {
@@ -285,15 +294,17 @@ __device__ __attribute__((always_inline)) inline void dequant_pairs(
 //   else:   W is [N][K], out = y [pos][N] fp32
 // `expert_fixed` >= 0 overrides the chunk's expert (the shared expert).
 template <int G, bool SWIGLU, bool NARROW>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2)))
-void bgemm_kernel(
+__global__ __launch_bounds__(64 * n_waves<NARROW>())
+__attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
     const uint16_t* __restrict__ in, int in_ld, const int32_t* __restrict__ perm, int kdiv,
     MwqView W, const int32_t* __restrict__ chunks, int f, int N, void* __restrict__ out,
     int out_ld, int split, size_t out_split) {
-  // narrow chunks stage only wave 0's activations (56 KB of LDS in all, two
-  // workgroups per compute unit); wide ones each wave's (140 KB, one)
+  // narrow chunks stage only wave 0's activations (77 KB of LDS in all),
+  // wide ones each wave's (73 KB); either way two workgroups share a compute
+  // unit
+  constexpr int NWV = n_waves<NARROW>(), RD = raw_dmas<NARROW>();
   constexpr int XL = x_lead<NARROW>(), kXRing = XL + 1;
-  __shared__ __attribute__((aligned(16))) uint8_t xring[kXRing][NARROW ? 1 : 8][kXStage];
+  __shared__ __attribute__((aligned(16))) uint8_t xring[kXRing][NARROW ? 1 : NWV][kXStage];
   constexpr int kRawRing = raw_ring<NARROW>();
   __shared__ __attribute__((aligned(16))) uint8_t rraw[kRawRing][kRawStage];
   __shared__ __attribute__((aligned(16))) uint8_t wtile[2][kWTile];
@@ -329,56 +340,68 @@ void bgemm_kernel(
   constexpr bool narrow = NARROW;
   if (NARROW ? m_cnt > kWaveM : (split && m_cnt <= kWaveM)) return;
 
-  // ---- raw weight DMA: this lane's 16-byte slot u of the stage ----
+  // ---- raw weight DMA: 16-byte slot u of the stage ----
   // global row of tile row r
   auto grow = [&](int r) { return SWIGLU ? (r < 64 ? n0 + r : f + n0 + r - 64) : n0 + r; };
   auto row_ok = [&](int r) { return SWIGLU ? n0 + (r & 63) < f : n0 + r < N; };
-  const int u = 64 * wave + lane;
-  const uint8_t* rsrc = (const uint8_t*)W.planes;  // address at step 0
-  int rstride_b = 0, rstride_c = 0;                 // per group, per 32-column step
-  bool rreal = false;
-  if (u < 256) {  // plane p = u / 32, tile rows 4 v .. 4 v + 3 of it
-    const int p = u >> 5, v = u & 31;
-    const int r = 4 * v;  // first tile row of the slot
-    if (p < bits && row_ok(r)) {
-      const int gr = grow(r);
-      const size_t blk = W.block(expert, gr / BR, 0);
-      rsrc = (const uint8_t*)(W.planes + W.plane_word(blk, p, gr % BR));
-      rstride_b = W.b_max * 64 * 4;
-      rstride_c = BR * 4;
-      rreal = true;
+  struct RawSlot {
+    const uint8_t* src;  // address at step 0
+    int sb, sc;          // bytes per group, per 32-column step
+    bool real;
+  };
+  auto raw_slot = [&](int u) {
+    RawSlot q{(const uint8_t*)W.planes, 0, 0, false};
+    if (u < 256) {  // plane p = u / 32, tile rows 4 v .. 4 v + 3 of it
+      const int p = u >> 5, v = u & 31;
+      const int r = 4 * v;  // first tile row of the slot
+      if (p < bits && row_ok(r)) {
+        const int gr = grow(r);
+        const size_t blk = W.block(expert, gr / BR, 0);
+        q = {(const uint8_t*)(W.planes + W.plane_word(blk, p, gr % BR)), W.b_max * 64 * 4, BR * 4,
+             true};
+      }
+    } else if (u < 256 + 16 * 8) {  // level l, tile rows 8 v .. 8 v + 7
+      const int l = (u - 256) >> 4, v = (u - 256) & 15;
+      const int r = 8 * v;
+      if (l < nlev && row_ok(r)) {
+        const int gr = grow(r);
+        const size_t blk = W.block(expert, gr / BR, 0);
+        q = {(const uint8_t*)(W.scales + W.scale_idx(blk, l, gr % BR)), W.levels() * BR * 2, 0,
+             true};
+      }
+    } else if (u < kRawSlots) {  // zero points, tile rows 16 z .. 16 z + 15
+      const int z = u - 256 - 16 * 8;
+      const int r = 16 * z;
+      if (row_ok(r)) {
+        const int gr = grow(r);
+        const size_t blk = W.block(expert, gr / BR, 0);
+        q = {W.zeros + W.zero_idx(blk, gr % BR), BR, 0, true};
+      }
     }
-  } else if (u < 256 + 16 * 8) {  // level l, tile rows 8 v .. 8 v + 7
-    const int l = (u - 256) >> 4, v = (u - 256) & 15;
-    const int r = 8 * v;
-    if (l < nlev && row_ok(r)) {
-      const int gr = grow(r);
-      const size_t blk = W.block(expert, gr / BR, 0);
-      rsrc = (const uint8_t*)(W.scales + W.scale_idx(blk, l, gr % BR));
-      rstride_b = W.levels() * BR * 2;
-      rreal = true;
-    }
-  } else if (u < kRawSlots) {  // zero points, tile rows 16 z .. 16 z + 15
-    const int z = u - 256 - 16 * 8;
-    const int r = 16 * z;
-    if (row_ok(r)) {
-      const int gr = grow(r);
-      const size_t blk = W.block(expert, gr / BR, 0);
-      rsrc = W.zeros + W.zero_idx(blk, gr % BR);
-      rstride_b = BR;
-      rreal = true;
-    }
+    return q;
+  };
+  // instruction i of this wave: slots ubase + lane, ubase = 256 i + 64 wave.
+  // Every wave issues RD raw DMAs per step (lane 0 at least), so that all
+  // waves count the same memory instructions: lanes whose slot is past the
+  // stage issue nothing, and an instruction with no slot of its own writes
+  // the dummy area from lane 0.
+  RawSlot rs[RD];
+  bool rissue[RD];
+#pragma unroll
+  for (int i = 0; i < RD; ++i) {
+    rs[i] = raw_slot(256 * i + 64 * wave + lane);
+    rissue[i] = rs[i].real || lane == 0;
   }
-  // every wave issues one raw DMA per step (lane 0 at least), so that all
-  // waves count the same memory instructions; idle slots write a dummy area
-  const bool rissue = rreal || lane == 0;
-  const uint32_t rdst_off = wave < kRawWaves ? 1024u * wave : 0u;
   auto raw_dma = [&](int step) {
     const int st = s_lo + (step < nsteps ? step : nsteps - 1);  // past the end: reload, unused
-    const uint8_t* src = rsrc + (size_t)(st / SPG) * rstride_b + (st % SPG) * rstride_c;
-    uint8_t* dst = wave < kRawWaves ? &rraw[step % kRawRing][rdst_off] : dummy[0];
-    if (rissue)
-      __builtin_amdgcn_global_load_lds(D2MOE_GPTR(src), D2MOE_LPTR(dst), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < RD; ++i) {
+      const int ubase = 256 * i + 64 * wave;  // wave-uniform
+      const uint8_t* src = rs[i].src + (size_t)(st / SPG) * rs[i].sb + (st % SPG) * rs[i].sc;
+      uint8_t* dst = ubase < kRawSlots ? &rraw[step % kRawRing][16 * ubase] : dummy[0];
+      if (rissue[i])
+        __builtin_amdgcn_global_load_lds(D2MOE_GPTR(src), D2MOE_LPTR(dst), 16, 0, 0);
+    }
   };
 
   // ---- activation DMA: instruction i moves tile rows 16 i .. 16 i + 15 ----
@@ -407,8 +430,10 @@ void bgemm_kernel(
                                          D2MOE_LPTR(dst + stride * i), 16, 0, 0);
   };
 
-  // ---- dequantization: tile row dr, columns 4 dq .. 4 dq + 3 and +16 ----
-  const int dr = tid >> 2, dq = tid & 3;
+  // ---- dequantization: tile row dr, columns 4 dq .. 4 dq + 3 and +16 for
+  // dq = dq0 .. dq0 + NDQ - 1 (8 waves: one dq per thread; 4 waves: two) ----
+  constexpr int NDQ = 8 / NWV;
+  const int dr = tid / (4 / NDQ), dq0 = (tid % (4 / NDQ)) * NDQ;
   uint32_t sh_m;  // opaque copy of the sign mask: keeps v_bfi on registers
   asm volatile("" : "=v"(sh_m) : "0"(0x80008000u));
   const int fr = lane & 15, fq = lane >> 4;
@@ -428,7 +453,7 @@ void bgemm_kernel(
   x_dma(0);
   raw_dma(kRawRing - 1);
   if constexpr (XL == 2) x_dma(1);
-  wait_vm<kRawRing + 3 + (XL == 2 ? 4 : 0)>();
+  wait_vm<(kRawRing - 1) * RD + 4 + (XL == 2 ? 4 : 0)>();
   bar();
 
   // The step loop is compiled for the chunk's bit-width MB (and for b_min 2,
@@ -527,15 +552,23 @@ void bgemm_kernel(
                   __builtin_bit_cast(bf16x8, nt < 4 ? R.B[nt] : R.B2[nt - 4]), acc[mt][nt], 0, 0, 0);
         }
       }
-      uint32_t o[4];
-      dequant_pairs<MB, BMIN>(R, b_min, sh_m, dq, o);
       const uint32_t wd = lds_addr(wtile[dstep & 1]);
-      st64(wd + swz(dr, dq >> 1) + 8 * (dq & 1), o[0], o[1]);
-      st64(wd + swz(dr, 2 + (dq >> 1)) + 8 * (dq & 1), o[2], o[3]);
+      if constexpr (NDQ == 1) {
+        uint32_t o[4];
+        dequant_pairs<MB, BMIN>(R, b_min, sh_m, dq0, o);
+        st64(wd + swz(dr, dq0 >> 1) + 8 * (dq0 & 1), o[0], o[1]);
+        st64(wd + swz(dr, 2 + (dq0 >> 1)) + 8 * (dq0 & 1), o[2], o[3]);
+      } else {  // dq0 even: the two halves of 16-byte chunks dq0 / 2 and 2 + dq0 / 2
+        uint32_t o0[4], o1[4];
+        dequant_pairs<MB, BMIN>(R, b_min, sh_m, dq0, o0);
+        dequant_pairs<MB, BMIN>(R, b_min, sh_m, dq0 + 1, o1);
+        st128(wd + swz(dr, dq0 >> 1), o0[0], o0[1], o1[0], o1[1]);
+        st128(wd + swz(dr, 2 + (dq0 >> 1)), o0[2], o0[3], o1[2], o1[3]);
+      }
       if constexpr (n_mfma > 0) {
         // one product, then its share of the dequantization's vector
-        // instructions (about 12 per plane and 40 more per step)
-        constexpr int nv = (12 * MB + 40 + n_mfma - 1) / n_mfma;
+        // instructions (about 12 per plane and 40 more per step and dq)
+        constexpr int nv = (NDQ * (12 * MB + 30) + 10 + n_mfma - 1) / n_mfma;
 #pragma unroll
         for (int i = 0; i < n_mfma; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -558,7 +591,7 @@ void bgemm_kernel(
     step(0, 0, std::false_type{});
     auto loop = [&](auto mma_c) {
       for (int s = 0; s < nsteps; ++s) {
-        wait_vm<XL == 2 ? 5 : 1>();
+        wait_vm<XL == 2 ? RD + 4 : RD>();
         bar();
         if constexpr (XL == 2) {
           raw_dma(s + kRawRing);
@@ -775,18 +808,19 @@ hipError_t run_gemm(const uint16_t* in, int in_ld, const int32_t* perm, int kdiv
   // chunks of more than 64 positions (all of them without split), then the
   // chunks of at most 64
   const int sp = split ? 1 : 0;
+  constexpr int kWide = 64 * n_waves<false>(), kNarrow = 64 * n_waves<true>();
   if (W.group == 128) {
-    bgemm_kernel<128, SWIGLU, false><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, chunks,
-                                                               f, N, out, out_ld, sp, out_split);
+    bgemm_kernel<128, SWIGLU, false><<<grid, kWide, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f, N,
+                                                            out, out_ld, sp, out_split);
     if (split)
-      bgemm_kernel<128, SWIGLU, true><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, chunks,
-                                                                f, N, out, out_ld, sp, out_split);
+      bgemm_kernel<128, SWIGLU, true><<<grid, kNarrow, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f,
+                                                               N, out, out_ld, sp, out_split);
   } else {
-    bgemm_kernel<64, SWIGLU, false><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, chunks,
-                                                              f, N, out, out_ld, sp, out_split);
+    bgemm_kernel<64, SWIGLU, false><<<grid, kWide, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f, N,
+                                                           out, out_ld, sp, out_split);
     if (split)
-      bgemm_kernel<64, SWIGLU, true><<<grid, kThreads, 0, s>>>(in, in_ld, perm, kdiv, W, chunks,
-                                                               f, N, out, out_ld, sp, out_split);
+      bgemm_kernel<64, SWIGLU, true><<<grid, kNarrow, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f,
+                                                              N, out, out_ld, sp, out_split);
   }
   return hipGetLastError();
 }
