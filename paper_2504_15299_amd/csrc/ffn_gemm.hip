@@ -467,8 +467,11 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
     StepRegs R;
     // One step: the products of `mstep` (if MMA) from the tile buffer and
     // activation stage written in earlier steps, and the dequantization of
-    // tile `dstep` from its raw stage into the other tile buffer.
-    auto step = [&](int dstep, int mstep, auto mma_c) {
+    // tile `dstep` from its raw stage into the other tile buffer.  `dma`
+    // issues the DMA of later steps once this step's LDS reads are issued, so
+    // that its issue overlaps their latency (it writes only stages that this
+    // step does not read).
+    auto step = [&](int dstep, int mstep, auto mma_c, auto&& dma) {
       constexpr bool MMA = decltype(mma_c)::value;
       // one address register per access width: the stage base plus this
       // thread's row, with the plane, level and operand block as offsets
@@ -518,6 +521,7 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
           });
         }
       }
+      dma();
       wait_lgkm();
       constexpr int NA = !MMA ? 0 : NARROW && SWIGLU ? 2 : 4;
       constexpr int NB = !MMA ? 0 : !NARROW ? 4 : SWIGLU ? 2 : 1;
@@ -578,29 +582,31 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
       wait_lgkm();
     };
 
-    // Tile 0 first; then step s issues raw s+kRawRing and activations s+XL,
-    // dequantizes s+1 and multiplies s.  With XL = 2 (order raw, x) the
-    // instructions issued after the activations of s at the top of step s are
-    // the 5 of step s-1 (raw s+kRawRing-1, activations s+1); with XL = 1
-    // (order x, raw) the one raw s+kRawRing-1.  Raw s+1 was issued before the
-    // activations of s (kRawRing > 3), so that wait makes both this wave's
-    // raw s+1 and its activations of s ready; the barrier then makes every
+    // Tile 0 first; then step s issues raw s+kRawRing and activations s+XL
+    // (RD and 4 instructions), dequantizes s+1 and multiplies s.  With XL = 2
+    // (order raw, x) the instructions issued after the activations of s, at
+    // the top of step s, are the RD + 4 of step s-1 (raw s+kRawRing-1,
+    // activations s+1); with XL = 1 (order x, raw) the RD of raw
+    // s+kRawRing-1.  Raw s+1 was issued before the activations of s
+    // (kRawRing > 3), so that wait makes both this wave's raw s+1 and its
+    // activations of s ready; the barrier then makes every
     // wave's raw s+1 and tile s visible, and retires all reads of the stages
     // and the tile buffer that this step overwrites.  In the last step the
     // dequantization works on a reloaded stage and its tile is never read.
-    step(0, 0, std::false_type{});
+    step(0, 0, std::false_type{}, [] {});
     auto loop = [&](auto mma_c) {
       for (int s = 0; s < nsteps; ++s) {
         wait_vm<XL == 2 ? RD + 4 : RD>();
         bar();
-        if constexpr (XL == 2) {
-          raw_dma(s + kRawRing);
-          x_dma(s + 2);
-        } else {
-          x_dma(s + 1);
-          raw_dma(s + kRawRing);
-        }
-        step(s + 1, s, mma_c);
+        step(s + 1, s, mma_c, [&] {
+          if constexpr (XL == 2) {
+            raw_dma(s + kRawRing);
+            x_dma(s + 2);
+          } else {
+            x_dma(s + 1);
+            raw_dma(s + kRawRing);
+          }
+        });
       }
     };
     if (active || narrow)
