@@ -404,30 +404,34 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
     }
   };
 
-  // ---- activation DMA: instruction i moves tile rows 16 i .. 16 i + 15 ----
-  const uint16_t* xsrc[4];
+  // ---- activation DMA: an instruction moves 16 positions' 64-byte rows.
+  // Wide: wave w stages its own 64 positions, instruction i the rows
+  // 16 i .. 16 i + 15 (XD = 4 per step).  Narrow: the chunk's (at most) 64
+  // positions are shared, wave w < 4 stages rows 16 w .. 16 w + 15 and the
+  // others issue one lane-0 load to the dummy area (XD = 1 per step), so
+  // that every wave counts the same memory instructions.
+  constexpr int XD = NARROW ? 1 : 4;
+  const uint16_t* xsrc[XD];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int rl = 16 * i + (lane >> 2);
-    int pos = m_first + kWaveM * wave + rl;
+  for (int i = 0; i < XD; ++i) {
+    const int rl = 16 * (NARROW ? (wave & 3) : i) + (lane >> 2);
+    int pos = m_first + (NARROW ? 0 : kWaveM * wave) + rl;
     pos = pos < m_first + m_cnt ? pos : m_first + m_cnt - 1;
     const int src = perm ? perm[pos] / kdiv : pos;
     const int q = (lane & 3) ^ ((rl >> 2) & 3);
     xsrc[i] = in + (size_t)src * in_ld + 8 * q;
   }
-  // every wave issues four per step (lane 0 at least) so that all waves
-  // count the same memory instructions; in a narrow chunk waves 1..7 hold no
-  // positions and their lane-0 loads go to the dummy area
+  const bool xissue = NARROW ? (wave < 4 || lane == 0) : (active || lane == 0);
   auto x_dma = [&](int step) {
     const int st = s_lo + (step < nsteps ? step : nsteps - 1);
-    uint8_t* dst = NARROW ? (wave == 0 ? xring[step % kXRing][0] : dummy[0])
-                          : xring[step % kXRing][wave];
-    const int stride = NARROW && wave != 0 ? 0 : 1024;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (active || lane == 0)
-        __builtin_amdgcn_global_load_lds(D2MOE_GPTR(xsrc[i] + kStepK * st),
-                                         D2MOE_LPTR(dst + stride * i), 16, 0, 0);
+    for (int i = 0; i < XD; ++i) {
+      uint8_t* dst = NARROW ? (wave < 4 ? xring[step % kXRing][0] + 1024 * wave : dummy[0])
+                            : xring[step % kXRing][wave] + 1024 * i;
+      if (xissue)
+        __builtin_amdgcn_global_load_lds(D2MOE_GPTR(xsrc[i] + kStepK * st), D2MOE_LPTR(dst), 16,
+                                         0, 0);
+    }
   };
 
   // ---- dequantization: tile row dr, columns 4 dq .. 4 dq + 3 and +16 for
@@ -446,14 +450,14 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
 
   // ---- prologue: raw 0..kRawRing-1 and activations 0..XL-1 in flight.
   // Issue order: raw 0 .. raw kRawRing-2, x 0, raw kRawRing-1 (, x 1); the
-  // wait leaves the instructions after raw 0 outstanding (one per raw stage,
-  // four per activation stage), i.e. raw 0 has landed.
+  // wait leaves the instructions after raw 0 outstanding (RD per raw stage,
+  // XD per activation stage), i.e. raw 0 has landed.
 #pragma unroll
   for (int i = 0; i + 1 < kRawRing; ++i) raw_dma(i);
   x_dma(0);
   raw_dma(kRawRing - 1);
   if constexpr (XL == 2) x_dma(1);
-  wait_vm<(kRawRing - 1) * RD + 4 + (XL == 2 ? 4 : 0)>();
+  wait_vm<(kRawRing - 1) * RD + XD + (XL == 2 ? XD : 0)>();
   bar();
 
   // The step loop is compiled for the chunk's bit-width MB (and for b_min 2,
@@ -583,9 +587,9 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
     };
 
     // Tile 0 first; then step s issues raw s+kRawRing and activations s+XL
-    // (RD and 4 instructions), dequantizes s+1 and multiplies s.  With XL = 2
+    // (RD and XD instructions), dequantizes s+1 and multiplies s.  With XL = 2
     // (order raw, x) the instructions issued after the activations of s, at
-    // the top of step s, are the RD + 4 of step s-1 (raw s+kRawRing-1,
+    // the top of step s, are the RD + XD of step s-1 (raw s+kRawRing-1,
     // activations s+1); with XL = 1 (order x, raw) the RD of raw
     // s+kRawRing-1.  Raw s+1 was issued before the activations of s
     // (kRawRing > 3), so that wait makes both this wave's raw s+1 and its
@@ -596,7 +600,7 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
     step(0, 0, std::false_type{}, [] {});
     auto loop = [&](auto mma_c) {
       for (int s = 0; s < nsteps; ++s) {
-        wait_vm<XL == 2 ? RD + 4 : RD>();
+        wait_vm<XL == 2 ? RD + XD : RD>();
         bar();
         step(s + 1, s, mma_c, [&] {
           if constexpr (XL == 2) {
