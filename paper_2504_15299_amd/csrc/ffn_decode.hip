@@ -1219,14 +1219,22 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   const dim3 g2(d / 16, ny);
   // W1/W3: each wave streams both matrices' blocks of its rows (one
   // activation load serves both), two waves per row block, each over half of
-  // the reduction (the fastest split at every batch measured, 1 to 64).
+  // the reduction, or four waves over a quarter each when the two-wave grid
+  // would not fill the GPU's 4096 wave slots (one or two active experts:
+  // the dense FFN, batch 1), so that more streams are in flight.
   // decode_path_ok has checked that the W3 block's 32-bit offset fits.
+  const long active_items = E < npos ? E : npos;
+  const bool ks4 = (long)(d_ff / 16) * active_items * 2 < 4096;
   if (ncb == 1)
-    err = launch_decode13_kernel<2, 1>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos, d_ff,
-                                       b.h32, d_ff, b.hmax, s, e0, e1);
+    err = ks4 ? launch_decode13_kernel<4, 1>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos,
+                                             d_ff, b.h32, d_ff, b.hmax, s, e0, e1)
+              : launch_decode13_kernel<2, 1>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos,
+                                             d_ff, b.h32, d_ff, b.hmax, s, e0, e1);
   else
-    err = launch_decode13_kernel<2, 2>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos, d_ff,
-                                       b.h32, d_ff, b.hmax, s, e0, e1);
+    err = ks4 ? launch_decode13_kernel<4, 2>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos,
+                                             d_ff, b.h32, d_ff, b.hmax, s, e0, e1)
+              : launch_decode13_kernel<2, 2>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos,
+                                             d_ff, b.h32, d_ff, b.hmax, s, e0, e1);
   if (err != hipSuccess) return err;
   err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.hmax, d_ff / 16, b.xq2, b.xs2, r,
                          false, E, L, nullptr, 0, item, s);
