@@ -45,9 +45,10 @@ constexpr int kChunk = n_waves<false>() * kWaveM;  // positions per chunk
 constexpr int kTileRows = 128;              // weight rows per workgroup
 constexpr int kStepK = 32;                  // reduction columns per step
 // raw stages: the DMA runs kRawRing - 1 steps ahead of dequantization (4
-// stages in the wide kernel; the narrow one has LDS to spare and takes 8)
+// stages; in the narrow kernel 8 measured the same and kept a third
+// workgroup off each compute unit)
 template <bool NARROW>
-constexpr int raw_ring() { return NARROW ? 8 : 4; }
+constexpr int raw_ring() { return 4; }
 // activation lookahead in steps: one in the wide kernel (its 2-stage ring
 // leaves LDS for the tiles; the activations mostly come from L2), two in the
 // narrow one
@@ -299,9 +300,9 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
     const uint16_t* __restrict__ in, int in_ld, const int32_t* __restrict__ perm, int kdiv,
     MwqView W, const int32_t* __restrict__ chunks, int f, int N, void* __restrict__ out,
     int out_ld, int split, size_t out_split) {
-  // narrow chunks stage only wave 0's activations (77 KB of LDS in all),
-  // wide ones each wave's (73 KB); either way two workgroups share a compute
-  // unit
+  // narrow chunks stage only the chunk's shared activations (54 KB of LDS
+  // in all: three workgroups per compute unit), wide ones each wave's
+  // (73 KB: two)
   constexpr int NWV = n_waves<NARROW>(), RD = raw_dmas<NARROW>();
   constexpr int XL = x_lead<NARROW>(), kXRing = XL + 1;
   __shared__ __attribute__((aligned(16))) uint8_t xring[kXRing][NARROW ? 1 : NWV][kXStage];
