@@ -208,9 +208,10 @@ FWD_SPECS = {
     "prefill_small": wl.scaled(wl.mixtral_prefill(), d=256, f=384, T=600),
     "fine_small": wl.scaled(wl.fine_grained(), d=256, f=128, T=200, shared_f=192),
     # the paper's two nests and its dense-model case, and other nest starts
-    # (decode kernels at b_min 1, 3, 5 and 8; two 8-token column blocks per
-    # work item once positions exceed 7 per expert: T 40 at top-2 of 8, and
-    # the b_min 1 and 3 cases at T 32)
+    # (decode kernels at every b_min; two 8-token column blocks per work item
+    # once positions exceed 7 per expert: T 40 at top-2 of 8, and the b_min
+    # 1 and 3 cases at T 32).  At these shapes the W1/W3 grid is small, so its
+    # reduction is split over four waves per row block.
     "decode_v1_T16": wl.scaled(wl.mixtral_decode_v1(T=16), d=512, f=384),
     "decode_v2_T16": wl.scaled(wl.mixtral_decode_v2(T=16), d=512, f=384),
     "decode_v2_T40": wl.scaled(wl.mixtral_decode_v2(T=40), d=256, f=256),
@@ -222,6 +223,21 @@ FWD_SPECS = {
                                bits_choices=(1, 2, 5), bits_probs=None),
     "decode_b8_T4": wl.scaled(wl.mixtral_decode(T=4), d=256, f=256, b_min=8, b_max=8,
                               bits_choices=(8,), bits_probs=None),
+    "decode_b4_T40": wl.scaled(wl.mixtral_decode(T=40), d=256, f=256, b_min=4, b_max=8,
+                               bits_choices=(4, 6, 8), bits_probs=None),
+    "decode_b6_T40": wl.scaled(wl.mixtral_decode(T=40), d=256, f=256, b_min=6, b_max=8,
+                               bits_choices=(6, 7, 8), bits_probs=None),
+    "decode_b7_T40": wl.scaled(wl.mixtral_decode(T=40), d=256, f=256, b_min=7, b_max=8,
+                               bits_choices=(7, 8), bits_probs=None),
+    "decode_b8_T40": wl.scaled(wl.mixtral_decode(T=40), d=256, f=256, b_min=8, b_max=8,
+                               bits_choices=(8,), bits_probs=None),
+    # 16 experts with d_ff 2048 fill the GPU's wave slots with two waves per
+    # W1/W3 row block (the split every full-size batch above 1 uses): one
+    # column block at T 32 (b_min 1), two at T 64 (b_min 3)
+    "decode_ks2_b1_T32": wl.scaled(wl.mixtral_decode(T=32), d=256, f=2048, E=16, b_min=1,
+                                   b_max=5, bits_choices=(1, 2, 5), bits_probs=None),
+    "decode_ks2_b3_T64": wl.scaled(wl.mixtral_decode(T=64), d=256, f=2048, E=16, b_min=3,
+                                   b_max=6, bits_choices=(3, 4, 6), bits_probs=None),
     "dense_T16": wl.scaled(wl.dense_decode(T=16), d=512, f=768),
     "dense_T64": wl.scaled(wl.dense_decode(T=64), d=256, f=512),
     "prefill_v2_small": wl.scaled(wl.mixtral_prefill(), d=256, f=384, T=300, b_min=5, b_max=8,
