@@ -118,7 +118,8 @@ __device__ inline int row_scale_exp(float amax) {
 // n = 4j'..4j'+3 (fixed d), so each thread reads four columns at stride 4 and
 // stores one dword per piece.  The zero-slot workgroup of slice 0 also writes
 // the work list of the decode kernels when `elist` is given: each active
-// expert's positions in runs of at most `item`, elist[4 i] = expert,
+// expert's positions in runs of at most `item` (experts widest first),
+// elist[4 i] = expert,
 // first position, end position, the expert's largest bit-width, and entries
 // with bit-width 0 (no work) up to `nitems`, the grid's work-item count, so
 // that a decode workgroup needs one load to learn its work.
@@ -168,16 +169,21 @@ __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
   __shared__ float wmax[kPrepThreads / 64];
   const int pos = blockIdx.x, NG = K / G;
   if (pos == npos && blockIdx.y == 0 && elist && threadIdx.x == 0) {
+    // experts in order of their largest bit-width, widest first, so that the
+    // longest work items are dispatched first and the short ones fill the
+    // end of the grid
     int n = 0;
-    for (int e = 0; e < E; ++e) {
-      if (maxbit[e] == 0) continue;
-      const int lo = offsets[e * L], hi = offsets[e * L + L];
-      for (int p = lo; p < hi; p += item) {
-        elist[4 * n] = e;
-        elist[4 * n + 1] = p;
-        elist[4 * n + 2] = min(p + item, hi);
-        elist[4 * n + 3] = maxbit[e];
-        ++n;
+    for (int b = 8; b >= 1; --b) {
+      for (int e = 0; e < E; ++e) {
+        if (maxbit[e] != b) continue;
+        const int lo = offsets[e * L], hi = offsets[e * L + L];
+        for (int p = lo; p < hi; p += item) {
+          elist[4 * n] = e;
+          elist[4 * n + 1] = p;
+          elist[4 * n + 2] = min(p + item, hi);
+          elist[4 * n + 3] = b;
+          ++n;
+        }
       }
     }
     // the remaining slots of the grid get no work (largest bit-width 0)
