@@ -44,23 +44,27 @@ template <bool NARROW> constexpr int n_waves() { return NARROW ? 8 : 4; }
 constexpr int kChunk = n_waves<false>() * kWaveM;  // positions per chunk
 constexpr int kTileRows = 128;              // weight rows per workgroup
 constexpr int kStepK = 32;                  // reduction columns per step
-// raw stages: the DMA runs kRawRing - 1 steps ahead of dequantization (4
-// stages; in the narrow kernel 8 measured the same and kept a third
-// workgroup off each compute unit)
-template <bool NARROW>
-constexpr int raw_ring() { return 4; }
 // activation lookahead in steps: one in the wide kernel (its 2-stage ring
 // leaves LDS for the tiles; the activations mostly come from L2), two in the
 // narrow one
 template <bool NARROW> constexpr int x_lead() { return NARROW ? 2 : 1; }
 constexpr int kXStage = kWaveM * kStepK * 2;  // bytes per wave and stage
-// Raw stage layout (bytes): plane p at 512 p (one word per tile row), scales
-// of level l at 4096 + 256 l (one binary16 per tile row, up to 8 levels),
-// zero points at 6144 (one byte per tile row).  16-byte DMA slots 0..391
-// carry them; DMA instruction i of wave w moves slots 256 i + 64 w .. + 63
-// (one instruction per wave in the 8-wave kernel, two in the 4-wave one).
-constexpr int kRawScaleOff = 4096, kRawZeroOff = 6144, kRawStage = 6272;
-constexpr int kRawSlots = 392;
+// Raw stage layout at MB planes and LS scale levels (bytes): plane p at
+// 512 p (one word per tile row), the scales of level l at 512 MB + 256 l (one
+// binary16 per tile row), then the zero points (one byte per tile row).
+// 16-byte DMA slots 0 .. raw_slots - 1 carry them; DMA instruction i of wave
+// w moves slots 256 i + 64 w .. + 63 (one instruction per wave in the 8-wave
+// kernel, two in the 4-wave one).  The ring holds as many stages as fit
+// kRawBytes, at most 8 (4 at 7 and 8 bits, 8 at 2 to 4), so the DMA runs
+// further ahead of the dequantization when a step has less to read.
+constexpr int kRawBytes = 25088;
+constexpr int raw_zero_off(int MB, int LS) { return 512 * MB + 256 * LS; }
+constexpr int raw_stage_bytes(int MB, int LS) { return raw_zero_off(MB, LS) + 128; }
+constexpr int raw_slots(int MB, int LS) { return raw_stage_bytes(MB, LS) / 16; }
+constexpr int raw_ring(int MB, int LS) {
+  return kRawBytes / raw_stage_bytes(MB, LS) < 8 ? kRawBytes / raw_stage_bytes(MB, LS) : 8;
+}
+static_assert(raw_ring(8, 8) >= 4, "at least 4 raw stages");
 template <bool NARROW> constexpr int raw_dmas() { return NARROW ? 1 : 2; }
 constexpr int kWTile = kTileRows * kStepK * 2;  // dequantized bf16 tile bytes
 
@@ -306,8 +310,7 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
   constexpr int NWV = n_waves<NARROW>(), RD = raw_dmas<NARROW>();
   constexpr int XL = x_lead<NARROW>(), kXRing = XL + 1;
   __shared__ __attribute__((aligned(16))) uint8_t xring[kXRing][NARROW ? 1 : NWV][kXStage];
-  constexpr int kRawRing = raw_ring<NARROW>();
-  __shared__ __attribute__((aligned(16))) uint8_t rraw[kRawRing][kRawStage];
+  __shared__ __attribute__((aligned(16))) uint8_t rraw[kRawBytes];  // ring of raw stages
   __shared__ __attribute__((aligned(16))) uint8_t wtile[2][kWTile];
   __shared__ __attribute__((aligned(16))) uint8_t dummy[1][16];
   constexpr int BR = 2048 / G, SPG = G / kStepK;  // rows per block, steps per group
@@ -341,7 +344,8 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
   constexpr bool narrow = NARROW;
   if (NARROW ? m_cnt > kWaveM : (split && m_cnt <= kWaveM)) return;
 
-  // ---- raw weight DMA: 16-byte slot u of the stage ----
+  // ---- raw weight DMA: 16-byte slot u of a stage laid out for MB planes
+  // and LS scale levels ----
   // global row of tile row r
   auto grow = [&](int r) { return SWIGLU ? (r < 64 ? n0 + r : f + n0 + r - 64) : n0 + r; };
   auto row_ok = [&](int r) { return SWIGLU ? n0 + (r & 63) < f : n0 + r < N; };
@@ -350,9 +354,10 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
     int sb, sc;          // bytes per group, per 32-column step
     bool real;
   };
-  auto raw_slot = [&](int u) {
+  auto raw_slot = [&](int u, int MB, int LS) {
     RawSlot q{(const uint8_t*)W.planes, 0, 0, false};
-    if (u < 256) {  // plane p = u / 32, tile rows 4 v .. 4 v + 3 of it
+    const int u1 = 32 * MB, u2 = u1 + 16 * LS;
+    if (u < u1) {  // plane p = u / 32, tile rows 4 v .. 4 v + 3 of it
       const int p = u >> 5, v = u & 31;
       const int r = 4 * v;  // first tile row of the slot
       if (p < bits && row_ok(r)) {
@@ -361,8 +366,8 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
         q = {(const uint8_t*)(W.planes + W.plane_word(blk, p, gr % BR)), W.b_max * 64 * 4, BR * 4,
              true};
       }
-    } else if (u < 256 + 16 * 8) {  // level l, tile rows 8 v .. 8 v + 7
-      const int l = (u - 256) >> 4, v = (u - 256) & 15;
+    } else if (u < u2) {  // level l, tile rows 8 v .. 8 v + 7
+      const int l = (u - u1) >> 4, v = (u - u1) & 15;
       const int r = 8 * v;
       if (l < nlev && row_ok(r)) {
         const int gr = grow(r);
@@ -370,8 +375,8 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
         q = {(const uint8_t*)(W.scales + W.scale_idx(blk, l, gr % BR)), W.levels() * BR * 2, 0,
              true};
       }
-    } else if (u < kRawSlots) {  // zero points, tile rows 16 z .. 16 z + 15
-      const int z = u - 256 - 16 * 8;
+    } else if (u < u2 + 8) {  // zero points, tile rows 16 z .. 16 z + 15
+      const int z = u - u2;
       const int r = 16 * z;
       if (row_ok(r)) {
         const int gr = grow(r);
@@ -380,29 +385,6 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
       }
     }
     return q;
-  };
-  // instruction i of this wave: slots ubase + lane, ubase = 256 i + 64 wave.
-  // Every wave issues RD raw DMAs per step (lane 0 at least), so that all
-  // waves count the same memory instructions: lanes whose slot is past the
-  // stage issue nothing, and an instruction with no slot of its own writes
-  // the dummy area from lane 0.
-  RawSlot rs[RD];
-  bool rissue[RD];
-#pragma unroll
-  for (int i = 0; i < RD; ++i) {
-    rs[i] = raw_slot(256 * i + 64 * wave + lane);
-    rissue[i] = rs[i].real || lane == 0;
-  }
-  auto raw_dma = [&](int step) {
-    const int st = s_lo + (step < nsteps ? step : nsteps - 1);  // past the end: reload, unused
-#pragma unroll
-    for (int i = 0; i < RD; ++i) {
-      const int ubase = 256 * i + 64 * wave;  // wave-uniform
-      const uint8_t* src = rs[i].src + (size_t)(st / SPG) * rs[i].sb + (st % SPG) * rs[i].sc;
-      uint8_t* dst = ubase < kRawSlots ? &rraw[step % kRawRing][16 * ubase] : dummy[0];
-      if (rissue[i])
-        __builtin_amdgcn_global_load_lds(D2MOE_GPTR(src), D2MOE_LPTR(dst), 16, 0, 0);
-    }
   };
 
   // ---- activation DMA: an instruction moves 16 positions' 64-byte rows.
@@ -449,18 +431,6 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
 #pragma unroll
     for (int b = 0; b < 8; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // ---- prologue: raw 0..kRawRing-1 and activations 0..XL-1 in flight.
-  // Issue order: raw 0 .. raw kRawRing-2, x 0, raw kRawRing-1 (, x 1); the
-  // wait leaves the instructions after raw 0 outstanding (RD per raw stage,
-  // XD per activation stage), i.e. raw 0 has landed.
-#pragma unroll
-  for (int i = 0; i + 1 < kRawRing; ++i) raw_dma(i);
-  x_dma(0);
-  raw_dma(kRawRing - 1);
-  if constexpr (XL == 2) x_dma(1);
-  wait_vm<(kRawRing - 1) * RD + XD + (XL == 2 ? XD : 0)>();
-  bar();
-
   // The step loop is compiled for the chunk's bit-width MB (and for b_min 2,
   // the common nest start, or any b_min) and separately for waves that
   // multiply and waves that only dequantize: every LDS read of a step, its
@@ -469,6 +439,48 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
   // instructions so that the matrix pipe and the vector ALU overlap.
   auto run = [&](auto mb_c, auto bmin_c) {
     constexpr int MB = decltype(mb_c)::value, BMIN = decltype(bmin_c)::value;
+    // scale levels reserved per stage: exact when b_min is fixed, else MB
+    constexpr int LS = BMIN > 0 ? MB - BMIN + 1 : MB;
+    constexpr int SB = raw_stage_bytes(MB, LS), NS = raw_slots(MB, LS);
+    constexpr int kRawRing = raw_ring(MB, LS);
+    constexpr int SOFF = 512 * MB, ZOFF = raw_zero_off(MB, LS);
+
+    // instruction i of this wave: slots ubase + lane, ubase = 256 i + 64 wave.
+    // Every wave issues RD raw DMAs per step (lane 0 at least), so that all
+    // waves count the same memory instructions: lanes whose slot is past the
+    // stage issue nothing, and an instruction with no slot of its own writes
+    // the dummy area from lane 0.
+    RawSlot rs[RD];
+    bool rissue[RD];
+#pragma unroll
+    for (int i = 0; i < RD; ++i) {
+      rs[i] = raw_slot(256 * i + 64 * wave + lane, MB, LS);
+      rissue[i] = rs[i].real || lane == 0;
+    }
+    auto raw_dma = [&](int step) {
+      const int st = s_lo + (step < nsteps ? step : nsteps - 1);  // past the end: reload, unused
+#pragma unroll
+      for (int i = 0; i < RD; ++i) {
+        const int ubase = 256 * i + 64 * wave;  // wave-uniform
+        const uint8_t* src = rs[i].src + (size_t)(st / SPG) * rs[i].sb + (st % SPG) * rs[i].sc;
+        uint8_t* dst = ubase < NS ? &rraw[(step % kRawRing) * SB + 16 * ubase] : dummy[0];
+        if (rissue[i])
+          __builtin_amdgcn_global_load_lds(D2MOE_GPTR(src), D2MOE_LPTR(dst), 16, 0, 0);
+      }
+    };
+
+    // ---- prologue: raw 0..kRawRing-1 and activations 0..XL-1 in flight.
+    // Issue order: raw 0 .. raw kRawRing-2, x 0, raw kRawRing-1 (, x 1); the
+    // wait leaves the instructions after raw 0 outstanding (RD per raw stage,
+    // XD per activation stage), i.e. raw 0 has landed.
+#pragma unroll
+    for (int i = 0; i + 1 < kRawRing; ++i) raw_dma(i);
+    x_dma(0);
+    raw_dma(kRawRing - 1);
+    if constexpr (XL == 2) x_dma(1);
+    wait_vm<(kRawRing - 1) * RD + XD + (XL == 2 ? XD : 0)>();
+    bar();
+
     StepRegs R;
     // One step: the products of `mstep` (if MMA) from the tile buffer and
     // activation stage written in earlier steps, and the dequantization of
@@ -480,23 +492,23 @@ __attribute__((amdgpu_waves_per_eu(NARROW ? 4 : 2))) void bgemm_kernel(
       constexpr bool MMA = decltype(mma_c)::value;
       // one address register per access width: the stage base plus this
       // thread's row, with the plane, level and operand block as offsets
-      const uint32_t rb = lds_addr(rraw[dstep % kRawRing]);
+      const uint32_t rb = lds_addr(rraw + (dstep % kRawRing) * SB);
       const uint32_t rb4 = rb + 4 * dr, rb2 = rb + 2 * dr, rb1 = rb + dr;
       static_for<MB>([&](auto pc) {
         constexpr int P = decltype(pc)::value;
         ld32<512 * P>(R.w[P], rb4);
       });
-      ldu16<kRawScaleOff>(R.s1, rb2);
+      ldu16<SOFF>(R.s1, rb2);
       static_for<MB>([&](auto pc) {  // level p - b_min + 1 holds the scale of plane p
         constexpr int P = decltype(pc)::value;
         if constexpr (BMIN > 0) {
-          if constexpr (P >= BMIN) ldu16<kRawScaleOff + 256 * (P - BMIN + 1)>(R.sp[P], rb2);
+          if constexpr (P >= BMIN) ldu16<SOFF + 256 * (P - BMIN + 1)>(R.sp[P], rb2);
         } else if constexpr (P >= 1) {  // below b_min the base scale is read and not used
           const int lvl = P >= b_min ? P - b_min + 1 : 0;
-          ldu16(R.sp[P], rb2 + kRawScaleOff + 256 * lvl);
+          ldu16(R.sp[P], rb2 + SOFF + 256 * lvl);
         }
       });
-      ldu8<kRawZeroOff>(R.z, rb1);
+      ldu8<ZOFF>(R.z, rb1);
       // a 16-row operand block m starts 1024 m bytes after block 0 (the
       // swizzle depends on the row within the block only)
       const uint32_t wb = lds_addr(wtile[mstep & 1]) + swz(fr, fq);
