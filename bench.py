@@ -285,12 +285,39 @@ def main():
         t_stop.record()
         torch.cuda.synchronize()
         ms = t_start.elapsed_time(t_stop) / steps
+        ms_eager = ms
+        if use_graphs:
+            # the kernel times above come from the eager steps' events; the
+            # step time from replays of one captured step per layer
+            cur = torch.cuda.current_stream()
+            side = torch.cuda.Stream()
+            side.wait_stream(cur)
+            with torch.cuda.stream(side):
+                for l in range(NL):
+                    step(l)
+            cur.wait_stream(side)
+            torch.cuda.synchronize()
+            graphs = []
+            for l in range(NL):
+                g_ = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g_):
+                    step(l)
+                graphs.append(g_)
+            wg = warm(lambda i: graphs[i % NL].replay(), warmup)
+            t_start.record()
+            for i in range(steps):
+                graphs[(wg + i) % NL].replay()
+            t_stop.record()
+            torch.cuda.synchronize()
+            ms = t_start.elapsed_time(t_stop) / steps
         d13 = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
         d2 = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
         flop13 = 2.0 * 2 * d * f * T * k
         flop2 = 2.0 * d * f * T * k
         hist = routs[(w0 + steps - 1) % NL].hist.cpu().numpy().sum(axis=1)
-        return {"tokens": T, "ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms * 1e-3), 1),
+        return {"tokens": T, "ms_per_step": round(ms, 4), "ms_per_step_eager": round(ms_eager, 4),
+                "launch": "hip graph per layer step" if use_graphs else "eager",
+                "tokens_per_s": round(T / (ms * 1e-3), 1),
                 "w13_ms": round(d13, 4), "w2_ms": round(d2, 4),
                 "w13_TFLOPs": round(flop13 / (d13 * 1e-3) / 1e12, 1),
                 "w2_TFLOPs": round(flop2 / (d2 * 1e-3) / 1e12, 1),
@@ -353,6 +380,31 @@ def main():
         t_stop.record()
         torch.cuda.synchronize()
         ms = t_start.elapsed_time(t_stop) / steps
+        ms_eager = ms
+        if use_graphs:
+            # one captured step (route + forward) per copy, replayed
+            cur = torch.cuda.current_stream()
+            side = torch.cuda.Stream()
+            side.wait_stream(cur)
+            with torch.cuda.stream(side):
+                for c in range(copies):
+                    step(c)
+            cur.wait_stream(side)
+            torch.cuda.synchronize()
+            graphs = []
+            for c in range(copies):
+                g_ = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g_):
+                    step(c)
+                graphs.append(g_)
+            wg = warm(lambda i: graphs[i % copies].replay(), warmup)
+            w0 = wg
+            t_start.record()
+            for i in range(steps):
+                graphs[(wg + i) % copies].replay()
+            t_stop.record()
+            torch.cuda.synchronize()
+            ms = t_start.elapsed_time(t_stop) / steps
         byts = []
         for c in range(copies):
             mb = sets[c][6].expert_maxbit.cpu().numpy()
@@ -366,8 +418,9 @@ def main():
         return {"workload": "fine-grained MoE layer (d_model 2048, 64 routed SwiGLU experts "
                             "d_ff 1408 top-6, shared expert d_ff 5632 at 8 bits, 512 tokens, "
                             "group 64, bits hottest-first 8/4/3/2), 4 rotating copies",
-                "tokens": T, "ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms * 1e-3), 1),
-                "alg_bytes": nbytes, "hbm_GBps": round(gbps, 1),
+                "tokens": T, "ms_per_step": round(ms, 4), "ms_per_step_eager": round(ms_eager, 4),
+                "launch": "hip graph per step" if use_graphs else "eager",
+                "tokens_per_s": round(T / (ms * 1e-3), 1), "alg_bytes": nbytes, "hbm_GBps": round(gbps, 1),
                 "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4), "alg_GFLOP": round(flop / 1e9, 2),
                 "TFLOPs": round(tflops, 1), "mfma_frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4)}
 

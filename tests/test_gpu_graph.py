@@ -21,30 +21,42 @@ def _snapshot(r: api.Routing, out):
     return {n: getattr(r, n).clone() for n in names} | {"out": out.clone()}
 
 
-@pytest.mark.parametrize("T", [4, 16])
-def test_captured_decode_step_replays_exactly(T):
-    L = Layer(wl.scaled(wl.mixtral_decode(T=T), d=512, f=384)).pack()
+GRAPH_SPECS = {
+    "decode_T4": wl.scaled(wl.mixtral_decode(T=4), d=512, f=384),
+    "decode_T16": wl.scaled(wl.mixtral_decode(T=16), d=512, f=384),
+    # the grouped-GEMM path: chunk tables built on the device, wide and narrow
+    # chunks, and a shared expert whose W2 reduction is split in parts
+    "prefill_small": wl.scaled(wl.mixtral_prefill(), d=256, f=384, T=600),
+    "fine_shared_split": wl.scaled(wl.fine_grained(), d=256, f=64, T=200, shared_f=1024),
+}
+
+
+@pytest.mark.parametrize("name", list(GRAPH_SPECS))
+def test_captured_step_replays_exactly(name):
+    L = Layer(GRAPH_SPECS[name]).pack()
     s = L.spec
     x = L.x_dev()
     Wg = torch.from_numpy(L.Wg).to(DEV)
+    bias = None if L.bias is None else torch.from_numpy(L.bias).to(DEV)
     req = torch.from_numpy(L.req).to(DEV)
     table = torch.from_numpy(L.table).to(DEV)
     r = api.Routing.empty(s.T, s.E, s.k, s.b_min, s.b_max, device=DEV)
     out = torch.empty_like(x)
-    ws = torch.empty(api.moe_forward_workspace(s.T, s.d, s.f, s.E, s.k), dtype=torch.uint8,
-                     device=DEV)
+    ws = torch.empty(api.moe_forward_workspace(s.T, s.d, s.f, s.E, s.k,
+                                               shared_d_ff=s.shared_f or 0),
+                     dtype=torch.uint8, device=DEV)
 
     def step():
-        api.route(x, Wg, None, s.k, req, table, s.b_min, s.b_max, out=r)
-        api.moe_forward(x, L.w13, L.w2, r, s.k, out=out, workspace=ws)
+        api.route(x, Wg, bias, s.k, req, table, s.b_min, s.b_max, out=r)
+        api.moe_forward(x, L.w13, L.w2, r, s.k, shared=L.shared, out=out, workspace=ws)
 
     step()
     torch.cuda.synchronize()
     want = _snapshot(r, out)
 
     # other eager work between replays: a different batch through the same layer
-    other = Layer(wl.scaled(wl.mixtral_decode(T=3), d=512, f=384))
-    other.w13, other.w2, other.shared = L.w13, L.w2, None
+    other = Layer(wl.scaled(s, T=3))
+    other.w13, other.w2, other.shared = L.w13, L.w2, L.shared
     other.route()
 
     g = torch.cuda.CUDAGraph()
