@@ -170,9 +170,11 @@ _VMEM_PREFIXES = ("global_", "buffer_", "flat_", "scratch_")
 
 def untracked_load_hazards(asm: str) -> list[tuple[str, str, str]]:
     """The decode kernels issue their activation loads as inline assembly
-    (global_load_dwordx4 under a narrowed EXEC) that the compiler does not
-    track: the data lands in the destination registers some time later, when
-    an explicit vmcnt wait covers it.  Vector-memory instructions of a wave
+    (global_load_dwordx4 under a narrowed EXEC), and so do the 4-wave GEMM
+    kernels (their A operands, one step ahead): the compiler does not track
+    them, and the data lands in the destination registers some time later,
+    when an explicit vmcnt wait covers it.  A load counts as untracked when it
+    sits inside an inline-asm block or right after an EXEC narrowing.  Vector-memory instructions of a wave
     complete in order, so a wait `s_waitcnt vmcnt(N)` covers the load once at
     most N vector-memory instructions were issued after it on the path taken.
     On every path from such a load, no instruction may read or write its
@@ -187,12 +189,17 @@ def untracked_load_hazards(asm: str) -> list[tuple[str, str, str]]:
     offending instruction) triples."""
     bad = []
     for fname, lines in _funcs(asm).items():
-        blocks = _basic_blocks(lines)
+        blocks = _basic_blocks(lines, asm_markers=True)
         for bi, b in enumerate(blocks):
+            inside = False
             for ii, x in enumerate(b["ins"]):
+                if x in ("ASMSTART", "ASMEND"):
+                    inside = x == "ASMSTART"
+                    continue
                 if not x.startswith("global_load_dwordx4"):
                     continue
-                if not any("s_and_saveexec" in y for y in b["ins"][max(0, ii - 2):ii]):
+                if not inside and not any("s_and_saveexec" in y
+                                          for y in b["ins"][max(0, ii - 3):ii]):
                     continue
                 dst = _vregs(x.split()[1].rstrip(","))
                 stack, seen = [(bi, ii + 1, 0)], set()
@@ -203,6 +210,8 @@ def untracked_load_hazards(asm: str) -> list[tuple[str, str, str]]:
                     seen.add((cb, ci, after))
                     stop = False
                     for y in blocks[cb]["ins"][ci:]:
+                        if y in ("ASMSTART", "ASMEND"):
+                            continue
                         op = y.split()[0]
                         if op == "s_waitcnt":
                             m = re.search(r"vmcnt\((\d+)\)", y)

@@ -65,6 +65,27 @@ def test_untracked_load_check_sees_overlapping_tracked_loads():
     assert build.untracked_load_hazards(TRACKED_WAW) == []
 
 
+# an inline-asm load (no EXEC narrowing), as the 4-wave GEMM kernels issue
+# their activation operands: the copy before the covering wait is flagged,
+# the same copy after vmcnt(1) (one DMA issued after the load) is not
+ASM_LOAD = HEAD + """
+	;;#ASMSTART
+	global_load_dwordx4 v[8:11], v[2:3], off
+	;;#ASMEND
+	global_load_lds_dwordx4 v[40:41], off
+	COPY_BEFORE
+	s_waitcnt vmcnt(1)
+	v_mov_b32_e32 v20, v9
+	s_endpgm
+"""
+
+
+def test_untracked_load_check_covers_inline_asm_loads():
+    assert build.untracked_load_hazards(ASM_LOAD.replace("\tCOPY_BEFORE\n", "")) == []
+    bad = build.untracked_load_hazards(ASM_LOAD.replace("COPY_BEFORE", "v_mov_b32_e32 v21, v10"))
+    assert len(bad) == 1 and "v10" in bad[0][2]
+
+
 def test_mfma_overlap_check():
     ok = "\tv_mfma_f32_16x16x32_bf16 v[0:3], v[4:7], v[8:11], v[0:3]\n"
     bad = "\tv_mfma_f32_16x16x32_bf16 v[4:7], v[4:7], v[8:11], 0\n"
