@@ -255,6 +255,14 @@ d2moe_status d2moe_moe_forward_workspace(int32_t T, int32_t d, int32_t d_ff,
  *   workspace: device buffer of at least d2moe_moe_forward_workspace bytes,
  *         256-byte aligned; contents need no initialisation.
  * Accumulation is fp32; bf16 outputs are rounded to nearest even.
+ * Parts of the layer that do not depend on each other (the shared expert;
+ * with more than 64 tokens, routed experts of at most 64 positions) run on
+ * two side streams of the calling host thread, forked from `stream` and
+ * joined back to it with events before the combine, so the call is ordered
+ * on `stream` like any other and can be captured in a HIP graph from it.
+ * The side streams and their events are created at the first such call of
+ * a host thread on a device and kept until the process ends: make that
+ * first call outside graph capture.
  */
 d2moe_status d2moe_moe_forward(const void* x, d2moe_dtype x_dtype, int32_t T,
                                int32_t d, int32_t d_ff, int32_t E, int32_t k,
@@ -267,7 +275,8 @@ d2moe_status d2moe_moe_forward(const void* x, d2moe_dtype x_dtype, int32_t T,
                                void* stream);
 
 /*
- * Same as d2moe_moe_forward, and additionally records events[0] / events[1]
+ * Same as d2moe_moe_forward, on `stream` alone (no side streams), and
+ * additionally records events[0] / events[1]
  * (hipEvent_t) at the start / end of the W1-W3 expert kernel and events[2] /
  * events[3] at the start / end of the W2 expert kernel, on `stream`, so a
  * caller can time the expert kernels on the stream they run on.  Up to 64
@@ -295,7 +304,8 @@ d2moe_status d2moe_moe_forward_profiled(const void* x, d2moe_dtype x_dtype, int3
  * GPU it runs on (a static device array, kept until the process ends; its
  * address is looked up once per device at the first call on it).  The call
  * allocates nothing; the caller still owns x, the weights, the routing and
- * out.  Sizes whose workspace (d2moe_moe_forward_workspace) exceeds the
+ * out, and everything runs on `stream` (no side streams are created).
+ * Sizes whose workspace (d2moe_moe_forward_workspace) exceeds the
  * array return D2MOE_ESCRATCH before anything is launched: 32 MiB covers,
  * for example, decode of up to 64 tokens of the Mixtral-8x7B layer shape.
  * Every call on one GPU uses that GPU's one array, whatever the stream:

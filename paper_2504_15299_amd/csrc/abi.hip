@@ -190,7 +190,7 @@ static d2moe_status forward_impl(const void* x, d2moe_dtype x_dtype, int32_t T, 
                                  const d2moe_mwq* shared_w13, const d2moe_mwq* shared_w2,
                                  int32_t shared_bits, int32_t shared_d_ff, void* out,
                                  void* workspace, size_t ws_bytes, void* stream,
-                                 void* const* events) {
+                                 void* const* events, bool concurrent) {
   if (T < 0 || d < 1 || d_ff < 1 || E < 1 || E > 64 || k < 1 || k > E) return D2MOE_EINVAL;
   if (x_dtype != D2MOE_F32 && x_dtype != D2MOE_BF16) return D2MOE_EUNSUPPORTED;
   if (!mwq_ok(w13) || !mwq_ok(w2) || !r) return D2MOE_EINVAL;
@@ -221,7 +221,7 @@ static d2moe_status forward_impl(const void* x, d2moe_dtype x_dtype, int32_t T, 
                                  has_shared ? shared_w13 : nullptr,
                                  has_shared ? shared_w2 : nullptr, shared_bits,
                                  has_shared ? shared_d_ff : 0, out, workspace,
-                                 (hipStream_t)stream, (hipEvent_t const*)events));
+                                 (hipStream_t)stream, (hipEvent_t const*)events, concurrent));
 }
 
 d2moe_status d2moe_moe_forward(const void* x, d2moe_dtype x_dtype, int32_t T, int32_t d,
@@ -231,7 +231,7 @@ d2moe_status d2moe_moe_forward(const void* x, d2moe_dtype x_dtype, int32_t T, in
                                int32_t shared_bits, int32_t shared_d_ff, void* out,
                                void* workspace, size_t ws_bytes, void* stream) {
   return forward_impl(x, x_dtype, T, d, d_ff, E, k, w13, w2, r, shared_w13, shared_w2,
-                      shared_bits, shared_d_ff, out, workspace, ws_bytes, stream, nullptr);
+                      shared_bits, shared_d_ff, out, workspace, ws_bytes, stream, nullptr, true);
 }
 
 d2moe_status d2moe_moe_forward_noalloc(const void* x, d2moe_dtype x_dtype, int32_t T,
@@ -252,7 +252,7 @@ d2moe_status d2moe_moe_forward_noalloc(const void* x, d2moe_dtype x_dtype, int32
   if (st != D2MOE_OK) return st;
   return forward_impl(x, x_dtype, T, d, d_ff, E, k, w13, w2, r, shared_w13, shared_w2,
                       shared_bits, shared_d_ff, out, ws, (size_t)D2MOE_NOALLOC_SCRATCH_BYTES,
-                      stream, nullptr);
+                      stream, nullptr, false);
 }
 
 d2moe_status d2moe_moe_forward_profiled(const void* x, d2moe_dtype x_dtype, int32_t T,
@@ -264,7 +264,7 @@ d2moe_status d2moe_moe_forward_profiled(const void* x, d2moe_dtype x_dtype, int3
                                         size_t ws_bytes, void* stream, void* const* events) {
   if (!events || !events[0] || !events[1] || !events[2] || !events[3]) return D2MOE_EINVAL;
   return forward_impl(x, x_dtype, T, d, d_ff, E, k, w13, w2, r, shared_w13, shared_w2,
-                      shared_bits, shared_d_ff, out, workspace, ws_bytes, stream, events);
+                      shared_bits, shared_d_ff, out, workspace, ws_bytes, stream, events, false);
 }
 
 d2moe_status d2moe_residual_rmsnorm(float* x, const void* y, d2moe_dtype y_dtype, int32_t T,

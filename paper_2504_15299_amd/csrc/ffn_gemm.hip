@@ -815,11 +815,12 @@ void shared_plan(int T, int d, int shared_d_ff, int* cs, int* ksplit) {
 
 // `split`: run chunks of at most 64 positions in the narrow kernel (worth
 // it when most chunks are narrow: a second launch runs after the first, and
-// its workgroups are as long as the reduction dimension).
+// its workgroups are as long as the reduction dimension).  `part` (with
+// split): 0 both launches, 1 the wide one only, 2 the narrow one only.
 template <bool SWIGLU>
 hipError_t run_gemm(const uint16_t* in, int in_ld, const int32_t* perm, int kdiv, const MwqView& W,
                     const int32_t* chunks, int n_ub, int f, void* out, int out_ld, bool split,
-                    hipStream_t s, int ksplit = 1, size_t out_split = 0) {
+                    hipStream_t s, int ksplit = 1, size_t out_split = 0, int part = 0) {
   const int N = SWIGLU ? W.rows / 2 : W.rows;
   const int per = SWIGLU ? kTileRows / 2 : kTileRows;
   // weight-row tiles vary fastest: consecutive workgroups, which the
@@ -832,16 +833,19 @@ hipError_t run_gemm(const uint16_t* in, int in_ld, const int32_t* perm, int kdiv
   // chunks of at most 64
   const int sp = split ? 1 : 0;
   constexpr int kWide = 64 * n_waves<false>(), kNarrow = 64 * n_waves<true>();
+  const bool wide = !split || part != 2, narrow = split && part != 1;
   if (W.group == 128) {
-    bgemm_kernel<128, SWIGLU, false><<<grid, kWide, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f, N,
-                                                            out, out_ld, sp, out_split);
-    if (split)
+    if (wide)
+      bgemm_kernel<128, SWIGLU, false><<<grid, kWide, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f,
+                                                              N, out, out_ld, sp, out_split);
+    if (narrow)
       bgemm_kernel<128, SWIGLU, true><<<grid, kNarrow, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f,
                                                                N, out, out_ld, sp, out_split);
   } else {
-    bgemm_kernel<64, SWIGLU, false><<<grid, kWide, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f, N,
-                                                           out, out_ld, sp, out_split);
-    if (split)
+    if (wide)
+      bgemm_kernel<64, SWIGLU, false><<<grid, kWide, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f,
+                                                             N, out, out_ld, sp, out_split);
+    if (narrow)
       bgemm_kernel<64, SWIGLU, true><<<grid, kNarrow, 0, s>>>(in, in_ld, perm, kdiv, W, chunks, f,
                                                               N, out, out_ld, sp, out_split);
   }
@@ -882,6 +886,37 @@ FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shar
   L.hmax_off = off;   off += align256(nd * ((size_t)(d_ff + 15) / 16) * sizeof(uint32_t));
   L.total = off;
   return L;
+}
+
+// Side streams of the calling host thread on the current device (created at
+// its first concurrent forward there, default priority, kept until the
+// process ends), and the events that fork work onto them from the caller's
+// stream and join it back.  Per thread, so that calls from different host
+// threads never wait on each other's events.
+struct SideStreams {
+  hipStream_t s[2] = {nullptr, nullptr};
+  hipEvent_t fork = nullptr, join[2] = {nullptr, nullptr};
+};
+constexpr int kMaxSideDevices = 64;
+hipError_t side_streams(SideStreams** out) {
+  thread_local SideStreams cache[kMaxSideDevices];
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return err;
+  if (dev < 0 || dev >= kMaxSideDevices) return hipErrorInvalidDevice;
+  SideStreams& ss = cache[dev];
+  if (ss.fork == nullptr) {
+    SideStreams n;
+    for (int i = 0; i < 2; ++i) {
+      if ((err = hipStreamCreateWithFlags(&n.s[i], hipStreamNonBlocking)) != hipSuccess) return err;
+      if ((err = hipEventCreateWithFlags(&n.join[i], hipEventDisableTiming)) != hipSuccess)
+        return err;
+    }
+    if ((err = hipEventCreateWithFlags(&n.fork, hipEventDisableTiming)) != hipSuccess) return err;
+    ss = n;
+  }
+  *out = &ss;
+  return hipSuccess;
 }
 
 // The layer with its expert weights streamed in (Sec. 3.4): units in the
@@ -951,7 +986,7 @@ hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff,
                           const d2moe_mwq* w13, const d2moe_mwq* w2, const d2moe_routing* r,
                           const d2moe_mwq* sw13, const d2moe_mwq* sw2, int shared_bits,
                           int shared_d_ff, void* out, void* ws, hipStream_t s,
-                          const hipEvent_t* events) {
+                          const hipEvent_t* events, bool concurrent) {
   if (T == 0) return hipSuccess;
   const bool has_shared = sw13 != nullptr;
   const FwdWorkspace L = fwd_workspace_layout(T, d, d_ff, E, k, has_shared ? shared_d_ff : 0);
@@ -977,7 +1012,40 @@ hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff,
   }
 
   hipError_t err;
-  if (decode_path_ok(w13, w2, T)) {
+  // Concurrency: the shared expert's chain, and with split the narrow
+  // routed chunks, run on side streams forked from `s` (they write disjoint
+  // workspace: hs / ys, and other rows of h / y than the wide chunks); the
+  // combine waits for both.  Not with events: those time the kernels on `s`.
+  const bool decode = decode_path_ok(w13, w2, T);
+  const bool split = !decode && (long)T * k <= 64L * E;
+  const bool fork_shared = concurrent && !events && has_shared;
+  const bool fork_narrow = concurrent && !events && split;
+  SideStreams* side = nullptr;
+  if (fork_shared || fork_narrow)
+    if ((err = side_streams(&side)) != hipSuccess) return err;
+
+  if (has_shared) {
+    hipStream_t ss = s;
+    if (fork_shared) {
+      ss = side->s[1];
+      if ((err = hipEventRecord(side->fork, s)) != hipSuccess) return err;
+      if ((err = hipStreamWaitEvent(ss, side->fork, 0)) != hipSuccess) return err;
+    }
+    const int ns_ub = L.schunk_n, cs = L.shared_chunk, ks = L.shared_ksplit;
+    chunk_kernel<<<1, kChunkThreads, 0, ss>>>(nullptr, nullptr, 0, 1, sw13->b_min, T, shared_bits,
+                                             cs, ns_ub, schunks);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    const MwqView S13 = view_of(sw13), S2 = view_of(sw2);
+    err = run_gemm<true>(xb, d, nullptr, 1, S13, schunks, ns_ub, shared_d_ff, hs, shared_d_ff,
+                         cs <= kWaveM, ss);
+    if (err != hipSuccess) return err;
+    err = run_gemm<false>(hs, shared_d_ff, nullptr, 1, S2, schunks, ns_ub, shared_d_ff, ys, d,
+                          cs <= kWaveM, ss, ks, (size_t)T * d);
+    if (err != hipSuccess) return err;
+    if (fork_shared && (err = hipEventRecord(side->join[1], ss)) != hipSuccess) return err;
+  }
+
+  if (decode) {
     DecodeBuffers db;
     db.elist = (int32_t*)(base + L.elist_off);
     db.xq13 = (uint8_t*)(base + L.xq13_off);
@@ -995,32 +1063,30 @@ hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff,
                                             kChunk, n_ub, chunks);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     const MwqView W13 = view_of(w13), W2 = view_of(w2);
-    if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
     // narrow chunks get their own launch when experts average at most 64
-    // positions
-    const bool split = (long)T * k <= 64L * E;
-    err = run_gemm<true>(xb, d, r->perm, k, W13, chunks, n_ub, d_ff, h, d_ff, split, s);
+    // positions; forked, they run beside the wide ones
+    if (fork_narrow) {
+      hipStream_t sn = side->s[0];
+      if ((err = hipEventRecord(side->fork, s)) != hipSuccess) return err;
+      if ((err = hipStreamWaitEvent(sn, side->fork, 0)) != hipSuccess) return err;
+      err = run_gemm<true>(xb, d, r->perm, k, W13, chunks, n_ub, d_ff, h, d_ff, true, sn, 1, 0, 2);
+      if (err != hipSuccess) return err;
+      err = run_gemm<false>(h, d_ff, nullptr, 1, W2, chunks, n_ub, d_ff, y, d, true, sn, 1, 0, 2);
+      if (err != hipSuccess) return err;
+      if ((err = hipEventRecord(side->join[0], sn)) != hipSuccess) return err;
+    }
+    const int part = fork_narrow ? 1 : 0;
+    if (events && (err = hipEventRecord(events[0], s)) != hipSuccess) return err;
+    err = run_gemm<true>(xb, d, r->perm, k, W13, chunks, n_ub, d_ff, h, d_ff, split, s, 1, 0, part);
     if (err != hipSuccess) return err;
     if (events && (err = hipEventRecord(events[1], s)) != hipSuccess) return err;
     if (events && (err = hipEventRecord(events[2], s)) != hipSuccess) return err;
-    err = run_gemm<false>(h, d_ff, nullptr, 1, W2, chunks, n_ub, d_ff, y, d, split, s);
+    err = run_gemm<false>(h, d_ff, nullptr, 1, W2, chunks, n_ub, d_ff, y, d, split, s, 1, 0, part);
     if (err != hipSuccess) return err;
     if (events && (err = hipEventRecord(events[3], s)) != hipSuccess) return err;
+    if (fork_narrow && (err = hipStreamWaitEvent(s, side->join[0], 0)) != hipSuccess) return err;
   }
-
-  if (has_shared) {
-    const int ns_ub = L.schunk_n, cs = L.shared_chunk, ks = L.shared_ksplit;
-    chunk_kernel<<<1, kChunkThreads, 0, s>>>(nullptr, nullptr, 0, 1, sw13->b_min, T, shared_bits,
-                                            cs, ns_ub, schunks);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
-    const MwqView S13 = view_of(sw13), S2 = view_of(sw2);
-    err = run_gemm<true>(xb, d, nullptr, 1, S13, schunks, ns_ub, shared_d_ff, hs, shared_d_ff,
-                         cs <= kWaveM, s);
-    if (err != hipSuccess) return err;
-    err = run_gemm<false>(hs, shared_d_ff, nullptr, 1, S2, schunks, ns_ub, shared_d_ff, ys, d,
-                          cs <= kWaveM, s, ks, (size_t)T * d);
-    if (err != hipSuccess) return err;
-  }
+  if (fork_shared && (err = hipStreamWaitEvent(s, side->join[1], 0)) != hipSuccess) return err;
 
   dim3 cg((d + 255) / 256, T);
   if (xd == D2MOE_BF16)

@@ -123,10 +123,13 @@ hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, int
 hipError_t launch_residual_rmsnorm(float* x, const void* y, d2moe_dtype yd, int T, int d,
                                    float eps, void* h, d2moe_dtype hd, hipStream_t s);
 
+// concurrent: independent parts of the layer (the shared expert, the
+// narrow routed chunks) may run on this host thread's side streams of the
+// current device, forked from and joined back to `s` with events.
 hipError_t launch_forward(const void* x, d2moe_dtype xd, int T, int d, int d_ff, int E, int k,
                           const d2moe_mwq* w13, const d2moe_mwq* w2, const d2moe_routing* r,
                           const d2moe_mwq* sw13, const d2moe_mwq* sw2, int shared_bits,
                           int shared_d_ff, void* out, void* ws, hipStream_t s,
-                          const hipEvent_t* events);
+                          const hipEvent_t* events, bool concurrent);
 
 }  // namespace d2moe
