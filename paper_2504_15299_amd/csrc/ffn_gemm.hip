@@ -73,9 +73,11 @@ constexpr int kWTile = kTileRows * kStepK * 2;  // dequantized bf16 tile bytes
 
 // Chunk table, written on the device from the routing histogram:
 // chunks[4 c] = first position, positions (0: no work), bit-width, expert.
-// Buckets are taken in order of size (largest first, ties in bucket order)
-// so that the longest workgroups start first.  One workgroup of kChunkThreads
-// threads, one bucket per thread (nb <= kChunkThreads, bucket index < 1024).
+// Buckets are taken in order of bit-width (widest first: a workgroup's time
+// grows with the planes it dequantizes), then of size (largest first, ties
+// in bucket order), so that the longest workgroups start first.  One
+// workgroup of kChunkThreads threads, one bucket per thread (nb <=
+// kChunkThreads, bucket index < 1024).
 constexpr int kChunkThreads = 512;
 __global__ __launch_bounds__(kChunkThreads) void chunk_kernel(
     const int32_t* __restrict__ hist, const int32_t* __restrict__ offsets, int nb, int L, int b_min,
@@ -93,11 +95,14 @@ __global__ __launch_bounds__(kChunkThreads) void chunk_kernel(
     }
     return;
   }
-  // sort buckets by (size descending, index ascending): bitonic sort of one
-  // 64-bit key per thread, size in the high bits and 1023 - index in the low
-  // ten (empty slots have key 0 and sort last)
+  // sort buckets by (bit-width, size) descending, index ascending: bitonic
+  // sort of one 64-bit key per thread, the width level in bits 50..53, size
+  // in bits 10..49 and 1023 - index in the low ten (empty buckets have key 0
+  // and sort last)
   const int cj = j < nb ? hist[j] : 0;
-  key[j] = j < nb ? ((unsigned long long)cj << 10) | (unsigned)(1023 - j) : 0ull;
+  key[j] = j < nb && cj > 0 ? ((unsigned long long)(j % L + 1) << 50) |
+                                  ((unsigned long long)cj << 10) | (unsigned)(1023 - j)
+                            : 0ull;
   __syncthreads();
   for (int kk = 2; kk <= kChunkThreads; kk <<= 1) {
     for (int jj = kk >> 1; jj > 0; jj >>= 1) {
@@ -115,7 +120,7 @@ __global__ __launch_bounds__(kChunkThreads) void chunk_kernel(
   }
   // chunks of the bucket at sorted position j, and their exclusive prefix
   const unsigned long long kj = key[j];
-  const int cnt_j = (int)(kj >> 10), bkt = 1023 - (int)(kj & 1023ull);
+  const int cnt_j = (int)((kj >> 10) & ((1ull << 40) - 1)), bkt = 1023 - (int)(kj & 1023ull);
   const int nch_j = (cnt_j + kChunk - 1) / kChunk;
   scan[j] = nch_j;
   __syncthreads();
