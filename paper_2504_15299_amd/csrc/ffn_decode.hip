@@ -699,10 +699,12 @@ __device__ inline void decode_groups(const WaveCtx<NCB>& c, uint8_t* ring, int g
 // One W2 row block per workgroup: its NW waves split the groups and combine
 // their partial sums through LDS (each wave's partial sums go to its own
 // ring, which is idle by then).  NCB column blocks of 8 tokens share every
-// plane operand (two when experts hold more than 7 positions on average), at
-// 4 waves per SIMD for one block and 3 for two.
+// plane operand (two when experts hold more than 7 positions on average,
+// three above 12), at 4 waves per SIMD for one block, 3 for two and 2 for
+// three (three blocks need more than the 168 registers of 3 waves).
 template <int NW, int NCB, int BMIN>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NCB == 1 ? 4 : 3)))
+__global__ __launch_bounds__(64 * NW)
+__attribute__((amdgpu_waves_per_eu(NCB == 1 ? 4 : NCB == 2 ? 3 : 2)))
 void decode_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* __restrict__ Xq,
                    const uint32_t* __restrict__ Xs, int npos, float* __restrict__ out,
                    int out_ld) {
@@ -954,7 +956,8 @@ __device__ inline void decode_pairs(const WaveCtx<NCB>& c, const W3Offsets& o3, 
 // Workgroup x covers NW / KS such units.  With KS > 1 the waves' partial sums
 // meet in their (then idle) rings and the first wave of each unit finishes.
 template <int NW, int KS, int NCB, int BMIN, bool SWIGLU>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NCB == 1 ? 4 : 3)))
+__global__ __launch_bounds__(64 * NW)
+__attribute__((amdgpu_waves_per_eu(NCB == 1 ? 4 : NCB == 2 ? 3 : 2)))
 void decode13_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* __restrict__ Xq,
                      const uint32_t* __restrict__ Xs, int npos, int f, float* __restrict__ out,
                      int out_ld, uint32_t* __restrict__ rowmax) {
@@ -1206,8 +1209,11 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   // its positions instead of once per 8).  Below that, streaming the few
   // experts with more than 8 positions twice costs less than doubling the
   // MFMAs and scale FMAs per plane for every expert (measured from 20 to 32
-  // tokens at the Mixtral shape).
-  const int ncb = npos > 7 * E ? 2 : 1;
+  // tokens at the Mixtral shape).  Three above 12 on average: at 16 (64
+  // tokens, top-2 of 8) about 4 experts in 10 hold more than 16 positions,
+  // and streaming them once for up to 24 took the step from 0.54-0.56 to
+  // 0.51-0.52 ms at the Mixtral shape.
+  const int ncb = npos > 12 * E ? 3 : npos > 7 * E ? 2 : 1;
   const int item = ncb * kDecodeCols;
   // work items: each active expert's positions in runs of `item`
   const int ny = (E < npos ? E : npos) + (npos + item - 1) / item;
@@ -1236,10 +1242,15 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
                                              d_ff, b.h32, d_ff, b.hmax, s, e0, e1)
               : launch_decode13_kernel<2, 1>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos,
                                              d_ff, b.h32, d_ff, b.hmax, s, e0, e1);
-  else
+  else if (ncb == 2)
     err = ks4 ? launch_decode13_kernel<4, 2>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos,
                                              d_ff, b.h32, d_ff, b.hmax, s, e0, e1)
               : launch_decode13_kernel<2, 2>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos,
+                                             d_ff, b.h32, d_ff, b.hmax, s, e0, e1);
+  else
+    err = ks4 ? launch_decode13_kernel<4, 3>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos,
+                                             d_ff, b.h32, d_ff, b.hmax, s, e0, e1)
+              : launch_decode13_kernel<2, 3>(w13->b_min, ny, W13, b.elist, b.xq13, b.xs13, npos,
                                              d_ff, b.h32, d_ff, b.hmax, s, e0, e1);
   if (err != hipSuccess) return err;
   err = run_xprep<float>(b.h32, d_ff, nullptr, 1, npos, d_ff, b.hmax, d_ff / 16, b.xq2, b.xs2, r,
@@ -1257,14 +1268,19 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   if (pairs2 && ncb == 1)
     err = launch_decode13_kernel<kW2Split, 1, false>(w2->b_min, ny, W2, b.elist, b.xq2, b.xs2,
                                                      npos, d, b.y, d, nullptr, s, e2, e3);
-  else if (pairs2)
+  else if (pairs2 && ncb == 2)
     err = launch_decode13_kernel<kW2Split, 2, false>(w2->b_min, ny, W2, b.elist, b.xq2, b.xs2,
                                                      npos, d, b.y, d, nullptr, s, e2, e3);
+  else if (pairs2)
+    err = launch_decode13_kernel<kW2Split, 3, false>(w2->b_min, ny, W2, b.elist, b.xq2, b.xs2,
+                                                     npos, d, b.y, d, nullptr, s, e2, e3);
   else
-    err = ncb == 1 ? launch_decode_kernel<1>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos, b.y,
-                                             d, s, e2, e3)
-                   : launch_decode_kernel<2>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos, b.y,
-                                             d, s, e2, e3);
+    err = ncb == 1   ? launch_decode_kernel<1>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
+                                               b.y, d, s, e2, e3)
+          : ncb == 2 ? launch_decode_kernel<2>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
+                                               b.y, d, s, e2, e3)
+                     : launch_decode_kernel<3>(w2->b_min, g2, W2, b.elist, b.xq2, b.xs2, npos,
+                                               b.y, d, s, e2, e3);
   if (err != hipSuccess) return err;
   return hipSuccess;
 }

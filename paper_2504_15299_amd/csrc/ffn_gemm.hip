@@ -882,7 +882,7 @@ FwdWorkspace fwd_workspace_layout(int T, int d, int d_ff, int E, int k, int shar
   L.elist_off = off;  off += align256(sizeof(int32_t) * (4 * ((size_t)E + (nd + 7) / 8) + 4));
   const size_t nz = nd ? nd + 1 : 0;  // plus one all-zero activation slot
   L.xq13_off = off;   off += align256(nz * d * 2);
-  const size_t nxs = nz ? nz + 16 : 0;  // info words, padded for 16-position reads
+  const size_t nxs = nz ? nz + 24 : 0;  // info words, padded for 24-position reads
   L.xs13_off = off;   off += align256(nxs * sizeof(uint32_t));
   L.h32_off = off;    off += align256(nd * d_ff * sizeof(float));
   L.xq2_off = off;    off += align256(nz * d_ff * 2);

@@ -231,6 +231,16 @@ FWD_SPECS = {
                                bits_choices=(7, 8), bits_probs=None),
     "decode_b8_T40": wl.scaled(wl.mixtral_decode(T=40), d=256, f=256, b_min=8, b_max=8,
                                bits_choices=(8,), bits_probs=None),
+    # three column blocks per work item (experts hold more than 12 positions
+    # on average): W2 in the 4-wave-per-row-block kernel at d 512, at nest
+    # starts 2 and 1; W1/W3 with two waves per row block and W2 in the pair
+    # kernel at 16 experts, d 1536, d_ff 2048, k 4
+    "decode_ncb3_b2_T64": wl.scaled(wl.mixtral_decode(T=64), d=512, f=384),
+    "decode_ncb3_b1_T64": wl.scaled(wl.mixtral_decode(T=64), d=512, f=384, b_min=1, b_max=5,
+                                    bits_choices=(1, 2, 5), bits_probs=None),
+    "decode_ncb3_pairs_T64": wl.scaled(wl.mixtral_decode(T=64), d=1536, f=2048, E=16, k=4,
+                                       b_min=3, b_max=6, bits_choices=(3, 4, 6),
+                                       bits_probs=None),
     # 16 experts with d_ff 2048 fill the GPU's wave slots with two waves per
     # W1/W3 row block (the split every full-size batch above 1 uses): one
     # column block at T 32 (b_min 1), two at T 64 (b_min 3)
