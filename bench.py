@@ -116,7 +116,7 @@ def main():
                          "hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build runs the MoE layer on a single "
+        print("bench.py measures one GPU only: the library runs the MoE layer on a single "
               "MI355X and has no multi-GPU path; run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
