@@ -255,6 +255,9 @@ FWD_SPECS = {
     # shared expert cut into 64-position chunks with its W2 reduction split in
     # two parts summed by the combine
     "fine_shared_split": wl.scaled(wl.fine_grained(), d=256, f=64, T=200, shared_f=1024),
+    # decode kernels for the routed experts on the caller's stream while the
+    # shared expert's grouped GEMM runs on a side stream
+    "decode_shared_T16": wl.scaled(wl.mixtral_decode(T=16), d=512, f=384, shared_f=512),
     # enough decode work items (64 experts) for the W2 kernel that streams
     # pairs of adjacent row blocks, at one column block (k 4: 256 positions)
     # and at two (k 10: 640 positions)
