@@ -28,14 +28,29 @@ __device__ inline void load8(const uint16_t* p, float (&v)[8]) {
   }
 }
 __device__ inline float load1(const float* p) { return *p; }
+
+// Sum over the wave, valid in lane 0: each row of 16 lanes is summed with DPP
+// row shifts (lane i adds lane i + 8, + 4, + 2, + 1), then lane 0 adds the
+// four row sums pairwise.  Six additions per term, as in a shuffle
+// butterfly, without the LDS permute path.
+__device__ inline float wave_sum_lane0(float v) {
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x108, 0xf, 0xf, true));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x104, 0xf, 0xf, true));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x102, 0xf, 0xf, true));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x101, 0xf, 0xf, true));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return (v + r1) + (r2 + r3);
+}
 __device__ inline float load1(const uint16_t* p) { return bf2f(*p); }
 
 // logits[t][e] = x[t] . Wg[e] (+ bias[e]) for a tile of TT tokens by EE
 // experts per workgroup.  Each thread takes 8 consecutive columns per step
 // (one 16-byte load of x per token, two of each gate row) with one fp32 fma
 // chain per (token, expert); the partial sums are reduced across the wave
-// with shuffles and across the waves through LDS.  A term passes through at
-// most ceil(d/256) + 11 roundings.  Small batches use 1 x 1 tiles, so that
+// (DPP row shifts, then the four rows) and across the waves through LDS.  A
+// term passes through at most ceil(d/256) + 11 roundings.  Small batches use 1 x 1 tiles, so that
 // many workgroups share the loads and every one of them is short; large
 // batches use 4 x 8 tiles, which read each gate row once per four tokens.
 template <typename XT, int TT, int EE>
@@ -93,8 +108,7 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(
   for (int i = 0; i < TT; ++i)
 #pragma unroll
     for (int j = 0; j < EE; ++j) {
-      float v = acc[i][j];
-      for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+      const float v = wave_sum_lane0(acc[i][j]);
       if (lane == 0) part[wave][i * EE + j] = v;
     }
   __syncthreads();
