@@ -190,54 +190,79 @@ def untracked_load_hazards(asm: str) -> list[tuple[str, str, str]]:
     bad = []
     for fname, lines in _funcs(asm).items():
         blocks = _basic_blocks(lines, asm_markers=True)
+        # each instruction parsed once: (text, kind, value, registers), kind
+        # "wait" (value: its vmcnt, or None), "mfma" (registers: its B
+        # operand; value: the registers it reads otherwise), or "ins"
+        # (registers: what it reads, value: whether it is vector memory)
+        parsed = []
+        for b in blocks:
+            pb = []
+            for y in b["ins"]:
+                if y in ("ASMSTART", "ASMEND"):
+                    continue
+                op = y.split()[0]
+                if op == "s_waitcnt":
+                    m = re.search(r"vmcnt\((\d+)\)", y)
+                    pb.append((y, "wait", int(m.group(1)) if m else None, None))
+                    continue
+                operands = y.split(None, 1)[1] if " " in y else ""
+                reads = set()
+                rd_ops = operands
+                if _is_vector_load(op):
+                    rd_ops = operands.split(",", 1)[1] if "," in operands else ""
+                for t in re.findall(r"v\[\d+:\d+\]|v\d+\b", rd_ops):
+                    reads |= _vregs(t)
+                if op.startswith("v_mfma"):
+                    ops = [o.strip() for o in operands.split(",")]
+                    pb.append((y, "mfma", reads, _vregs(ops[2].split()[0])))
+                else:
+                    pb.append((y, "ins", op.startswith(_VMEM_PREFIXES), reads))
+            parsed.append(pb)
         for bi, b in enumerate(blocks):
             inside = False
+            k = 0  # index of the next parsed instruction of this block
             for ii, x in enumerate(b["ins"]):
                 if x in ("ASMSTART", "ASMEND"):
                     inside = x == "ASMSTART"
                     continue
+                k += 1
                 if not x.startswith("global_load_dwordx4"):
                     continue
                 if not inside and not any("s_and_saveexec" in y
                                           for y in b["ins"][max(0, ii - 3):ii]):
                     continue
                 dst = _vregs(x.split()[1].rstrip(","))
-                stack, seen = [(bi, ii + 1, 0)], set()
+                stack, seen = [(bi, k, 0)], set()
                 while stack:
                     cb, ci, after = stack.pop()
                     if (cb, ci, after) in seen:
                         continue
                     seen.add((cb, ci, after))
                     stop = False
-                    for y in blocks[cb]["ins"][ci:]:
-                        if y in ("ASMSTART", "ASMEND"):
-                            continue
-                        op = y.split()[0]
-                        if op == "s_waitcnt":
-                            m = re.search(r"vmcnt\((\d+)\)", y)
-                            if m and int(m.group(1)) <= after:
+                    for y, kind, val, regs in parsed[cb][ci:]:
+                        if kind == "wait":
+                            if val is not None and val <= after:
                                 stop = True      # the load has landed
                                 break
                             continue
-                        if op.startswith("v_mfma"):
-                            ops = [o.strip() for o in y.split(None, 1)[1].split(",")]
-                            if _vregs(ops[2].split()[0]) & dst:
+                        if kind == "mfma":
+                            if regs & dst:
                                 stop = True      # the consuming MFMA
                                 break
-                        # a later load may write the same registers (its data
-                        # lands after this load's: loads complete in order),
-                        # but none may read them, e.g. as its address
-                        operands = y.split(None, 1)[1] if " " in y else ""
-                        if _is_vector_load(op):
-                            operands = operands.split(",", 1)[1] if "," in operands else ""
-                        hit = set()
-                        for t in re.findall(r"v\[\d+:\d+\]|v\d+\b", operands):
-                            hit |= _vregs(t)
-                        if hit & dst:
+                            # a later load may write the same registers (its
+                            # data lands after this load's: loads complete in
+                            # order), but none may read them, e.g. as its
+                            # address
+                            if val & dst:
+                                bad.append((fname, x, y))
+                                stop = True
+                                break
+                            continue
+                        if regs & dst:
                             bad.append((fname, x, y))
                             stop = True
                             break
-                        if op.startswith(_VMEM_PREFIXES):
+                        if val:
                             after = min(after + 1, 64)
                     if not stop:
                         stack.extend((sb, 0, after) for sb in blocks[cb]["succ"])

@@ -428,13 +428,13 @@ __device__ inline void gload16(v4i& v, const uint8_t* p, uint64_t m) {
       : "memory", "scc");
 }
 
-// Two memory instructions per column block, issued by the lanes that hold a
-// token (lane 0 always does); the other lanes keep the zeros they were given
-// before the loop.
-template <int NCB>
+// Two memory instructions per live column block (the first NL), issued by the
+// lanes that hold a token (lane 0 always does); the other lanes keep the zeros
+// they were given before the loop.
+template <int NL, int NCB>
 __device__ inline void load_b(BData<NCB>& t, const WaveCtx<NCB>& c, int g) {
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) {
+  for (int cb = 0; cb < NL; ++cb) {
     const uint8_t* src = c.xq[cb] + (size_t)g * 256;
     gload16(t.lo[cb], src, c.lmask[cb]);
     gload16(t.hi[cb], src + 16, c.lmask[cb]);
@@ -558,13 +558,14 @@ __device__ inline v8i ones_operand() {
 // block scale: E8M0 code 0 scales that column's products by 2^-127, which
 // leaves at most ~1e-33 (|x| < 2^9 per fp8 piece, 128 terms) in place of an
 // exact zero.
-template <int MB, int BMIN, int SOFF, int NCB>
+template <int MB, int BMIN, int SOFF, int NL, int NCB>
 __device__ inline void compute_group(const BData<NCB>& t, const WaveCtx<NCB>& c,
                                      v4f (&acc)[NCB]) {
+  static_assert(NL >= 1 && NL <= NCB, "live column blocks");
   using SL = StageLayout<MB, BMIN>;
   int bit[NCB], bsc[NCB];
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) {
+  for (int cb = 0; cb < NL; ++cb) {
     bit[cb] = (int)(c.info[cb] & 0xffu);                     // token's bit-width
     bsc[cb] = (int)((c.info[cb] >> c.info_shift) & 0xffu);   // its activation scale code
   }
@@ -586,20 +587,20 @@ __device__ inline void compute_group(const BData<NCB>& t, const WaveCtx<NCB>& c,
   if constexpr (BMIN <= 2) {
     const v8i au = zero_operand<BMIN>(z);
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) m[cb] = mfma_fp4_fp8(au, b8(t, cb), 127, bsc[cb]);
+    for (int cb = 0; cb < NL; ++cb) m[cb] = mfma_fp4_fp8(au, b8(t, cb), 127, bsc[cb]);
   } else {
     const v8i a0 = expand_sigma(w[0], k);
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) m[cb] = mfma_fp4_fp8(a0, b8(t, cb), 127, bsc[cb]);
+    for (int cb = 0; cb < NL; ++cb) m[cb] = mfma_fp4_fp8(a0, b8(t, cb), 127, bsc[cb]);
   }
 #pragma unroll
   for (int p = BMIN <= 2 ? 0 : 1; p < BMIN; ++p) {
     const v8i ap = expand_sigma(w[p], k);
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) m[cb] = mfma_fp4_fp8(ap, b8(t, cb), m[cb], 127 + p, bsc[cb]);
+    for (int cb = 0; cb < NL; ++cb) m[cb] = mfma_fp4_fp8(ap, b8(t, cb), m[cb], 127 + p, bsc[cb]);
   }
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) {
+  for (int cb = 0; cb < NL; ++cb) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) acc[cb][r] = fmaf(-s1[r], m[cb][r], acc[cb][r]);
     if constexpr (BMIN >= 3) {
@@ -614,7 +615,7 @@ __device__ inline void compute_group(const BData<NCB>& t, const WaveCtx<NCB>& c,
     float sp[4];
     scales4(sw[p - BMIN + 1], sp);
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
+    for (int cb = 0; cb < NL; ++cb) {
       const int bs = p < bit[cb] ? bsc[cb] : 0;
       const v4f d = mfma_fp4_fp8(ap, b8(t, cb), 128, bs);
 #pragma unroll
@@ -645,13 +646,16 @@ __device__ inline void wait_vm() {
 // waiting until only those remain outstanding makes the stage and the
 // activations of g ready.  The DMA of g+3 overwrites the stage of g-1, whose
 // LDS reads completed in the previous step.  The loop is unrolled by kDepth
-// so every stage offset is a constant.
-template <int MB, int BMIN, int NCB>
+// so every stage offset is a constant; the steps past the end are skipped by
+// guards rather than left by `break`, so the loop has one exit and the
+// compiler adds no exit flag that carries undefined loop values.  NL: the
+// column blocks that hold positions (the first NL of NCB).
+template <int MB, int BMIN, int NL, int NCB>
 __device__ inline void decode_groups(const WaveCtx<NCB>& c, uint8_t* ring, int g0, int g1,
                                      v4f (&acc)[NCB]) {
   static_assert(kDepth == 4, "the unrolled step below assumes four stages");
   if (g0 >= g1) return;
-  constexpr int ND = StageLayout<MB, BMIN>::ops, NB = 2 * NCB;
+  constexpr int ND = StageLayout<MB, BMIN>::ops, NB = 2 * NL;
   constexpr int kStage = stage_bytes<BMIN>();
   const DmaPlan<MB, BMIN> plan = dma_plan<MB, BMIN>(c);
   BData<NCB> B[2];
@@ -661,13 +665,12 @@ __device__ inline void decode_groups(const WaveCtx<NCB>& c, uint8_t* ring, int g
     for (int cb = 0; cb < NCB; ++cb) B[i].lo[cb] = B[i].hi[cb] = v4i{0, 0, 0, 0};
   dma_group<MB, BMIN>(plan, c, g0, ring);
   if (g0 + 1 < g1) dma_group<MB, BMIN>(plan, c, g0 + 1, ring + kStage);
-  load_b(B[0], c, g0);
+  load_b<NL>(B[0], c, g0);
   if (g0 + 2 < g1) dma_group<MB, BMIN>(plan, c, g0 + 2, ring + 2 * kStage);
 #define D2MOE_STEP(K)                                                        \
-  {                                                                          \
+  if (g + (K) < g1) {                                                        \
     const int gg = g + (K);                                                  \
-    if (gg >= g1) break;                                                     \
-    if (gg + 1 < g1) load_b(B[((K) + 1) & 1], c, gg + 1);                    \
+    if (gg + 1 < g1) load_b<NL>(B[((K) + 1) & 1], c, gg + 1);                \
     if (gg + 3 < g1) {                                                       \
       dma_group<MB, BMIN>(plan, c, gg + 3, ring + (((K) + 3) % kDepth) * kStage); \
       wait_vm<2 * ND + NB>();                                                \
@@ -679,7 +682,7 @@ __device__ inline void decode_groups(const WaveCtx<NCB>& c, uint8_t* ring, int g
       wait_vm<0>();                                                          \
     }                                                                        \
     ready_b(B[(K) & 1]);                                                     \
-    compute_group<MB, BMIN, ((K) % kDepth) * kStage, NCB>(B[(K) & 1], c, acc); \
+    compute_group<MB, BMIN, ((K) % kDepth) * kStage, NL>(B[(K) & 1], c, acc); \
   }
   for (int g = g0; g < g1; g += kDepth) {
     D2MOE_STEP(0)
@@ -781,10 +784,19 @@ void decode_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* 
   v4f acc[NCB];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) acc[cb] = v4f{0.f, 0.f, 0.f, 0.f};
+  // column blocks past the item's last position are skipped: with more
+  // than one block, the item's block count picks the group loop (three-block
+  // kernels serve items of two or three, two-block kernels of one or two)
+  const bool full = ncol > kDecodeCols * (NCB - 1);
   switch (mb) {
-#define D2MOE_CASE(MB) \
-  case MB:             \
-    if constexpr (MB >= BMIN) decode_groups<MB, BMIN, NCB>(c, ring[wave], g0, g1, acc); \
+#define D2MOE_CASE(MB)                                                                   \
+  case MB:                                                                               \
+    if constexpr (MB >= BMIN) {                                                          \
+      if (full || NCB == 1)                                                              \
+        decode_groups<MB, BMIN, NCB>(c, ring[wave], g0, g1, acc);                        \
+      else                                                                               \
+        decode_groups<MB, BMIN, NCB == 1 ? 1 : NCB - 1>(c, ring[wave], g0, g1, acc);     \
+    }                                                                                    \
     break;
     D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
     D2MOE_CASE(7) D2MOE_CASE(8)
@@ -836,7 +848,8 @@ void decode_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t* 
 // outstanding makes the stage and its activations ready.  The DMA of stage
 // s + 3 overwrites the stage of s - 1, whose LDS reads completed in the
 // previous step.  The loop is unrolled by kDepth stages (two groups) so that
-// every ring offset and activation buffer index is a constant.
+// every ring offset and activation buffer index is a constant, with guards
+// on the steps past the end as in decode_groups.
 // DMA of one stage.  Instructions that carry only plane words address them
 // from the wave-uniform base of group g's planes (16 bytes per lane, 1 KB per
 // instruction), so they hold no per-lane pointer.  The last, mixed
@@ -895,12 +908,12 @@ __device__ inline void settle(v4f (&acc)[NCB]) {
   for (int cb = 0; cb < NCB; ++cb) asm volatile("" : "+v"(acc[cb]));
 }
 
-template <int MB, int BMIN, int NCB>
+template <int MB, int BMIN, int NL, int NCB>
 __device__ inline void decode_pairs(const WaveCtx<NCB>& c, const W3Offsets& o3, uint8_t* ring,
                                     int g0, int g1, v4f (&acc)[2][NCB]) {
   static_assert(kDepth == 4, "the unrolled step below assumes four stages");
   using SL = StageLayout<MB, BMIN>;
-  constexpr int ND = SL::ops, NB = 2 * NCB;
+  constexpr int ND = SL::ops, NB = 2 * NL;
   constexpr int kStage = stage_bytes<BMIN>();
   const MixedDma mx = mixed_dma<MB, BMIN>(c, o3);
   const int N = 2 * (g1 - g0);  // stages
@@ -911,14 +924,13 @@ __device__ inline void decode_pairs(const WaveCtx<NCB>& c, const W3Offsets& o3, 
     for (int cb = 0; cb < NCB; ++cb) B[i].lo[cb] = B[i].hi[cb] = v4i{0, 0, 0, 0};
   if (N <= 0) return;
   dma_stage<MB, BMIN, false>(c, mx, o3.pl, g0, ring);
-  load_b(B[0], c, g0);
+  load_b<NL>(B[0], c, g0);
   if (1 < N) dma_stage<MB, BMIN, true>(c, mx, o3.pl, g0, ring + kStage);
   if (2 < N) dma_stage<MB, BMIN, false>(c, mx, o3.pl, g0 + 1, ring + 2 * kStage);
 #define D2MOE_PSTEP(K)                                                                   \
-  {                                                                                      \
+  if (s + (K) < N) {                                                                     \
     const int ss = s + (K);                                                              \
-    if (ss >= N) break;                                                                  \
-    if (((K) & 1) == 0 && ss + 2 < N) load_b(B[(((K) >> 1) + 1) & 1], c, g0 + (ss >> 1) + 1); \
+    if (((K) & 1) == 0 && ss + 2 < N) load_b<NL>(B[(((K) >> 1) + 1) & 1], c, g0 + (ss >> 1) + 1); \
     if (ss + 3 < N) {                                                                    \
       dma_stage<MB, BMIN, ((K) + 3) & 1>(c, mx, o3.pl, g0 + ((ss + 3) >> 1),            \
                                          ring + (((K) + 3) % kDepth) * kStage);          \
@@ -931,7 +943,7 @@ __device__ inline void decode_pairs(const WaveCtx<NCB>& c, const W3Offsets& o3, 
       wait_vm<0>();                                                                      \
     }                                                                                    \
     if (((K) & 1) == 0) ready_b(B[(K) >> 1]);                                            \
-    compute_group<MB, BMIN, ((K) % kDepth) * kStage, NCB>(B[(K) >> 1], c, acc[(K) & 1]); \
+    compute_group<MB, BMIN, ((K) % kDepth) * kStage, NL>(B[(K) >> 1], c, acc[(K) & 1]); \
     settle(acc[(K) & 1]);                                                                \
   }
   for (int s = 0; s < N; s += kDepth) {
@@ -1038,10 +1050,18 @@ void decode13_kernel(MwqView W, const int32_t* __restrict__ elist, const uint8_t
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) acc[h][cb] = v4f{0.f, 0.f, 0.f, 0.f};
   if (active) {
+    // as in decode_kernel: items that leave the last column block empty
+    // run the group loop of one block fewer
+    const bool full = ncol > kDecodeCols * (NCB - 1);
     switch (mb) {
-#define D2MOE_CASE(MB) \
-  case MB:             \
-    if constexpr (MB >= BMIN) decode_pairs<MB, BMIN, NCB>(c, o3, ring[wave], 0, g1 - g0, acc); \
+#define D2MOE_CASE(MB)                                                                   \
+  case MB:                                                                               \
+    if constexpr (MB >= BMIN) {                                                          \
+      if (full || NCB == 1)                                                              \
+        decode_pairs<MB, BMIN, NCB>(c, o3, ring[wave], 0, g1 - g0, acc);                 \
+      else                                                                               \
+        decode_pairs<MB, BMIN, NCB == 1 ? 1 : NCB - 1>(c, o3, ring[wave], 0, g1 - g0, acc); \
+    }                                                                                    \
     break;
       D2MOE_CASE(1) D2MOE_CASE(2) D2MOE_CASE(3) D2MOE_CASE(4) D2MOE_CASE(5) D2MOE_CASE(6)
       D2MOE_CASE(7) D2MOE_CASE(8)
