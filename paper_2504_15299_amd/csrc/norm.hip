@@ -11,40 +11,50 @@ namespace d2moe {
 namespace {
 
 constexpr int kNormThreads = 256;
-constexpr int kNormPer = 64;  // values per thread: d <= 256 * 64
+constexpr int kNormPer = 64;  // values per thread at most: d <= 256 * 64
 
-template <typename TY, typename TH>
+// NPER values per thread (NPER * 256 >= d).  Every load of the row is issued
+// before any value is used: with each value's add and store beside its load,
+// the compiler waited for every load before issuing the next, and a 4096-wide
+// row took 16 serial memory round trips (12 us for 64 rows).
+template <int NPER, typename TY, typename TH>
 __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
     float* __restrict__ x, const TY* __restrict__ y, int d, float eps, TH* __restrict__ h) {
   __shared__ float part[kNormThreads / 64];
   const size_t row = (size_t)blockIdx.x * d;
-  float v[kNormPer];
-  float ss = 0.0f;
+  float v[NPER], w[NPER];
 #pragma unroll
-  for (int i = 0; i < kNormPer; ++i) {
+  for (int i = 0; i < NPER; ++i) {
     const int c = threadIdx.x + i * kNormThreads;
-    v[i] = 0.0f;
-    if (c < d) {
-      float a = x[row + c];
-      if (y) {
-        if constexpr (sizeof(TY) == 2)
-          a += bf2f(((const uint16_t*)y)[row + c]);
-        else
-          a += ((const float*)y)[row + c];
-        x[row + c] = a;
-      }
-      v[i] = a;
-      ss = fmaf(a, a, ss);
+    v[i] = c < d ? x[row + c] : 0.0f;
+  }
+  if (y) {
+#pragma unroll
+    for (int i = 0; i < NPER; ++i) {
+      const int c = threadIdx.x + i * kNormThreads;
+      if constexpr (sizeof(TY) == 2)
+        w[i] = c < d ? bf2f(((const uint16_t*)y)[row + c]) : 0.0f;
+      else
+        w[i] = c < d ? ((const float*)y)[row + c] : 0.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < NPER; ++i) {
+      const int c = threadIdx.x + i * kNormThreads;
+      v[i] += w[i];
+      if (c < d) x[row + c] = v[i];
     }
   }
+  float ss = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NPER; ++i) ss = fmaf(v[i], v[i], ss);  // zero past the row
   for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
   __syncthreads();
   ss = 0.0f;
-  for (int w = 0; w < kNormThreads / 64; ++w) ss += part[w];
+  for (int k = 0; k < kNormThreads / 64; ++k) ss += part[k];
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
 #pragma unroll
-  for (int i = 0; i < kNormPer; ++i) {
+  for (int i = 0; i < NPER; ++i) {
     const int c = threadIdx.x + i * kNormThreads;
     if (c < d) {
       const float o = v[i] * inv;
@@ -56,16 +66,27 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
   }
 }
 
+template <int NPER, typename TY>
+hipError_t run_norm_n(float* x, const void* y, int T, int d, float eps, void* h, d2moe_dtype hd,
+                      hipStream_t s) {
+  if (hd == D2MOE_BF16)
+    residual_rmsnorm_kernel<NPER, TY, uint16_t><<<T, kNormThreads, 0, s>>>(
+        x, (const TY*)y, d, eps, (uint16_t*)h);
+  else
+    residual_rmsnorm_kernel<NPER, TY, float><<<T, kNormThreads, 0, s>>>(
+        x, (const TY*)y, d, eps, (float*)h);
+  return hipGetLastError();
+}
+
 template <typename TY>
 hipError_t run_norm(float* x, const void* y, int T, int d, float eps, void* h, d2moe_dtype hd,
                     hipStream_t s) {
-  if (hd == D2MOE_BF16)
-    residual_rmsnorm_kernel<TY, uint16_t><<<T, kNormThreads, 0, s>>>(x, (const TY*)y, d, eps,
-                                                                    (uint16_t*)h);
-  else
-    residual_rmsnorm_kernel<TY, float><<<T, kNormThreads, 0, s>>>(x, (const TY*)y, d, eps,
-                                                                 (float*)h);
-  return hipGetLastError();
+  const int per = (d + kNormThreads - 1) / kNormThreads;  // 1 .. kNormPer (checked by the caller)
+  if (per <= 4) return run_norm_n<4, TY>(x, y, T, d, eps, h, hd, s);
+  if (per <= 8) return run_norm_n<8, TY>(x, y, T, d, eps, h, hd, s);
+  if (per <= 16) return run_norm_n<16, TY>(x, y, T, d, eps, h, hd, s);
+  if (per <= 32) return run_norm_n<32, TY>(x, y, T, d, eps, h, hd, s);
+  return run_norm_n<kNormPer, TY>(x, y, T, d, eps, h, hd, s);
 }
 
 }  // namespace

@@ -17,8 +17,12 @@ from paper_2504_15299_amd import workloads as wl
 pytestmark = pytest.mark.gpu
 
 
+# widths that take each register-array size of the kernel (values per
+# thread 4, 8, 16, 32, 64), ragged and whole
 @pytest.mark.parametrize("d,y_dtype,h_dtype", [(4096, torch.bfloat16, torch.bfloat16),
                                                (300, torch.float32, torch.float32),
+                                               (2048, torch.float32, torch.bfloat16),
+                                               (5000, torch.bfloat16, torch.float32),
                                                (16384, None, torch.bfloat16)])
 def test_residual_rmsnorm(d, y_dtype, h_dtype):
     rng = np.random.default_rng(d)
