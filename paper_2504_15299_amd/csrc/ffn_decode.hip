@@ -167,27 +167,39 @@ __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
     const uint8_t* __restrict__ maxbit, int E, int L, int32_t* __restrict__ elist, int nitems,
     int item) {
   __shared__ float wmax[kPrepThreads / 64];
+  __shared__ int e_mb[64], e_lo[64], e_hi[64], e_cnt[64];  // per expert (E <= 64)
   const int pos = blockIdx.x, NG = K / G;
-  if (pos == npos && blockIdx.y == 0 && elist && threadIdx.x == 0) {
-    // experts in order of their largest bit-width, widest first, so that the
-    // longest work items are dispatched first and the short ones fill the
-    // end of the grid
-    int n = 0;
-    for (int b = 8; b >= 1; --b) {
-      for (int e = 0; e < E; ++e) {
-        if (maxbit[e] != b) continue;
-        const int lo = offsets[e * L], hi = offsets[e * L + L];
-        for (int p = lo; p < hi; p += item) {
-          elist[4 * n] = e;
-          elist[4 * n + 1] = p;
-          elist[4 * n + 2] = min(p + item, hi);
-          elist[4 * n + 3] = b;
-          ++n;
-        }
+  if (pos == npos && blockIdx.y == 0 && elist) {  // workgroup-uniform
+    // experts in order of their largest bit-width, widest first (then by
+    // index), so that the longest work items are dispatched first and the
+    // short ones fill the end of the grid.  One thread per expert: its rank
+    // in that order gives its first slot.
+    const int tid = threadIdx.x;
+    if (tid < E) {
+      const int mb = maxbit[tid], lo = offsets[tid * L], hi = offsets[tid * L + L];
+      e_mb[tid] = mb;
+      e_lo[tid] = lo;
+      e_hi[tid] = hi;
+      e_cnt[tid] = mb >= 1 && mb <= 8 ? (hi - lo + item - 1) / item : 0;
+    }
+    __syncthreads();
+    int total = 0;
+    for (int e = 0; e < E; ++e) total += e_cnt[e];
+    if (tid < E && e_cnt[tid] > 0) {
+      const int mb = e_mb[tid], hi = e_hi[tid];
+      int n = 0;
+      for (int e = 0; e < E; ++e)
+        if (e_mb[e] > mb || (e_mb[e] == mb && e < tid)) n += e_cnt[e];
+      for (int p = e_lo[tid]; p < hi; p += item, ++n) {
+        elist[4 * n] = tid;
+        elist[4 * n + 1] = p;
+        elist[4 * n + 2] = min(p + item, hi);
+        elist[4 * n + 3] = mb;
       }
     }
     // the remaining slots of the grid get no work (largest bit-width 0)
-    for (; n < nitems; ++n) elist[4 * n] = elist[4 * n + 1] = elist[4 * n + 2] = elist[4 * n + 3] = 0;
+    for (int n = total + tid; n < nitems; n += kPrepThreads)
+      elist[4 * n] = elist[4 * n + 1] = elist[4 * n + 2] = elist[4 * n + 3] = 0;
   }
   const TIN* src = nullptr;
   if (pos < npos) src = in + (long)(perm ? perm[pos] / kdiv : pos) * in_ld;
