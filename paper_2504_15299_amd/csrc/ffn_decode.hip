@@ -126,23 +126,41 @@ __device__ inline int row_scale_exp(float amax) {
 template <typename TIN>
 __device__ inline float row_absmax(const TIN* row, int K);
 template <>
+// Two 16-byte loads per thread in flight per round (a 4096-wide bf16 row is
+// one round); the maximum does not depend on the order.
 __device__ inline float row_absmax<uint16_t>(const uint16_t* row, int K) {
   float m = 0.0f;
-  for (int c = 8 * threadIdx.x; c < K; c += 8 * kPrepThreads) {
-    const uint4 u = *(const uint4*)(row + c);
-    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+  for (int c0 = 8 * threadIdx.x; c0 < K; c0 += 16 * kPrepThreads) {
+    uint4 u[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      m = fmaxf(m, fmaxf(fabsf(bf2f((uint16_t)(w[i] & 0xffff))), fabsf(bf2f((uint16_t)(w[i] >> 16)))));
+    for (int j = 0; j < 2; ++j) {
+      const int c = c0 + 8 * kPrepThreads * j;
+      u[j] = c < K ? *(const uint4*)(row + c) : uint4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const uint32_t w[4] = {u[j].x, u[j].y, u[j].z, u[j].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        m = fmaxf(m, fmaxf(fabsf(bf2f((uint16_t)(w[i] & 0xffff))),
+                           fabsf(bf2f((uint16_t)(w[i] >> 16)))));
+    }
   }
   return m;
 }
 template <>
 __device__ inline float row_absmax<float>(const float* row, int K) {
   float m = 0.0f;
-  for (int c = 4 * threadIdx.x; c < K; c += 4 * kPrepThreads) {
-    const float4 v = *(const float4*)(row + c);
-    m = fmaxf(m, fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w))));
+  for (int c0 = 4 * threadIdx.x; c0 < K; c0 += 8 * kPrepThreads) {
+    float4 v[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int c = c0 + 4 * kPrepThreads * j;
+      v[j] = c < K ? *(const float4*)(row + c) : float4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      m = fmaxf(m, fmaxf(fmaxf(fabsf(v[j].x), fabsf(v[j].y)), fmaxf(fabsf(v[j].z), fabsf(v[j].w))));
   }
   return m;
 }
@@ -206,8 +224,18 @@ __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
   float amax = 0.0f;
   if (src) {
     if (rowmax) {
-      for (int i = threadIdx.x; i < rowmax_parts; i += kPrepThreads)
-        amax = fmaxf(amax, __uint_as_float(rowmax[(size_t)pos * rowmax_parts + i]));
+      // four words per thread in flight per round (896 per row at the
+      // Mixtral width: one round), not one dependent load per step
+      const uint32_t* rm = rowmax + (size_t)pos * rowmax_parts;
+      for (int i0 = threadIdx.x; i0 < rowmax_parts; i0 += 4 * kPrepThreads) {
+        float v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int i = i0 + j * kPrepThreads;
+          v[j] = i < rowmax_parts ? __uint_as_float(rm[i]) : 0.0f;
+        }
+        amax = fmaxf(amax, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+      }
     } else {
       amax = row_absmax<TIN>(src, K);
     }
@@ -221,25 +249,44 @@ __global__ __launch_bounds__(kPrepThreads) void xprep_kernel(
   uint32_t* row = (uint32_t*)(Xq + (size_t)pos * NG * 256);
   const int c0 = blockIdx.y * kPrepCols, c1 = min(K, c0 + kPrepCols);
   // one dword per thread per step: output dword u of the row covers
-  // group u / 64, piece 0 (hi) dwords 0..31 of the group's 64
-  for (int u = c0 / 4 + threadIdx.x; u < c1 / 4; u += kPrepThreads) {
-    const int g = u >> 5, w = u & 31;                 // hi dword w of group g
-    const int qq = w >> 3, e4 = (w & 7) * 4;          // lane group, first byte
-    const int khw = e4 < 16 ? 16 * qq + e4 : 64 + 16 * qq + (e4 - 16);
-    const int kb = khw >> 5, dd = (khw & 31) >> 3, n0 = khw & 7;
-    uint32_t hi = 0, lo = 0;
+  // group u / 64, piece 0 (hi) dwords 0..31 of the group's 64.  Two steps
+  // per round, both steps' loads issued before either converts (a slice of
+  // 2048 columns is one round).
+  constexpr int kSteps = 2;
+  for (int u0 = c0 / 4 + threadIdx.x; u0 < c1 / 4; u0 += kSteps * kPrepThreads) {
+    float xv[kSteps][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int col = g * G + 32 * kb + 4 * (n0 + i) + dd;
-      const float x = src ? ldexpf(ld_act<TIN>(src + col), -s) : 0.0f;
-      const uint32_t ch = e4m3_rne(x);
-      const float r = x - e4m3_val(ch);
-      const uint32_t cl = e4m3_rne(r * 16.0f);
-      hi |= ch << (8 * i);
-      lo |= cl << (8 * i);
+    for (int j = 0; j < kSteps; ++j) {
+      const int u = u0 + j * kPrepThreads;
+      const int g = u >> 5, w = u & 31;                 // hi dword w of group g
+      const int qq = w >> 3, e4 = (w & 7) * 4;          // lane group, first byte
+      const int khw = e4 < 16 ? 16 * qq + e4 : 64 + 16 * qq + (e4 - 16);
+      const int kb = khw >> 5, dd = (khw & 31) >> 3, n0 = khw & 7;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int col = g * G + 32 * kb + 4 * (n0 + i) + dd;
+        xv[j][i] = src && u < c1 / 4 ? ld_act<TIN>(src + col) : 0.0f;
+      }
     }
-    row[g * 64 + w] = hi;
-    row[g * 64 + 32 + w] = lo;
+#pragma unroll
+    for (int j = 0; j < kSteps; ++j) {
+      const int u = u0 + j * kPrepThreads;
+      if (u < c1 / 4) {
+        const int g = u >> 5, w = u & 31;
+        uint32_t hi = 0, lo = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float x = ldexpf(xv[j][i], -s);
+          const uint32_t ch = e4m3_rne(x);
+          const float r = x - e4m3_val(ch);
+          const uint32_t cl = e4m3_rne(r * 16.0f);
+          hi |= ch << (8 * i);
+          lo |= cl << (8 * i);
+        }
+        row[g * 64 + w] = hi;
+        row[g * 64 + 32 + w] = lo;
+      }
+    }
   }
   if (threadIdx.x == 0 && blockIdx.y == 0) {
     const uint32_t bits = pos < npos ? tbits[bperm[pos]] : 0u;
