@@ -182,7 +182,8 @@ __device__ inline TopkIn topk_load(const float* __restrict__ logits, int t, int 
 
 __device__ inline int topk_wave(const TopkIn& in, int t, int E, int k, int b_min, int b_max,
                                 int lane, int32_t* __restrict__ topk_idx,
-                                float* __restrict__ topk_w, uint8_t* __restrict__ topk_bits) {
+                                float* __restrict__ topk_w, uint8_t* __restrict__ topk_bits,
+                                int* lkeys = nullptr, int L = 0) {
   uint64_t avail = E >= 64 ? ~0ull : ((1ull << E) - 1);
   float lmax = 0.0f, den = 0.0f;
   int my_idx = 0, my_b = 0;
@@ -209,9 +210,11 @@ __device__ inline int topk_wave(const TopkIn& in, int t, int E, int k, int b_min
   const bool clamp = lane < k && (my_b < b_min || my_b > b_max);
   if (__ballot(clamp)) flag |= 1;
   if (lane < k) {
+    const int b = my_b < b_min ? b_min : (my_b > b_max ? b_max : my_b);
     topk_idx[t * k + lane] = my_idx;
-    topk_bits[t * k + lane] = (uint8_t)(my_b < b_min ? b_min : (my_b > b_max ? b_max : my_b));
+    topk_bits[t * k + lane] = (uint8_t)b;
     topk_w[t * k + lane] = expf(my_v - lmax) / den;
+    if (lkeys) lkeys[t * k + lane] = my_idx * L + (b - b_min);  // the slot's histogram key
   }
   return flag;
 }
@@ -255,6 +258,10 @@ __global__ __launch_bounds__(kHistThreads) void hist_perm_kernel(
   __shared__ int off[kMaxKeys + 1];
   __shared__ int run[kMaxKeys];
   __shared__ int wave_cnt[kHistWaves][kMaxKeys];
+  // slot keys of the batches whose top-k runs here (T k <= 64 * 64), so that
+  // the histogram and placement read them from LDS rather than back from
+  // global memory
+  __shared__ int lkey[kInlineTopk * 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nkeys = E * L;
   __shared__ int flag_acc;
@@ -274,7 +281,8 @@ __global__ __launch_bounds__(kHistThreads) void hist_perm_kernel(
 #pragma unroll
     for (int j = 0; j < TPW; ++j) {
       const int t = wave + kHistWaves * j;
-      if (t < T) fl |= topk_wave(in[j], t, E, k, b_min, b_max, lane, topk_idx, topk_w, topk_bits);
+      if (t < T)
+        fl |= topk_wave(in[j], t, E, k, b_min, b_max, lane, topk_idx, topk_w, topk_bits, lkey, L);
     }
     if (lane != 0) fl = 0;
   } else {
@@ -287,8 +295,9 @@ __global__ __launch_bounds__(kHistThreads) void hist_perm_kernel(
   // selections before the reads below
   __syncthreads();
   if (tid == 0) *flags = flag_acc;
+  const bool inline_keys = T <= kInlineTopk;
   for (int s = tid; s < n; s += kHistThreads)
-    atomicAdd(&cnt[topk_idx[s] * L + (topk_bits[s] - b_min)], 1);
+    atomicAdd(&cnt[inline_keys ? lkey[s] : topk_idx[s] * L + (topk_bits[s] - b_min)], 1);
   __syncthreads();
   if (tid == 0) {
     int acc = 0;
@@ -311,7 +320,8 @@ __global__ __launch_bounds__(kHistThreads) void hist_perm_kernel(
     __syncthreads();
     const int s = base + tid;
     const bool valid = s < n;
-    const int key = valid ? topk_idx[s] * L + (topk_bits[s] - b_min) : 0;
+    const int key =
+        !valid ? 0 : inline_keys ? lkey[s] : topk_idx[s] * L + (topk_bits[s] - b_min);
     uint64_t same = __ballot(valid);
     for (int bit = 0; bit < 10; ++bit) {
       const bool b = (key >> bit) & 1;
