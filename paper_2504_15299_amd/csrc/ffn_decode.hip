@@ -15,9 +15,10 @@
 // -s_b * D (A scale 2).  The base code Q (b_min planes) folds into chained
 // MFMAs with A scales 2^p; at b_min = 2 a constant fp4 operand z - 1.5 joins
 // the chain, so (Q - z) . x = -D as well (larger b_min: one more MFMA with an
-// all-ones operand gives the activation sum for the zero-point term).  Every
-// plane thus costs one MFMA and one fp16-scaled FMA per output, and no weight
-// is ever materialised as a number.  Tokens whose bit-width is below a plane get
+// all-ones operand gives the activation sum for the zero-point term).  The
+// first two base planes share one operand (values +-1/2, +-3/2).  Every
+// residual plane thus costs one MFMA and one fp16-scaled FMA per output, and
+// no weight is ever materialised as a number.  Tokens whose bit-width is below a plane get
 // a zero coefficient for it; they share the loads.
 //
 // Work split: W1/W3 (decode13_kernel) gives each 16-row block of one active
@@ -319,6 +320,22 @@ __device__ inline v8i expand_sigma(uint32_t w, const SigmaConsts& k) {
   return a;
 }
 
+// fp4 e2m1 operand of the first two planes of the base code together: the
+// weight with bit b0 in plane 0 and b1 in plane 1 reads 3/2 - (b0 + 2 b1),
+// one of +-1/2, +-3/2 (sign b1; the exponent bit of value 1 set when
+// b0 == b1; mantissa bit 1), in the nibble order of expand_sigma.
+__device__ inline v8i expand_pair(uint32_t w0, uint32_t w1, const SigmaConsts& k) {
+  const uint32_t e = ~(w0 ^ w1);
+  constexpr uint32_t m2 = 0x22222222u;
+  v8i a;
+  a[0] = (int)((((w1 << 3) & k.m8) | k.c1) | ((e << 1) & m2));
+  a[1] = (int)((((w1 << 2) & k.m8) | k.c1) | (e & m2));
+  a[2] = (int)((((w1 << 1) & k.m8) | k.c1) | ((e >> 1) & m2));
+  a[3] = (int)(((w1 & k.m8) | k.c1) | ((e >> 2) & m2));
+  a[4] = a[5] = a[6] = a[7] = 0;
+  return a;
+}
+
 // Cross-lane product: every call sits in wave-uniform control flow (no
 // per-lane condition guards an MFMA or the use of its result in this file;
 // per-token predication is done through the activation block scale).
@@ -605,9 +622,10 @@ __device__ inline v8i ones_operand() {
 }
 
 // One group of the wave's 16 rows against the column blocks' activations.
-//   Base level: plane p < BMIN with A scale 2^p reads 2^p (1/2 - bit p), so
-//   the chained MFMAs give m = h S - Q.x with h = (2^BMIN - 1)/2 and S the
-//   column's activation sum, and s1 (Q - z).x = -s1 m + s1 (h - z) S.  For
+//   Base level: plane p < BMIN with A scale 2^p reads 2^p (1/2 - bit p)
+//   (planes 0 and 1 as one operand, 3/2 - (b0 + 2 b1)), so the chained
+//   MFMAs give m = h S - Q.x with h = (2^BMIN - 1)/2 and S the column's
+//   activation sum, and s1 (Q - z).x = -s1 m + s1 (h - z) S.  For
 //   BMIN <= 2 the constant operand z - h joins the chain, leaving -s1 m; for
 //   larger BMIN, S comes from one MFMA with an all-ones operand and the
 //   second term is one FMA per output.
@@ -641,19 +659,24 @@ __device__ inline void compute_group(const BData<NCB>& t, const WaveCtx<NCB>& c,
 #pragma unroll
     for (int r = 0; r < 4; ++r) zc[r] = s1[r] * (h - (float)((z >> (8 * r)) & 0xffu));
   }
-  // base chain, one expanded plane operand at a time for all column blocks
+  // base chain, one expanded operand at a time for all column blocks;
+  // planes 0 and 1 share one operand (A scale 1), so a nest from 2 bits
+  // chains the zero-point operand and the pair
   v4f m[NCB];
   if constexpr (BMIN <= 2) {
     const v8i au = zero_operand<BMIN>(z);
 #pragma unroll
     for (int cb = 0; cb < NL; ++cb) m[cb] = mfma_fp4_fp8(au, b8(t, cb), 127, bsc[cb]);
-  } else {
-    const v8i a0 = expand_sigma(w[0], k);
+    const v8i ap = BMIN == 2 ? expand_pair(w[0], w[BMIN - 1], k) : expand_sigma(w[0], k);
 #pragma unroll
-    for (int cb = 0; cb < NL; ++cb) m[cb] = mfma_fp4_fp8(a0, b8(t, cb), 127, bsc[cb]);
+    for (int cb = 0; cb < NL; ++cb) m[cb] = mfma_fp4_fp8(ap, b8(t, cb), m[cb], 127, bsc[cb]);
+  } else {
+    const v8i a01 = expand_pair(w[0], w[1], k);
+#pragma unroll
+    for (int cb = 0; cb < NL; ++cb) m[cb] = mfma_fp4_fp8(a01, b8(t, cb), 127, bsc[cb]);
   }
 #pragma unroll
-  for (int p = BMIN <= 2 ? 0 : 1; p < BMIN; ++p) {
+  for (int p = 2; p < BMIN; ++p) {
     const v8i ap = expand_sigma(w[p], k);
 #pragma unroll
     for (int cb = 0; cb < NL; ++cb) m[cb] = mfma_fp4_fp8(ap, b8(t, cb), m[cb], 127 + p, bsc[cb]);
