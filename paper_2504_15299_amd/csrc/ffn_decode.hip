@@ -784,7 +784,7 @@ __device__ inline void decode_groups(const WaveCtx<NCB>& c, uint8_t* ring, int g
 // One W2 row block per workgroup: its NW waves split the groups and combine
 // their partial sums through LDS (each wave's partial sums go to its own
 // ring, which is idle by then).  NCB column blocks of 8 tokens share every
-// plane operand (two when experts hold more than 7 positions on average,
+// plane operand (two when experts hold more than 4 positions on average,
 // three above 12), at 4 waves per SIMD for one block, 3 for two and 2 for
 // three (three blocks need more than the 168 registers of 3 waves).
 template <int NW, int NCB, int BMIN>
@@ -1306,16 +1306,17 @@ hipError_t launch_decode_ffn(const void* x, d2moe_dtype xd, int T, int d, int d_
   hipError_t err;
   const int L = w13->b_max - w13->b_min + 1;
   const int npos = T * k;
-  // two column blocks per work item once experts hold more than 7 positions
+  // two column blocks per work item once experts hold more than 4 positions
   // on average (an expert's planes are then streamed once for up to 16 of
-  // its positions instead of once per 8).  Below that, streaming the few
-  // experts with more than 8 positions twice costs less than doubling the
-  // MFMAs and scale FMAs per plane for every expert (measured from 20 to 32
-  // tokens at the Mixtral shape).  Three above 12 on average: at 16 (64
-  // tokens, top-2 of 8) about 4 experts in 10 hold more than 16 positions,
-  // and streaming them once for up to 24 took the step from 0.54-0.56 to
-  // 0.51-0.52 ms at the Mixtral shape.
-  const int ncb = npos > 12 * E ? 3 : npos > 7 * E ? 2 : 1;
+  // its positions instead of once per 8, and an item of 8 or fewer runs the
+  // one-block loop of the two-block kernel, its empty block skipped): at the
+  // Mixtral shape 20, 24 and 28 tokens took 0.243-0.246, 0.277 and
+  // 0.290-0.295 ms per step against 0.251, 0.287 and 0.331 ms with the
+  // threshold at 7.  Three above 12 on average: at 16 (64 tokens, top-2 of
+  // 8) about 4 experts in 10 hold more than 16 positions, and streaming them
+  // once for up to 24 took the step from 0.54-0.56 to 0.51-0.52 ms; from 7
+  // or 9 instead of 12 it was slower from 32 or 40 tokens on.
+  const int ncb = npos > 12 * E ? 3 : npos > 4 * E ? 2 : 1;
   const int item = ncb * kDecodeCols;
   // work items: each active expert's positions in runs of `item`
   const int ny = (E < npos ? E : npos) + (npos + item - 1) / item;
